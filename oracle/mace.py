@@ -1,0 +1,348 @@
+"""Plain FP64 MACE energy and forces on the CPU (oracle).
+
+Follows the paper's model section: the graph problem statement, the two-body
+edge embedding A (Eq. 26), the product basis B (Eq. 27), the message as a
+weighted sum over correlation orders and couplings, the linear update with a
+residual, the readouts, E = sum_i eps_i and F_i = -dE/dr_i; and the module
+and parameter table of the architecture-breakdown appendix (ScaleShiftMACE:
+embedding, radial embedding, harmonics, Interactions[0] = non-residual block
+with a species-dependent linear on the message, Interactions[t>=1] = residual
+block, product-basis linears, linear readout then a 128->16->1 MLP readout).
+
+Readings where the paper is silent, ambiguous or garbled (each one fixed
+here and followed identically by the HIP library, which is written
+separately):
+
+R1  Harmonics, CG couplings, U basis: see ``oracle.so3``.
+R2  Path set of the edge product: (l_h, l_Y, l_out) with l_h over the hidden
+    irreps entering the layer, l_Y = 0..3, l_out = 0..3, l_h+l_Y+l_out even
+    (natural parity), sorted lexicographically; the coupling is
+    C^{l_out}_{l_h l_Y}: hidden feature first, harmonic second.  Reproduces
+    the appendix's 4 / 10 paths and 16x / 40x mid dimensions.
+R3  Edge vector d = r_sender + shift - r_receiver.
+R4  Radial basis: e_n(r) = sqrt(2/rc) sin(n pi r/rc)/r * u(r/rc), n = 1..8,
+    polynomial envelope u(x) = 1 - (p+1)(p+2)/2 x^p + p(p+2) x^(p+1)
+    - p(p+1)/2 x^(p+2) for x < 1, else 0, with p = 5 (the text's value; the
+    appendix config lists 6).
+R5  Radial MLP [8, 64, 64, 64, P*K], bias-free, plain SiLU between layers.
+R6  Neighbour sum divided by a model constant c_norm.
+R7  Layer 0 applies the species-dependent linear to the message after the
+    path-merging linear (no residual); layers t >= 1 add a species-dependent
+    linear of h^t (residual) to the product linear's output.
+R8  The product basis of the last layer outputs scalars only.
+R9  Readouts act on the scalars of h^{t+1}: a K->1 linear for t < T-1, and
+    K->16->SiLU->1 for the last layer, all bias-free.  E0 = 0, scale 1,
+    shift 0.
+R10 Every linear is y_k = sum_k' W[k', k] x_k'; weights are N(0,1)/sqrt(fan_in)
+    (fan_in of a species-dependent linear = K; of a path-merging linear =
+    number of paths into that l times K; of a product-basis weight block =
+    number of couplings eta for that (nu, L)).
+R11 BF16-linear mode (emulation): inputs and weights of the channel-mixing
+    linears (linear_up, path-merging linear, species linears, product linear,
+    readout linears) rounded to bfloat16 (round to nearest even); all sums
+    and every other step in FP64.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import so3
+from .neighbors import neighbor_list
+
+DT = torch.float64
+
+
+@dataclass(frozen=True)
+class ModelDesc:
+    n_species: int
+    K: int
+    hidden_lmax: int            # lmax of the hidden irreps leaving non-last layers
+    r_cut: float
+    c_norm: float
+    n_layers: int = 2
+    sh_lmax: int = 3
+    correlation: int = 3
+    n_bessel: int = 8
+    envelope_p: int = 5
+    radial_hidden: tuple = (64, 64, 64)
+    readout_hidden: int = 16
+
+
+def layer_in_ls(d: ModelDesc, t: int):
+    return [0] if t == 0 else list(range(d.hidden_lmax + 1))
+
+
+def layer_out_ls(d: ModelDesc, t: int):
+    return [0] if t == d.n_layers - 1 else list(range(d.hidden_lmax + 1))
+
+
+def tp_paths(d: ModelDesc, t: int):
+    """Edge tensor-product paths (l_h, l_Y, l_out), reading R2."""
+    paths = []
+    for lh in layer_in_ls(d, t):
+        for ly in range(d.sh_lmax + 1):
+            for lo in range(abs(lh - ly), min(lh + ly, d.sh_lmax) + 1):
+                if (lh + ly + lo) % 2 == 0:
+                    paths.append((lh, ly, lo))
+    return paths
+
+
+def weight_layout(d: ModelDesc):
+    """[(name, shape, fan_in)] in blob order."""
+    S, K = d.n_species, d.K
+    lay = [("embed", (S, K), S)]
+    for t in range(d.n_layers):
+        in_ls, out_ls = layer_in_ls(d, t), layer_out_ls(d, t)
+        paths = tp_paths(d, t)
+        P = len(paths)
+        for l in in_ls:
+            lay.append((f"{t}.up.{l}", (K, K), K))
+        h = (d.n_bessel,) + tuple(d.radial_hidden)
+        for i in range(len(h) - 1):
+            lay.append((f"{t}.radial.{i}", (h[i], h[i + 1]), h[i]))
+        lay.append((f"{t}.radial.{len(h) - 1}", (h[-1], P * K), h[-1]))
+        for p, (lh, ly, lo) in enumerate(paths):
+            n_in = sum(1 for q in paths if q[2] == lo)
+            lay.append((f"{t}.linear.{p}", (K, K), n_in * K))
+        if t == 0:
+            for l in range(d.sh_lmax + 1):
+                lay.append((f"{t}.skip.{l}", (S, K, K), K))
+        else:
+            for L in out_ls:
+                if L in in_ls:
+                    lay.append((f"{t}.skip.{L}", (S, K, K), K))
+        for L in out_ls:
+            for nu in range(1, d.correlation + 1):
+                ne = so3.n_eta(nu, L)
+                if ne:
+                    lay.append((f"{t}.symc.{L}.{nu}", (S, ne, K), ne))
+        for L in out_ls:
+            lay.append((f"{t}.prod.{L}", (K, K), K))
+        if t < d.n_layers - 1:
+            lay.append((f"{t}.readout", (K,), K))
+        else:
+            lay.append((f"{t}.readout.0", (K, d.readout_hidden), K))
+            lay.append((f"{t}.readout.1", (d.readout_hidden,), d.readout_hidden))
+    return lay
+
+
+def unpack_weights(d: ModelDesc, blob: np.ndarray):
+    out, o = {}, 0
+    for name, shape, _ in weight_layout(d):
+        n = int(np.prod(shape))
+        out[name] = torch.from_numpy(np.asarray(blob[o:o + n], dtype=np.float64).reshape(shape).copy())
+        o += n
+    if o != len(blob):
+        raise ValueError(f"weight blob has {len(blob)} floats, layout needs {o}")
+    return out
+
+
+# --------------------------------------------------------------------------
+# per-edge features (Eq. 26 ingredients)
+# --------------------------------------------------------------------------
+
+def envelope(x: torch.Tensor, p: int) -> torch.Tensor:
+    """Polynomial cutoff envelope, reading R4."""
+    v = (1.0 - (p + 1) * (p + 2) / 2.0 * x ** p + p * (p + 2) * x ** (p + 1)
+         - p * (p + 1) / 2.0 * x ** (p + 2))
+    return torch.where(x < 1.0, v, torch.zeros_like(x))
+
+
+def bessel_basis(r: torch.Tensor, r_cut: float, n_basis: int, p: int) -> torch.Tensor:
+    """e_n(r), n = 1..n_basis, reading R4 -> [E, n_basis]."""
+    n = torch.arange(1, n_basis + 1, dtype=r.dtype)
+    b = math.sqrt(2.0 / r_cut) * torch.sin(n[None, :] * math.pi * r[:, None] / r_cut) / r[:, None]
+    return b * envelope(r / r_cut, p)[:, None]
+
+
+def silu(x):
+    return x * torch.sigmoid(x)
+
+
+def radial_mlp(e: torch.Tensor, W: dict, t: int, n_hidden: int) -> torch.Tensor:
+    """Reading R5: e @ W0 -> SiLU -> ... -> @ W_last."""
+    h = e
+    for i in range(n_hidden):
+        h = silu(h @ W[f"{t}.radial.{i}"])
+    return h @ W[f"{t}.radial.{n_hidden}"]
+
+
+# --------------------------------------------------------------------------
+# model
+# --------------------------------------------------------------------------
+
+def _round_bf16(x: torch.Tensor) -> torch.Tensor:
+    return x.to(torch.bfloat16).to(DT)
+
+
+class _Lin:
+    """Channel-mixing linear y = x @ W with optional BF16 emulation (R11)."""
+
+    def __init__(self, bf16: bool):
+        self.bf16 = bf16
+
+    def __call__(self, x, W):
+        if self.bf16:
+            return _round_bf16(x) @ _round_bf16(W)
+        return x @ W
+
+    def species(self, x, W, z):
+        """x [N, c, K], W [S, K, K], z [N]: y[n] = x[n] @ W[z[n]]."""
+        Wz = W[z]
+        if self.bf16:
+            return torch.bmm(_round_bf16(x), _round_bf16(Wz))
+        return torch.bmm(x, Wz)
+
+
+def symmetric_contraction(A: torch.Tensor, W: dict, t: int, L: int, z: torch.Tensor,
+                          correlation: int, chunk: int = 64) -> torch.Tensor:
+    """Eq. 27 + message: B_{n,k,M} = sum_nu sum_eta W^{nu}_{z_n,L}[eta,k]
+    sum_{a_1..a_nu} U^{nu,L}_eta[M, a_1..a_nu] prod_xi A_{n,k,a_xi}.
+
+    A: [N, 16, K] -> [N, 2L+1, K].  Dense U, node chunks to bound memory.
+    """
+    N, ncomp, K = A.shape
+    outs = []
+    Us = {}
+    for nu in range(1, correlation + 1):
+        _trees, us = so3.u_basis(nu, L)
+        if us:
+            Us[nu] = torch.from_numpy(np.stack(us).reshape(len(us) * (2 * L + 1), -1))
+    for c0 in range(0, N, chunk):
+        a = A[c0:c0 + chunk].transpose(1, 2)                  # [n, K, 16]
+        n = a.shape[0]
+        zc = z[c0:c0 + chunk]
+        acc = torch.zeros(n, K, 2 * L + 1, dtype=DT)
+        mono = None
+        for nu in range(1, correlation + 1):
+            mono = a if nu == 1 else (mono[..., :, None] * a[..., None, :]).reshape(n, K, -1)
+            if nu not in Us:
+                continue
+            ne = Us[nu].shape[0] // (2 * L + 1)
+            Bnu = (mono @ Us[nu].T).reshape(n, K, ne, 2 * L + 1)   # [n,K,eta,M]
+            w = W[f"{t}.symc.{L}.{nu}"][zc]                          # [n, eta, K]
+            acc = acc + torch.einsum("nkem,nek->nkm", Bnu, w)
+        outs.append(acc.transpose(1, 2))
+    return torch.cat(outs, dim=0)
+
+
+@dataclass
+class Graph:
+    sender: torch.Tensor
+    receiver: torch.Tensor
+    shift_vec: torch.Tensor     # [E,3] float64 (S . cell)
+    species: torch.Tensor
+    graph_of_atom: torch.Tensor
+    n_graphs: int
+
+
+def build_graph(system, d: ModelDesc) -> Graph:
+    s, r, S = neighbor_list(system.positions, d.r_cut, system.cells, system.graph_of_atom)
+    if system.cells is not None and len(s):
+        g = system.graph_of_atom[r]
+        cells = np.asarray(system.cells, dtype=np.float64)[g]          # [E,3,3]
+        Sf = S.astype(np.float64)
+        sv = ((Sf[:, 0:1] * cells[:, 0]) + (Sf[:, 1:2] * cells[:, 1])) + (Sf[:, 2:3] * cells[:, 2])
+    else:
+        sv = np.zeros((len(s), 3))
+    return Graph(torch.from_numpy(s), torch.from_numpy(r), torch.from_numpy(sv),
+                 torch.from_numpy(np.asarray(system.species, dtype=np.int64)),
+                 torch.from_numpy(np.asarray(system.graph_of_atom, dtype=np.int64)),
+                 int(system.n_graphs))
+
+
+def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
+                  bf16_linear: bool = False, edge_chunk: int = 1 << 16,
+                  return_intermediates: bool = False):
+    """Per-atom energies eps_i [N] for positions pos [N,3] (float64)."""
+    lin = _Lin(bf16_linear)
+    z = graph.species
+    N = pos.shape[0]
+    K = d.K
+    snd, rcv = graph.sender, graph.receiver
+    E = len(snd)
+    vec = pos[snd] + graph.shift_vec - pos[rcv]                          # R3
+    r = torch.sqrt((vec * vec).sum(-1))
+    u = vec / r[:, None]
+    Y = so3.sh_all(u, d.sh_lmax)                                         # [E,16]
+    rb = bessel_basis(r, d.r_cut, d.n_bessel, d.envelope_p)              # [E,8]
+    inter = {"Y": Y, "rbf": rb}
+
+    # node embedding: linear on one-hot species
+    h = {0: W["embed"][z][:, None, :]}                                   # {l: [N, 2l+1, K]}
+    eps = torch.zeros(N, dtype=DT)
+    nh = len(d.radial_hidden)
+    for t in range(d.n_layers):
+        in_ls, out_ls = layer_in_ls(d, t), layer_out_ls(d, t)
+        paths = tp_paths(d, t)
+        sc = {}
+        if t > 0:
+            for L in out_ls:
+                if L in in_ls:
+                    sc[L] = lin.species(h[L], W[f"{t}.skip.{L}"], z)
+        ht = {l: lin(h[l], W[f"{t}.up.{l}"]) for l in in_ls}            # linear_up
+        At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
+        for e0 in range(0, E, edge_chunk):
+            sl = slice(e0, e0 + edge_chunk)
+            R = radial_mlp(rb[sl], W, t, nh).reshape(-1, len(paths), K)  # [e,P,K]
+            for p, (lh, ly, lo) in enumerate(paths):
+                C = torch.from_numpy(so3.real_cg(lh, ly, lo))
+                hs = ht[lh][snd[sl]]                                      # [e, 2lh+1, K]
+                Yl = Y[sl, ly * ly: ly * ly + 2 * ly + 1]                 # [e, 2ly+1]
+                msg = torch.einsum("abc,eak,eb->eck", C, hs, Yl) * R[:, p, None, :]
+                At[p] = At[p].index_add(0, rcv[sl], msg)
+        At = [a / d.c_norm for a in At]                                   # R6
+        A = []
+        for l in range(d.sh_lmax + 1):
+            acc = torch.zeros(N, 2 * l + 1, K, dtype=DT)
+            for p, (_, _, lo) in enumerate(paths):
+                if lo == l:
+                    acc = acc + lin(At[p], W[f"{t}.linear.{p}"])
+            A.append(acc)
+        if t == 0:                                                         # R7
+            A = [lin.species(A[l], W[f"{t}.skip.{l}"], z) for l in range(d.sh_lmax + 1)]
+        Afull = torch.cat(A, dim=1)                                        # [N,16,K]
+        hn = {}
+        for L in out_ls:
+            B = symmetric_contraction(Afull, W, t, L, z, d.correlation)
+            hn[L] = lin(B, W[f"{t}.prod.{L}"])
+            if L in sc:
+                hn[L] = hn[L] + sc[L]
+        s0 = hn[0][:, 0, :]                                                # [N,K]
+        if t < d.n_layers - 1:
+            eps = eps + lin(s0, W[f"{t}.readout"][:, None])[:, 0]
+        else:
+            hid = silu(lin(s0, W[f"{t}.readout.0"]))
+            eps = eps + lin(hid, W[f"{t}.readout.1"][:, None])[:, 0]
+        if return_intermediates:
+            inter[f"{t}.A"] = Afull
+            inter[f"{t}.h"] = hn
+        h = hn
+    if return_intermediates:
+        return eps, inter
+    return eps
+
+
+def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
+    return torch.zeros(graph.n_graphs, dtype=DT).index_add(0, graph.graph_of_atom, eps)
+
+
+def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
+                  bf16_linear: bool = False, forces: bool = True):
+    """Returns dict(eps [N], energy [G], forces [N,3] or None, graph)."""
+    W = unpack_weights(d, blob)
+    if graph is None:
+        graph = build_graph(system, d)
+    pos = torch.tensor(system.positions, dtype=DT, requires_grad=forces)
+    eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear)
+    Eg = graph_energies(eps, graph)
+    F = None
+    if forces:
+        (g,) = torch.autograd.grad(Eg.sum(), pos)
+        F = -g
+    return {"eps": eps.detach().numpy(), "energy": Eg.detach().numpy(),
+            "forces": None if F is None else F.numpy(), "graph": graph}
