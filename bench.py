@@ -1,0 +1,193 @@
+"""Throughput of MACE energy + forces on one MI355X through the C ABI.
+
+One step = one mace_forces call (energy forward + force backward, every
+kernel of the path) over periodic water, 1536 atoms (512 H2O, 1 g/cm^3,
+cutoff 5 A, ~54 neighbours per atom), K = 128, hidden 128x0e+128x1o,
+correlation 3, 2 layers; synthetic positions and N(0,1)/sqrt(fan_in) weights.
+Inputs are resident in HBM before the timed region.
+
+Prints one JSON line: atoms/s (value), edges/s, ms per step, the roofline
+of the dominant kernel (measured with HIP events on the library's stream
+over the timed region), and the FP64 CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP32_VALU_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def kernel_work(name, model, N, E):
+    """Algorithmic (bytes, flops) of every launch of kernel class `name` in
+    one step, summed.  Bytes count each compulsory HBM read/write once."""
+    K, nb, layers = model["K"], model["n_bessel"], model["layers"]
+    tot_b = tot_f = 0.0
+    for t, L in enumerate(layers):
+        P, mid, din, dout, nnz = L["P"], L["mid"], L["din"], L["dout"], L["nnz"]
+        if name == "tp_fwd_kernel":
+            tot_b += E * (P * K * 4 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4
+            tot_f += E * 2 * K * (nnz + mid)
+        elif name == "tp_bwd_kernel":
+            q = din * K * 4 if t > 0 else 0
+            tot_b += E * (2 * P * K * 4 + 64 + 64 * (t < len(layers) - 1) + 64 + 4 + q) + N * (din + mid) * K * 4
+            tot_f += E * 2 * K * (3 * nnz + 2 * mid)
+        elif name == "radial_fwd_kernel":
+            tot_b += E * (nb * 4 + P * K * 4)
+            tot_f += E * 2 * (nb * 64 + 2 * 64 * 64 + 64 * P * K)
+        elif name == "radial_bwd_kernel":
+            tot_b += E * (nb * 4 + P * K * 4 + nb * 4 * (1 + (t < len(layers) - 1)))
+            tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64 + 64 * P * K)
+    return tot_b, tot_f
+
+
+def cpu_baseline(params, seconds_hint=20.0):
+    """FP64 oracle E+F on a 64-molecule periodic water box with the same
+    model (a bounded sample of the workload; atoms/s scales with atoms)."""
+    import torch
+
+    import synth
+    from oracle import mace
+    torch.set_num_threads(os.cpu_count() or 1)
+    sysm = synth.water_box(64, seed=11)
+    d = mace.ModelDesc(**params)
+    blob = synth.weight_blob(mace.weight_layout(d), 0)
+    graph = mace.build_graph(sysm, d)
+    t0 = time.perf_counter()
+    mace.energy_forces(d, blob, sysm, graph=graph)
+    t1 = time.perf_counter()
+    reps = 1
+    if (t1 - t0) < seconds_hint / 2:
+        mace.energy_forces(d, blob, sysm, graph=graph)
+        reps = 2
+    t2 = time.perf_counter()
+    per = (t2 - t0) / reps
+    return {"value": sysm.n_atoms / per, "unit": "atoms/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": f"FP64 oracle energy+forces, periodic water 64 H2O ({sysm.n_atoms} atoms, "
+                      f"{len(graph.sender)} edges), same model; {reps} evaluation(s), {per:.2f} s each"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--prec", choices=["fp32", "bf16"], default="fp32")
+    ap.add_argument("--kernel", default="auto", help="kernel class whose roofline is reported")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for {max(args.gpus, world)}): this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2510_23621_amd import binding as B
+    from paper_2510_23621_amd.graph import MaceGraph
+    from synth.configs import CONFIGS, make_system, model_params
+
+    cfg = args.config
+    params = model_params(cfg)
+    prec = B.MACE_FP32 if args.prec == "fp32" else B.MACE_BF16_LINEAR
+    sysm = make_system(cfg, seed=0)
+    desc = B.make_desc(**params)
+    lay, _ = B.mace_weight_layout(desc)
+    blob = synth.weight_blob([(n, (s,), f) for n, s, f in lay], 0)
+    snd, rcv, sh = B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells, sysm.graph_of_atom,
+                                        sysm.n_graphs)
+    N, E = sysm.n_atoms, len(snd)
+    periodic = sysm.cells is not None
+    g = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                  sh if periodic else None, sysm.cells if periodic else None,
+                  sysm.graph_of_atom.astype(np.int32) if sysm.n_graphs > 1 else None, sysm.n_graphs, prec)
+    pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
+    eps, Eg, F = g.outputs(True)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        B.mace_forces(g.handle, pos, eps, Eg, F, stream)
+    torch.cuda.synchronize()
+
+    # dominant kernel: the class with the most time in one profiled step
+    kids = B.kernel_ids()
+    kname = args.kernel
+    if kname == "auto":
+        best, best_ms = None, -1.0
+        for name, kid in kids.items():
+            B.mace_profile_select(g.handle, kid)
+            B.mace_forces(g.handle, pos, eps, Eg, F, stream)
+            ms, _ = B.mace_profile_read(g.handle)
+            if ms > best_ms:
+                best, best_ms = name, ms
+        kname = best
+    B.mace_profile_select(g.handle, kids[kname])
+    torch.cuda.synchronize()
+
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        B.mace_forces(g.handle, pos, eps, Eg, F, stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    k_ms, k_launches = B.mace_profile_read(g.handle)
+    B.mace_profile_select(g.handle, -1)
+    ms_step = total_ms / args.steps
+
+    from paper_2510_23621_amd.csrc_info import layer_shapes
+    model = layer_shapes(params)
+    byts, flops = kernel_work(kname, model, N, E)
+    per_launch = k_launches / args.steps
+    avg_launch_ms = k_ms / max(k_launches, 1)
+    bytes_per_launch = byts / max(per_launch, 1)
+    flops_per_launch = flops / max(per_launch, 1)
+    gbs = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
+    tfl = flops_per_launch / (avg_launch_ms * 1e-3) / 1e12
+    if kname in ("radial_fwd_kernel", "radial_bwd_kernel"):
+        roof = {"bound": "alu", "achieved": round(tfl, 3), "peak": FP32_VALU_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tfl / FP32_VALU_PEAK_TFLOPS, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    roof.update({"traffic": None, "kernel": kname, "avg_launch_ms": round(avg_launch_ms, 5),
+                 "launches_per_step": per_launch, "algorithmic_bytes_per_launch": int(bytes_per_launch),
+                 "algorithmic_flops_per_launch": int(flops_per_launch),
+                 "kernel_share_of_step": round(k_ms / total_ms, 4)})
+
+    out = {
+        "metric": "atoms/s and edges/s for MACE energy+forces (FP32, BF16-linear); % roofline",
+        "value": round(N * args.steps / (total_ms * 1e-3), 1),
+        "unit": "atoms/s",
+        "edges_per_s": round(E * args.steps / (total_ms * 1e-3), 1),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if prec == B.MACE_FP32 else "f32+bf16-linear",
+        "data": "synthetic",
+        "config": {"workload": CONFIGS[cfg]["name"], "n_atoms": N, "n_edges": E, "K": params["K"],
+                   "hidden_lmax": params["hidden_lmax"], "r_cut": params["r_cut"], "correlation": 3,
+                   "layers": 2, "precision": args.prec},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(params)
+    g.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,154 @@
+/* mace.h -- C ABI of the MI355X (gfx950) MACE layer library.
+ *
+ * Computes, for a batch of atomic graphs, per-atom energies eps_i, per-graph
+ * energies E_g = sum_{i in g} eps_i and forces F_i = -dE/dr_i of a MACE model
+ * (arXiv 2510.23621: graph problem statement; two-body edge embedding,
+ * Eq. 26; product basis, Eq. 27; message/update/readout paragraph; energy and
+ * force equations; architecture table of the appendix).  Inputs follow the
+ * problem statement: species, positions, directed edges j -> i within the
+ * cutoff with their periodic image shifts, and model weights.
+ *
+ * Pointers marked (dev) are device memory owned by the caller; pointers
+ * marked (host) are host memory owned by the caller.  The library never
+ * allocates or frees device memory: every buffer it needs is carved from
+ * the caller's workspace.  Entry points taking a stream enqueue on it.
+ *
+ * Errors: every entry point validates its arguments synchronously and
+ * returns a mace_status; nothing is enqueued when it returns an error.
+ */
+#ifndef MACE_H_
+#define MACE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MACE_OK = 0,
+  MACE_EINVAL = -1,       /* null pointer, bad size, inconsistent arguments */
+  MACE_ERANGE = -2,       /* index or species out of range, unsorted edges */
+  MACE_ENOSPACE = -3,     /* workspace or output capacity too small */
+  MACE_EHIP = -4,         /* a HIP runtime call failed */
+  MACE_ENONFINITE = -5,   /* non-finite input detected */
+  MACE_ESTATE = -6,       /* handle in a state that does not allow the call */
+  MACE_EUNSUPPORTED = -7  /* model shape outside what the kernels implement */
+} mace_status;
+
+typedef enum {
+  MACE_FP32 = 0,          /* every step in FP32 */
+  MACE_BF16_LINEAR = 1    /* channel-mixing linears with BF16 inputs and weights,
+                             FP32 accumulation; everything else FP32 */
+} mace_precision;
+
+/* Model hyper-parameters (host).  Supported: sh_lmax = 3, correlation = 3,
+ * 1 <= n_bessel <= 16, radial_hidden = {64, 64, 64}, 1 <= readout_hidden <= 16,
+ * 0 <= hidden_lmax <= 2, K in {32, 64, 96, 128}, n_layers >= 1. */
+typedef struct mace_model_desc {
+  int32_t n_species;       /* S */
+  int32_t K;               /* channels */
+  int32_t n_layers;        /* interaction layers T */
+  int32_t sh_lmax;         /* edge harmonics l <= sh_lmax */
+  int32_t correlation;     /* nu <= correlation */
+  int32_t n_bessel;        /* radial basis size */
+  int32_t envelope_p;      /* polynomial envelope exponent */
+  int32_t radial_hidden[3];
+  int32_t readout_hidden;  /* hidden width of the last readout MLP */
+  int32_t hidden_lmax;     /* lmax of hidden features leaving non-last layers */
+  double r_cut;            /* cutoff radius (A) */
+  double c_norm;           /* neighbour-sum normalisation constant */
+} mace_model_desc;
+
+typedef struct mace_graph mace_graph;  /* opaque handle (host metadata) */
+
+/* Layout of the FP32 weight blob: tensor t occupies sizes[t] floats, in
+ * this order: "embed" [S][K]; then per layer t: "t.up.l" [K][K] per input l;
+ * "t.radial.0..3" ([nb][64], [64][64], [64][64], [64][P*K], path-major);
+ * "t.linear.p" [K][K] per edge-product path p; species linears "t.skip.l"
+ * [S][K][K]; symmetric-contraction weights "t.symc.L.nu" [S][n_eta][K];
+ * "t.prod.L" [K][K]; readout "t.readout" [K] (non-last layers) or
+ * "t.readout.0" [K][16], "t.readout.1" [16] (last layer).  Every matrix is
+ * row-major [in][out].  fan_in[t] is the fan-in used for N(0,1)/sqrt(fan_in)
+ * initialisation.  sizes, fan_in (host) of capacity max_tensors; names
+ * (host, may be NULL) of capacity max_tensors * name_len, each entry
+ * NUL-terminated.  Returns MACE_ENOSPACE (with *n_tensors set) when the
+ * capacity is too small. */
+mace_status mace_weight_layout(const mace_model_desc* desc, int32_t max_tensors, int64_t* sizes,
+                               int64_t* fan_in, char* names, int32_t name_len, int32_t* n_tensors,
+                               int64_t* total_floats);
+
+/* Bytes of device workspace a graph of this size needs. 0 on invalid input. */
+size_t mace_workspace_bytes(const mace_model_desc* desc, int64_t n_atoms, int64_t n_edges, int32_t n_graphs,
+                            mace_precision prec);
+
+/* Neighbour list (host, FP64 cell list) of the graph problem statement:
+ * edge j -> i with shift S is kept iff 0 < |(x_j - x_i) + S.cell|^2 < r_cut^2,
+ * every periodic image enumerated, atoms of different graphs never joined,
+ * sorted by (receiver, sender, S).  positions (host) [N][3]; cells (host)
+ * [G][3][3] rows = lattice vectors, or NULL (no periodicity);
+ * graph_of_atom (host) [N] nondecreasing or NULL.  Outputs (host) of
+ * capacity max_edges: sender [E], receiver [E], shifts [E][3].  When the
+ * capacity is too small returns MACE_ENOSPACE with *n_edges = the count. */
+mace_status mace_neighbor_list(int64_t n_atoms, const double* positions, const double* cells,
+                               const int32_t* graph_of_atom, int32_t n_graphs, double r_cut, int64_t max_edges,
+                               int32_t* sender, int32_t* receiver, int32_t* shifts, int64_t* n_edges);
+
+/* Validate and pack a graph and the weights into the workspace.
+ * weights (dev) FP32 blob in mace_weight_layout order; species (dev) [N] in
+ * 0..S-1; edge_index (dev) [2][E]: row 0 senders j, row 1 receivers i,
+ * receivers nondecreasing; unit_shifts (dev) [E][3] or NULL (no
+ * periodicity); cells (dev) [G][3][3] FP64 or NULL; graph_of_atom (dev) [N]
+ * nondecreasing or NULL (one graph); workspace (dev) of at least
+ * mace_workspace_bytes.  Synchronises the stream (setup is not on the hot
+ * path).  After it returns the caller may free weights, species,
+ * edge_index, unit_shifts, cells and graph_of_atom. */
+mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, int64_t weight_floats,
+                             int64_t n_atoms, const int32_t* species, int64_t n_edges, const int32_t* edge_index,
+                             const int32_t* unit_shifts, const double* cells, const int32_t* graph_of_atom,
+                             int32_t n_graphs, mace_precision prec, void* workspace, size_t workspace_bytes,
+                             void* stream, mace_graph** out);
+
+/* Energies: positions (dev) [N][3] FP32; node_energy (dev) [N] FP32;
+ * graph_energy (dev) [G] FP64.  No host synchronisation, no allocation. */
+mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                                void* stream);
+
+/* Energies and forces: as mace_forward_energy plus forces (dev) [N][3] FP32. */
+mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                        float* forces, void* stream);
+
+/* Releases the host handle (the workspace stays the caller's). */
+void mace_graph_destroy(mace_graph* g);
+
+const char* mace_status_string(mace_status s);
+
+/* Kernel timing (profiling aid, host): while kernel class `kernel` is
+ * selected (0 <= kernel < number of classes; -1 = none), every launch of
+ * that class made by mace_forward_energy / mace_forces is bracketed by a
+ * pair of HIP events recorded on the call's stream (at most 4096 launches
+ * between reads).  mace_profile_read waits for those events and returns the
+ * summed kernel milliseconds and the launch count since the last select or
+ * read; MACE_ENOSPACE if launches were dropped.  mace_kernel_name gives the
+ * class's kernel symbol stem ("" when out of range). */
+mace_status mace_profile_select(mace_graph* g, int32_t kernel);
+mace_status mace_profile_read(mace_graph* g, double* total_ms, int64_t* launches);
+const char* mace_kernel_name(int32_t kernel);
+
+/* Table export for checking the library's couplings (host). */
+/* real CG C^{l3}_{l1 l2}[m1][m2][m3] into out (host) [(2l1+1)(2l2+1)(2l3+1)] */
+mace_status mace_debug_real_cg(int32_t l1, int32_t l2, int32_t l3, double* out);
+/* coupling trees kept for (nu, L, parity): trees (host) [max][4] = (l1, l2, l3, l12), scales (host) [max] */
+mace_status mace_debug_trees(int32_t nu, int32_t L, int32_t parity, int32_t max_trees, int32_t* trees,
+                             double* scales, int32_t* n_trees);
+/* harmonics and radial basis of the kernels, evaluated on the host:
+ * vec (host) [n][3] edge vectors -> Y (host) [n][16], rbf (host) [n][n_bessel] */
+mace_status mace_debug_edge_features(int64_t n, const float* vec, double r_cut, int32_t envelope_p,
+                                     int32_t n_bessel, float* Y, float* rbf);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MACE_H_ */

@@ -342,7 +342,10 @@ def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = 
     Eg = graph_energies(eps, graph)
     F = None
     if forces:
-        (g,) = torch.autograd.grad(Eg.sum(), pos)
-        F = -g
+        # F = -dE/dr; with no edge at all E does not depend on r and F = 0
+        g = None
+        if Eg.requires_grad:
+            (g,) = torch.autograd.grad(Eg.sum(), pos, allow_unused=True)
+        F = -g if g is not None else torch.zeros_like(pos)
     return {"eps": eps.detach().numpy(), "energy": Eg.detach().numpy(),
             "forces": None if F is None else F.numpy(), "graph": graph}

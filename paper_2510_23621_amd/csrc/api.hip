@@ -1,0 +1,838 @@
+// Host runtime of the MACE layer library: argument checks, model and layer
+// plans, workspace carving, graph setup (CSR by receiver, sender lists,
+// species tiles, image shift vectors), the host neighbour list, and the
+// launch sequences of the energy forward pass and the force backward pass.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/mace.h"
+#include "mace_internal.h"
+#include "so3_tables.hpp"
+
+using namespace mace;
+
+namespace {
+
+struct Tensor {
+  std::string name;
+  std::vector<int64_t> shape;
+  int64_t fan_in;
+  int64_t offset;  // floats
+  int64_t size() const {
+    int64_t n = 1;
+    for (auto d : shape) n *= d;
+    return n;
+  }
+};
+
+struct LayerPlan {
+  int t = 0;
+  bool last = false;
+  std::vector<int> in_ls, out_ls;
+  std::vector<so3h::Path> paths;
+  int P = 0, mid = 0, din = 0, dout = 0, lh_max = 0, lout_max = 0;
+  std::vector<int> path_off;
+};
+
+struct Model {
+  mace_model_desc d{};
+  int dh = 0;  // hidden components
+  std::vector<LayerPlan> layers;
+  std::vector<Tensor> tensors;
+  std::map<std::string, int64_t> off;
+  int64_t total = 0;
+  int max_P = 0, max_mid = 0, max_din = 0, max_dout = 0;
+};
+
+int n_eta(int nu, int L) {
+  static std::map<std::pair<int, int>, int> cache;
+  auto key = std::make_pair(nu, L);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int n = (int)so3h::select_trees(nu, L, (L % 2) ? -1 : 1).size();
+  cache[key] = n;
+  return n;
+}
+
+mace_status build_model(const mace_model_desc* desc, Model& m) {
+  if (!desc) return MACE_EINVAL;
+  const mace_model_desc& d = *desc;
+  if (d.n_species < 1 || d.n_layers < 1 || !(d.r_cut > 0) || !(d.c_norm > 0) || d.envelope_p < 1)
+    return MACE_EINVAL;
+  if (d.sh_lmax != 3 || d.correlation != 3 || d.n_bessel < 1 || d.n_bessel > 16 || d.radial_hidden[0] != 64 ||
+      d.radial_hidden[1] != 64 || d.radial_hidden[2] != 64 || d.readout_hidden < 1 || d.readout_hidden > 16 ||
+      d.hidden_lmax < 0 || d.hidden_lmax > 2 || !(d.K == 32 || d.K == 64 || d.K == 96 || d.K == 128))
+    return MACE_EUNSUPPORTED;
+  m.d = d;
+  m.dh = (d.hidden_lmax + 1) * (d.hidden_lmax + 1);
+  const int64_t S = d.n_species, K = d.K;
+  int64_t o = 0;
+  auto add = [&](const std::string& name, std::vector<int64_t> shape, int64_t fan) {
+    Tensor t{name, shape, fan, o};
+    o += t.size();
+    m.off[name] = t.offset;
+    m.tensors.push_back(t);
+  };
+  add("embed", {S, K}, S);
+  for (int t = 0; t < d.n_layers; ++t) {
+    LayerPlan L;
+    L.t = t;
+    L.last = (t == d.n_layers - 1);
+    if (t == 0) L.in_ls = {0};
+    else for (int l = 0; l <= d.hidden_lmax; ++l) L.in_ls.push_back(l);
+    if (L.last) L.out_ls = {0};
+    else for (int l = 0; l <= d.hidden_lmax; ++l) L.out_ls.push_back(l);
+    L.lh_max = L.in_ls.back();
+    L.lout_max = L.out_ls.back();
+    L.paths = so3h::tp_paths(L.lh_max, d.sh_lmax);
+    L.P = (int)L.paths.size();
+    for (auto& p : L.paths) {
+      L.path_off.push_back(L.mid);
+      L.mid += 2 * p.lo + 1;
+    }
+    L.din = (L.lh_max + 1) * (L.lh_max + 1);
+    L.dout = (L.lout_max + 1) * (L.lout_max + 1);
+    std::string pre = std::to_string(t) + ".";
+    for (int l : L.in_ls) add(pre + "up." + std::to_string(l), {K, K}, K);
+    const int64_t h[4] = {d.n_bessel, 64, 64, 64};
+    for (int i = 0; i < 3; ++i) add(pre + "radial." + std::to_string(i), {h[i], h[i + 1]}, h[i]);
+    add(pre + "radial.3", {64, (int64_t)L.P * K}, 64);
+    for (int p = 0; p < L.P; ++p) {
+      int nin = 0;
+      for (auto& q : L.paths) nin += (q.lo == L.paths[p].lo);
+      add(pre + "linear." + std::to_string(p), {K, K}, nin * K);
+    }
+    if (t == 0) {
+      for (int l = 0; l <= d.sh_lmax; ++l) add(pre + "skip." + std::to_string(l), {S, K, K}, K);
+    } else {
+      for (int Lo : L.out_ls)
+        if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end())
+          add(pre + "skip." + std::to_string(Lo), {S, K, K}, K);
+    }
+    for (int Lo : L.out_ls)
+      for (int nu = 1; nu <= d.correlation; ++nu) {
+        int ne = n_eta(nu, Lo);
+        if (ne) add(pre + "symc." + std::to_string(Lo) + "." + std::to_string(nu), {S, ne, K}, ne);
+      }
+    for (int Lo : L.out_ls) add(pre + "prod." + std::to_string(Lo), {K, K}, K);
+    if (!L.last) {
+      add(pre + "readout", {K}, K);
+    } else {
+      add(pre + "readout.0", {K, d.readout_hidden}, K);
+      add(pre + "readout.1", {d.readout_hidden}, d.readout_hidden);
+    }
+    m.max_P = std::max(m.max_P, L.P);
+    m.max_mid = std::max(m.max_mid, L.mid);
+    m.max_din = std::max(m.max_din, L.din);
+    m.max_dout = std::max(m.max_dout, L.dout);
+    m.layers.push_back(L);
+  }
+  m.total = o;
+  return MACE_OK;
+}
+
+// ------------------------------------------------------------ workspace
+struct Carver {
+  char* base;
+  size_t used = 0;
+  template <class T>
+  T* take(size_t count) {
+    used = (used + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + used) : nullptr;
+    used += count * sizeof(T);
+    return p;
+  }
+};
+
+struct Buffers {
+  float *w = nullptr, *wT = nullptr, *sp_table = nullptr;
+  int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
+      *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
+      *tile_count = nullptr, *tile_species = nullptr;
+  double4* shift = nullptr;
+  float *Y = nullptr, *rbf = nullptr;
+  std::vector<float*> R, A, hin, ht;
+  float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
+  // backward
+  float *dh0 = nullptr, *dh1 = nullptr, *dB = nullptr, *dA = nullptr, *dApre = nullptr, *dAt = nullptr,
+        *dY = nullptr, *de = nullptr, *Q = nullptr, *dht = nullptr;
+  float4* g = nullptr;
+};
+
+int64_t n_tiles_bound(int64_t N, int S) { return (N + kLinTileNodes - 1) / kLinTileNodes + S; }
+
+void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
+  const int64_t K = m.d.K, S = m.d.n_species, T = m.d.n_layers;
+  const int nb = m.d.n_bessel;
+  b.w = c.take<float>(m.total);
+  b.wT = c.take<float>(m.total);
+  b.sp_table = c.take<float>(S * K);
+  b.species = c.take<int>(N);
+  b.snd = c.take<int>(std::max<int64_t>(E, 1));
+  b.rcv = c.take<int>(std::max<int64_t>(E, 1));
+  b.rcv_off = c.take<int>(N + 1);
+  b.snd_off = c.take<int>(N + 1);
+  b.snd_perm = c.take<int>(std::max<int64_t>(E, 1));
+  b.graph_off = c.take<int>(G + 1);
+  b.node_order = c.take<int>(N);
+  int64_t nt = n_tiles_bound(N, (int)S);
+  b.tile_start = c.take<int>(nt);
+  b.tile_count = c.take<int>(nt);
+  b.tile_species = c.take<int>(nt);
+  b.shift = c.take<double4>(std::max<int64_t>(E, 1));
+  b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
+  b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
+  b.R.resize(T);
+  b.A.resize(T);
+  b.hin.assign(T, nullptr);
+  b.ht.assign(T, nullptr);
+  for (int t = 0; t < T; ++t) {
+    const LayerPlan& L = m.layers[t];
+    b.R[t] = c.take<float>(std::max<int64_t>(E, 1) * L.P * K);
+    b.A[t] = c.take<float>(N * 16 * K);
+    if (t > 0) {
+      b.hin[t] = c.take<float>(N * L.din * K);
+      b.ht[t] = c.take<float>(N * L.din * K);
+    }
+  }
+  b.hlast = c.take<float>(N * K);
+  b.sc = c.take<float>(N * m.max_dout * K);
+  b.At = c.take<float>(N * m.max_mid * K);
+  b.Apre = c.take<float>(N * 16 * K);
+  b.B = c.take<float>(N * m.max_dout * K);
+  const int64_t dmax = std::max<int64_t>(m.dh, 1);
+  b.dh0 = c.take<float>(N * dmax * K);
+  b.dh1 = c.take<float>(N * dmax * K);
+  b.dB = c.take<float>(N * m.max_dout * K);
+  b.dA = c.take<float>(N * 16 * K);
+  b.dApre = c.take<float>(N * 16 * K);
+  b.dAt = c.take<float>(N * m.max_mid * K);
+  b.dY = c.take<float>(std::max<int64_t>(E, 1) * 16);
+  b.de = c.take<float>(std::max<int64_t>(E, 1) * nb);
+  b.Q = c.take<float>(std::max<int64_t>(E, 1) * m.max_din * K);
+  b.dht = c.take<float>(N * m.max_din * K);
+  b.g = c.take<float4>(std::max<int64_t>(E, 1));
+}
+
+}  // namespace
+
+enum KernelId {
+  KID_EDGE_FEATURES = 0, KID_RADIAL_FWD, KID_TP_FWD, KID_LINEAR, KID_SYMCON_FWD, KID_READOUT,
+  KID_TP_BWD, KID_RADIAL_BWD, KID_SYMCON_BWD, KID_SENDER_SUM, KID_EDGE_BWD, KID_FORCES, KID_GRAPH_ENERGY,
+  KID_FILL, KID_COUNT
+};
+const char* kKernelNames[KID_COUNT] = {
+  "edge_features_kernel", "radial_fwd_kernel", "tp_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
+  "readout_kernel", "tp_bwd_kernel", "radial_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
+  "edge_backward_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel"};
+constexpr int kProfPairs = 4096;
+
+struct mace_graph {
+  // profiling: events around every launch of one kernel class
+  int prof_kernel = -1;
+  std::vector<hipEvent_t> prof_ev;   // 2 * kProfPairs
+  int prof_used = 0;
+  int64_t prof_dropped = 0;
+  Model m;
+  Buffers b;
+  int64_t N = 0, E = 0;
+  int G = 1;
+  int n_tiles = 0;
+  mace_precision prec = MACE_FP32;
+  // linear plans per layer
+  std::vector<LinPlan> up, upT, lin, linT, skip_sc, skip_scT, prod, prodT;
+  LinPlan skip0, skip0T;
+};
+
+namespace {
+
+struct ProfScope {
+  mace_graph* h;
+  hipStream_t s;
+  bool on;
+  int slot;
+  ProfScope(mace_graph* h_, int kid, hipStream_t s_) : h(h_), s(s_), on(false), slot(0) {
+    if (h->prof_kernel != kid) return;
+    if (h->prof_used >= kProfPairs) {
+      h->prof_dropped++;
+      return;
+    }
+    slot = h->prof_used++;
+    on = true;
+    hipEventRecord(h->prof_ev[2 * slot], s);
+  }
+  ~ProfScope() {
+    if (on) hipEventRecord(h->prof_ev[2 * slot + 1], s);
+  }
+};
+#define PROF(kid) ProfScope _prof_##__LINE__(h, kid, s)
+
+mace_status hip_ok(hipError_t e) { return e == hipSuccess ? MACE_OK : MACE_EHIP; }
+
+LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, const Model& m, int cin, int cout,
+                          bool species) {
+  LinPlan p;
+  p.cin = cin;
+  p.cout = cout;
+  p.species = species;
+  p.w_sstride = (int64_t)m.d.K * m.d.K;
+  for (int l : ls) {
+    LinGroup g{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1};
+    p.t[p.n_terms++] = LinTerm{l * l, m.off.at(pre + std::to_string(l))};
+    p.g[p.n_groups++] = g;
+  }
+  return p;
+}
+
+void make_plans(mace_graph* h) {
+  const Model& m = h->m;
+  const int T = m.d.n_layers;
+  h->up.resize(T); h->upT.resize(T); h->lin.resize(T); h->linT.resize(T);
+  h->skip_sc.resize(T); h->skip_scT.resize(T); h->prod.resize(T); h->prodT.resize(T);
+  for (int t = 0; t < T; ++t) {
+    const LayerPlan& L = m.layers[t];
+    const std::string pre = std::to_string(t) + ".";
+    h->up[t] = plan_single_per_l(L.in_ls, pre + "up.", m, L.din, L.din, false);
+    h->upT[t] = h->up[t];
+    // path-merging linear: output l collects every path with l_out = l
+    LinPlan lp;
+    lp.cin = L.mid;
+    lp.cout = 16;
+    for (int l = 0; l <= 3; ++l) {
+      LinGroup g{l * l, 2 * l + 1, lp.n_terms, lp.n_terms};
+      for (int p = 0; p < L.P; ++p)
+        if (L.paths[p].lo == l) lp.t[lp.n_terms++] = LinTerm{L.path_off[p], m.off.at(pre + "linear." + std::to_string(p))};
+      g.t1 = lp.n_terms;
+      lp.g[lp.n_groups++] = g;
+    }
+    h->lin[t] = lp;
+    LinPlan lt;
+    lt.cin = 16;
+    lt.cout = L.mid;
+    for (int p = 0; p < L.P; ++p) {
+      int lo = L.paths[p].lo;
+      lt.g[lt.n_groups++] = LinGroup{L.path_off[p], 2 * lo + 1, lt.n_terms, lt.n_terms + 1};
+      lt.t[lt.n_terms++] = LinTerm{lo * lo, m.off.at(pre + "linear." + std::to_string(p))};
+    }
+    h->linT[t] = lt;
+    if (t > 0) {
+      std::vector<int> both;
+      for (int Lo : L.out_ls)
+        if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end()) both.push_back(Lo);
+      h->skip_sc[t] = plan_single_per_l(both, pre + "skip.", m, L.din, L.dout, true);
+      h->skip_scT[t] = plan_single_per_l(both, pre + "skip.", m, L.dout, L.din, true);
+    }
+    h->prod[t] = plan_single_per_l(L.out_ls, pre + "prod.", m, L.dout, L.dout, false);
+    h->prodT[t] = h->prod[t];
+  }
+  h->skip0 = plan_single_per_l({0, 1, 2, 3}, "0.skip.", m, 16, 16, true);
+  h->skip0T = h->skip0;
+}
+
+LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bool transposed, int accumulate) {
+  LinArgs a;
+  a.x = x;
+  a.y = y;
+  a.residual = residual;
+  a.w = transposed ? h->b.wT : h->b.w;
+  a.tile_start = h->b.tile_start;
+  a.tile_count = h->b.tile_count;
+  a.tile_species = h->b.tile_species;
+  a.node_order = h->b.node_order;
+  a.n_tiles = h->n_tiles;
+  a.K = h->m.d.K;
+  a.accumulate = accumulate;
+  a.bf16 = h->prec == MACE_BF16_LINEAR;
+  return a;
+}
+
+SymW symw(mace_graph* h, int t) {
+  SymW w;
+  std::memset(&w, 0, sizeof(w));
+  const LayerPlan& L = h->m.layers[t];
+  for (int Lo : L.out_ls)
+    for (int nu = 1; nu <= 3; ++nu) {
+      auto it = h->m.off.find(std::to_string(t) + ".symc." + std::to_string(Lo) + "." + std::to_string(nu));
+      if (it != h->m.off.end()) w.w[Lo][nu] = h->b.w + it->second;
+    }
+  return w;
+}
+
+// Forward pass; keeps every intermediate the backward pass reads.
+void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
+  const Model& m = h->m;
+  Buffers& b = h->b;
+  const int N = (int)h->N, E = (int)h->E, K = m.d.K;
+  const bool bf16 = h->prec == MACE_BF16_LINEAR;
+  {
+    PROF(KID_EDGE_FEATURES);
+    launch_edge_features(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf);
+  }
+  const float inv_c = (float)(1.0 / m.d.c_norm);
+  for (int t = 0; t < m.d.n_layers; ++t) {
+    const LayerPlan& L = m.layers[t];
+    const std::string pre = std::to_string(t) + ".";
+    const float* src;
+    const int* src_map;
+    if (t == 0) {
+      src = b.sp_table;
+      src_map = b.species;
+    } else {
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->up[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0));
+      }
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->skip_sc[t], largs(h, b.hin[t], b.sc, nullptr, false, 0));
+      }
+      src = b.ht[t];
+      src_map = nullptr;
+    }
+    {
+      PROF(KID_RADIAL_FWD);
+      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t]);
+    }
+    {
+      PROF(KID_TP_FWD);
+      launch_tp_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.R[t], b.Y, src, 0, inv_c, b.At);
+    }
+    if (t == 0) {
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
+      }
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->skip0, largs(h, b.Apre, b.A[t], nullptr, false, 0));
+      }
+    } else {
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->lin[t], largs(h, b.At, b.A[t], nullptr, false, 0));
+      }
+    }
+    {
+      PROF(KID_SYMCON_FWD);
+      launch_symcon_fwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.B);
+    }
+    float* hout = L.last ? b.hlast : b.hin[t + 1];
+    {
+      PROF(KID_LINEAR);
+      launch_linear(s, h->prod[t], largs(h, b.B, hout, t > 0 ? b.sc : nullptr, false, 0));
+    }
+    if (!L.last)
+      {
+        PROF(KID_READOUT);
+        launch_readout_fwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, bf16,
+                           t > 0, eps);
+      }
+    else
+      {
+        PROF(KID_READOUT);
+        launch_readout_fwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, bf16, t > 0, eps);
+      }
+  }
+}
+
+void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
+  const Model& m = h->m;
+  Buffers& b = h->b;
+  const int N = (int)h->N, E = (int)h->E, K = m.d.K, T = m.d.n_layers;
+  const bool bf16 = h->prec == MACE_BF16_LINEAR;
+  const float inv_c = (float)(1.0 / m.d.c_norm);
+  float* dnext = b.dh0;
+  float* dprev = b.dh1;
+  for (int t = T - 1; t >= 0; --t) {
+    const LayerPlan& L = m.layers[t];
+    const std::string pre = std::to_string(t) + ".";
+    float* hout = L.last ? b.hlast : b.hin[t + 1];
+    if (L.last) {
+      {
+        PROF(KID_FILL);
+        launch_fill(s, dnext, (size_t)N * L.dout * K, 0.f);
+      }
+      {
+        PROF(KID_READOUT);
+        launch_readout_bwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, bf16, dnext);
+      }
+    } else {
+      {
+        PROF(KID_READOUT);
+        launch_readout_bwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, bf16,
+                           dnext);
+      }
+    }
+    {
+      PROF(KID_LINEAR);
+      launch_linear(s, h->prodT[t], largs(h, dnext, b.dB, nullptr, true, 0));
+    }
+    {
+      PROF(KID_SYMCON_BWD);
+      launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
+    }
+    const float* dApre = b.dA;
+    if (t == 0) {
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
+      }
+      dApre = b.dApre;
+    }
+    {
+      PROF(KID_LINEAR);
+      launch_linear(s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
+    }
+    const float* src = t == 0 ? b.sp_table : b.ht[t];
+    const int* src_map = t == 0 ? b.species : nullptr;
+    {
+      PROF(KID_TP_BWD);
+      launch_tp_bwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.R[t], b.Y, src, inv_c, b.dAt, b.dY, t < T - 1,
+                    t > 0 ? b.Q : nullptr);
+    }
+    {
+      PROF(KID_RADIAL_BWD);
+      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t], b.de, t < T - 1);
+    }
+    if (t > 0) {
+      {
+        PROF(KID_SENDER_SUM);
+        launch_sender_sum(s, N, L.din, K, b.snd_off, b.snd_perm, b.Q, b.dht);
+      }
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->upT[t], largs(h, b.dht, dprev, nullptr, true, 0));
+      }
+      {
+        PROF(KID_LINEAR);
+        launch_linear(s, h->skip_scT[t], largs(h, dnext, dprev, nullptr, true, 1));
+      }
+      std::swap(dnext, dprev);
+    }
+  }
+  {
+    PROF(KID_EDGE_BWD);
+    launch_edge_backward(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.dY,
+                         b.de, b.g);
+  }
+  {
+    PROF(KID_FORCES);
+    launch_forces(s, N, b.rcv_off, b.snd_off, b.snd_perm, b.g, F);
+  }
+}
+
+}  // namespace
+
+// ================================================================== C ABI
+extern "C" {
+
+const char* mace_status_string(mace_status s) {
+  switch (s) {
+    case MACE_OK: return "ok";
+    case MACE_EINVAL: return "invalid argument";
+    case MACE_ERANGE: return "index out of range or edges not sorted by receiver";
+    case MACE_ENOSPACE: return "workspace or output capacity too small";
+    case MACE_EHIP: return "HIP runtime error";
+    case MACE_ENONFINITE: return "non-finite input";
+    case MACE_ESTATE: return "invalid handle state";
+    case MACE_EUNSUPPORTED: return "model shape not supported by the kernels";
+  }
+  return "unknown status";
+}
+
+mace_status mace_weight_layout(const mace_model_desc* desc, int32_t max_tensors, int64_t* sizes, int64_t* fan_in,
+                               char* names, int32_t name_len, int32_t* n_tensors, int64_t* total_floats) {
+  Model m;
+  mace_status st = build_model(desc, m);
+  if (st != MACE_OK) return st;
+  if (n_tensors) *n_tensors = (int32_t)m.tensors.size();
+  if (total_floats) *total_floats = m.total;
+  if ((int)m.tensors.size() > max_tensors) return MACE_ENOSPACE;
+  for (size_t i = 0; i < m.tensors.size(); ++i) {
+    if (sizes) sizes[i] = m.tensors[i].size();
+    if (fan_in) fan_in[i] = m.tensors[i].fan_in;
+    if (names && name_len > 0) {
+      char* dst = names + (size_t)i * name_len;
+      size_t n = std::min<size_t>(m.tensors[i].name.size(), (size_t)name_len - 1);
+      std::memcpy(dst, m.tensors[i].name.data(), n);
+      dst[n] = 0;
+    }
+  }
+  return MACE_OK;
+}
+
+size_t mace_workspace_bytes(const mace_model_desc* desc, int64_t n_atoms, int64_t n_edges, int32_t n_graphs,
+                            mace_precision prec) {
+  (void)prec;
+  Model m;
+  if (build_model(desc, m) != MACE_OK || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return 0;
+  Carver c{nullptr};
+  Buffers b;
+  carve(m, n_atoms, n_edges, n_graphs, c, b);
+  return c.used + 256;
+}
+
+mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, int64_t weight_floats,
+                             int64_t n_atoms, const int32_t* species, int64_t n_edges, const int32_t* edge_index,
+                             const int32_t* unit_shifts, const double* cells, const int32_t* graph_of_atom,
+                             int32_t n_graphs, mace_precision prec, void* workspace, size_t workspace_bytes,
+                             void* stream, mace_graph** out) {
+  if (!out) return MACE_EINVAL;
+  *out = nullptr;
+  Model m;
+  mace_status st = build_model(desc, m);
+  if (st != MACE_OK) return st;
+  if (!weights || !species || !workspace || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return MACE_EINVAL;
+  if (n_edges > 0 && !edge_index) return MACE_EINVAL;
+  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR) return MACE_EINVAL;
+  if (weight_floats != m.total) return MACE_EINVAL;
+  if (n_atoms > (1LL << 30) || n_edges > (1LL << 31) - 1) return MACE_EUNSUPPORTED;
+  if (!graph_of_atom && n_graphs != 1) return MACE_EINVAL;
+  if (unit_shifts && !cells) return MACE_EINVAL;
+  if (mace_workspace_bytes(desc, n_atoms, n_edges, n_graphs, prec) > workspace_bytes) return MACE_ENOSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t N = n_atoms, E = n_edges, K = m.d.K, S = m.d.n_species;
+  const int G = n_graphs;
+
+  // --- host copies of the graph description
+  std::vector<int32_t> hs(N), he(2 * E), hsh(unit_shifts ? 3 * E : 0), hg(N, 0);
+  std::vector<double> hc(cells ? 9 * G : 0);
+  std::vector<float> hw(m.total);
+  auto cp = [&](void* dst, const void* src, size_t bytes) {
+    return bytes ? hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s) : hipSuccess;
+  };
+  if (cp(hs.data(), species, N * 4) != hipSuccess || cp(he.data(), edge_index, 2 * E * 4) != hipSuccess ||
+      (unit_shifts && cp(hsh.data(), unit_shifts, 3 * E * 4) != hipSuccess) ||
+      (cells && cp(hc.data(), cells, 9 * G * 8) != hipSuccess) ||
+      (graph_of_atom && cp(hg.data(), graph_of_atom, N * 4) != hipSuccess) ||
+      cp(hw.data(), weights, m.total * 4) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return MACE_EHIP;
+
+  // --- validation
+  for (int64_t i = 0; i < N; ++i) {
+    if (hs[i] < 0 || hs[i] >= S) return MACE_ERANGE;
+    if (hg[i] < 0 || hg[i] >= G || (i > 0 && hg[i] < hg[i - 1])) return MACE_ERANGE;
+  }
+  const int32_t* hsnd = he.data();
+  const int32_t* hrcv = he.data() + E;
+  for (int64_t e = 0; e < E; ++e) {
+    if (hsnd[e] < 0 || hsnd[e] >= N || hrcv[e] < 0 || hrcv[e] >= N) return MACE_ERANGE;
+    if (e > 0 && hrcv[e] < hrcv[e - 1]) return MACE_ERANGE;
+    if (hg[hsnd[e]] != hg[hrcv[e]]) return MACE_ERANGE;
+    bool zero_shift = !unit_shifts || (hsh[3 * e] == 0 && hsh[3 * e + 1] == 0 && hsh[3 * e + 2] == 0);
+    if (hsnd[e] == hrcv[e] && zero_shift) return MACE_ERANGE;
+  }
+  for (float v : hw)
+    if (!std::isfinite(v)) return MACE_ENONFINITE;
+
+  // --- derived topology
+  std::vector<int32_t> rcv_off(N + 1, 0), snd_off(N + 1, 0), snd_perm(E), goff(G + 1, 0);
+  for (int64_t e = 0; e < E; ++e) {
+    rcv_off[hrcv[e] + 1]++;
+    snd_off[hsnd[e] + 1]++;
+  }
+  for (int64_t i = 0; i < N; ++i) {
+    rcv_off[i + 1] += rcv_off[i];
+    snd_off[i + 1] += snd_off[i];
+  }
+  {
+    std::vector<int32_t> fillp(snd_off.begin(), snd_off.end() - 1);
+    for (int64_t e = 0; e < E; ++e) snd_perm[fillp[hsnd[e]]++] = (int32_t)e;  // increasing e per sender
+  }
+  for (int64_t i = 0; i < N; ++i) goff[hg[i] + 1]++;
+  for (int gi = 0; gi < G; ++gi) goff[gi + 1] += goff[gi];
+  std::vector<double4> shv(std::max<int64_t>(E, 1), make_double4(0, 0, 0, 0));
+  if (unit_shifts) {
+    for (int64_t e = 0; e < E; ++e) {
+      const double* c = hc.data() + 9 * hg[hrcv[e]];
+      double S0 = hsh[3 * e], S1 = hsh[3 * e + 1], S2 = hsh[3 * e + 2];
+      double v[3];
+      for (int a = 0; a < 3; ++a) v[a] = ((S0 * c[a]) + (S1 * c[3 + a])) + (S2 * c[6 + a]);
+      shv[e] = make_double4(v[0], v[1], v[2], 0.0);
+    }
+  }
+  // nodes grouped by species, tiles of <= kLinTileNodes nodes of one species
+  std::vector<int32_t> order, tstart, tcount, tspec;
+  for (int z = 0; z < S; ++z) {
+    int64_t first = (int64_t)order.size();
+    for (int64_t i = 0; i < N; ++i)
+      if (hs[i] == z) order.push_back((int32_t)i);
+    for (int64_t q = first; q < (int64_t)order.size(); q += kLinTileNodes) {
+      tstart.push_back((int32_t)q);
+      tcount.push_back((int32_t)std::min<int64_t>(kLinTileNodes, (int64_t)order.size() - q));
+      tspec.push_back(z);
+    }
+  }
+  // transposed copy of every K x K block (used by the backward linears)
+  std::vector<float> hwT(hw);
+  for (auto& t : m.tensors) {
+    const auto& sh = t.shape;
+    if (sh.size() >= 2 && sh[sh.size() - 1] == K && sh[sh.size() - 2] == K) {
+      int64_t blocks = t.size() / (K * K);
+      for (int64_t q = 0; q < blocks; ++q) {
+        const float* src = hw.data() + t.offset + q * K * K;
+        float* dst = hwT.data() + t.offset + q * K * K;
+        for (int64_t r = 0; r < K; ++r)
+          for (int64_t c2 = 0; c2 < K; ++c2) dst[c2 * K + r] = src[r * K + c2];
+      }
+    }
+  }
+
+  auto* h = new mace_graph();
+  h->m = m;
+  h->N = N;
+  h->E = E;
+  h->G = G;
+  h->prec = prec;
+  h->n_tiles = (int)tstart.size();
+  Carver c{reinterpret_cast<char*>(workspace)};
+  carve(h->m, N, E, G, c, h->b);
+  Buffers& b = h->b;
+  auto up = [&](void* dst, const void* src, size_t bytes) {
+    return bytes ? hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s) : hipSuccess;
+  };
+  hipError_t err = hipSuccess;
+  auto chk = [&](hipError_t e) { if (e != hipSuccess && err == hipSuccess) err = e; };
+  chk(up(b.w, hw.data(), m.total * 4));
+  chk(up(b.wT, hwT.data(), m.total * 4));
+  chk(up(b.species, hs.data(), N * 4));
+  chk(up(b.snd, hsnd, E * 4));
+  chk(up(b.rcv, hrcv, E * 4));
+  chk(up(b.rcv_off, rcv_off.data(), (N + 1) * 4));
+  chk(up(b.snd_off, snd_off.data(), (N + 1) * 4));
+  chk(up(b.snd_perm, snd_perm.data(), E * 4));
+  chk(up(b.graph_off, goff.data(), (G + 1) * 4));
+  chk(up(b.node_order, order.data(), N * 4));
+  chk(up(b.tile_start, tstart.data(), tstart.size() * 4));
+  chk(up(b.tile_count, tcount.data(), tcount.size() * 4));
+  chk(up(b.tile_species, tspec.data(), tspec.size() * 4));
+  chk(up(b.shift, shv.data(), E * sizeof(double4)));
+  launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
+                       prec == MACE_BF16_LINEAR, b.sp_table);
+  chk(hipGetLastError());
+  chk(hipStreamSynchronize(s));  // host vectors go out of scope below
+  if (err != hipSuccess) {
+    delete h;
+    return MACE_EHIP;
+  }
+  make_plans(h);
+  *out = h;
+  return MACE_OK;
+}
+
+mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                                void* stream) {
+  if (!g || !positions || !node_energy || !graph_energy) return MACE_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  run_forward(g, s, positions, node_energy);
+  {
+    mace_graph* h = g;
+    PROF(KID_GRAPH_ENERGY);
+    launch_graph_energy(s, g->G, g->b.graph_off, node_energy, graph_energy);
+  }
+  return hip_ok(hipGetLastError());
+}
+
+mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                        float* forces, void* stream) {
+  if (!g || !positions || !node_energy || !graph_energy || !forces) return MACE_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  run_forward(g, s, positions, node_energy);
+  {
+    mace_graph* h = g;
+    PROF(KID_GRAPH_ENERGY);
+    launch_graph_energy(s, g->G, g->b.graph_off, node_energy, graph_energy);
+  }
+  run_backward(g, s, positions, forces);
+  return hip_ok(hipGetLastError());
+}
+
+void mace_graph_destroy(mace_graph* g) {
+  if (!g) return;
+  for (auto e : g->prof_ev) hipEventDestroy(e);
+  delete g;
+}
+
+mace_status mace_profile_select(mace_graph* g, int32_t kernel) {
+  if (!g || kernel < -1 || kernel >= KID_COUNT) return MACE_EINVAL;
+  if (kernel >= 0 && g->prof_ev.empty()) {
+    g->prof_ev.resize(2 * kProfPairs);
+    for (auto& e : g->prof_ev)
+      if (hipEventCreate(&e) != hipSuccess) return MACE_EHIP;
+  }
+  g->prof_kernel = kernel;
+  g->prof_used = 0;
+  g->prof_dropped = 0;
+  return MACE_OK;
+}
+
+mace_status mace_profile_read(mace_graph* g, double* total_ms, int64_t* launches) {
+  if (!g || !total_ms || !launches) return MACE_EINVAL;
+  double tot = 0.0;
+  for (int i = 0; i < g->prof_used; ++i) {
+    if (hipEventSynchronize(g->prof_ev[2 * i + 1]) != hipSuccess) return MACE_EHIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g->prof_ev[2 * i], g->prof_ev[2 * i + 1]) != hipSuccess) return MACE_EHIP;
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = g->prof_used;
+  g->prof_used = 0;
+  return g->prof_dropped ? MACE_ENOSPACE : MACE_OK;
+}
+
+const char* mace_kernel_name(int32_t kernel) {
+  return (kernel >= 0 && kernel < KID_COUNT) ? kKernelNames[kernel] : "";
+}
+
+mace_status mace_debug_real_cg(int32_t l1, int32_t l2, int32_t l3, double* out) {
+  if (!out || l1 < 0 || l2 < 0 || l3 < std::abs(l1 - l2) || l3 > l1 + l2 || l1 > 8 || l2 > 8) return MACE_EINVAL;
+  auto C = so3h::real_cg(l1, l2, l3);
+  std::copy(C.v.begin(), C.v.end(), out);
+  return MACE_OK;
+}
+
+mace_status mace_debug_trees(int32_t nu, int32_t L, int32_t parity, int32_t max_trees, int32_t* trees,
+                             double* scales, int32_t* n_trees) {
+  if (nu < 1 || nu > 3 || L < 0 || L > 6 || (parity != 1 && parity != -1) || !n_trees) return MACE_EINVAL;
+  auto sel = so3h::select_trees(nu, L, parity);
+  *n_trees = (int32_t)sel.size();
+  if ((int)sel.size() > max_trees) return MACE_ENOSPACE;
+  for (size_t i = 0; i < sel.size(); ++i) {
+    if (trees) {
+      trees[4 * i + 0] = sel[i].l1;
+      trees[4 * i + 1] = sel[i].l2;
+      trees[4 * i + 2] = sel[i].l3;
+      trees[4 * i + 3] = sel[i].l12;
+    }
+    if (scales) scales[i] = sel[i].scale;
+  }
+  return MACE_OK;
+}
+
+mace_status mace_debug_edge_features(int64_t n, const float* vec, double r_cut, int32_t envelope_p, int32_t n_bessel,
+                                     float* Y, float* rbf) {
+  if (n < 0 || !vec || !Y || !rbf || n_bessel < 1 || n_bessel > 16 || !(r_cut > 0)) return MACE_EINVAL;
+  for (int64_t e = 0; e < n; ++e) {
+    double dx = vec[3 * e], dy = vec[3 * e + 1], dz = vec[3 * e + 2];
+    double rr = sqrt(dx * dx + dy * dy + dz * dz);
+    double inv = 1.0 / rr;
+    double y[16], eb[16];
+    sh16<double>(dx * inv, dy * inv, dz * inv, y);
+    bessel_env<double>(rr, r_cut, envelope_p, n_bessel, eb);
+    for (int q = 0; q < 16; ++q) Y[16 * e + q] = (float)y[q];
+    for (int q = 0; q < n_bessel; ++q) rbf[e * n_bessel + q] = (float)eb[q];
+  }
+  return MACE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,226 @@
+// Internal declarations shared by the kernel files and the host runtime of
+// the MACE layer library (gfx950). Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mace {
+
+constexpr int kMaxTerms = 48;
+constexpr int kMaxGroups = 24;
+constexpr int kLinTileNodes = 16;   // nodes per block of the channel-mixing linear
+
+// ----------------------------------------------------------------- numerics
+__host__ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+__host__ __device__ __forceinline__ float silu_grad(float x) {
+  float s = 1.0f / (1.0f + expf(-x));
+  return s * (1.0f + x * (1.0f - s));
+}
+
+// Round-to-nearest-even float -> bfloat16 -> float (inputs of BF16 linears).
+__host__ __device__ __forceinline__ float bf16_round(float x) {
+  uint32_t u;
+  __builtin_memcpy(&u, &x, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) {           // inf / nan: truncate, keep nan quiet
+    u &= 0xffff0000u;
+    if ((u & 0x007f0000u) == 0 && (x != x)) u |= 0x00400000u;
+  } else {
+    u += 0x7fffu + ((u >> 16) & 1u);
+    u &= 0xffff0000u;
+  }
+  float r;
+  __builtin_memcpy(&r, &u, 4);
+  return r;
+}
+
+// Forward-mode dual number carrying d/d(vx, vy, vz) of an edge vector.
+template <class S>
+struct Dual3 {
+  S v, x, y, z;
+  __host__ __device__ Dual3() : v(0), x(0), y(0), z(0) {}
+  __host__ __device__ Dual3(S a) : v(a), x(0), y(0), z(0) {}
+  __host__ __device__ Dual3(S a, S b, S c, S d) : v(a), x(b), y(c), z(d) {}
+};
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator+(Dual3<S> a, Dual3<S> b) {
+  return Dual3<S>(a.v + b.v, a.x + b.x, a.y + b.y, a.z + b.z);
+}
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator-(Dual3<S> a, Dual3<S> b) {
+  return Dual3<S>(a.v - b.v, a.x - b.x, a.y - b.y, a.z - b.z);
+}
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator*(Dual3<S> a, Dual3<S> b) {
+  return Dual3<S>(a.v * b.v, a.x * b.v + a.v * b.x, a.y * b.v + a.v * b.y, a.z * b.v + a.v * b.z);
+}
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator*(S s, Dual3<S> a) {
+  return Dual3<S>(s * a.v, s * a.x, s * a.y, s * a.z);
+}
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator*(Dual3<S> a, S s) { return s * a; }
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator+(Dual3<S> a, S s) { return Dual3<S>(a.v + s, a.x, a.y, a.z); }
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator-(Dual3<S> a, S s) { return Dual3<S>(a.v - s, a.x, a.y, a.z); }
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator-(S s, Dual3<S> a) { return Dual3<S>(s - a.v, -a.x, -a.y, -a.z); }
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> operator/(Dual3<S> a, Dual3<S> b) {
+  S ib = S(1) / b.v;
+  S q = a.v * ib;
+  return Dual3<S>(q, (a.x - q * b.x) * ib, (a.y - q * b.y) * ib, (a.z - q * b.z) * ib);
+}
+template <class S>
+__host__ __device__ __forceinline__ Dual3<S> dsqrt(Dual3<S> a) {
+  S s = sqrt(a.v);
+  S h = S(0.5) / s;
+  return Dual3<S>(s, a.x * h, a.y * h, a.z * h);
+}
+__host__ __device__ __forceinline__ double dsqrt(double a) { return sqrt(a); }
+__host__ __device__ __forceinline__ void dsincos(double a, double* s, double* c) { sincos(a, s, c); }
+template <class S>
+__host__ __device__ __forceinline__ void dsincos(Dual3<S> a, Dual3<S>* s, Dual3<S>* c) {
+  S sv, cv;
+  dsincos(a.v, &sv, &cv);
+  *s = Dual3<S>(sv, cv * a.x, cv * a.y, cv * a.z);
+  *c = Dual3<S>(cv, -sv * a.x, -sv * a.y, -sv * a.z);
+}
+__host__ __device__ __forceinline__ bool lt(double a, double b) { return a < b; }
+template <class S>
+__host__ __device__ __forceinline__ bool lt(Dual3<S> a, double b) { return a.v < b; }
+
+template <class T> struct ScalarOf { using type = T; };
+template <class S> struct ScalarOf<Dual3<S>> { using type = S; };
+
+// Real spherical harmonics l <= 3 of a unit vector, component normalised
+// (sum_m Y_lm^2 = 2l+1), m = -l..l with m<0 ~ sin, m>0 ~ cos, no
+// Condon-Shortley phase. Closed forms of
+//   Y_lm = sqrt(2l+1) sqrt((l-|m|)!/(l+|m|)!) c_m P_l^(|m|)(z) T_m(x, y).
+template <class T>
+__host__ __device__ __forceinline__ void sh16(T x, T y, T z, T* Y) {
+  using S = typename ScalarOf<T>::type;
+  const S s3 = S(1.7320508075688772);
+  const S s15 = S(3.8729833462074170);
+  const S s5h = S(1.1180339887498949);     // sqrt(5)/2
+  const S s15h = S(1.9364916731037085);    // sqrt(15)/2
+  const S c31 = S(0.5400617248673217);     // sqrt(7)/sqrt(6)/2
+  const S c32 = S(5.1234753829797990);     // sqrt(105)/2
+  const S c33 = S(2.0916500663351889);     // sqrt(35/8)
+  const S s7h = S(1.3228756555322954);     // sqrt(7)/2
+  T x2 = x * x, y2 = y * y, z2 = z * z;
+  Y[0] = T(S(1));
+  Y[1] = s3 * y;
+  Y[2] = s3 * z;
+  Y[3] = s3 * x;
+  Y[4] = s15 * (x * y);
+  Y[5] = s15 * (y * z);
+  Y[6] = s5h * (S(3) * z2 - S(1));
+  Y[7] = s15 * (x * z);
+  Y[8] = s15h * (x2 - y2);
+  T p31 = c31 * (S(15) * z2 - S(3));
+  T t3c = x * (x2 - S(3) * y2);              // Re (x+iy)^3
+  T t3s = y * (S(3) * x2 - y2);              // Im (x+iy)^3
+  Y[9] = c33 * t3s;
+  Y[10] = (S(2) * c32) * ((x * y) * z);
+  Y[11] = p31 * y;
+  Y[12] = s7h * (z * (S(5) * z2 - S(3)));
+  Y[13] = p31 * x;
+  Y[14] = c32 * (z * (x2 - y2));
+  Y[15] = c33 * t3c;
+}
+
+// Bessel radial basis times the polynomial cutoff envelope:
+//   e_n(r) = sqrt(2/rc) sin(n pi r / rc) / r * u(r/rc),  n = 1..nb,
+//   u(x) = 1 - (p+1)(p+2)/2 x^p + p(p+2) x^(p+1) - p(p+1)/2 x^(p+2), x < 1,
+// evaluated as u(x) = (1-x)^3 sum_{j<p} (j+1)(j+2)/2 x^j (the same polynomial,
+// free of the cancellation the expanded form suffers near the cutoff), and
+// every sin(n theta) evaluated directly.
+template <class T>
+__host__ __device__ __forceinline__ void bessel_env(T r, double rc, int p, int nb, T* e) {
+  using S = typename ScalarOf<T>::type;
+  const S pi = S(3.14159265358979323846);
+  T xr = r * S(1.0 / rc);
+  T q = T(S(0.5 * p * (p + 1)));
+  for (int j = p - 2; j >= 0; --j) q = q * xr + S(0.5 * (j + 1) * (j + 2));
+  T om = S(1) - xr;
+  T env = (om * om) * (om * q);
+  if (!lt(xr, 1.0)) env = T(S(0));
+  T pre = (S(sqrt(2.0 / rc)) * env) / r;
+  for (int n = 0; n < nb; ++n) {
+    T s, c;
+    dsincos(r * S((n + 1) * pi / rc), &s, &c);
+    e[n] = pre * s;
+  }
+}
+
+// --------------------------------------------------------------- launchers
+struct LinTerm {
+  int in_c0;          // first input component of this term
+  int64_t w_off;      // float offset of the K x K weight (species 0)
+};
+struct LinGroup {
+  int out_c0, ncomp;  // output components [out_c0, out_c0 + ncomp)
+  int t0, t1;         // terms [t0, t1) accumulate into this output
+};
+struct LinPlan {
+  int n_groups = 0, n_terms = 0;
+  LinGroup g[kMaxGroups];
+  LinTerm t[kMaxTerms];
+  int species = 0;          // weights depend on the node's species
+  int64_t w_sstride = 0;    // float stride between species blocks
+  int cin = 0, cout = 0;    // components per node of input / output arrays
+};
+
+struct LinArgs {
+  const float* x;           // [N][cin][K]
+  float* y;                 // [N][cout][K]
+  const float* residual;    // [N][cout][K] or null, added to every written comp
+  const float* w;           // weight base
+  const int* tile_start;    // [n_tiles] start in node_order
+  const int* tile_count;    // [n_tiles]
+  const int* tile_species;  // [n_tiles]
+  const int* node_order;    // nodes grouped by species
+  int n_tiles;
+  int K;
+  int accumulate;           // y += instead of y =
+  int bf16;                 // round x and w to bf16 before multiplying
+};
+
+void launch_edge_features(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
+                          const double4* shift, double rc, int p, int nb, float* Y, float* rbf);
+void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
+                          const double4* shift, double rc, int p, int nb, const float* dY, const float* de,
+                          float4* g);
+void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
+                   const float4* g, float* F);
+void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R);
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, const float* dR,
+                       float* de, int accumulate);
+void launch_tp_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+                   const int* src_map, const float* R, const float* Y, const float* h, int h_stride_nodes,
+                   float inv_c, float* At);
+void launch_tp_bwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+                   const int* src_map, float* R_dR, const float* Y, const float* h, float inv_c,
+                   const float* dAt, float* dY, int accumulate_dY, float* Q);
+void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
+                       const float* Q, float* out);
+struct SymW {
+  const float* w[4][4];     // [L][nu] -> [S][n_eta][K] or null
+};
+void launch_symcon_fwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
+                       SymW w, float* B);
+void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
+                       SymW w, const float* dB, float* dA);
+void launch_linear(hipStream_t s, const LinPlan& plan, const LinArgs& a);
+void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
+                        const float* w1, const float* w2, int hidden, int bf16, int accumulate, float* eps);
+void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
+                        const float* w1, const float* w2, int hidden, int bf16, float* dh);
+void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E);
+void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int bf16,
+                          float* table);
+void launch_fill(hipStream_t s, float* p, size_t n, float v);
+
+}  // namespace mace

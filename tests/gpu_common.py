@@ -1,0 +1,77 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C ABI
+and the oracle on the same seeded inputs, and compare with the documented
+metrics (energy error relative to sum_i |eps_i|, per-atom relative L2,
+force relative RMS)."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import synth
+from oracle import mace
+from paper_2510_23621_amd import binding as B
+from paper_2510_23621_amd.graph import MaceGraph
+
+STRESS = dict(c_norm=1.0)
+STRESS_GAINS = {".radial.3": 4.0}
+
+TOL = {B.MACE_FP32: dict(energy=1e-6, forces=1e-5), B.MACE_BF16_LINEAR: dict(energy=5e-3, forces=2e-2)}
+
+
+def lib_blob(params: dict, seed: int, gains=None) -> np.ndarray:
+    lay, _ = B.mace_weight_layout(B.make_desc(**params))
+    return synth.weight_blob([(name, (n,), f) for name, n, f in lay], seed, gains)
+
+
+def oracle_blob(params: dict, seed: int, gains=None) -> np.ndarray:
+    return synth.weight_blob(mace.weight_layout(mace.ModelDesc(**params)), seed, gains)
+
+
+def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1):
+    desc = B.make_desc(**params)
+    snd, rcv, sh = B.mace_neighbor_list(system.positions, params["r_cut"], system.cells, system.graph_of_atom,
+                                        system.n_graphs)
+    ei = np.stack([snd, rcv]).astype(np.int32)
+    periodic = system.cells is not None
+    g = MaceGraph(desc, blob, system.species.astype(np.int32), ei, sh if periodic else None,
+                  system.cells if periodic else None,
+                  system.graph_of_atom.astype(np.int32) if system.n_graphs > 1 else None, system.n_graphs, prec)
+    pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
+    outs = []
+    for _ in range(repeats):
+        if forces:
+            eps, E, F = g.energy_forces(pos)
+        else:
+            (eps, E), F = g.energy(pos), None
+        torch.cuda.synchronize()
+        outs.append(dict(eps=eps.cpu().numpy().astype(np.float64), energy=E.cpu().numpy(),
+                         forces=None if F is None else F.cpu().numpy().astype(np.float64), n_edges=len(snd)))
+    g.close()
+    return outs if repeats > 1 else outs[0]
+
+
+def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True):
+    return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16, forces=forces)
+
+
+def errors(gpu: dict, ref: dict) -> dict:
+    eps_g, eps_r = gpu["eps"], ref["eps"]
+    scale = np.abs(eps_r).sum()
+    out = dict(
+        energy=float(np.abs(gpu["energy"] - ref["energy"]).max() / max(scale, 1e-300)),
+        eps_l2=float(np.linalg.norm(eps_g - eps_r) / max(np.linalg.norm(eps_r), 1e-300)),
+    )
+    if gpu.get("forces") is not None and ref.get("forces") is not None:
+        out["forces"] = float(np.linalg.norm(gpu["forces"] - ref["forces"]) /
+                              max(np.linalg.norm(ref["forces"]), 1e-300))
+    return out
+
+
+def assert_parity(gpu: dict, ref: dict, prec, label=""):
+    err = errors(gpu, ref)
+    tol = TOL[prec]
+    print(f"[parity] {label} prec={prec} {err}", flush=True)
+    assert err["energy"] <= tol["energy"], (label, err)
+    if "forces" in err:
+        assert err["forces"] <= tol["forces"], (label, err)
+    return err

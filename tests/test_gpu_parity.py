@@ -1,0 +1,128 @@
+"""Parity of the HIP path (through the C ABI) against the FP64 oracle on the
+same seeded inputs: energies within 1e-6 (FP32) / 5e-3 (BF16-linear) of
+sum_i |eps_i|, forces within 1e-5 / 2e-2 relative RMS.  Sizes span several
+node tiles and ragged tails; edge cases: empty neighbourhoods, isolated
+atoms, a batch of graphs, determinism.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from synth.configs import CONFIGS, make_system, model_params
+
+pytestmark = pytest.mark.gpu
+
+B = pytest.importorskip("paper_2510_23621_amd.binding")
+from gpu_common import (STRESS, STRESS_GAINS, TOL, assert_parity, errors, lib_blob, oracle_blob,  # noqa: E402
+                        run_gpu, run_oracle)
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _case(cfg, seed=0, gains=None, **kw):
+    params = model_params(cfg, **kw)
+    blob_o = oracle_blob(params, seed, gains)
+    blob_l = lib_blob(params, seed, gains)
+    assert np.array_equal(blob_o, blob_l)
+    return params, blob_o, blob_l
+
+
+def test_cfg0_nominal_fp32():
+    params, bo, bl = _case(0)
+    sysm = make_system(0, seed=0)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert gpu["n_edges"] == len(ref["graph"].sender)
+    assert_parity(gpu, ref, B.MACE_FP32, "cfg0 nominal")
+
+
+def test_cfg0_stress_fp32():
+    params, bo, bl = _case(0, gains=STRESS_GAINS, **STRESS)
+    sysm = make_system(0, seed=1)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert_parity(gpu, ref, B.MACE_FP32, "cfg0 stress")
+
+
+@pytest.mark.parametrize("K,hl", [(64, 1), (96, 1), (128, 1), (128, 2), (32, 2)])
+def test_small_water_variants_fp32(K, hl):
+    """34 molecules = 102 atoms: species tiles of 16 are ragged (34 O, 68 H)."""
+    params = model_params(0, K=K, hidden_lmax=hl, **STRESS)
+    bo = oracle_blob(params, 3, STRESS_GAINS)
+    bl = lib_blob(params, 3, STRESS_GAINS)
+    sysm = synth.water_box(34, seed=7, box=10.0)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert_parity(gpu, ref, B.MACE_FP32, f"water102 K={K} l={hl}")
+
+
+def test_molecule_batch_fp32_and_bf16():
+    params = model_params(4, K=64, **STRESS)
+    bo = oracle_blob(params, 4, STRESS_GAINS)
+    bl = lib_blob(params, 4, STRESS_GAINS)
+    sysm = synth.molecule_batch(12, seed=2)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert gpu["energy"].shape == (12,)
+    assert_parity(gpu, ref, B.MACE_FP32, "molecules12")
+    gpu16 = run_gpu(params, sysm, bl, prec=B.MACE_BF16_LINEAR)
+    assert_parity(gpu16, ref, B.MACE_BF16_LINEAR, "molecules12 bf16 vs fp64")
+
+
+def test_bf16_linear_vs_fp64_and_fp32():
+    params, bo, bl = _case(0, gains=STRESS_GAINS, **STRESS)
+    sysm = make_system(0, seed=2)
+    ref = run_oracle(params, sysm, bo)
+    g32 = run_gpu(params, sysm, bl)
+    g16 = run_gpu(params, sysm, bl, prec=B.MACE_BF16_LINEAR)
+    assert_parity(g16, ref, B.MACE_BF16_LINEAR, "cfg0 bf16 vs fp64")
+    assert_parity(g16, g32, B.MACE_BF16_LINEAR, "cfg0 bf16 vs gpu fp32")
+    # the oracle's own BF16 emulation lands in the same band
+    ref16 = run_oracle(params, sysm, bo, bf16=True)
+    err = errors(g16, ref16)
+    print("[parity] bf16 gpu vs bf16-emulating oracle", err, flush=True)
+    assert err["energy"] < 5e-3
+
+
+def test_isolated_atoms_and_empty_neighbourhoods():
+    """Atoms with no neighbour (and a graph with no edge at all) get the
+    species-only energy and zero force."""
+    params = model_params(4, K=32, **STRESS)
+    bo = oracle_blob(params, 5, STRESS_GAINS)
+    bl = lib_blob(params, 5, STRESS_GAINS)
+    pos = np.array([[0.0, 0, 0], [1.2, 0.1, 0], [30.0, 0, 0], [60.0, 1.0, 2.0], [200.0, 0, 0]])
+    sysm = synth.System(pos, np.array([0, 1, 2, 3, 4], np.int32), None, np.array([0, 0, 0, 1, 2], np.int32), 3)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert_parity(gpu, ref, B.MACE_FP32, "isolated")
+    assert np.all(gpu["forces"][2:] == 0.0)
+    lone = synth.System(pos[4:], np.array([3], np.int32), None, np.zeros(1, np.int32), 1)
+    ref1 = run_oracle(params, lone, bo)
+    gpu1 = run_gpu(params, lone, bl)
+    assert gpu1["n_edges"] == 0
+    assert abs(gpu1["energy"][0] - ref1["energy"][0]) <= 1e-6 * max(1e-30, abs(ref1["energy"][0]))
+
+
+def test_deterministic_bitwise():
+    params, bo, bl = _case(0, gains=STRESS_GAINS, **STRESS)
+    sysm = make_system(0, seed=3)
+    outs = run_gpu(params, sysm, bl, repeats=3)
+    for o in outs[1:]:
+        assert np.array_equal(o["eps"], outs[0]["eps"])
+        assert np.array_equal(o["energy"], outs[0]["energy"])
+        assert np.array_equal(o["forces"], outs[0]["forces"])
+    e_only = run_gpu(params, sysm, bl, forces=False)
+    assert np.array_equal(e_only["eps"], outs[0]["eps"])
+
+
+def test_forces_sum_to_zero_on_gpu():
+    params, bo, bl = _case(1, gains=STRESS_GAINS, **STRESS)
+    sysm = make_system(1, seed=0)
+    gpu = run_gpu(params, sysm, bl)
+    F = gpu["forces"]
+    assert np.abs(F.sum(0)).max() <= 1e-4 * np.abs(F).max() * np.sqrt(len(F))

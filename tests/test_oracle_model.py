@@ -381,3 +381,16 @@ def test_planted_transposed_harmonic_breaks_invariance(monkeypatch, cfg0):
     R = so3.random_rotation(np.random.default_rng(12))
     out = mace.energy_forces(d, blob, _rotated(sysm, R), forces=False)["eps"]
     assert np.abs(out - ref).max() > 1e-6 * np.abs(ref).max()
+
+
+def test_no_edges_energy_constant_zero_force():
+    """Force equation: with no atom pair inside the cutoff E does not depend
+    on positions, so F = 0 exactly."""
+    d = _small_desc(hidden_lmax=1, K=4, rc=2.0)
+    blob = synth.weight_blob(mace.weight_layout(d), 8, STRESS_GAINS)
+    sysm = synth.System(np.array([[0.0, 0, 0], [5.0, 0, 0]]), np.array([0, 1], np.int32), None,
+                        np.zeros(2, np.int32), 1)
+    out = mace.energy_forces(d, blob, sysm)
+    assert np.all(out["forces"] == 0.0)
+    moved = synth.System(sysm.positions + 1.0, sysm.species, None, sysm.graph_of_atom, 1)
+    assert _energy(d, blob, moved) == out["energy"][0]
