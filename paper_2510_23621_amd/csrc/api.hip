@@ -153,6 +153,7 @@ struct Carver {
 
 struct Buffers {
   float *w = nullptr, *wT = nullptr, *sp_table = nullptr;
+  unsigned short *wbf = nullptr, *wbfT = nullptr;   // bf16 K-packed copies (BF16-linear mode)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
       *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
       *tile_count = nullptr, *tile_species = nullptr;
@@ -173,6 +174,8 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   const int nb = m.d.n_bessel;
   b.w = c.take<float>(m.total);
   b.wT = c.take<float>(m.total);
+  b.wbf = c.take<unsigned short>(m.total);
+  b.wbfT = c.take<unsigned short>(m.total);
   b.sp_table = c.take<float>(S * K);
   b.species = c.take<int>(N);
   b.snd = c.take<int>(std::max<int64_t>(E, 1));
@@ -342,6 +345,7 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.y = y;
   a.residual = residual;
   a.w = transposed ? h->b.wT : h->b.w;
+  a.wbf = transposed ? h->b.wbfT : h->b.wbf;
   a.tile_start = h->b.tile_start;
   a.tile_count = h->b.tile_count;
   a.tile_species = h->b.tile_species;
@@ -501,7 +505,8 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     }
     {
       PROF(KID_RADIAL_BWD);
-      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t], b.de, t < T - 1);
+      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"),
+                        b.wT + m.off.at(pre + "radial.3"), L.P * K, b.R[t], b.de, t < T - 1);
     }
     if (t > 0) {
       {
@@ -672,10 +677,17 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       tspec.push_back(z);
     }
   }
-  // transposed copy of every K x K block (used by the backward linears)
+  // transposed copy of every K x K block (backward linears) and of the last
+  // radial layer [64][P*K] -> [P*K][64] (radial-MLP backward)
   std::vector<float> hwT(hw);
   for (auto& t : m.tensors) {
     const auto& sh = t.shape;
+    if (t.name.size() > 9 && t.name.compare(t.name.size() - 9, 9, ".radial.3") == 0) {
+      const int64_t rows = sh[0], cols = sh[1];
+      for (int64_t r = 0; r < rows; ++r)
+        for (int64_t c2 = 0; c2 < cols; ++c2) hwT[t.offset + c2 * rows + r] = hw[t.offset + r * cols + c2];
+      continue;
+    }
     if (sh.size() >= 2 && sh[sh.size() - 1] == K && sh[sh.size() - 2] == K) {
       int64_t blocks = t.size() / (K * K);
       for (int64_t q = 0; q < blocks; ++q) {
@@ -684,6 +696,30 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
         for (int64_t r = 0; r < K; ++r)
           for (int64_t c2 = 0; c2 < K; ++c2) dst[c2 * K + r] = src[r * K + c2];
       }
+    }
+  }
+
+  // bf16 copies of every K x K block, packed [K/8][K][8] (element (k, n) at
+  // ((k/8) K + n) 8 + k%8) for the MFMA B operand of the BF16 linears
+  std::vector<uint16_t> hbf(m.total, 0), hbfT(m.total, 0);
+  auto to_bf16 = [](float x) -> uint16_t {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+  };
+  for (auto& t : m.tensors) {
+    const auto& sh = t.shape;
+    if (!(sh.size() >= 2 && sh[sh.size() - 1] == K && sh[sh.size() - 2] == K)) continue;
+    const int64_t blocks = t.size() / (K * K);
+    for (int64_t q = 0; q < blocks; ++q) {
+      const int64_t base = t.offset + q * K * K;
+      for (int64_t k = 0; k < K; ++k)
+        for (int64_t n = 0; n < K; ++n) {
+          const int64_t dst = base + ((k / 8) * K + n) * 8 + (k % 8);
+          hbf[dst] = to_bf16(hw[base + k * K + n]);
+          hbfT[dst] = to_bf16(hwT[base + k * K + n]);
+        }
     }
   }
 
@@ -704,6 +740,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   auto chk = [&](hipError_t e) { if (e != hipSuccess && err == hipSuccess) err = e; };
   chk(up(b.w, hw.data(), m.total * 4));
   chk(up(b.wT, hwT.data(), m.total * 4));
+  chk(up(b.wbf, hbf.data(), m.total * 2));
+  chk(up(b.wbfT, hbfT.data(), m.total * 2));
   chk(up(b.species, hs.data(), N * 4));
   chk(up(b.snd, hsnd, E * 4));
   chk(up(b.rcv, hrcv, E * 4));

@@ -80,27 +80,36 @@ __global__ void __launch_bounds__(256) edge_backward_kernel(int E, const float* 
   g[e] = make_float4((float)gx, (float)gy, (float)gz, 0.f);
 }
 
-// One thread per atom; receiver edges are contiguous, sender edges are
-// listed by snd_perm in increasing edge order. Fixed summation order.
+// One wave per atom: lanes take the atom's receiver edges and sender edges
+// in strides of 64, FP64 partial sums (the two sums cancel to a small net
+// force), then a fixed xor-tree across lanes: deterministic.
 __global__ void __launch_bounds__(256) forces_kernel(int N, const int* __restrict__ rcv_off,
                                                      const int* __restrict__ snd_off,
                                                      const int* __restrict__ snd_perm,
                                                      const float4* __restrict__ g, float* __restrict__ F) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (i >= N) return;
-  // FP64 accumulation: the two sums cancel to a small net force
   double fx = 0.0, fy = 0.0, fz = 0.0;
-  for (int e = rcv_off[i]; e < rcv_off[i + 1]; ++e) {
+  for (int e = rcv_off[i] + lane; e < rcv_off[i + 1]; e += 64) {
     float4 v = g[e];
     fx += v.x; fy += v.y; fz += v.z;
   }
-  for (int q = snd_off[i]; q < snd_off[i + 1]; ++q) {
+  for (int q = snd_off[i] + lane; q < snd_off[i + 1]; q += 64) {
     float4 v = g[snd_perm[q]];
     fx -= v.x; fy -= v.y; fz -= v.z;
   }
-  F[3 * i + 0] = (float)fx;
-  F[3 * i + 1] = (float)fy;
-  F[3 * i + 2] = (float)fz;
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) {
+    fx += __shfl_xor(fx, m);
+    fy += __shfl_xor(fy, m);
+    fz += __shfl_xor(fz, m);
+  }
+  if (lane == 0) {
+    F[3 * i + 0] = (float)fx;
+    F[3 * i + 1] = (float)fy;
+    F[3 * i + 2] = (float)fz;
+  }
 }
 
 __global__ void fill_kernel(float* p, size_t n, float v) {
@@ -125,7 +134,7 @@ void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F) {
   if (N <= 0) return;
-  forces_kernel<<<(N + 255) / 256, 256, 0, s>>>(N, rcv_off, snd_off, snd_perm, g, F);
+  forces_kernel<<<(N + 3) / 4, 256, 0, s>>>(N, rcv_off, snd_off, snd_perm, g, F);
 }
 
 void launch_fill(hipStream_t s, float* p, size_t n, float v) {

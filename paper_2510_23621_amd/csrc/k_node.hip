@@ -5,10 +5,15 @@
 
 namespace mace {
 
-// One block = one tile of up to kLinTileNodes nodes (same species) x one
-// output component; threads = output channels k. For each term of the
-// component's group: stage the tile's input row in LDS (k'-major, so a
-// thread reads 4 nodes per ds_read_b128), then acc[q] += x[q][k'] W[k'][k].
+// Channel-mixing linear on MFMA. A block is one wave and owns one tile of up
+// to 16 nodes of one species (the 16 MFMA rows), one output component of one
+// group and up to 64 output channels (4 column tiles of 16; blockIdx.z picks
+// which 64); the reduction runs over the input channels of every term of the
+// group. FP32: v_mfma_f32_16x16x4_f32 with A[l%16][l/16], B[l/16][l%16].
+// BF16 (inputs and weights rounded to nearest even, FP32 accumulation):
+// v_mfma_f32_16x16x32_bf16 with A[l%16][8(l/16)+i], B[8(l/16)+i][l%16]; the
+// weights come pre-packed as [K/8][K][8] bf16 so a lane's 8 k-values are one
+// 16-byte load. Result register r of lane l holds D[4(l/16)+r][l%16].
 struct LinGC {
   unsigned char g, c;
 };
@@ -17,64 +22,131 @@ struct LinLaunch {
   LinGC gc[96];
 };
 
-__global__ void __launch_bounds__(128) linear_kernel(LinLaunch L, LinArgs a) {
-  __shared__ float xs[128 * kLinTileNodes];
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef unsigned short us8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ unsigned short bf16_bits(float x) {
+  float r = bf16_round(x);
+  unsigned int u;
+  __builtin_memcpy(&u, &r, 4);
+  return (unsigned short)(u >> 16);
+}
+
+constexpr int kLinCt = 4;       // column tiles per wave
+constexpr int kLinKsBatch = 8;  // FP32 k-steps whose B fragments are in flight together
+
+template <int K, bool BF16>
+__global__ void __launch_bounds__(64) linear_kernel(LinLaunch L, LinArgs a) {
+  constexpr int ldx = K + 4;    // floats per staged row
+  constexpr int ldb = K + 8;    // bf16 per staged row (16-byte aligned rows)
+  static_assert((K / 4) % kLinKsBatch == 0 && K % 32 == 0, "k-step batches must tile K");
+  __shared__ __align__(16) float xs[kLinTileNodes * ldx];
   const int tile = blockIdx.x;
   const LinGC gcx = L.gc[blockIdx.y];
   const LinGroup grp = L.plan.g[gcx.g];
   const int c = gcx.c;
-  const int K = a.K;
-  const int k = threadIdx.x;
+  const int ct0 = blockIdx.z * kLinCt;
+  constexpr int nct = K / 16;
+  const int l = threadIdx.x;
   const int t0 = a.tile_start[tile], cnt = a.tile_count[tile];
   const int z = a.tile_species[tile];
   const int cin = L.plan.cin, cout = L.plan.cout;
-  float acc[kLinTileNodes];
+  unsigned short* xb = reinterpret_cast<unsigned short*>(xs);
+  const int64_t zoff = L.plan.species ? (int64_t)z * L.plan.w_sstride : 0;
+  f4 acc[kLinCt];
 #pragma unroll
-  for (int q = 0; q < kLinTileNodes; ++q) acc[q] = 0.f;
+  for (int j = 0; j < kLinCt; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
   for (int tm = grp.t0; tm < grp.t1; ++tm) {
     const LinTerm term = L.plan.t[tm];
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < K * kLinTileNodes; idx += blockDim.x) {
-      int q = idx / K, kk = idx % K;
-      float v = 0.f;
-      if (q < cnt) {
-        int node = a.node_order[t0 + q];
-        v = a.x[((size_t)node * cin + term.in_c0 + c) * K + kk];
-        if (a.bf16) v = bf16_round(v);
-      }
-      xs[kk * kLinTileNodes + q] = v;
-    }
-    __syncthreads();
-    if (k < K) {
-      const float* W = a.w + term.w_off + (L.plan.species ? (int64_t)z * L.plan.w_sstride : 0);
-      for (int kk = 0; kk < K; ++kk) {
-        float wv = W[(size_t)kk * K + k];
-        if (a.bf16) wv = bf16_round(wv);
-        const float4* xr = reinterpret_cast<const float4*>(xs + kk * kLinTileNodes);
+    if (tm > grp.t0) __syncthreads();
+    // stage the tile's 16 input rows. Node indices are wave-uniform (scalar
+    // loads); rows past the tile's count re-read its last node and are zeroed
+    // by a select, so no load sits behind a branch and all 16 x K/64 row
+    // loads are in flight together.
+    {
+      constexpr int H = (K + 63) / 64;
+      float v[kLinTileNodes][H];
 #pragma unroll
-        for (int q4 = 0; q4 < kLinTileNodes / 4; ++q4) {
-          float4 xv = xr[q4];
-          acc[4 * q4 + 0] += xv.x * wv;
-          acc[4 * q4 + 1] += xv.y * wv;
-          acc[4 * q4 + 2] += xv.z * wv;
-          acc[4 * q4 + 3] += xv.w * wv;
+      for (int q = 0; q < kLinTileNodes; ++q) {
+        const int node = a.node_order[t0 + min(q, cnt - 1)];
+        const float* row = a.x + ((size_t)node * cin + term.in_c0 + c) * K;
+#pragma unroll
+        for (int h = 0; h < H; ++h) v[q][h] = row[min(l + 64 * h, K - 1)];
+      }
+#pragma unroll
+      for (int q = 0; q < kLinTileNodes; ++q)
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+          const int kk = l + 64 * h;
+          const float x = q < cnt ? v[q][h] : 0.f;
+          if (kk < K) {
+            if constexpr (BF16) xb[q * ldb + kk] = bf16_bits(x);
+            else xs[q * ldx + kk] = x;
+          }
         }
+    }
+    // column tiles past K/16 (K = 32 or 96) load a valid tile and their
+    // results are never stored: no branch around loads or MFMAs
+    int ctc[kLinCt];
+#pragma unroll
+    for (int j = 0; j < kLinCt; ++j) ctc[j] = min(ct0 + j, nct - 1);
+    if constexpr (!BF16) {
+      const float* W = a.w + term.w_off + zoff + (l >> 4) * K + (l & 15);
+#pragma unroll
+      for (int kb = 0; kb < K / 4; kb += kLinKsBatch) {
+        constexpr int nb = kLinKsBatch;
+        float bv[nb][kLinCt];
+#pragma unroll
+        for (int ks = 0; ks < nb; ++ks)
+#pragma unroll
+          for (int j = 0; j < kLinCt; ++j) bv[ks][j] = W[(size_t)(4 * (kb + ks)) * K + 16 * ctc[j]];
+        if (kb == 0) __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < nb; ++ks) {
+          const float av = xs[(l & 15) * ldx + 4 * (kb + ks) + (l >> 4)];
+#pragma unroll
+          for (int j = 0; j < kLinCt; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[ks][j], acc[j], 0, 0, 0);
+        }
+      }
+    } else {
+      const unsigned short* Wp = a.wbf + term.w_off + zoff;
+      us8 bq[K / 32][kLinCt];
+#pragma unroll
+      for (int ks = 0; ks < K / 32; ++ks)
+#pragma unroll
+        for (int j = 0; j < kLinCt; ++j)
+          bq[ks][j] = *reinterpret_cast<const us8*>(Wp + ((size_t)(4 * ks + (l >> 4)) * K + 16 * ctc[j] + (l & 15)) * 8);
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < K / 32; ++ks) {
+        const us8 av = *reinterpret_cast<const us8*>(xb + (l & 15) * ldb + 32 * ks + 8 * (l >> 4));
+#pragma unroll
+        for (int j = 0; j < kLinCt; ++j)
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, av), __builtin_bit_cast(bf8, bq[ks][j]),
+                                                           acc[j], 0, 0, 0);
       }
     }
   }
-  if (k >= K) return;
-  for (int q = 0; q < cnt; ++q) {
-    int node = a.node_order[t0 + q];
-    size_t o = ((size_t)node * cout + grp.out_c0 + c) * K + k;
-    float v = acc[q];
-    if (a.residual) v += a.residual[o];
-    if (a.accumulate) v += a.y[o];
-    a.y[o] = v;
+#pragma unroll
+  for (int j = 0; j < kLinCt; ++j) {
+    const int ct = ct0 + j;
+    if (ct >= nct) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int q = 4 * (l >> 4) + r;
+      if (q >= cnt) continue;
+      const size_t o = ((size_t)a.node_order[t0 + q] * cout + grp.out_c0 + c) * K + 16 * ct + (l & 15);
+      float v = acc[j][r];
+      if (a.residual) v += a.residual[o];
+      if (a.accumulate) v += a.y[o];
+      a.y[o] = v;
+    }
   }
 }
 
 void launch_linear(hipStream_t s, const LinPlan& plan, const LinArgs& a) {
-  if (a.n_tiles <= 0) return;
+  if (a.n_tiles <= 0 || plan.n_groups <= 0) return;
   LinLaunch L;
   L.plan = plan;
   int n = 0;
@@ -84,8 +156,20 @@ void launch_linear(hipStream_t s, const LinPlan& plan, const LinArgs& a) {
       L.gc[n].c = (unsigned char)c;
       ++n;
     }
-  dim3 grid(a.n_tiles, n), block(((a.K + 63) / 64) * 64);
-  linear_kernel<<<grid, block, 0, s>>>(L, a);
+  const int halves = (a.K / 16 + kLinCt - 1) / kLinCt;
+  dim3 grid(a.n_tiles, n, halves), block(64);
+#define MACE_LIN(KK)                                                        \
+  case KK:                                                                 \
+    if (a.bf16) linear_kernel<KK, true><<<grid, block, 0, s>>>(L, a);      \
+    else linear_kernel<KK, false><<<grid, block, 0, s>>>(L, a);            \
+    break;
+  switch (a.K) {
+    MACE_LIN(32)
+    MACE_LIN(64)
+    MACE_LIN(96)
+    MACE_LIN(128)
+  }
+#undef MACE_LIN
 }
 
 // ---------------------------------------------------------------- readouts

@@ -29,18 +29,19 @@ __global__ void __launch_bounds__(128) tp_fwd_kernel(int N, int K, const int* __
 #pragma unroll
   for (int c = 0; c < MID; ++c) acc[c] = 0.f;
   const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
-  for (int e = e_beg; e < e_end; ++e) {
+  // operands of one edge; two sets so that the loads of edge e+1 are in
+  // flight while edge e is being contracted
+  auto load = [&](int e, float* hv, float* y, float* r) {
     const int s = snd[e];
     const int src = src_map ? src_map[s] : s;
-    float hv[DIN];
 #pragma unroll
     for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
-    float y[16];
 #pragma unroll
     for (int m = 0; m < 16; ++m) y[m] = Y[(size_t)e * 16 + m];
-    float r[P];
 #pragma unroll
     for (int p = 0; p < P; ++p) r[p] = R[((size_t)e * P + p) * K + k];
+  };
+  auto contract = [&](const float* hv, const float* y, const float* r) {
     for_paths<LHMAX>([&](auto tag) {
       using T = decltype(tag);
       constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
@@ -53,6 +54,16 @@ __global__ void __launch_bounds__(128) tp_fwd_kernel(int N, int K, const int* __
 #pragma unroll
       for (int m = 0; m < 2 * lo + 1; ++m) acc[T::offset + m] += r[T::index] * t[m];
     });
+  };
+  float hA[DIN], yA[16], rA[P], hB[DIN], yB[16], rB[P];
+  if (e_beg < e_end) load(e_beg, hA, yA, rA);
+  for (int e = e_beg; e < e_end; e += 2) {
+    if (e + 1 < e_end) load(e + 1, hB, yB, rB);
+    contract(hA, yA, rA);
+    if (e + 1 < e_end) {
+      if (e + 2 < e_end) load(e + 2, hA, yA, rA);
+      contract(hB, yB, rB);
+    }
   }
 #pragma unroll
   for (int c = 0; c < MID; ++c) At[((size_t)i * MID + c) * K + k] = acc[c] * inv_c;
@@ -126,9 +137,11 @@ __global__ void __launch_bounds__(128) tp_bwd_kernel(int N, int K, const int* __
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   const bool active = k < K;
+  const int kc = min(k, K - 1);             // lanes past K read a valid channel ...
+  const float gs = active ? inv_c : 0.f;   // ... and contribute nothing
   float g[MID];
 #pragma unroll
-  for (int c = 0; c < MID; ++c) g[c] = active ? dAt[((size_t)i * MID + c) * K + k] * inv_c : 0.f;
+  for (int c = 0; c < MID; ++c) g[c] = dAt[((size_t)i * MID + c) * K + kc] * gs;
   const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
   for (int c0 = e_beg; c0 < e_end; c0 += kTpChunk) {
     const int c1 = min(e_end, c0 + kTpChunk);
@@ -137,13 +150,13 @@ __global__ void __launch_bounds__(128) tp_bwd_kernel(int N, int K, const int* __
       const int src = src_map ? src_map[s] : s;
       float hv[DIN];
 #pragma unroll
-      for (int c = 0; c < DIN; ++c) hv[c] = active ? h[((size_t)src * DIN + c) * K + k] : 0.f;
+      for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + kc];
       float y[16];
 #pragma unroll
       for (int m = 0; m < 16; ++m) y[m] = Y[(size_t)e * 16 + m];
       float r[P];
 #pragma unroll
-      for (int p = 0; p < P; ++p) r[p] = active ? R_dR[((size_t)e * P + p) * K + k] : 0.f;
+      for (int p = 0; p < P; ++p) r[p] = R_dR[((size_t)e * P + p) * K + kc];
       float dr[P], dy[16], dh[DIN];
 #pragma unroll
       for (int m = 0; m < 16; ++m) dy[m] = 0.f;
@@ -199,7 +212,16 @@ __global__ void __launch_bounds__(256) sender_sum_kernel(int N, int CK, const in
   const int q0 = snd_off[j], q1 = snd_off[j + 1];
   for (int ck = threadIdx.x; ck < CK; ck += blockDim.x) {
     float acc = 0.f;
-    for (int q = q0; q < q1; ++q) acc += Q[(size_t)snd_perm[q] * CK + ck];
+    int q = q0;
+    for (; q + 4 <= q1; q += 4) {
+      const float v0 = Q[(size_t)snd_perm[q] * CK + ck], v1 = Q[(size_t)snd_perm[q + 1] * CK + ck];
+      const float v2 = Q[(size_t)snd_perm[q + 2] * CK + ck], v3 = Q[(size_t)snd_perm[q + 3] * CK + ck];
+      acc += v0;
+      acc += v1;
+      acc += v2;
+      acc += v3;
+    }
+    for (; q < q1; ++q) acc += Q[(size_t)snd_perm[q] * CK + ck];
     out[(size_t)j * CK + ck] = acc;
   }
 }

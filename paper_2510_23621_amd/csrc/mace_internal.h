@@ -177,7 +177,8 @@ struct LinArgs {
   const float* x;           // [N][cin][K]
   float* y;                 // [N][cout][K]
   const float* residual;    // [N][cout][K] or null, added to every written comp
-  const float* w;           // weight base
+  const float* w;           // weight base (FP32, row-major [in][out])
+  const unsigned short* wbf;  // same tensors as bf16, each K x K block packed [K/8][K][8]
   const int* tile_start;    // [n_tiles] start in node_order
   const int* tile_count;    // [n_tiles]
   const int* tile_species;  // [n_tiles]
@@ -196,8 +197,8 @@ void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
 void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R);
-void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, const float* dR,
-                       float* de, int accumulate);
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* W3T, int PK,
+                       const float* dR, float* de, int accumulate);
 void launch_tp_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                    const int* src_map, const float* R, const float* Y, const float* h, int h_stride_nodes,
                    float inv_c, float* At);
