@@ -57,6 +57,20 @@ constexpr int path_offset(int lh, int ly, int lo) {
   return -1;
 }
 
+// (l_h, l_Y, l_out) of the idx-th path in sorted order (any lhmax: the
+// order does not depend on it)
+constexpr int path_at(int idx, int which) {
+  int n = 0;
+  for (int a = 0; a <= 3; ++a)
+    for (int b = 0; b <= 3; ++b)
+      for (int c = 0; c <= 3; ++c)
+        if (path_ok(a, b, c)) {
+          if (n == idx) return which == 0 ? a : (which == 1 ? b : c);
+          ++n;
+        }
+  return -1;
+}
+
 template <int LH, int LY, int LO>
 struct PathTag {
   static constexpr int lh = LH, ly = LY, lo = LO;
@@ -76,5 +90,8 @@ __device__ __forceinline__ void for_paths(F&& f) {
     });
   });
 }
+
+template <int I>
+using PathAt = PathTag<path_at(I, 0), path_at(I, 1), path_at(I, 2)>;
 
 }  // namespace mace

@@ -75,3 +75,34 @@ def assert_parity(gpu: dict, ref: dict, prec, label=""):
     if "forces" in err:
         assert err["forces"] <= tol["forces"], (label, err)
     return err
+
+
+def cluster_cut(system, i, radius):
+    """Non-periodic system of every image of every atom within `radius` of
+    atom i (atom i first, at its own position)."""
+    x0 = system.positions[i]
+    if system.cells is None:
+        g = system.graph_of_atom[i]
+        idx = np.nonzero(system.graph_of_atom == g)[0]
+        d = np.linalg.norm(system.positions[idx] - x0, axis=1)
+        keep = idx[d < radius]
+        keep = np.concatenate([[i], keep[keep != i]])
+        return synth.System(system.positions[keep], system.species[keep], None, np.zeros(len(keep), np.int32), 1), keep
+    cell = system.cells[0]
+    L = np.linalg.norm(cell, axis=1).min()
+    n = int(np.ceil(radius / L)) + 1
+    pos, spec, src = [x0[None]], [system.species[i:i + 1]], [np.array([i])]
+    for a in range(-n, n + 1):
+        for b in range(-n, n + 1):
+            for c in range(-n, n + 1):
+                shift = a * cell[0] + b * cell[1] + c * cell[2]
+                p = system.positions + shift
+                d = np.linalg.norm(p - x0, axis=1)
+                sel = d < radius
+                if a == 0 and b == 0 and c == 0:
+                    sel[i] = False
+                pos.append(p[sel])
+                spec.append(system.species[sel])
+                src.append(np.nonzero(sel)[0])
+    P = np.vstack(pos)
+    return synth.System(P, np.concatenate(spec), None, np.zeros(len(P), np.int32), 1), np.concatenate(src)
