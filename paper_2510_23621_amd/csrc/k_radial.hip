@@ -86,11 +86,8 @@ __global__ void __launch_bounds__(256) radial_fwd_kernel(int E, const float* __r
   hidden_layer<kH>(hb, kPad, kH, W2, ha, z);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-  float af[4][kH / 4];
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-    for (int ks = 0; ks < kH / 4; ++ks) af[rt][ks] = ha[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)];
+  // the A operand (a3) is read from LDS at each MFMA: keeping its 64
+  // fragments in registers would halve the occupancy
   const int nct = PK / 16;
   // B fragments of column tile ct: W3[4 ks + l/16][16 ct + l%16], ks = 0..15
   auto load_b = [&](float* bq, int ct) {
@@ -105,7 +102,7 @@ __global__ void __launch_bounds__(256) radial_fwd_kernel(int E, const float* __r
 #pragma unroll
     for (int ks = 0; ks < kH / 4; ++ks)
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma4(af[rt][ks], bq[ks], acc[rt]);
+      for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma4(ha[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], bq[ks], acc[rt]);
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
@@ -147,14 +144,6 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   const int tid = threadIdx.x;
   const int l = tid & 63, w = tid >> 6;
   const int col = 16 * w + (l & 15);
-  load_basis_tile(E, e0, rbf, nb, nb_pad, xs);
-  __syncthreads();
-  f4 z0[4], z1[4], z2[4];
-  hidden_layer<NBP>(xs, kXPad, nb, W0, ta, z0);
-  __syncthreads();
-  hidden_layer<kH>(ta, kPad, kH, W1, tb, z1);
-  __syncthreads();
-  hidden_layer<kH>(tb, kPad, kH, W2, ta, z2);   // a2 itself is not needed below
   // da3[e][j] = sum_n dR[e][n] W3[j][n]: dR staged through LDS 64 columns at
   // a time, double-buffered (the global loads of chunk i+1 are in flight
   // while chunk i feeds the MFMAs); W3^T fragments prefetched likewise.
@@ -195,7 +184,6 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   };
   fetch(0);
   load_w(bw[0], 0);
-  __syncthreads();               // layer-3 reads of tb are done
   stash(tb);
   __syncthreads();
   for (int ch = 0; ch < nchunk; ch += 2) {
@@ -218,6 +206,17 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
       __syncthreads();
     }
   }
+  __syncthreads();
+  // the hidden layers are recomputed only now, so their pre-activations are
+  // not live across the long dR loop above
+  load_basis_tile(E, e0, rbf, nb, nb_pad, xs);
+  __syncthreads();
+  f4 z0[4], z1[4], z2[4];
+  hidden_layer<NBP>(xs, kXPad, nb, W0, ta, z0);
+  __syncthreads();
+  hidden_layer<kH>(ta, kPad, kH, W1, tb, z1);
+  __syncthreads();
+  hidden_layer<kH>(tb, kPad, kH, W2, ta, z2);   // a2 itself is not needed below
   __syncthreads();
   // dz2 -> ta
 #pragma unroll
