@@ -159,6 +159,7 @@ struct Buffers {
       *tile_count = nullptr, *tile_species = nullptr;
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
+  float* a3 = nullptr;   // [E][64] last radial hidden layer (also holds dE/da3 in the backward)
   std::vector<float*> R, A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
@@ -192,6 +193,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.shift = c.take<double4>(std::max<int64_t>(E, 1));
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
+  b.a3 = c.take<float>(std::max<int64_t>(E, 1) * 64);
   b.R.resize(T);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
@@ -402,7 +404,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     }
     {
       PROF(KID_RADIAL_FWD);
-      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t]);
+      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t], b.a3);
     }
     {
       PROF(KID_TP_FWD);
@@ -506,7 +508,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     {
       PROF(KID_RADIAL_BWD);
       launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"),
-                        b.wT + m.off.at(pre + "radial.3"), L.P * K, b.R[t], b.de, t < T - 1);
+                        b.wT + m.off.at(pre + "radial.3"), L.P * K, b.R[t], b.de, t < T - 1, b.a3);
     }
     if (t > 0) {
       {

@@ -196,9 +196,10 @@ void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd
                           float4* g);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
-void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R);
+void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R,
+                       float* a3);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* W3T, int PK,
-                       const float* dR, float* de, int accumulate);
+                       const float* dR, float* de, int accumulate, float* da3);
 void launch_tp_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                    const int* src_map, const float* R, const float* Y, const float* h, int h_stride_nodes,
                    float inv_c, float* At);
