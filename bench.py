@@ -27,8 +27,11 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-KERNEL_SOURCES = {"radial_fwd_kernel": "k_radial.hip", "radial_bwd_kernel": "k_radial.hip",
-                  "tp_fwd_kernel": "k_tp.hip", "tp_bwd_kernel": "k_tp.hip", "linear_kernel": "k_node.hip"}
+KERNEL_SOURCES = {"radial_hidden_fwd_kernel": "k_radial.hip", "radial_hidden_bwd_kernel": "k_radial.hip",
+                  "tpr_fwd_kernel": "k_tpr.hip", "tpr_bwd_kernel": "k_tpr.hip", "linear_kernel": "k_node.hip"}
+# kernel classes whose roofline is the FP32 MFMA peak (dense contractions);
+# the others are priced against HBM bandwidth
+MFMA_BOUND = ("radial_hidden_fwd_kernel", "radial_hidden_bwd_kernel", "tpr_fwd_kernel", "tpr_bwd_kernel")
 
 
 def source_hash(kname):
@@ -57,24 +60,29 @@ def measured_traffic(kname, workload):
 
 def kernel_work(name, model, N, E):
     """Algorithmic (bytes, flops) of every launch of kernel class `name` in
-    one step, summed.  Bytes count each compulsory HBM read/write once."""
+    one step, summed.  Bytes count each compulsory HBM read/write once; flops
+    of the MFMA-bound classes count the dense contractions only (the radial
+    MLP layers, including the last one formed inside the tensor-product
+    kernels), not the Clebsch-Gordan arithmetic on the vector ALUs."""
     K, nb, layers = model["K"], model["n_bessel"], model["layers"]
+    n_ct = K // 16
     tot_b = tot_f = 0.0
     for t, L in enumerate(layers):
-        P, mid, din, dout, nnz = L["P"], L["mid"], L["din"], L["dout"], L["nnz"]
-        if name == "tp_fwd_kernel":
-            tot_b += E * (P * K * 4 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4
-            tot_f += E * 2 * K * (nnz + mid)
-        elif name == "tp_bwd_kernel":
+        P, mid, din = L["P"], L["mid"], L["din"]
+        acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
+        if name == "tpr_fwd_kernel":
+            tot_b += E * (256 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4 + 64 * P * K * 4
+            tot_f += E * 2 * 64 * P * K
+        elif name == "tpr_bwd_kernel":
             q = din * K * 4 if t > 0 else 0
-            tot_b += E * (2 * P * K * 4 + 64 + 64 * (t < len(layers) - 1) + 64 + 4 + q) + N * (din + mid) * K * 4
-            tot_f += E * 2 * K * (3 * nnz + 2 * mid)
-        elif name == "radial_fwd_kernel":
-            tot_b += E * (nb * 4 + P * K * 4)
-            tot_f += E * 2 * (nb * 64 + 2 * 64 * 64 + 64 * P * K)
-        elif name == "radial_bwd_kernel":
-            tot_b += E * (nb * 4 + P * K * 4 + nb * 4 * (1 + (t < len(layers) - 1)))
-            tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64 + 64 * P * K)
+            tot_b += E * (256 + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
+            tot_f += E * 2 * 2 * 64 * P * K
+        elif name == "radial_hidden_fwd_kernel":
+            tot_b += E * (nb * 4 + 256)
+            tot_f += E * 2 * (nb * 64 + 2 * 64 * 64)
+        elif name == "radial_hidden_bwd_kernel":
+            tot_b += E * (nb * 4 + n_ct * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
+            tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64)
     return tot_b, tot_f
 
 
@@ -193,7 +201,7 @@ def main():
     flops_per_launch = flops / max(per_launch, 1)
     gbs = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
     tfl = flops_per_launch / (avg_launch_ms * 1e-3) / 1e12
-    if kname in ("radial_fwd_kernel", "radial_bwd_kernel"):
+    if kname in MFMA_BOUND:
         roof = {"bound": "mfma", "achieved": round(tfl, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tfl / FP32_MFMA_PEAK_TFLOPS, 4)}
     else:

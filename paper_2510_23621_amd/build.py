@@ -16,7 +16,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmace_amd.so")
-HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_gemm.hip", "k_tp.hip", "k_symcon.hip", "k_node.hip"]
+HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip"]
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall", "-Wno-unused-function",
     "-Wno-unused-variable", "-Wno-unused-but-set-variable",

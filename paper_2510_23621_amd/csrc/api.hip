@@ -159,12 +159,13 @@ struct Buffers {
       *tile_count = nullptr, *tile_species = nullptr;
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
-  float* a3 = nullptr;   // [E][64] last radial hidden layer (also holds dE/da3 in the backward)
-  std::vector<float*> R, A, hin, ht;
+  std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
+  std::vector<float*> A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
   float *dh0 = nullptr, *dh1 = nullptr, *dB = nullptr, *dA = nullptr, *dApre = nullptr, *dAt = nullptr,
         *dY = nullptr, *de = nullptr, *Q = nullptr, *dht = nullptr;
+  float *da3p = nullptr, *dYp = nullptr;   // per-channel-tile partials [K/16][E][64], [K/16][E][16]
   float4* g = nullptr;
 };
 
@@ -193,14 +194,13 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.shift = c.take<double4>(std::max<int64_t>(E, 1));
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
-  b.a3 = c.take<float>(std::max<int64_t>(E, 1) * 64);
-  b.R.resize(T);
+  b.a3.resize(T);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
   b.ht.assign(T, nullptr);
   for (int t = 0; t < T; ++t) {
     const LayerPlan& L = m.layers[t];
-    b.R[t] = c.take<float>(std::max<int64_t>(E, 1) * L.P * K);
+    b.a3[t] = c.take<float>(std::max<int64_t>(E, 1) * 64);
     b.A[t] = c.take<float>(N * 16 * K);
     if (t > 0) {
       b.hin[t] = c.take<float>(N * L.din * K);
@@ -220,6 +220,8 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.dApre = c.take<float>(N * 16 * K);
   b.dAt = c.take<float>(N * m.max_mid * K);
   b.dY = c.take<float>(std::max<int64_t>(E, 1) * 16);
+  b.da3p = c.take<float>((K / 16) * std::max<int64_t>(E, 1) * 64);
+  b.dYp = c.take<float>((K / 16) * std::max<int64_t>(E, 1) * 16);
   b.de = c.take<float>(std::max<int64_t>(E, 1) * nb);
   b.Q = c.take<float>(std::max<int64_t>(E, 1) * m.max_din * K);
   b.dht = c.take<float>(N * m.max_din * K);
@@ -234,8 +236,8 @@ enum KernelId {
   KID_FILL, KID_COUNT
 };
 const char* kKernelNames[KID_COUNT] = {
-  "edge_features_kernel", "radial_fwd_kernel", "tp_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
-  "readout_kernel", "tp_bwd_kernel", "radial_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
+  "edge_features_kernel", "radial_hidden_fwd_kernel", "tpr_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
+  "readout_kernel", "tpr_bwd_kernel", "radial_hidden_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
   "edge_backward_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel"};
 constexpr int kProfPairs = 4096;
 
@@ -404,11 +406,12 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     }
     {
       PROF(KID_RADIAL_FWD);
-      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), L.P * K, b.R[t], b.a3);
+      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.a3[t]);
     }
     {
       PROF(KID_TP_FWD);
-      launch_tp_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.R[t], b.Y, src, 0, inv_c, b.At);
+      launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"), b.Y,
+                     src, inv_c, b.At);
     }
     if (t == 0) {
       {
@@ -502,13 +505,13 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     const int* src_map = t == 0 ? b.species : nullptr;
     {
       PROF(KID_TP_BWD);
-      launch_tp_bwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.R[t], b.Y, src, inv_c, b.dAt, b.dY, t < T - 1,
-                    t > 0 ? b.Q : nullptr);
+      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
+                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p);
     }
     {
       PROF(KID_RADIAL_BWD);
-      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"),
-                        b.wT + m.off.at(pre + "radial.3"), L.P * K, b.R[t], b.de, t < T - 1, b.a3);
+      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, K / 16, b.dY,
+                        b.de, t < T - 1);
     }
     if (t > 0) {
       {

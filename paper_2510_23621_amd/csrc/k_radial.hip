@@ -5,10 +5,13 @@
 // [P*K][64] from the transposed blob.
 //
 // The three hidden layers run here (a3 [E][64] is written out, 256 bytes per
-// edge); the wide last layer and its transpose are the plain GEMMs of
-// k_gemm.hip. Hidden layers on FP32 MFMA (v_mfma_f32_16x16x4_f32): a block
+// edge); the wide last layer is computed inside the tensor-product kernels,
+// which also hand back dE/da3 as per-channel-tile partials. Hidden layers on
+// FP32 MFMA (v_mfma_f32_16x16x4_f32): a block
 // owns a 64-edge tile (4 row tiles of 16) and has 4 waves; lane l supplies
 // A[l%16][l/16], B[l/16][l%16], and result register r holds D[4*(l/16)+r][l%16].
+#include <type_traits>
+
 #include "mace_internal.h"
 
 namespace mace {
@@ -90,12 +93,17 @@ __global__ void __launch_bounds__(256) radial_hidden_fwd_kernel(int E, const flo
   }
 }
 
-// de = VJP of the hidden layers given da3 (recomputes the pre-activations)
-template <int NBP>
+// de = VJP of the hidden layers given dE/da3, which arrives as n_part partials
+// da3p[part][E][64] summed here in part order (the pre-activations are
+// recomputed). The same pass folds the partials dYp[part][E][16] of dE/dY into
+// dY. With accumulate set, de and dY are added to instead of overwritten.
+template <int NBP, int NPART>
 __global__ void __launch_bounds__(256) radial_hidden_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                                 const float* __restrict__ W,
-                                                                const float* __restrict__ da3,
-                                                                float* __restrict__ de, int accumulate) {
+                                                                const float* __restrict__ da3p,
+                                                                const float* __restrict__ dYp,
+                                                                float* __restrict__ dY, float* __restrict__ de,
+                                                                int accumulate) {
   __shared__ float xs[kTE * kXPad];
   __shared__ float ta[kTE * kPad];
   __shared__ float tb[kTE * kPad];
@@ -115,14 +123,24 @@ __global__ void __launch_bounds__(256) radial_hidden_bwd_kernel(int E, const flo
   __syncthreads();
   hidden_layer<kH>(tb, kPad, kH, W2, ta, z2);   // a2 itself is not needed below
   __syncthreads();
-  // dz2 = da3 * silu'(z2) -> ta (result layout: row 16 rt + 4 (l/16) + r, column col)
+  // dE/da3 = the partials summed in part order, as float4 rows into ta
+  for (int idx = tid; idx < kTE * kH / 4; idx += blockDim.x) {
+    const int row = idx >> 4, c4 = idx & 15;
+    const int e = min(e0 + row, E - 1);
+    f4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(da3p + ((size_t)q * E + e) * kH + 4 * c4);
+    if (e0 + row >= E) v = f4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f4*>(ta + row * kPad + 4 * c4) = v;
+  }
+  __syncthreads();
+  // dz2 = da3 * silu'(z2), in place (result layout: row 16 rt + 4 (l/16) + r, column col)
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = 16 * rt + 4 * (l >> 4) + r;
-      const float g = da3[(size_t)min(e0 + row, E - 1) * kH + col] * (e0 + row < E ? 1.f : 0.f);
-      ta[row * kPad + col] = g * silu_grad(z2[rt][r]);
+      ta[row * kPad + col] *= silu_grad(z2[rt][r]);
     }
   __syncthreads();
   f4 acc[4];
@@ -164,26 +182,39 @@ __global__ void __launch_bounds__(256) radial_hidden_bwd_kernel(int E, const flo
     size_t o = (size_t)(e0 + e) * nb + i;
     de[o] = accumulate ? de[o] + sacc : sacc;
   }
+  for (int idx = tid; idx < kTE * 4; idx += blockDim.x) {
+    const int e = e0 + (idx >> 2), c4 = idx & 3;
+    if (e >= E) continue;
+    f4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(dYp + ((size_t)q * E + e) * 16 + 4 * c4);
+    f4* o = reinterpret_cast<f4*>(dY + (size_t)e * 16 + 4 * c4);
+    *o = accumulate ? *o + v : v;
+  }
 }
 
-void launch_gemm_radial_out(hipStream_t s, int E, int PK, const float* a3, const float* W3, float* R);
-void launch_gemm_radial_in(hipStream_t s, int E, int PK, const float* dR, const float* W3T, float* da3);
-
-void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R, float* a3) {
+void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, float* a3) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
   if (nb <= 8) radial_hidden_fwd_kernel<8><<<g, 256, 0, s>>>(E, rbf, nb, W, a3);
   else radial_hidden_fwd_kernel<16><<<g, 256, 0, s>>>(E, rbf, nb, W, a3);
-  launch_gemm_radial_out(s, E, PK, a3, W + nb * kH + 2 * kH * kH, R);
 }
 
-void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* W3T, int PK,
-                       const float* dR, float* de, int accumulate, float* da3) {
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
+                       const float* dYp, int n_part, float* dY, float* de, int accumulate) {
   if (E <= 0) return;
-  launch_gemm_radial_in(s, E, PK, dR, W3T, da3);
   const int g = (E + kTE - 1) / kTE;
-  if (nb <= 8) radial_hidden_bwd_kernel<8><<<g, 256, 0, s>>>(E, rbf, nb, W, da3, de, accumulate);
-  else radial_hidden_bwd_kernel<16><<<g, 256, 0, s>>>(E, rbf, nb, W, da3, de, accumulate);
+  auto go = [&](auto NP) {
+    constexpr int NPART = decltype(NP)::value;
+    if (nb <= 8) radial_hidden_bwd_kernel<8, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+    else radial_hidden_bwd_kernel<16, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+  };
+  switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}
+    case 2: go(std::integral_constant<int, 2>{}); break;
+    case 4: go(std::integral_constant<int, 4>{}); break;
+    case 6: go(std::integral_constant<int, 6>{}); break;
+    case 8: go(std::integral_constant<int, 8>{}); break;
+  }
 }
 
 }  // namespace mace

@@ -1,0 +1,390 @@
+// Edge tensor product of Eq. 26 with the last radial layer computed in place,
+// fused with the receiver neighbour sum; and its vector-Jacobian product.
+//
+//   R[e][p][k]  = sum_j a3[e][j] W3[j][p K + k]                 (last radial layer)
+//   At[i][p][m3][k] = inv_c * sum_{e: rcv_e = i} R[e][p][k]
+//                     * sum_{m1,m2} C^{lo}_{lh ly}[m1][m2][m3] h[src_e][lh,m1][k] Y[e][ly,m2]
+//
+// R is never stored: for a K = 128 model with ten paths it would be 5 KB per
+// edge each way. One wave owns a (receiver, 16-channel tile) pair and walks
+// the receiver's edges (CSR order) in tiles of 16. For each tile it forms R
+// with FP32 MFMA (v_mfma_f32_16x16x4_f32; lane l supplies A[l%16][l/16] and
+// B[l/16][l%16], result register r holds D[4(l/16)+r][l%16]): rows are the
+// tile's edges, columns the wave's channels. Lane l therefore holds R for
+// channel l%16 and the four edges 4(l/16)..4(l/16)+3, and contracts exactly
+// those edges; the four lane groups are summed by a fixed butterfly at the
+// end of the receiver, so the result does not depend on scheduling.
+//
+// A block is a few waves on as many receivers, sharing one channel tile; the
+// tile's slice of W3 (64 x P x 16 floats) sits in LDS for the block's life,
+// and each wave stages the Y rows of its current edge tile in LDS.
+#include <algorithm>
+
+#include "mace_internal.h"
+#include "static_loops.h"
+
+namespace mace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWPitch = 68;   // LDS row pitch of the W3 slice: 64 + 4 (4 mod 32)
+constexpr int kTPitch = 17;   // 16 x 16 transpose tile
+constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
+// Launch shape per (l_max, direction): waves per block (all on one channel
+// tile) and the waves per SIMD the register budget is cut for. Two 8-wave
+// blocks per CU fit the LDS below l = 2 and give four waves per SIMD at 128
+// VGPRs; the l = 1 backward needs more registers (dE/dAt of the receiver
+// stays live) and runs three 4-wave blocks per CU at 168; for l = 2 the W3
+// slice alone fills half the LDS.
+template <int LHMAX, bool BWD>
+struct TprShape {
+  static constexpr int waves = (BWD && LHMAX == 1) ? 4 : 8;
+  static constexpr int per_simd = LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 3 : 4);
+  static constexpr int blocks_per_cu = 4 * per_simd / waves;
+};
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// sW[(p*16 + kk)*kWPitch + j] = W3[j][p K + 16 ct + kk]
+template <int P>
+__device__ __forceinline__ void load_w3_slice(const float* __restrict__ W3, int K, int ct, float* sW) {
+  const int PK = P * K;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    sW[(p * 16 + kk) * kWPitch + j] = W3[(size_t)j * PK + p * K + 16 * ct + kk];
+  }
+}
+
+// R of the 16 edges e0 .. e0+15 (edges at or past e_end get R = 0) for the
+// wave's channel tile: r[p][q] = R[e0 + 4(l/16) + q][p][16 ct + l%16].
+// The 64-long reduction runs in the order j = 16 qq + 4 s + c so that every
+// lane reads its A operand as four float4.
+template <int P>
+__device__ __forceinline__ void tile_radial(const float* __restrict__ a3, int e0, int e_end,
+                                            const float* __restrict__ sW, f4* r) {
+  const int l = threadIdx.x & 63;
+  const int row = e0 + (l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 4 * (l >> 4));
+  f4 a[4];
+#pragma unroll
+  for (int qq = 0; qq < 4; ++qq) a[qq] = arow[4 * qq] * keep;
+  const float* wb = sW + (l & 15) * kWPitch + 4 * (l >> 4);
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    __builtin_amdgcn_sched_barrier(0);   // B fragments are loaded path by path
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const f4 b = *reinterpret_cast<const f4*>(wb + p * 16 * kWPitch + 16 * qq);
+      acc = mfma4(a[qq][0], b[0], acc);
+      acc = mfma4(a[qq][1], b[1], acc);
+      acc = mfma4(a[qq][2], b[2], acc);
+      acc = mfma4(a[qq][3], b[3], acc);
+    }
+    r[p] = acc;
+  }
+}
+
+// Y rows of the wave's 16-edge tile into LDS: sy[row][m], row pitch kYPitch.
+// Lane l moves float4 number l%4 of row l/4.
+__device__ __forceinline__ void stage_y(const float* __restrict__ Y, int e0, int e_end, float* sy) {
+  const int l = threadIdx.x & 63;
+  const int row = l >> 2, ch = l & 3;
+  const int e = min(e0 + row, e_end - 1);
+  const f4 v = reinterpret_cast<const f4*>(Y + (size_t)e * 16)[ch];
+  *reinterpret_cast<f4*>(sy + row * kYPitch + 4 * ch) = v;
+}
+
+__device__ __forceinline__ void read_y(const float* sy, int row, float* y) {
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const f4 t4 = *reinterpret_cast<const f4*>(sy + row * kYPitch + 4 * v);
+    y[4 * v] = t4[0];
+    y[4 * v + 1] = t4[1];
+    y[4 * v + 2] = t4[2];
+    y[4 * v + 3] = t4[3];
+  }
+}
+
+template <int LHMAX, int NW = TprShape<LHMAX, false>::waves>
+__global__ void __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
+tpr_fwd_kernel(
+    int N, int K, const int* __restrict__ rcv_off, const int* __restrict__ snd, const int* __restrict__ src_map,
+    const float* __restrict__ a3, const float* __restrict__ W3, const float* __restrict__ Y,
+    const float* __restrict__ h, float inv_c, float* __restrict__ At) {
+  constexpr int P = path_count(LHMAX);
+  constexpr int MID = mid_count(LHMAX);
+  constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
+  __shared__ float sW[P * 16 * kWPitch];
+  __shared__ float sY[NW][16 * kYPitch];
+  const int ct = blockIdx.y;
+  load_w3_slice<P>(W3, K, ct, sW);
+  __syncthreads();
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int g = l >> 4;
+  const int k = 16 * ct + (l & 15);
+  float* sy = sY[w];
+  for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
+    float acc[MID];
+#pragma unroll
+    for (int c = 0; c < MID; ++c) acc[c] = 0.f;
+    const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      stage_y(Y, e0, e_end, sy);
+      f4 r[P];
+      tile_radial<P>(a3, e0, e_end, sW, r);
+      // lane group 0 holds the tile's first edges, so nq covers every valid one;
+      // the scheduling barrier keeps one edge's operands live at a time
+      const int nq = min(4, e_end - e0);
+      static_for<0, 4>([&](auto QI) {
+        constexpr int q = decltype(QI)::value;
+        __builtin_amdgcn_sched_barrier(0);
+        if (q >= nq) return;
+        const int row = 4 * g + q;
+        const int e = min(e0 + row, e_end - 1);   // edges past e_end carry R = 0
+        const int s = snd[e];
+        const int src = src_map ? src_map[s] : s;
+        float hv[DIN];
+#pragma unroll
+        for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
+        float y[16];
+        read_y(sy, row, y);
+        for_paths<LHMAX>([&](auto tag) {
+          using T = decltype(tag);
+          constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
+          float t[2 * lo + 1];
+#pragma unroll
+          for (int m = 0; m < 2 * lo + 1; ++m) t[m] = 0.f;
+          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
+            t[m3] += cg * (hv[lh * lh + m1] * y[ly * ly + m2]);
+          });
+          const float rv = r[T::index][q];
+#pragma unroll
+          for (int m = 0; m < 2 * lo + 1; ++m) acc[T::offset + m] += rv * t[m];
+        });
+      });
+    }
+    // lane groups 0+1 and 2+3, then the two pairs: every lane ends with the same sum
+#pragma unroll
+    for (int c = 0; c < MID; ++c) {
+      acc[c] += __shfl_xor(acc[c], 16);
+      acc[c] += __shfl_xor(acc[c], 32);
+    }
+#pragma unroll
+    for (int c = 0; c < MID; ++c)
+      if ((c & 3) == g) At[((size_t)i * MID + c) * K + k] = acc[c] * inv_c;
+  }
+}
+
+// One halving step of group_reduce16: lanes with bit HALF set keep the upper
+// half of v[0 .. 2 HALF) and receive their partner's, the others the lower.
+template <int HALF>
+__device__ __forceinline__ void reduce_stage(float* v, int lane) {
+  const bool hi = lane & HALF;
+#pragma unroll
+  for (int q = 0; q < HALF; ++q) {
+    const float send = hi ? v[q] : v[q + HALF];
+    const float keep = hi ? v[q + HALF] : v[q];
+    v[q] = keep + __shfl_xor(send, HALF);
+  }
+}
+
+// Sum of 16 values over the 16 lanes of a lane group: afterwards lane l holds
+// the total of index l%16.
+__device__ __forceinline__ float group_reduce16(float* v, int lane) {
+  reduce_stage<8>(v, lane);
+  reduce_stage<4>(v, lane);
+  reduce_stage<2>(v, lane);
+  reduce_stage<1>(v, lane);
+  return v[0];
+}
+
+// VJP of tpr_fwd. Given g = dE/dAt, per edge e (receiver i) and channel k,
+// with Bm_p[m2] = sum_{m1,m3} C h[m1] g[i][p][m3] and Dm_p[m1] = sum_{m2,m3} C Y[m2] g[i][p][m3]:
+//   dR[e][p][k]    = inv_c sum_m2 Bm_p[m2] Y[m2]
+//   dY[e][ly,m2]  += inv_c sum_k sum_p R Bm_p[m2]                    (channel-tile partial)
+//   Q[e][lh,m1][k] = inv_c sum_p R Dm_p[m1]                          (per-edge sender gradient)
+//   da3[e][j]     += sum_{p,k} dR[e][p][k] W3[j][p K + k]           (channel-tile partial)
+// The partials of channel tile ct go to dYp[ct][e][16] and da3p[ct][e][64];
+// their sum over tiles (fixed order) is taken by the hidden-layer backward.
+template <int LHMAX, int NW = TprShape<LHMAX, true>::waves>
+__global__ void __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true>::per_simd, TprShape<LHMAX, true>::per_simd)))
+tpr_bwd_kernel(
+    int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
+    const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
+    const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p) {
+  constexpr int P = path_count(LHMAX);
+  constexpr int MID = mid_count(LHMAX);
+  constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
+  __shared__ float sW[P * 16 * kWPitch];
+  __shared__ float sY[NW][16 * kYPitch];
+  __shared__ float sT[NW][16 * kTPitch];
+  const int ct = blockIdx.y;
+  load_w3_slice<P>(W3, K, ct, sW);
+  __syncthreads();
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int g = l >> 4, kk = l & 15;
+  const int k = 16 * ct + kk;
+  float* sy = sY[w];
+  float* tw = sT[w];
+  float* dYc = dYp + (size_t)ct * E * 16;
+  float* da3c = da3p + (size_t)ct * E * 64;
+  for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
+    float gv[MID];
+#pragma unroll
+    for (int c = 0; c < MID; ++c) gv[c] = dAt[((size_t)i * MID + c) * K + k] * inv_c;
+    const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      stage_y(Y, e0, e_end, sy);
+      f4 r[P];   // R on entry; dR (zero for edges past e_end) after the edge loop
+      tile_radial<P>(a3, e0, e_end, sW, r);
+      const int nq = min(4, e_end - e0);
+      static_for<0, 4>([&](auto QI) {
+        constexpr int q = decltype(QI)::value;
+        __builtin_amdgcn_sched_barrier(0);
+        if (q >= nq) return;
+        const int row = 4 * g + q;
+        const int e_raw = e0 + row;
+        const bool valid = e_raw < e_end;
+        const int e = min(e_raw, e_end - 1);
+        const int s = snd[e];
+        const int src = src_map ? src_map[s] : s;
+        float hv[DIN];
+#pragma unroll
+        for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
+        float y[16];
+        read_y(sy, row, y);
+        float dy[16], dh[DIN];
+#pragma unroll
+        for (int m = 0; m < 16; ++m) dy[m] = 0.f;
+#pragma unroll
+        for (int c = 0; c < DIN; ++c) dh[c] = 0.f;
+        for_paths<LHMAX>([&](auto tag) {
+          using T = decltype(tag);
+          constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
+          __builtin_amdgcn_sched_barrier(0);
+          const float rv = r[T::index][q];
+          // Bm[m2] = sum C h[m1] g[m3], Dm[m1] = sum C Y[m2] g[m3]; then
+          // dR = Bm . Y, dY += R Bm, dh += R Dm. (C g is not formed on its own:
+          // it would be hoisted out of the edge loop as 86 live registers.)
+          float Bm[2 * ly + 1], Dm[2 * lh + 1];
+#pragma unroll
+          for (int m = 0; m < 2 * ly + 1; ++m) Bm[m] = 0.f;
+#pragma unroll
+          for (int m = 0; m < 2 * lh + 1; ++m) Dm[m] = 0.f;
+          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
+            Bm[m2] += cg * (gv[T::offset + m3] * hv[lh * lh + m1]);
+            Dm[m1] += cg * (gv[T::offset + m3] * y[ly * ly + m2]);
+          });
+          float d = 0.f;
+#pragma unroll
+          for (int m = 0; m < 2 * ly + 1; ++m) {
+            d += Bm[m] * y[ly * ly + m];
+            dy[ly * ly + m] += rv * Bm[m];
+          }
+#pragma unroll
+          for (int m = 0; m < 2 * lh + 1; ++m) dh[lh * lh + m] += rv * Dm[m];
+          r[T::index][q] = valid ? d : 0.f;
+        });
+        const float tot = group_reduce16(dy, l);
+        if (valid) {
+          dYc[(size_t)e * 16 + kk] = tot;
+          if (Q) {
+#pragma unroll
+            for (int c = 0; c < DIN; ++c) Q[((size_t)e * DIN + c) * K + k] = dh[c];
+          }
+        }
+      });
+      // da3 partial: D[e][j] = sum_{p, k} dR[e][p][k] W3[j][p K + 16 ct + k]. The
+      // A operand wants the edge on l%16, so each dR tile is transposed through LDS.
+      f4 d3[4];
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) tw[(4 * g + q) * kTPitch + kk] = r[p][q];
+        __builtin_amdgcn_wave_barrier();
+        float av[4];
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) av[kq] = tw[kk * kTPitch + 4 * kq + g];
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int kq = 0; kq < 4; ++kq) {
+          const float* wrow = sW + (p * 16 + 4 * kq + g) * kWPitch + kk;
+#pragma unroll
+          for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(av[kq], wrow[16 * jt], d3[jt]);
+        }
+      }
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int e = e0 + 4 * g + rr;
+        if (e < e_end) {
+#pragma unroll
+          for (int jt = 0; jt < 4; ++jt) da3c[(size_t)e * 64 + 16 * jt + kk] = d3[jt][rr];
+        }
+      }
+    }
+  }
+}
+
+namespace {
+// blocks per channel tile: the resident blocks of the whole chip shared
+// among the channel tiles, a multiple of 8 where possible so that the channel
+// tiles of one receiver group land on the same XCD (same L2)
+int tpr_grid_x(int N, int n_ct, int waves, int blocks_per_cu) {
+  const int want = std::max(8, (256 * blocks_per_cu / n_ct) & ~7);
+  return std::max(1, std::min(want, (N + waves - 1) / waves));
+}
+
+template <int LH>
+void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* snd, const int* src_map,
+                    const float* a3, const float* W3, const float* Y, const float* h, float inv_c, float* At) {
+  using S = TprShape<LH, false>;
+  const int n_ct = K / 16;
+  dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
+  tpr_fwd_kernel<LH><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
+}
+
+template <int LH>
+void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
+                    const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
+                    const float* dAt, float* dYp, float* Q, float* da3p) {
+  using S = TprShape<LH, true>;
+  const int n_ct = K / 16;
+  dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
+  tpr_bwd_kernel<LH><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
+                                                    Q, da3p);
+}
+}  // namespace
+
+void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+                    const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
+                    float inv_c, float* At) {
+  if (N <= 0) return;
+  switch (lh_max) {
+    case 0: tpr_fwd_launch<0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
+    case 1: tpr_fwd_launch<1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
+    case 2: tpr_fwd_launch<2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
+  }
+}
+
+void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
+                    const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p) {
+  if (N <= 0 || E <= 0) return;
+  switch (lh_max) {
+    case 0: tpr_bwd_launch<0>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
+    case 1: tpr_bwd_launch<1>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
+    case 2: tpr_bwd_launch<2>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
+  }
+}
+
+}  // namespace mace

@@ -196,16 +196,15 @@ void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd
                           float4* g);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
-void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, int PK, float* R,
-                       float* a3);
-void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* W3T, int PK,
-                       const float* dR, float* de, int accumulate, float* da3);
-void launch_tp_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
-                   const int* src_map, const float* R, const float* Y, const float* h, int h_stride_nodes,
-                   float inv_c, float* At);
-void launch_tp_bwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
-                   const int* src_map, float* R_dR, const float* Y, const float* h, float inv_c,
-                   const float* dAt, float* dY, int accumulate_dY, float* Q);
+void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, float* a3);
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
+                       const float* dYp, int n_part, float* dY, float* de, int accumulate);
+void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+                    const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
+                    float inv_c, float* At);
+void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
+                    const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p);
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
 struct SymW {
