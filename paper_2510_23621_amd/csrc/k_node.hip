@@ -34,13 +34,16 @@ __device__ __forceinline__ unsigned short bf16_bits(float x) {
 }
 
 constexpr int kLinCt = 4;       // column tiles per wave
-constexpr int kLinKsBatch = 8;  // FP32 k-steps whose B fragments are in flight together
+// FP32: the B fragments of all K/4 k-steps are loaded in one batch (K VGPRs
+// per lane at K = 128), so a term costs one memory round trip, not K/32
+template <int K>
+constexpr int lin_ks_batch() { return K / 4; }
 
 template <int K, bool BF16>
 __global__ void __launch_bounds__(64) linear_kernel(LinLaunch L, LinArgs a) {
   constexpr int ldx = K + 4;    // floats per staged row
   constexpr int ldb = K + 8;    // bf16 per staged row (16-byte aligned rows)
-  static_assert((K / 4) % kLinKsBatch == 0 && K % 32 == 0, "k-step batches must tile K");
+  static_assert(K % 32 == 0, "K is a multiple of 32");
   __shared__ __align__(16) float xs[kLinTileNodes * ldx];
   const int tile = blockIdx.x;
   const LinGC gcx = L.gc[blockIdx.y];
@@ -94,8 +97,8 @@ __global__ void __launch_bounds__(64) linear_kernel(LinLaunch L, LinArgs a) {
     if constexpr (!BF16) {
       const float* W = a.w + term.w_off + zoff + (l >> 4) * K + (l & 15);
 #pragma unroll
-      for (int kb = 0; kb < K / 4; kb += kLinKsBatch) {
-        constexpr int nb = kLinKsBatch;
+      for (int kb = 0; kb < K / 4; kb += lin_ks_batch<K>()) {
+        constexpr int nb = lin_ks_batch<K>();
         float bv[nb][kLinCt];
 #pragma unroll
         for (int ks = 0; ks < nb; ++ks)

@@ -34,12 +34,14 @@ constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
 // tile) and the waves per SIMD the register budget is cut for. Two 8-wave
 // blocks per CU fit the LDS below l = 2 and give four waves per SIMD at 128
 // VGPRs; the l = 1 backward needs more registers (dE/dAt of the receiver
-// stays live) and runs three 4-wave blocks per CU at 168; for l = 2 the W3
-// slice alone fills half the LDS.
+// stays live) and runs two 4-wave blocks per CU at 256 (at 168 it spills);
+// for l = 2 the W3 slice alone fills half the LDS. The MFMA phases raise
+// the wave's priority so that they issue ahead of the other waves' vector
+// work on the SIMD.
 template <int LHMAX, bool BWD>
 struct TprShape {
   static constexpr int waves = (BWD && LHMAX == 1) ? 4 : 8;
-  static constexpr int per_simd = LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 3 : 4);
+  static constexpr int per_simd = LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 2 : 4);
   static constexpr int blocks_per_cu = 4 * per_simd / waves;
 };
 
@@ -72,6 +74,7 @@ __device__ __forceinline__ void tile_radial(const float* __restrict__ a3, int e0
 #pragma unroll
   for (int qq = 0; qq < 4; ++qq) a[qq] = arow[4 * qq] * keep;
   const float* wb = sW + (l & 15) * kWPitch + 4 * (l >> 4);
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int p = 0; p < P; ++p) {
     __builtin_amdgcn_sched_barrier(0);   // B fragments are loaded path by path
@@ -86,6 +89,7 @@ __device__ __forceinline__ void tile_radial(const float* __restrict__ a3, int e0
     }
     r[p] = acc;
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // Y rows of the wave's 16-edge tile into LDS: sy[row][m], row pitch kYPitch.
@@ -303,6 +307,7 @@ tpr_bwd_kernel(
       });
       // da3 partial: D[e][j] = sum_{p, k} dR[e][p][k] W3[j][p K + 16 ct + k]. The
       // A operand wants the edge on l%16, so each dR tile is transposed through LDS.
+      __builtin_amdgcn_s_setprio(1);
       f4 d3[4];
 #pragma unroll
       for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
@@ -323,6 +328,7 @@ tpr_bwd_kernel(
           for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(av[kq], wrow[16 * jt], d3[jt]);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int e = e0 + 4 * g + rr;
