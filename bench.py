@@ -27,11 +27,11 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-KERNEL_SOURCES = {"radial_hidden_fwd_kernel": "k_radial.hip", "radial_hidden_bwd_kernel": "k_radial.hip",
+KERNEL_SOURCES = {"edge_prologue_kernel": "k_radial.hip", "radial_bwd_kernel": "k_radial.hip",
                   "tpr_fwd_kernel": "k_tpr.hip", "tpr_bwd_kernel": "k_tpr.hip", "linear_kernel": "k_node.hip"}
 # kernel classes whose roofline is the FP32 MFMA peak (dense contractions);
 # the others are priced against HBM bandwidth
-MFMA_BOUND = ("radial_hidden_fwd_kernel", "radial_hidden_bwd_kernel", "tpr_fwd_kernel", "tpr_bwd_kernel")
+MFMA_BOUND = ("edge_prologue_kernel", "radial_bwd_kernel", "tpr_fwd_kernel", "tpr_bwd_kernel")
 
 
 def source_hash(kname):
@@ -69,7 +69,6 @@ def kernel_work(name, model, N, E):
     tot_b = tot_f = 0.0
     for t, L in enumerate(layers):
         P, mid, din = L["P"], L["mid"], L["din"]
-        acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
         if name == "tpr_fwd_kernel":
             tot_b += E * (256 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4 + 64 * P * K * 4
             tot_f += E * 2 * 64 * P * K
@@ -77,10 +76,11 @@ def kernel_work(name, model, N, E):
             q = din * K * 4 if t > 0 else 0
             tot_b += E * (256 + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
             tot_f += E * 2 * 2 * 64 * P * K
-        elif name == "radial_hidden_fwd_kernel":
-            tot_b += E * (nb * 4 + 256)
+        elif name == "edge_prologue_kernel":      # geometry once, hidden layers of every layer
+            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * 256
             tot_f += E * 2 * (nb * 64 + 2 * 64 * 64)
-        elif name == "radial_hidden_bwd_kernel":
+        elif name == "radial_bwd_kernel":
+            acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
             tot_b += E * (nb * 4 + n_ct * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
             tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64)
     return tot_b, tot_f

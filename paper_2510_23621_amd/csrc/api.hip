@@ -231,14 +231,14 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
 }  // namespace
 
 enum KernelId {
-  KID_EDGE_FEATURES = 0, KID_RADIAL_FWD, KID_TP_FWD, KID_LINEAR, KID_SYMCON_FWD, KID_READOUT,
+  KID_EDGE_FEATURES = 0, KID_TP_FWD, KID_LINEAR, KID_SYMCON_FWD, KID_READOUT,
   KID_TP_BWD, KID_RADIAL_BWD, KID_SYMCON_BWD, KID_SENDER_SUM, KID_EDGE_BWD, KID_FORCES, KID_GRAPH_ENERGY,
   KID_FILL, KID_COUNT
 };
 const char* kKernelNames[KID_COUNT] = {
-  "edge_features_kernel", "radial_hidden_fwd_kernel", "tpr_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
-  "readout_kernel", "tpr_bwd_kernel", "radial_hidden_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
-  "edge_backward_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel"};
+  "edge_prologue_kernel", "tpr_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
+  "readout_kernel", "tpr_bwd_kernel", "radial_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
+  "edge_vjp_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel"};
 constexpr int kProfPairs = 4096;
 
 struct mace_graph {
@@ -381,7 +381,19 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
   const bool bf16 = h->prec == MACE_BF16_LINEAR;
   {
     PROF(KID_EDGE_FEATURES);
-    launch_edge_features(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf);
+    // geometry and the radial hidden layers of every interaction layer, in
+    // launches of up to kMaxRadialLayers layers
+    for (int t0 = 0; t0 < m.d.n_layers; t0 += kMaxRadialLayers) {
+      RadialSet rs;
+      rs.n = std::min(kMaxRadialLayers, m.d.n_layers - t0);
+      for (int q = 0; q < rs.n; ++q) {
+        rs.W[q] = b.w + m.off.at(std::to_string(t0 + q) + ".radial.0");
+        rs.a3[q] = b.a3[t0 + q];
+      }
+      // (a later chunk recomputes the same Y and rbf)
+      launch_edge_prologue(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf,
+                           rs);
+    }
   }
   const float inv_c = (float)(1.0 / m.d.c_norm);
   for (int t = 0; t < m.d.n_layers; ++t) {
@@ -403,10 +415,6 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       }
       src = b.ht[t];
       src_map = nullptr;
-    }
-    {
-      PROF(KID_RADIAL_FWD);
-      launch_radial_fwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.a3[t]);
     }
     {
       PROF(KID_TP_FWD);
@@ -509,6 +517,8 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p);
     }
     {
+      // right after the partials are written, while they are still in the
+      // last-level cache
       PROF(KID_RADIAL_BWD);
       launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, K / 16, b.dY,
                         b.de, t < T - 1);
@@ -531,8 +541,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
   }
   {
     PROF(KID_EDGE_BWD);
-    launch_edge_backward(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.dY,
-                         b.de, b.g);
+    launch_edge_vjp(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.dY, b.de, b.g);
   }
   {
     PROF(KID_FORCES);

@@ -67,29 +67,56 @@ __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __re
   }
 }
 
-// a3 = SiLU(SiLU(SiLU(e W0) W1) W2) for a 64-edge tile
+// Edge prologue for a 64-edge tile: geometry of every edge (Y and the radial
+// basis e, written out; the first wave computes one edge per lane in FP64),
+// then the hidden layers a3 = SiLU(SiLU(SiLU(e W0) W1) W2) of the radial MLP
+// of every interaction layer in rs, all from the same e.
 template <int NBP>
-__global__ void __launch_bounds__(256) radial_hidden_fwd_kernel(int E, const float* __restrict__ rbf, int nb,
-                                                                const float* __restrict__ W, float* __restrict__ a3) {
+__global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* __restrict__ pos,
+                                                            const int* __restrict__ snd, const int* __restrict__ rcv,
+                                                            const double4* __restrict__ shift, double rc, int p,
+                                                            int nb, float* __restrict__ Y, float* __restrict__ rbf,
+                                                            RadialSet rs) {
   __shared__ float xs[kTE * kXPad];
   __shared__ float ha[kTE * kPad];
   __shared__ float hb[kTE * kPad];
   const int e0 = blockIdx.x * kTE;
-  const float* W0 = W;
-  const float* W1 = W0 + nb * kH;
-  const float* W2 = W1 + kH * kH;
-  load_basis_tile(E, e0, rbf, nb, (nb + 3) & ~3, xs);
+  if (threadIdx.x < kTE) {
+    const int e = e0 + threadIdx.x;
+    float row[kXPad];
+#pragma unroll
+    for (int i = 0; i < kXPad; ++i) row[i] = 0.f;
+    if (e < E) {
+      float y[16];
+      edge_geometry(e, pos, snd, rcv, shift, rc, p, nb, y, row);
+      float4* Yv = reinterpret_cast<float4*>(Y + (size_t)e * 16);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Yv[v] = make_float4(y[4 * v], y[4 * v + 1], y[4 * v + 2], y[4 * v + 3]);
+      for (int n = 0; n < nb; ++n) rbf[(size_t)e * nb + n] = row[n];
+    }
+#pragma unroll
+    for (int i = 0; i < kXPad; ++i) xs[threadIdx.x * kXPad + i] = row[i];
+  }
   __syncthreads();
-  f4 z[4];
-  hidden_layer<NBP>(xs, kXPad, nb, W0, ha, z);
-  __syncthreads();
-  hidden_layer<kH>(ha, kPad, kH, W1, hb, z);
-  __syncthreads();
-  hidden_layer<kH>(hb, kPad, kH, W2, ha, z);
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < kTE * kH; idx += blockDim.x) {
-    const int e = idx / kH, j = idx % kH;
-    if (e0 + e < E) a3[(size_t)(e0 + e) * kH + j] = ha[e * kPad + j];
+  for (int t = 0; t < rs.n; ++t) {
+    const float* W0 = rs.W[t];
+    const float* W1 = W0 + nb * kH;
+    const float* W2 = W1 + kH * kH;
+    f4 z[4];
+    hidden_layer<NBP>(xs, kXPad, nb, W0, ha, z);
+    __syncthreads();
+    hidden_layer<kH>(ha, kPad, kH, W1, hb, z);
+    __syncthreads();
+    hidden_layer<kH>(hb, kPad, kH, W2, ha, z);
+    __syncthreads();
+    float* a3 = rs.a3[t];
+    for (int idx = threadIdx.x; idx < kTE * kH / 4; idx += blockDim.x) {
+      const int e = idx >> 4, c4 = idx & 15;
+      if (e0 + e < E)
+        *reinterpret_cast<f4*>(a3 + (size_t)(e0 + e) * kH + 4 * c4) =
+            *reinterpret_cast<const f4*>(ha + e * kPad + 4 * c4);
+    }
+    __syncthreads();   // ha is rewritten by the next layer's MLP
   }
 }
 
@@ -98,7 +125,7 @@ __global__ void __launch_bounds__(256) radial_hidden_fwd_kernel(int E, const flo
 // recomputed). The same pass folds the partials dYp[part][E][16] of dE/dY into
 // dY. With accumulate set, de and dY are added to instead of overwritten.
 template <int NBP, int NPART>
-__global__ void __launch_bounds__(256) radial_hidden_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                                 const float* __restrict__ W,
                                                                 const float* __restrict__ da3p,
                                                                 const float* __restrict__ dYp,
@@ -193,11 +220,13 @@ __global__ void __launch_bounds__(256) radial_hidden_bwd_kernel(int E, const flo
   }
 }
 
-void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, float* a3) {
+void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
+                          const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
+                          const RadialSet& rs) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
-  if (nb <= 8) radial_hidden_fwd_kernel<8><<<g, 256, 0, s>>>(E, rbf, nb, W, a3);
-  else radial_hidden_fwd_kernel<16><<<g, 256, 0, s>>>(E, rbf, nb, W, a3);
+  if (nb <= 8) edge_prologue_kernel<8><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs);
+  else edge_prologue_kernel<16><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs);
 }
 
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
@@ -206,8 +235,8 @@ void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const flo
   const int g = (E + kTE - 1) / kTE;
   auto go = [&](auto NP) {
     constexpr int NPART = decltype(NP)::value;
-    if (nb <= 8) radial_hidden_bwd_kernel<8, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
-    else radial_hidden_bwd_kernel<16, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+    if (nb <= 8) radial_bwd_kernel<8, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+    else radial_bwd_kernel<16, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
   };
   switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}
     case 2: go(std::integral_constant<int, 2>{}); break;

@@ -155,6 +155,62 @@ __host__ __device__ __forceinline__ void bessel_env(T r, double rc, int p, int n
   }
 }
 
+// g = dE/dd of edge e from dE/dY (dy[16]) and dE/de (de[nb]), by forward-mode
+// differentiation (FP64 dual numbers) of the same closed forms with respect to
+// the three components of d.
+__device__ __forceinline__ float4 edge_geometry_vjp(int e, const float* __restrict__ pos,
+                                                    const int* __restrict__ snd, const int* __restrict__ rcv,
+                                                    const double4* __restrict__ shift, double rc, int p, int nb,
+                                                    const float* dy, const float* de) {
+  using D3 = Dual3<double>;
+  const int s = snd[e], r = rcv[e];
+  const double4 sh = shift[e];
+  const D3 dx(((double)pos[3 * s + 0] - (double)pos[3 * r + 0]) + sh.x, 1.0, 0.0, 0.0);
+  const D3 dyv(((double)pos[3 * s + 1] - (double)pos[3 * r + 1]) + sh.y, 0.0, 1.0, 0.0);
+  const D3 dz(((double)pos[3 * s + 2] - (double)pos[3 * r + 2]) + sh.z, 0.0, 0.0, 1.0);
+  const D3 rr = dsqrt(dx * dx + dyv * dyv + dz * dz);
+  const D3 inv = D3(1.0) / rr;
+  D3 y[16];
+  sh16<D3>(dx * inv, dyv * inv, dz * inv, y);
+  double gx = 0.0, gy = 0.0, gz = 0.0;
+  for (int m = 1; m < 16; ++m) {
+    gx += (double)dy[m] * y[m].x;
+    gy += (double)dy[m] * y[m].y;
+    gz += (double)dy[m] * y[m].z;
+  }
+  D3 eb[16];
+  bessel_env<D3>(rr, rc, p, nb, eb);
+  for (int n = 0; n < nb; ++n) {
+    const double w = de[n];
+    gx += w * eb[n].x;
+    gy += w * eb[n].y;
+    gz += w * eb[n].z;
+  }
+  return make_float4((float)gx, (float)gy, (float)gz, 0.f);
+}
+
+// Geometry of edge e in FP64, rounded to FP32 once: d = (x_snd - x_rcv) +
+// shift, r = |d|, u = d / r; Y[16] (real harmonics of u) and eb[nb] (radial
+// basis times envelope). The periodic shift and the difference of wrapped
+// positions would otherwise carry FP32 rounding into every edge.
+__device__ __forceinline__ void edge_geometry(int e, const float* __restrict__ pos, const int* __restrict__ snd,
+                                              const int* __restrict__ rcv, const double4* __restrict__ shift,
+                                              double rc, int p, int nb, float* yout, float* ebout) {
+  const int s = snd[e], r = rcv[e];
+  const double4 sh = shift[e];
+  const double dx = ((double)pos[3 * s + 0] - (double)pos[3 * r + 0]) + sh.x;
+  const double dy = ((double)pos[3 * s + 1] - (double)pos[3 * r + 1]) + sh.y;
+  const double dz = ((double)pos[3 * s + 2] - (double)pos[3 * r + 2]) + sh.z;
+  const double rr = sqrt(dx * dx + dy * dy + dz * dz);
+  const double inv = 1.0 / rr;
+  double y[16];
+  sh16<double>(dx * inv, dy * inv, dz * inv, y);
+  for (int m = 0; m < 16; ++m) yout[m] = (float)y[m];
+  double eb[16];
+  bessel_env<double>(rr, rc, p, nb, eb);
+  for (int n = 0; n < nb; ++n) ebout[n] = (float)eb[n];
+}
+
 // --------------------------------------------------------------- launchers
 struct LinTerm {
   int in_c0;          // first input component of this term
@@ -189,16 +245,23 @@ struct LinArgs {
   int bf16;                 // round x and w to bf16 before multiplying
 };
 
-void launch_edge_features(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
-                          const double4* shift, double rc, int p, int nb, float* Y, float* rbf);
-void launch_edge_backward(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
-                          const double4* shift, double rc, int p, int nb, const float* dY, const float* de,
-                          float4* g);
+constexpr int kMaxRadialLayers = 4;
+// hidden-layer weights (W0 of the layer, W1 and W2 follow it) and a3 outputs
+// of up to kMaxRadialLayers interaction layers
+struct RadialSet {
+  const float* W[kMaxRadialLayers];
+  float* a3[kMaxRadialLayers];
+  int n;
+};
+void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
+                          const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
+                          const RadialSet& rs);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
-void launch_radial_fwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, float* a3);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate);
+void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv, const double4* shift,
+                     double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, float* At);

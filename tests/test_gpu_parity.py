@@ -61,6 +61,20 @@ def test_small_water_variants_fp32(K, hl):
     assert_parity(gpu, ref, B.MACE_FP32, f"water102 K={K} l={hl}")
 
 
+def test_many_layers_fp32():
+    """Five interaction layers: more than the four layers one launch of the
+    edge prologue (geometry plus the radial hidden layers) takes, so the
+    chunked launches are exercised; the backward accumulates dE/dY and dE/de
+    over five layers."""
+    params = model_params(0, K=32, hidden_lmax=1, n_layers=5, **STRESS)
+    bo = oracle_blob(params, 5, STRESS_GAINS)
+    bl = lib_blob(params, 5, STRESS_GAINS)
+    sysm = synth.water_box(12, seed=11, box=7.5)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert_parity(gpu, ref, B.MACE_FP32, "water36 five layers")
+
+
 def test_molecule_batch_fp32_and_bf16():
     params = model_params(4, K=64, **STRESS)
     bo = oracle_blob(params, 4, STRESS_GAINS)
