@@ -59,6 +59,41 @@ __device__ __forceinline__ void hidden_layer(const float* __restrict__ in, int l
   }
 }
 
+// The two halves of hidden_layer, so that the next layer's B fragments can
+// be in flight while the current layer's MFMAs run.
+template <int NIN_PAD>
+__device__ __forceinline__ void load_b_frag(const float* __restrict__ W, int nin, float* b) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = 16 * w + (l & 15);
+#pragma unroll
+  for (int ks = 0; ks < NIN_PAD / 4; ++ks) {
+    const int k = 4 * ks + (l >> 4);
+    b[ks] = (k < nin) ? W[k * kH + col] : 0.f;
+  }
+}
+
+template <int NIN_PAD>
+__device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldin, const float* b,
+                                           float* __restrict__ out, f4* z) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = 16 * w + (l & 15);
+  f4 acc[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < NIN_PAD / 4; ++ks) {
+    const int k = 4 * ks + (l >> 4);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma4(in[(16 * rt + (l & 15)) * ldin + k], b[ks], acc[rt]);
+  }
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    z[rt] = acc[rt];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(acc[rt][r]);
+  }
+}
+
 __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __restrict__ rbf, int nb, int nb_pad,
                                                 float* xs) {
   for (int idx = threadIdx.x; idx < kTE * kXPad; idx += blockDim.x) {
@@ -81,6 +116,10 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
   __shared__ float ha[kTE * kPad];
   __shared__ float hb[kTE * kPad];
   const int e0 = blockIdx.x * kTE;
+  // B fragments: bc for the layer being computed, bn for the next one (in
+  // flight meanwhile); the first is requested before the geometry
+  float bc[kH / 4], bn[kH / 4];
+  load_b_frag<NBP>(rs.W[0], nb, bc);
   if (threadIdx.x < kTE) {
     const int e = e0 + threadIdx.x;
     float row[kXPad];
@@ -103,12 +142,17 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
     const float* W1 = W0 + nb * kH;
     const float* W2 = W1 + kH * kH;
     f4 z[4];
-    hidden_layer<NBP>(xs, kXPad, nb, W0, ha, z);
+    load_b_frag<kH>(W1, kH, bn);
+    hidden_mma<NBP>(xs, kXPad, bc, ha, z);
     __syncthreads();
-    hidden_layer<kH>(ha, kPad, kH, W1, hb, z);
+    load_b_frag<kH>(W2, kH, bc);
+    hidden_mma<kH>(ha, kPad, bn, hb, z);
     __syncthreads();
-    hidden_layer<kH>(hb, kPad, kH, W2, ha, z);
+    if (t + 1 < rs.n) load_b_frag<NBP>(rs.W[t + 1], nb, bn);
+    hidden_mma<kH>(hb, kPad, bc, ha, z);
     __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
     float* a3 = rs.a3[t];
     for (int idx = threadIdx.x; idx < kTE * kH / 4; idx += blockDim.x) {
       const int e = idx >> 4, c4 = idx & 15;
