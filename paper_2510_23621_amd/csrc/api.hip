@@ -47,7 +47,9 @@ struct Model {
   std::vector<LayerPlan> layers;
   std::vector<Tensor> tensors;
   std::map<std::string, int64_t> off;
-  int64_t total = 0;
+  int64_t total = 0;       // floats of the weight blob
+  int64_t comb_off = 0;    // after the blob: layer-0 path-merging x species weights [4][S][K][K]
+  int64_t total_ext = 0;   // blob + combined weights (FP32 copies only)
   int max_P = 0, max_mid = 0, max_din = 0, max_dout = 0;
 };
 
@@ -135,6 +137,8 @@ mace_status build_model(const mace_model_desc* desc, Model& m) {
     m.layers.push_back(L);
   }
   m.total = o;
+  m.comb_off = o;
+  m.total_ext = o + 4 * S * K * K;
   return MACE_OK;
 }
 
@@ -156,7 +160,7 @@ struct Buffers {
   unsigned short *wbf = nullptr, *wbfT = nullptr;   // bf16 K-packed copies (BF16-linear mode)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
       *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
-      *tile_count = nullptr, *tile_species = nullptr;
+      *tile_count = nullptr, *tile_species = nullptr, *quad_tile = nullptr, *quad_count = nullptr;
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
@@ -167,6 +171,7 @@ struct Buffers {
         *dY = nullptr, *de = nullptr, *Q = nullptr, *dht = nullptr;
   float *da3p = nullptr, *dYp = nullptr;   // per-channel-tile partials [K/16][E][64], [K/16][E][16]
   float4* g = nullptr;
+  LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 4
 };
 
 int64_t n_tiles_bound(int64_t N, int S) { return (N + kLinTileNodes - 1) / kLinTileNodes + S; }
@@ -174,8 +179,8 @@ int64_t n_tiles_bound(int64_t N, int S) { return (N + kLinTileNodes - 1) / kLinT
 void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   const int64_t K = m.d.K, S = m.d.n_species, T = m.d.n_layers;
   const int nb = m.d.n_bessel;
-  b.w = c.take<float>(m.total);
-  b.wT = c.take<float>(m.total);
+  b.w = c.take<float>(m.total_ext);
+  b.wT = c.take<float>(m.total_ext);
   b.wbf = c.take<unsigned short>(m.total);
   b.wbfT = c.take<unsigned short>(m.total);
   b.sp_table = c.take<float>(S * K);
@@ -191,6 +196,8 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.tile_start = c.take<int>(nt);
   b.tile_count = c.take<int>(nt);
   b.tile_species = c.take<int>(nt);
+  b.quad_tile = c.take<int>(nt);
+  b.quad_count = c.take<int>(nt);
   b.shift = c.take<double4>(std::max<int64_t>(E, 1));
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
@@ -226,6 +233,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.Q = c.take<float>(std::max<int64_t>(E, 1) * m.max_din * K);
   b.dht = c.take<float>(N * m.max_din * K);
   b.g = c.take<float4>(std::max<int64_t>(E, 1));
+  b.lin_dev = c.take<LinLaunch>(6 * T + 4);
 }
 
 }  // namespace
@@ -251,11 +259,11 @@ struct mace_graph {
   Buffers b;
   int64_t N = 0, E = 0;
   int G = 1;
-  int n_tiles = 0;
+  int n_tiles = 0, n_quads = 0;
   mace_precision prec = MACE_FP32;
-  // linear plans per layer
-  std::vector<LinPlan> up, upT, lin, linT, skip_sc, skip_scT, prod, prodT;
-  LinPlan skip0, skip0T;
+  // linear plans per layer (host copy for the grid, device copy for the kernel)
+  std::vector<LinPlanRef> upskip, upskipT, lin, linT, prod, prodT;
+  LinPlanRef skip0, skip0T, comb0, comb0T;
 };
 
 namespace {
@@ -288,11 +296,10 @@ LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, co
   LinPlan p;
   p.cin = cin;
   p.cout = cout;
-  p.species = species;
   p.w_sstride = (int64_t)m.d.K * m.d.K;
   for (int l : ls) {
-    LinGroup g{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1};
-    p.t[p.n_terms++] = LinTerm{l * l, m.off.at(pre + std::to_string(l))};
+    LinGroup g{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1, 0};
+    p.t[p.n_terms++] = LinTerm{l * l, 0, species ? 1 : 0, m.off.at(pre + std::to_string(l))};
     p.g[p.n_groups++] = g;
   }
   return p;
@@ -301,60 +308,132 @@ LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, co
 void make_plans(mace_graph* h) {
   const Model& m = h->m;
   const int T = m.d.n_layers;
-  h->up.resize(T); h->upT.resize(T); h->lin.resize(T); h->linT.resize(T);
-  h->skip_sc.resize(T); h->skip_scT.resize(T); h->prod.resize(T); h->prodT.resize(T);
+  h->upskip.resize(T); h->upskipT.resize(T); h->lin.resize(T); h->linT.resize(T);
+  h->prod.resize(T); h->prodT.resize(T);
+  const int64_t KK = (int64_t)m.d.K * m.d.K;
   for (int t = 0; t < T; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
-    h->up[t] = plan_single_per_l(L.in_ls, pre + "up.", m, L.din, L.din, false);
-    h->upT[t] = h->up[t];
+    std::vector<int> both;   // l in the layer's input and output irreps: residual species linear
+    for (int Lo : L.out_ls)
+      if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end()) both.push_back(Lo);
+    // forward, t >= 1: linear_up (hin -> ht) and the residual species linear
+    // (hin -> sc) read the same input: one launch, two outputs
+    {
+      LinPlan p;
+      p.cin = L.din;
+      p.cout = L.din;
+      p.cout2 = L.dout;
+      p.w_sstride = KK;
+      for (int l : L.in_ls) {
+        p.g[p.n_groups++] = LinGroup{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1, 0};
+        p.t[p.n_terms++] = LinTerm{l * l, 0, 0, m.off.at(pre + "up." + std::to_string(l))};
+      }
+      if (t > 0)
+        for (int l : both) {
+          p.g[p.n_groups++] = LinGroup{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1, 1};
+          p.t[p.n_terms++] = LinTerm{l * l, 0, 1, m.off.at(pre + "skip." + std::to_string(l))};
+        }
+      h->upskip[t].host = make_lin_launch(p);
+    }
+    // backward, t >= 1: dh^t = dE/dht upT + dE/dsc skipT, one output, two inputs
+    {
+      LinPlan p;
+      p.cin = L.din;    // x = dE/dht
+      p.cin2 = L.dout;  // x2 = dE/dsc (the gradient of this layer's output)
+      p.cout = L.din;
+      p.w_sstride = KK;
+      for (int l : L.in_ls) {
+        const int t0 = p.n_terms;
+        p.t[p.n_terms++] = LinTerm{l * l, 0, 0, m.off.at(pre + "up." + std::to_string(l))};
+        if (t > 0 && std::find(both.begin(), both.end(), l) != both.end())
+          p.t[p.n_terms++] = LinTerm{l * l, 1, 1, m.off.at(pre + "skip." + std::to_string(l))};
+        p.g[p.n_groups++] = LinGroup{l * l, 2 * l + 1, t0, p.n_terms, 0};
+      }
+      h->upskipT[t].host = make_lin_launch(p);
+    }
     // path-merging linear: output l collects every path with l_out = l
     LinPlan lp;
     lp.cin = L.mid;
     lp.cout = 16;
     for (int l = 0; l <= 3; ++l) {
-      LinGroup g{l * l, 2 * l + 1, lp.n_terms, lp.n_terms};
+      LinGroup g{l * l, 2 * l + 1, lp.n_terms, lp.n_terms, 0};
       for (int p = 0; p < L.P; ++p)
-        if (L.paths[p].lo == l) lp.t[lp.n_terms++] = LinTerm{L.path_off[p], m.off.at(pre + "linear." + std::to_string(p))};
+        if (L.paths[p].lo == l)
+          lp.t[lp.n_terms++] = LinTerm{L.path_off[p], 0, 0, m.off.at(pre + "linear." + std::to_string(p))};
       g.t1 = lp.n_terms;
       lp.g[lp.n_groups++] = g;
     }
-    h->lin[t] = lp;
+    h->lin[t].host = make_lin_launch(lp);
     LinPlan lt;
     lt.cin = 16;
     lt.cout = L.mid;
     for (int p = 0; p < L.P; ++p) {
       int lo = L.paths[p].lo;
-      lt.g[lt.n_groups++] = LinGroup{L.path_off[p], 2 * lo + 1, lt.n_terms, lt.n_terms + 1};
-      lt.t[lt.n_terms++] = LinTerm{lo * lo, m.off.at(pre + "linear." + std::to_string(p))};
+      lt.g[lt.n_groups++] = LinGroup{L.path_off[p], 2 * lo + 1, lt.n_terms, lt.n_terms + 1, 0};
+      lt.t[lt.n_terms++] = LinTerm{lo * lo, 0, 0, m.off.at(pre + "linear." + std::to_string(p))};
     }
-    h->linT[t] = lt;
-    if (t > 0) {
-      std::vector<int> both;
-      for (int Lo : L.out_ls)
-        if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end()) both.push_back(Lo);
-      h->skip_sc[t] = plan_single_per_l(both, pre + "skip.", m, L.din, L.dout, true);
-      h->skip_scT[t] = plan_single_per_l(both, pre + "skip.", m, L.dout, L.din, true);
-    }
-    h->prod[t] = plan_single_per_l(L.out_ls, pre + "prod.", m, L.dout, L.dout, false);
+    h->linT[t].host = make_lin_launch(lt);
+    h->prod[t].host = make_lin_launch(plan_single_per_l(L.out_ls, pre + "prod.", m, L.dout, L.dout, false));
     h->prodT[t] = h->prod[t];
   }
-  h->skip0 = plan_single_per_l({0, 1, 2, 3}, "0.skip.", m, 16, 16, true);
+  h->skip0.host = make_lin_launch(plan_single_per_l({0, 1, 2, 3}, "0.skip.", m, 16, 16, true));
   h->skip0T = h->skip0;
+  // FP32: layer 0's path-merging linear followed by its species linear is one
+  // species linear with the product weights (one path per l_out at layer 0)
+  {
+    LinPlan p;
+    p.cin = m.layers[0].mid;
+    p.cout = 16;
+    p.w_sstride = KK;
+    for (int l = 0; l <= 3; ++l) {
+      p.g[p.n_groups++] = LinGroup{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1, 0};
+      p.t[p.n_terms++] = LinTerm{l * l, 0, 1, m.comb_off + (int64_t)l * m.d.n_species * KK};
+    }
+    h->comb0.host = make_lin_launch(p);
+    p.cin = 16;
+    p.cout = m.layers[0].mid;
+    h->comb0T.host = make_lin_launch(p);
+  }
 }
 
-LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bool transposed, int accumulate) {
+// copy every plan to the device buffer carved for them; the kernels read it there
+hipError_t upload_plans(mace_graph* h, hipStream_t s) {
+  const int T = h->m.d.n_layers;
+  std::vector<LinPlanRef*> refs;
+  for (int t = 0; t < T; ++t)
+    for (auto* v : {&h->upskip, &h->upskipT, &h->lin, &h->linT, &h->prod, &h->prodT})
+      refs.push_back(&(*v)[t]);
+  for (auto* r : {&h->skip0, &h->skip0T, &h->comb0, &h->comb0T}) refs.push_back(r);
+  std::vector<LinLaunch> host(refs.size());
+  for (size_t q = 0; q < refs.size(); ++q) {
+    host[q] = refs[q]->host;
+    refs[q]->dev = h->b.lin_dev + q;
+  }
+  hipError_t e = hipMemcpyAsync(h->b.lin_dev, host.data(), host.size() * sizeof(LinLaunch), hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(s);
+}
+
+LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bool transposed, int accumulate,
+              const float* x2 = nullptr, float* y2 = nullptr) {
   LinArgs a;
   a.x = x;
   a.y = y;
+  a.x2 = x2;
+  a.y2 = y2;
   a.residual = residual;
   a.w = transposed ? h->b.wT : h->b.w;
+  a.wt = transposed ? h->b.w : h->b.wT;
   a.wbf = transposed ? h->b.wbfT : h->b.wbf;
   a.tile_start = h->b.tile_start;
   a.tile_count = h->b.tile_count;
   a.tile_species = h->b.tile_species;
   a.node_order = h->b.node_order;
   a.n_tiles = h->n_tiles;
+  a.quad_tile = h->b.quad_tile;
+  a.quad_count = h->b.quad_count;
+  a.n_quads = h->n_quads;
   a.K = h->m.d.K;
   a.accumulate = accumulate;
   a.bf16 = h->prec == MACE_BF16_LINEAR;
@@ -407,11 +486,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     } else {
       {
         PROF(KID_LINEAR);
-        launch_linear(s, h->up[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0));
-      }
-      {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->skip_sc[t], largs(h, b.hin[t], b.sc, nullptr, false, 0));
+        launch_linear(s, h->upskip[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0, nullptr, b.sc));
       }
       src = b.ht[t];
       src_map = nullptr;
@@ -421,7 +496,10 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"), b.Y,
                      src, inv_c, b.At);
     }
-    if (t == 0) {
+    if (t == 0 && !bf16) {
+      PROF(KID_LINEAR);
+      launch_linear(s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
+    } else if (t == 0) {   // BF16-linear: each linear rounds its own inputs and weights
       {
         PROF(KID_LINEAR);
         launch_linear(s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
@@ -497,15 +575,18 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
     }
-    const float* dApre = b.dA;
-    if (t == 0) {
-      {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
+    if (t == 0 && !bf16) {
+      PROF(KID_LINEAR);
+      launch_linear(s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
+    } else {
+      const float* dApre = b.dA;
+      if (t == 0) {
+        {
+          PROF(KID_LINEAR);
+          launch_linear(s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
+        }
+        dApre = b.dApre;
       }
-      dApre = b.dApre;
-    }
-    {
       PROF(KID_LINEAR);
       launch_linear(s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
     }
@@ -530,11 +611,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       }
       {
         PROF(KID_LINEAR);
-        launch_linear(s, h->upT[t], largs(h, b.dht, dprev, nullptr, true, 0));
-      }
-      {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->skip_scT[t], largs(h, dnext, dprev, nullptr, true, 1));
+        launch_linear(s, h->upskipT[t], largs(h, b.dht, dprev, nullptr, true, 0, dnext));
       }
       std::swap(dnext, dprev);
     }
@@ -713,6 +790,32 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     }
   }
 
+  // layer 0: path-merging weight of the path into l_out = l times the species
+  // weight of l, W_comb[l][z] = W_lin[p(l)] W_skip[l][z] (FP64 sums, one rounding),
+  // and its transpose, after the blob
+  hw.resize(m.total_ext, 0.f);
+  hwT.resize(m.total_ext, 0.f);
+  {
+    const LayerPlan& L0 = m.layers[0];
+    for (int l = 0; l <= 3; ++l) {
+      int p = -1;
+      for (int q = 0; q < L0.P; ++q)
+        if (L0.paths[q].lo == l) p = q;
+      const float* wl = hw.data() + m.off.at("0.linear." + std::to_string(p));
+      for (int64_t z = 0; z < S; ++z) {
+        const float* ws = hw.data() + m.off.at("0.skip." + std::to_string(l)) + z * K * K;
+        const int64_t base = m.comb_off + ((int64_t)l * S + z) * K * K;
+        for (int64_t k = 0; k < K; ++k)
+          for (int64_t n = 0; n < K; ++n) {
+            double acc = 0.0;
+            for (int64_t j = 0; j < K; ++j) acc += (double)wl[k * K + j] * (double)ws[j * K + n];
+            hw[base + k * K + n] = (float)acc;
+            hwT[base + n * K + k] = (float)acc;
+          }
+      }
+    }
+  }
+
   // bf16 copies of every K x K block, packed [K/8][K][8] (element (k, n) at
   // ((k/8) K + n) 8 + k%8) for the MFMA B operand of the BF16 linears
   std::vector<uint16_t> hbf(m.total, 0), hbfT(m.total, 0);
@@ -744,6 +847,16 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   h->G = G;
   h->prec = prec;
   h->n_tiles = (int)tstart.size();
+  // runs of up to kLinQuad consecutive tiles of one species (one linear block each)
+  std::vector<int32_t> qtile, qcount;
+  for (int t = 0; t < h->n_tiles;) {
+    int n = 1;
+    while (n < kLinQuad && t + n < h->n_tiles && tspec[t + n] == tspec[t]) ++n;
+    qtile.push_back(t);
+    qcount.push_back(n);
+    t += n;
+  }
+  h->n_quads = (int)qtile.size();
   Carver c{reinterpret_cast<char*>(workspace)};
   carve(h->m, N, E, G, c, h->b);
   Buffers& b = h->b;
@@ -752,8 +865,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   };
   hipError_t err = hipSuccess;
   auto chk = [&](hipError_t e) { if (e != hipSuccess && err == hipSuccess) err = e; };
-  chk(up(b.w, hw.data(), m.total * 4));
-  chk(up(b.wT, hwT.data(), m.total * 4));
+  chk(up(b.w, hw.data(), m.total_ext * 4));
+  chk(up(b.wT, hwT.data(), m.total_ext * 4));
   chk(up(b.wbf, hbf.data(), m.total * 2));
   chk(up(b.wbfT, hbfT.data(), m.total * 2));
   chk(up(b.species, hs.data(), N * 4));
@@ -767,6 +880,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(up(b.tile_start, tstart.data(), tstart.size() * 4));
   chk(up(b.tile_count, tcount.data(), tcount.size() * 4));
   chk(up(b.tile_species, tspec.data(), tspec.size() * 4));
+  chk(up(b.quad_tile, qtile.data(), qtile.size() * 4));
+  chk(up(b.quad_count, qcount.data(), qcount.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
                        prec == MACE_BF16_LINEAR, b.sp_table);
@@ -777,6 +892,10 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     return MACE_EHIP;
   }
   make_plans(h);
+  if (upload_plans(h, s) != hipSuccess) {
+    delete h;
+    return MACE_EHIP;
+  }
   *out = h;
   return MACE_OK;
 }

@@ -5,23 +5,20 @@
 
 namespace mace {
 
-// Channel-mixing linear on MFMA. A block is one wave and owns one tile of up
-// to 16 nodes of one species (the 16 MFMA rows), one output component of one
-// group and up to 64 output channels (4 column tiles of 16; blockIdx.z picks
-// which 64); the reduction runs over the input channels of every term of the
-// group. FP32: v_mfma_f32_16x16x4_f32 with A[l%16][l/16], B[l/16][l%16].
+// Channel-mixing linear on MFMA. A block of kLinQuad waves owns up to four
+// 16-node tiles of one species (one per wave, the 16 MFMA rows), one output
+// component of one group and up to 64 output channels (4 column tiles of 16;
+// blockIdx.z picks which 64). For every term of the group the block stages the
+// term's weight panel (64 output columns x K inputs, stored [col][k]) in LDS
+// once for its four tiles; each wave reads its A operand straight from memory
+// as float4 rows and its B operand from LDS as 16-byte reads.
+// FP32: v_mfma_f32_16x16x4_f32 with A[l%16][l/16], B[l/16][l%16]; the K-long
+// reduction runs in the order k = 16 q + 4 s + c (s = l/16 the MFMA's k slot,
+// c the float4 component), so a lane's A values for four MFMAs are one float4.
 // BF16 (inputs and weights rounded to nearest even, FP32 accumulation):
 // v_mfma_f32_16x16x32_bf16 with A[l%16][8(l/16)+i], B[8(l/16)+i][l%16]; the
-// weights come pre-packed as [K/8][K][8] bf16 so a lane's 8 k-values are one
-// 16-byte load. Result register r of lane l holds D[4(l/16)+r][l%16].
-struct LinGC {
-  unsigned char g, c;
-};
-struct LinLaunch {
-  LinPlan plan;
-  LinGC gc[96];
-};
-
+// weights come pre-packed as [K/8][K][8] bf16, i.e. 16-byte runs along k.
+// Result register r of lane l holds D[4(l/16)+r][l%16].
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef unsigned short us8 __attribute__((ext_vector_type(8)));
@@ -33,104 +30,104 @@ __device__ __forceinline__ unsigned short bf16_bits(float x) {
   return (unsigned short)(u >> 16);
 }
 
-constexpr int kLinCt = 4;       // column tiles per wave
-// FP32: the B fragments of all K/4 k-steps are loaded in one batch (K VGPRs
-// per lane at K = 128), so a term costs one memory round trip, not K/32
-template <int K>
-constexpr int lin_ks_batch() { return K / 4; }
+constexpr int kLinCt = 4;   // column tiles per block
 
 template <int K, bool BF16>
-__global__ void __launch_bounds__(64) linear_kernel(LinLaunch L, LinArgs a) {
-  constexpr int ldx = K + 4;    // floats per staged row
-  constexpr int ldb = K + 8;    // bf16 per staged row (16-byte aligned rows)
+__global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* __restrict__ Lp, LinArgs a) {
+  const LinLaunch& L = *Lp;
   static_assert(K % 32 == 0, "K is a multiple of 32");
-  __shared__ __align__(16) float xs[kLinTileNodes * ldx];
-  const int tile = blockIdx.x;
+  constexpr int PF = K + 4;    // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
+  constexpr int PB = K + 8;    // BF16 panel row pitch in bf16 (68 dwords at K = 128)
+  constexpr int kPanel = BF16 ? (64 * PB + 1) / 2 : 64 * PF;
+  __shared__ __align__(16) float sB[kPanel];
+  unsigned short* sBb = reinterpret_cast<unsigned short*>(sB);
   const LinGC gcx = L.gc[blockIdx.y];
   const LinGroup grp = L.plan.g[gcx.g];
   const int c = gcx.c;
   const int ct0 = blockIdx.z * kLinCt;
   constexpr int nct = K / 16;
-  const int l = threadIdx.x;
+  const int ncol = min(64, K - 16 * ct0);   // valid panel columns (K = 32 or 96: the last 64 are partial)
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int quad = blockIdx.x;
+  const int tile0 = a.quad_tile[quad], ntile = a.quad_count[quad];
+  const int tile = tile0 + min(w, ntile - 1);   // spare waves shadow a valid tile and store nothing
+  const bool active = w < ntile;
   const int t0 = a.tile_start[tile], cnt = a.tile_count[tile];
-  const int z = a.tile_species[tile];
-  const int cin = L.plan.cin, cout = L.plan.cout;
-  unsigned short* xb = reinterpret_cast<unsigned short*>(xs);
-  const int64_t zoff = L.plan.species ? (int64_t)z * L.plan.w_sstride : 0;
+  const int z = a.tile_species[tile0];
+  const int64_t zstride = (int64_t)z * L.plan.w_sstride;
+  // A rows: node of MFMA row l%16 (rows past the tile's count re-read its
+  // last node and are zeroed)
+  const int node = a.node_order[t0 + min(l & 15, cnt - 1)];
+  const float keep = (l & 15) < cnt ? 1.f : 0.f;
   f4 acc[kLinCt];
 #pragma unroll
   for (int j = 0; j < kLinCt; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
   for (int tm = grp.t0; tm < grp.t1; ++tm) {
     const LinTerm term = L.plan.t[tm];
-    if (tm > grp.t0) __syncthreads();
-    // stage the tile's 16 input rows. Node indices are wave-uniform (scalar
-    // loads); rows past the tile's count re-read its last node and are zeroed
-    // by a select, so no load sits behind a branch and all 16 x K/64 row
-    // loads are in flight together.
-    {
-      constexpr int H = (K + 63) / 64;
-      float v[kLinTileNodes][H];
-#pragma unroll
-      for (int q = 0; q < kLinTileNodes; ++q) {
-        const int node = a.node_order[t0 + min(q, cnt - 1)];
-        const float* row = a.x + ((size_t)node * cin + term.in_c0 + c) * K;
-#pragma unroll
-        for (int h = 0; h < H; ++h) v[q][h] = row[min(l + 64 * h, K - 1)];
-      }
-#pragma unroll
-      for (int q = 0; q < kLinTileNodes; ++q)
-#pragma unroll
-        for (int h = 0; h < H; ++h) {
-          const int kk = l + 64 * h;
-          const float x = q < cnt ? v[q][h] : 0.f;
-          if (kk < K) {
-            if constexpr (BF16) xb[q * ldb + kk] = bf16_bits(x);
-            else xs[q * ldx + kk] = x;
-          }
-        }
-    }
-    // column tiles past K/16 (K = 32 or 96) load a valid tile and their
-    // results are never stored: no branch around loads or MFMAs
-    int ctc[kLinCt];
-#pragma unroll
-    for (int j = 0; j < kLinCt; ++j) ctc[j] = min(ct0 + j, nct - 1);
+    const int64_t zoff = term.species ? zstride : 0;
+    const float* xrow = term.src ? a.x2 + ((size_t)node * L.plan.cin2 + term.in_c0 + c) * K
+                                 : a.x + ((size_t)node * L.plan.cin + term.in_c0 + c) * K;
+    // A operand first, so that its loads overlap the panel staging
+    f4 av[BF16 ? 1 : K / 16];
+    us8 ab[BF16 ? K / 32 : 1];
     if constexpr (!BF16) {
-      const float* W = a.w + term.w_off + zoff + (l >> 4) * K + (l & 15);
 #pragma unroll
-      for (int kb = 0; kb < K / 4; kb += lin_ks_batch<K>()) {
-        constexpr int nb = lin_ks_batch<K>();
-        float bv[nb][kLinCt];
+      for (int q = 0; q < K / 16; ++q) av[q] = *reinterpret_cast<const f4*>(xrow + 16 * q + 4 * (l >> 4)) * keep;
+    } else {
 #pragma unroll
-        for (int ks = 0; ks < nb; ++ks)
-#pragma unroll
-          for (int j = 0; j < kLinCt; ++j) bv[ks][j] = W[(size_t)(4 * (kb + ks)) * K + 16 * ctc[j]];
-        if (kb == 0) __syncthreads();
-#pragma unroll
-        for (int ks = 0; ks < nb; ++ks) {
-          const float av = xs[(l & 15) * ldx + 4 * (kb + ks) + (l >> 4)];
-#pragma unroll
-          for (int j = 0; j < kLinCt; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[ks][j], acc[j], 0, 0, 0);
-        }
+      for (int ks = 0; ks < K / 32; ++ks) {
+        const f4 lo = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4)) * keep;
+        const f4 hi = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4) + 4) * keep;
+        us8 v;
+        v[0] = bf16_bits(lo[0]); v[1] = bf16_bits(lo[1]); v[2] = bf16_bits(lo[2]); v[3] = bf16_bits(lo[3]);
+        v[4] = bf16_bits(hi[0]); v[5] = bf16_bits(hi[1]); v[6] = bf16_bits(hi[2]); v[7] = bf16_bits(hi[3]);
+        ab[ks] = v;
+      }
+    }
+    __syncthreads();   // the previous term's MFMAs have read the panel
+    if constexpr (!BF16) {
+      // panel row = output column n: the transposed blob holds W^T[n][0..K) contiguous
+      const float* Wt = a.wt + term.w_off + zoff;
+      for (int idx = tid; idx < 64 * (K / 4); idx += blockDim.x) {
+        const int col = idx / (K / 4), k4 = idx % (K / 4);
+        const int n = 16 * ct0 + min(col, ncol - 1);
+        *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = *reinterpret_cast<const f4*>(Wt + (size_t)n * K + 4 * k4);
       }
     } else {
+      // packed [K/8][K][8]: 8 consecutive k of output column n are 16 contiguous bytes
       const unsigned short* Wp = a.wbf + term.w_off + zoff;
-      us8 bq[K / 32][kLinCt];
+      for (int idx = tid; idx < 64 * (K / 8); idx += blockDim.x) {
+        const int col = idx / (K / 8), kc = idx % (K / 8);
+        const int n = 16 * ct0 + min(col, ncol - 1);
+        *reinterpret_cast<us8*>(sBb + col * PB + 8 * kc) =
+            *reinterpret_cast<const us8*>(Wp + ((size_t)kc * K + n) * 8);
+      }
+    }
+    __syncthreads();
+    if constexpr (!BF16) {
+#pragma unroll
+      for (int q = 0; q < K / 16; ++q)
+#pragma unroll
+        for (int j = 0; j < kLinCt; ++j) {
+          const f4 b = *reinterpret_cast<const f4*>(sB + (16 * j + (l & 15)) * PF + 16 * q + 4 * (l >> 4));
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[q][cc], b[cc], acc[j], 0, 0, 0);
+        }
+    } else {
 #pragma unroll
       for (int ks = 0; ks < K / 32; ++ks)
 #pragma unroll
-        for (int j = 0; j < kLinCt; ++j)
-          bq[ks][j] = *reinterpret_cast<const us8*>(Wp + ((size_t)(4 * ks + (l >> 4)) * K + 16 * ctc[j] + (l & 15)) * 8);
-      __syncthreads();
-#pragma unroll
-      for (int ks = 0; ks < K / 32; ++ks) {
-        const us8 av = *reinterpret_cast<const us8*>(xb + (l & 15) * ldb + 32 * ks + 8 * (l >> 4));
-#pragma unroll
-        for (int j = 0; j < kLinCt; ++j)
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, av), __builtin_bit_cast(bf8, bq[ks][j]),
+        for (int j = 0; j < kLinCt; ++j) {
+          const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, ab[ks]), __builtin_bit_cast(bf8, b),
                                                            acc[j], 0, 0, 0);
-      }
+        }
     }
   }
+  if (!active) return;
+  float* y = grp.dst ? a.y2 : a.y;
+  const int cout = grp.dst ? L.plan.cout2 : L.plan.cout;
+  const float* residual = grp.dst ? nullptr : a.residual;
 #pragma unroll
   for (int j = 0; j < kLinCt; ++j) {
     const int ct = ct0 + j;
@@ -141,26 +138,32 @@ __global__ void __launch_bounds__(64) linear_kernel(LinLaunch L, LinArgs a) {
       if (q >= cnt) continue;
       const size_t o = ((size_t)a.node_order[t0 + q] * cout + grp.out_c0 + c) * K + 16 * ct + (l & 15);
       float v = acc[j][r];
-      if (a.residual) v += a.residual[o];
-      if (a.accumulate) v += a.y[o];
-      a.y[o] = v;
+      if (residual) v += residual[o];
+      if (a.accumulate) v += y[o];
+      y[o] = v;
     }
   }
 }
 
-void launch_linear(hipStream_t s, const LinPlan& plan, const LinArgs& a) {
-  if (a.n_tiles <= 0 || plan.n_groups <= 0) return;
+LinLaunch make_lin_launch(const LinPlan& plan) {
   LinLaunch L;
   L.plan = plan;
   int n = 0;
   for (int g = 0; g < plan.n_groups; ++g)
-    for (int c = 0; c < plan.g[g].ncomp; ++c) {
+    for (int c = 0; c < plan.g[g].ncomp && n < kMaxLinGC; ++c) {
       L.gc[n].g = (unsigned char)g;
       L.gc[n].c = (unsigned char)c;
       ++n;
     }
+  L.n_gc = n;
+  return L;
+}
+
+void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
+  if (a.n_quads <= 0 || P.host.plan.n_groups <= 0 || !P.dev) return;
+  const LinLaunch* L = P.dev;
   const int halves = (a.K / 16 + kLinCt - 1) / kLinCt;
-  dim3 grid(a.n_tiles, n, halves), block(64);
+  dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
 #define MACE_LIN(KK)                                                        \
   case KK:                                                                 \
     if (a.bf16) linear_kernel<KK, true><<<grid, block, 0, s>>>(L, a);      \

@@ -9,7 +9,8 @@ namespace mace {
 
 constexpr int kMaxTerms = 48;
 constexpr int kMaxGroups = 24;
-constexpr int kLinTileNodes = 16;   // nodes per block of the channel-mixing linear
+constexpr int kLinTileNodes = 16;   // nodes per MFMA tile of the channel-mixing linear
+constexpr int kLinQuad = 4;         // node tiles (one per wave) per block of the linear
 
 // ----------------------------------------------------------------- numerics
 __host__ __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
@@ -214,32 +215,60 @@ __device__ __forceinline__ void edge_geometry(int e, const float* __restrict__ p
 // --------------------------------------------------------------- launchers
 struct LinTerm {
   int in_c0;          // first input component of this term
+  int src;            // 0: input x, 1: input x2
+  int species;        // weights depend on the node's species (stride w_sstride)
   int64_t w_off;      // float offset of the K x K weight (species 0)
 };
 struct LinGroup {
   int out_c0, ncomp;  // output components [out_c0, out_c0 + ncomp)
   int t0, t1;         // terms [t0, t1) accumulate into this output
+  int dst;            // 0: output y, 1: output y2
 };
 struct LinPlan {
   int n_groups = 0, n_terms = 0;
   LinGroup g[kMaxGroups];
   LinTerm t[kMaxTerms];
-  int species = 0;          // weights depend on the node's species
   int64_t w_sstride = 0;    // float stride between species blocks
-  int cin = 0, cout = 0;    // components per node of input / output arrays
+  int cin = 0, cout = 0;    // components per node of x / y
+  int cin2 = 0, cout2 = 0;  // components per node of x2 / y2
 };
+
+// One output component of one group: the unit of blockIdx.y of the linear.
+struct LinGC {
+  unsigned char g, c;
+};
+constexpr int kMaxLinGC = 96;
+// What a linear launch reads besides its LinArgs. Kept in device memory
+// (written once at graph setup) rather than passed by value: at about 1.4 KB
+// it would make every wave fetch its plan from the kernel-argument segment.
+struct LinLaunch {
+  LinPlan plan;
+  LinGC gc[kMaxLinGC];
+  int n_gc = 0;
+};
+// host copy (grid shape) and device copy (read by the kernel) of one plan
+struct LinPlanRef {
+  LinLaunch host;
+  const LinLaunch* dev = nullptr;
+};
+LinLaunch make_lin_launch(const LinPlan& plan);
 
 struct LinArgs {
   const float* x;           // [N][cin][K]
   float* y;                 // [N][cout][K]
-  const float* residual;    // [N][cout][K] or null, added to every written comp
+  const float* x2;          // [N][cin2][K] (terms with src 1) or null
+  float* y2;                // [N][cout2][K] (groups with dst 1) or null
+  const float* residual;    // [N][cout][K] or null, added to every comp written to y
   const float* w;           // weight base (FP32, row-major [in][out])
+  const float* wt;          // the same blob with every K x K block transposed ([out][in])
   const unsigned short* wbf;  // same tensors as bf16, each K x K block packed [K/8][K][8]
   const int* tile_start;    // [n_tiles] start in node_order
   const int* tile_count;    // [n_tiles]
   const int* tile_species;  // [n_tiles]
   const int* node_order;    // nodes grouped by species
-  int n_tiles;
+  const int* quad_tile;     // [n_quads] first tile of a run of <= kLinQuad tiles of one species
+  const int* quad_count;    // [n_quads] tiles in the run
+  int n_tiles, n_quads;
   int K;
   int accumulate;           // y += instead of y =
   int bf16;                 // round x and w to bf16 before multiplying
@@ -277,7 +306,7 @@ void launch_symcon_fwd(hipStream_t s, int lout_max, int N, int K, const int* spe
                        SymW w, float* B);
 void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
                        SymW w, const float* dB, float* dA);
-void launch_linear(hipStream_t s, const LinPlan& plan, const LinArgs& a);
+void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
                         const float* w1, const float* w2, int hidden, int bf16, int accumulate, float* eps);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
