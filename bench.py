@@ -213,6 +213,40 @@ def main():
                  "algorithmic_flops_per_launch": int(flops_per_launch),
                  "kernel_share_of_step": round(k_ms / total_ms, 4)})
 
+    # outside the timed region: per-call spread, the forward pass alone, and
+    # the other precision mode on the same workload
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in evs:
+        a.record(stream)
+        B.mace_forces(g.handle, pos, eps, Eg, F, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    per_call = np.array([a.elapsed_time(b) for a, b in evs])
+    f0 = torch.cuda.Event(enable_timing=True)
+    f1 = torch.cuda.Event(enable_timing=True)
+    for _ in range(args.warmup):
+        B.mace_forward_energy(g.handle, pos, eps, Eg, stream)
+    f0.record(stream)
+    for _ in range(args.steps):
+        B.mace_forward_energy(g.handle, pos, eps, Eg, stream)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fwd_ms = f0.elapsed_time(f1) / args.steps
+    other = B.MACE_BF16_LINEAR if prec == B.MACE_FP32 else B.MACE_FP32
+    g2 = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                   sh if periodic else None, sysm.cells if periodic else None,
+                   sysm.graph_of_atom.astype(np.int32) if sysm.n_graphs > 1 else None, sysm.n_graphs, other)
+    eps2, Eg2, F2 = g2.outputs(True)
+    for _ in range(args.warmup):
+        B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
+    f0.record(stream)
+    for _ in range(args.steps):
+        B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    other_ms = f0.elapsed_time(f1) / args.steps
+    g2.close()
+
     out = {
         "metric": "atoms/s and edges/s for MACE energy+forces (FP32, BF16-linear); % roofline",
         "value": round(N * args.steps / (total_ms * 1e-3), 1),
@@ -226,6 +260,11 @@ def main():
                    "hidden_lmax": params["hidden_lmax"], "r_cut": params["r_cut"], "correlation": 3,
                    "layers": 2, "precision": args.prec},
         "roofline": roof,
+        "step_ms_p10_p50_p90": [round(float(np.percentile(per_call, q)), 4) for q in (10, 50, 90)],
+        "forward_only": {"atoms_per_s": round(N / (fwd_ms * 1e-3), 1), "ms": round(fwd_ms, 4)},
+        ("bf16_linear" if other == B.MACE_BF16_LINEAR else "fp32"): {
+            "atoms_per_s": round(N / (other_ms * 1e-3), 1), "edges_per_s": round(E / (other_ms * 1e-3), 1),
+            "ms_per_step": round(other_ms, 4)},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params)

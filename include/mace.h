@@ -119,6 +119,18 @@ mace_status mace_forward_energy(mace_graph* g, const float* positions, float* no
 mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                         float* forces, void* stream);
 
+/* Energies, forces and the stress of every graph (the pressure of the paper's
+ * NPT metrics is p = -tr(sigma)/3). stress (dev) [G][3][3] FP64 row-major:
+ * sigma_g[a][b] = (1/V_g) dE_g/d(epsilon_ab) for a homogeneous strain acting
+ * on row vectors, x -> x (I + epsilon), applied to the graph's positions and
+ * cell rows; equivalently (1/V_g) sum over the graph's edges of d_e[a] g_e[b]
+ * with d_e the edge vector and g_e = dE/dd_e. V_g = |det cell_g|; for a
+ * handle set up without cells V = 1 (the bare strain derivative). Summed in
+ * FP64 in a fixed order (bitwise reproducible). Other arguments and behaviour
+ * as mace_forces. */
+mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                               float* forces, double* stress, void* stream);
+
 /* Releases the host handle (the workspace stays the caller's). */
 void mace_graph_destroy(mace_graph* g);
 

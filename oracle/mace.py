@@ -41,6 +41,10 @@ R11 BF16-linear mode (emulation): inputs and weights of the channel-mixing
     linears (linear_up, path-merging linear, species linears, product linear,
     readout linears) rounded to bfloat16 (round to nearest even); all sums
     and every other step in FP64.
+R12 Stress: the NPT metrics paragraph takes the pressure as -tr(sigma)/3 and
+    does not define sigma. Here sigma = (1/V) dE/d(epsilon) for a homogeneous
+    strain acting on row vectors, x -> x (I + epsilon), on positions and cell
+    rows alike; V = |det cell|, or 1 for a graph without a cell.
 """
 from __future__ import annotations
 
@@ -349,3 +353,39 @@ def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = 
         F = -g if g is not None else torch.zeros_like(pos)
     return {"eps": eps.detach().numpy(), "energy": Eg.detach().numpy(),
             "forces": None if F is None else F.numpy(), "graph": graph}
+
+
+def stress(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
+           bf16_linear: bool = False):
+    """Stress of every graph, sigma_g = (1/V_g) dE_g/d(epsilon_g) [G,3,3].
+
+    The pressure of the NPT metrics paragraph is p = -tr(sigma)/3. A
+    homogeneous strain epsilon acts on row vectors, x -> x (I + epsilon), on
+    the positions of the graph's atoms and on the rows of its cell (so every
+    periodic shift S.cell transforms the same way); the derivative is taken
+    at epsilon = 0 by autograd. V_g = |det cell_g|; a graph without a cell
+    gets V = 1, i.e. the bare strain derivative.
+    """
+    W = unpack_weights(d, blob)
+    if graph is None:
+        graph = build_graph(system, d)
+    G = graph.n_graphs
+    strain = torch.zeros(G, 3, 3, dtype=DT, requires_grad=True)
+    Fm = torch.eye(3, dtype=DT)[None] + strain                           # [G,3,3]
+    pos0 = torch.tensor(system.positions, dtype=DT)
+    pos = torch.einsum("na,nab->nb", pos0, Fm[graph.graph_of_atom])
+    g_edge = graph.graph_of_atom[graph.receiver]
+    shifted = Graph(graph.sender, graph.receiver, torch.einsum("ea,eab->eb", graph.shift_vec, Fm[g_edge]),
+                    graph.species, graph.graph_of_atom, graph.n_graphs)
+    eps = node_energies(d, W, shifted, pos, bf16_linear=bf16_linear)
+    Eg = graph_energies(eps, graph)
+    dE = None
+    if Eg.requires_grad:
+        (dE,) = torch.autograd.grad(Eg.sum(), strain, allow_unused=True)
+    dE = torch.zeros(G, 3, 3, dtype=DT) if dE is None else dE.detach()
+    if system.cells is not None:
+        vol = torch.tensor([abs(np.linalg.det(np.asarray(c, dtype=np.float64))) for c in system.cells], dtype=DT)
+    else:
+        vol = torch.ones(G, dtype=DT)
+    return (dE / vol[:, None, None]).numpy()
+

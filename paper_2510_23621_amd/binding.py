@@ -21,7 +21,7 @@ STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 
 EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", "mace_graph_setup",
-            "mace_forward_energy", "mace_forces", "mace_graph_destroy", "mace_status_string",
+            "mace_forward_energy", "mace_forces", "mace_forces_stress", "mace_graph_destroy", "mace_status_string",
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name"]
 
@@ -69,6 +69,7 @@ def lib() -> ctypes.CDLL:
         L.mace_graph_setup.argtypes = [dp, P, I64, I64, P, I64, P, P, P, P, I32, I32, P, Z, P, P]
         L.mace_forward_energy.argtypes = [P, P, P, P, P]
         L.mace_forces.argtypes = [P, P, P, P, P, P]
+        L.mace_forces_stress.argtypes = [P, P, P, P, P, P, P]
         L.mace_graph_destroy.argtypes = [P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
@@ -174,6 +175,11 @@ def mace_forward_energy(handle, positions, node_energy, graph_energy, stream=Non
 def mace_forces(handle, positions, node_energy, graph_energy, forces, stream=None):
     _check(lib().mace_forces(handle, _ptr(positions), _ptr(node_energy), _ptr(graph_energy), _ptr(forces),
                              _stream(stream)), "mace_forces")
+
+
+def mace_forces_stress(handle, positions, node_energy, graph_energy, forces, stress, stream=None):
+    _check(lib().mace_forces_stress(handle, _ptr(positions), _ptr(node_energy), _ptr(graph_energy), _ptr(forces),
+                                    _ptr(stress), _stream(stream)), "mace_forces_stress")
 
 
 def mace_graph_destroy(handle):

@@ -171,6 +171,7 @@ struct Buffers {
         *dY = nullptr, *de = nullptr, *Q = nullptr, *dht = nullptr;
   float *da3p = nullptr, *dYp = nullptr;   // per-channel-tile partials [K/16][E][64], [K/16][E][16]
   float4* g = nullptr;
+  double* inv_vol = nullptr;      // [G] 1/|det cell|, or 1 without cells
   LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 4
 };
 
@@ -233,6 +234,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.Q = c.take<float>(std::max<int64_t>(E, 1) * m.max_din * K);
   b.dht = c.take<float>(N * m.max_din * K);
   b.g = c.take<float4>(std::max<int64_t>(E, 1));
+  b.inv_vol = c.take<double>(G);
   b.lin_dev = c.take<LinLaunch>(6 * T + 4);
 }
 
@@ -876,6 +878,15 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(up(b.snd_off, snd_off.data(), (N + 1) * 4));
   chk(up(b.snd_perm, snd_perm.data(), E * 4));
   chk(up(b.graph_off, goff.data(), (G + 1) * 4));
+  std::vector<double> inv_vol(G, 1.0);
+  if (cells)
+    for (int gi = 0; gi < G; ++gi) {
+      const double* c = hc.data() + 9 * gi;
+      const double det = c[0] * (c[4] * c[8] - c[5] * c[7]) - c[1] * (c[3] * c[8] - c[5] * c[6]) +
+                         c[2] * (c[3] * c[7] - c[4] * c[6]);
+      inv_vol[gi] = det != 0.0 ? 1.0 / std::fabs(det) : 0.0;
+    }
+  chk(up(b.inv_vol, inv_vol.data(), G * 8));
   chk(up(b.node_order, order.data(), N * 4));
   chk(up(b.tile_start, tstart.data(), tstart.size() * 4));
   chk(up(b.tile_count, tcount.data(), tcount.size() * 4));
@@ -924,6 +935,21 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
     launch_graph_energy(s, g->G, g->b.graph_off, node_energy, graph_energy);
   }
   run_backward(g, s, positions, forces);
+  return hip_ok(hipGetLastError());
+}
+
+mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+                               float* forces, double* stress, void* stream) {
+  if (!g || !positions || !node_energy || !graph_energy || !forces || !stress) return MACE_EINVAL;
+  mace_status st = mace_forces(g, positions, node_energy, graph_energy, forces, stream);
+  if (st != MACE_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  {
+    mace_graph* h = g;
+    PROF(KID_FORCES);
+    launch_stress(s, g->G, g->b.graph_off, g->b.rcv_off, positions, g->b.snd, g->b.rcv, g->b.shift, g->b.g,
+                  g->b.inv_vol, stress);
+  }
   return hip_ok(hipGetLastError());
 }
 

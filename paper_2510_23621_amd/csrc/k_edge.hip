@@ -66,6 +66,55 @@ __global__ void fill_kernel(float* p, size_t n, float v) {
   for (; i < n; i += stride) p[i] = v;
 }
 
+// stress[gi][a][b] = inv_vol[gi] * sum over the graph's edges of d_e[a] g_e[b]
+// (d_e = x_snd - x_rcv + shift in FP64). One block per graph; the graph's
+// edges are contiguous (atoms are grouped by graph, edges by receiver).
+// FP64 partial sums per thread in edge order, then a fixed tree: bitwise
+// reproducible.
+__global__ void __launch_bounds__(256) stress_kernel(int G, const int* __restrict__ graph_off,
+                                                     const int* __restrict__ rcv_off, const float* __restrict__ pos,
+                                                     const int* __restrict__ snd, const int* __restrict__ rcv,
+                                                     const double4* __restrict__ shift,
+                                                     const float4* __restrict__ g, const double* __restrict__ inv_vol,
+                                                     double* __restrict__ stress) {
+  __shared__ double red[9][256];
+  const int gi = blockIdx.x, t = threadIdx.x;
+  const int e_beg = rcv_off[graph_off[gi]], e_end = rcv_off[graph_off[gi + 1]];
+  double acc[9];
+#pragma unroll
+  for (int c = 0; c < 9; ++c) acc[c] = 0.0;
+  for (int e = e_beg + t; e < e_end; e += blockDim.x) {
+    const int s = snd[e], r = rcv[e];
+    const double4 sh = shift[e];
+    const double d[3] = {((double)pos[3 * s + 0] - (double)pos[3 * r + 0]) + sh.x,
+                         ((double)pos[3 * s + 1] - (double)pos[3 * r + 1]) + sh.y,
+                         ((double)pos[3 * s + 2] - (double)pos[3 * r + 2]) + sh.z};
+    const float4 gv = g[e];
+    const double gg[3] = {gv.x, gv.y, gv.z};
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+      for (int b = 0; b < 3; ++b) acc[3 * a + b] += d[a] * gg[b];
+  }
+#pragma unroll
+  for (int c = 0; c < 9; ++c) red[c][t] = acc[c];
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (t < st)
+#pragma unroll
+      for (int c = 0; c < 9; ++c) red[c][t] += red[c][t + st];
+    __syncthreads();
+  }
+  if (t < 9) stress[(size_t)gi * 9 + t] = red[t][0] * inv_vol[gi];
+}
+
+void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
+                   const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
+                   double* stress) {
+  if (G <= 0) return;
+  stress_kernel<<<G, 256, 0, s>>>(G, graph_off, rcv_off, pos, snd, rcv, shift, g, inv_vol, stress);
+}
+
 void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv, const double4* shift,
                      double rc, int p, int nb, const float* dY, const float* de, float4* g) {
   if (E <= 0) return;

@@ -289,6 +289,9 @@ void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off,
                    const float4* g, float* F);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate);
+void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
+                   const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
+                   double* stress);
 void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv, const double4* shift,
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,

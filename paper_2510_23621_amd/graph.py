@@ -60,6 +60,13 @@ class MaceGraph:
         B.mace_forces(self.handle, pos, eps, E, F, stream)
         return eps, E, F
 
+    def energy_forces_stress(self, positions, stream=None):
+        pos = positions.to(device=self.device, dtype=torch.float32).contiguous()
+        eps, E, F = self.outputs(True)
+        S = torch.empty(self.n_graphs, 3, 3, dtype=torch.float64, device=self.device)
+        B.mace_forces_stress(self.handle, pos, eps, E, F, S, stream)
+        return eps, E, F, S
+
     def close(self):
         if getattr(self, "handle", None):
             B.mace_graph_destroy(self.handle)

@@ -27,7 +27,7 @@ def oracle_blob(params: dict, seed: int, gains=None) -> np.ndarray:
     return synth.weight_blob(mace.weight_layout(mace.ModelDesc(**params)), seed, gains)
 
 
-def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1):
+def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1, stress=False):
     desc = B.make_desc(**params)
     snd, rcv, sh = B.mace_neighbor_list(system.positions, params["r_cut"], system.cells, system.graph_of_atom,
                                         system.n_graphs)
@@ -39,19 +39,32 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
     outs = []
     for _ in range(repeats):
-        if forces:
+        S = None
+        if stress:
+            eps, E, F, S = g.energy_forces_stress(pos)
+        elif forces:
             eps, E, F = g.energy_forces(pos)
         else:
             (eps, E), F = g.energy(pos), None
         torch.cuda.synchronize()
         outs.append(dict(eps=eps.cpu().numpy().astype(np.float64), energy=E.cpu().numpy(),
-                         forces=None if F is None else F.cpu().numpy().astype(np.float64), n_edges=len(snd)))
+                         forces=None if F is None else F.cpu().numpy().astype(np.float64), n_edges=len(snd),
+                         stress=None if S is None else S.cpu().numpy()))
     g.close()
     return outs if repeats > 1 else outs[0]
 
 
 def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True):
     return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16, forces=forces)
+
+
+def oracle_stress(params: dict, system, blob: np.ndarray, bf16=False):
+    return mace.stress(mace.ModelDesc(**params), blob, system, bf16_linear=bf16)
+
+
+def stress_error(gpu_stress: np.ndarray, ref_stress: np.ndarray) -> float:
+    """Relative Frobenius error over all graphs (the stress tolerance is the force one)."""
+    return float(np.linalg.norm(gpu_stress - ref_stress) / max(np.linalg.norm(ref_stress), 1e-300))
 
 
 def errors(gpu: dict, ref: dict) -> dict:

@@ -6,8 +6,9 @@
   the oracle evaluated on a cluster cut of radius 2 r_c + margin around the
   atom (eps_i depends only on atoms within 2 r_c: layer 1 sums h^(1) of
   neighbours, which sum their own neighbours), plus properties that hold at
-  any size: sum F = 0, rotation covariance of the whole periodic box,
-  determinism, BF16-linear vs FP32.
+  any size: sum F = 0, rotation covariance of the whole periodic box (forces
+  and stress), determinism, BF16-linear vs FP32.
+* 1536-atom water also checks the stress against the oracle.
 * 512-molecule batch: sampled molecules are whole graphs, so their energy
   and forces are compared exactly.
 """
@@ -21,8 +22,8 @@ from synth.configs import CONFIGS, make_system, model_params
 pytestmark = pytest.mark.gpu
 
 B = pytest.importorskip("paper_2510_23621_amd.binding")
-from gpu_common import (TOL, assert_parity, cluster_cut, errors, lib_blob, oracle_blob, run_gpu,  # noqa: E402
-                        run_oracle)
+from gpu_common import (TOL, assert_parity, cluster_cut, errors, lib_blob, oracle_blob, oracle_stress,  # noqa: E402
+                        run_gpu, run_oracle, stress_error)
 from oracle import so3  # noqa: E402
 
 PER_ATOM_TOL = {B.MACE_FP32: 2e-5, B.MACE_BF16_LINEAR: 5e-2}
@@ -59,9 +60,13 @@ def cfg1():
 
 def test_cfg1_full_fp32(cfg1):
     params, sysm, blob, ref = cfg1
-    gpu = run_gpu(params, sysm, blob)
+    gpu = run_gpu(params, sysm, blob, stress=True)
     assert gpu["n_edges"] == len(ref["graph"].sender)
     assert_parity(gpu, ref, B.MACE_FP32, "water1536 full")
+    sref = oracle_stress(params, sysm, blob)
+    err = stress_error(gpu["stress"], sref)
+    print(f"[fullsize] water1536 stress rel {err:.3e} (pressure {-np.trace(sref[0]) / 3:.4e})", flush=True)
+    assert err <= TOL[B.MACE_FP32]["forces"]
 
 
 def test_cfg1_full_bf16(cfg1):
@@ -97,11 +102,15 @@ def test_large_water_sampled_and_properties(cfg):
     # rotation covariance of the whole box (GPU against GPU)
     R = so3.random_rotation(np.random.default_rng(100 + cfg))
     rot = _rotate(sysm, R)
-    g_rot = run_gpu(params, rot, blob)
+    g_rot = run_gpu(params, rot, blob, stress=True)
     e_err = np.abs(g_rot["energy"] - g32["energy"]).max() / np.abs(g32["eps"]).sum()
     f_err = np.linalg.norm(g_rot["forces"] - F @ R.T) / np.linalg.norm(F)
-    print(f"[fullsize] water{N} rotation: energy {e_err:.2e} forces {f_err:.2e}", flush=True)
+    # stress is a rank-2 tensor: sigma(x R^T) = R sigma R^T
+    s32 = run_gpu(params, sysm, blob, stress=True)["stress"]
+    s_err = stress_error(g_rot["stress"], R @ s32 @ R.T)
+    print(f"[fullsize] water{N} rotation: energy {e_err:.2e} forces {f_err:.2e} stress {s_err:.2e}", flush=True)
     assert e_err <= 2 * TOL[B.MACE_FP32]["energy"] and f_err <= 2 * TOL[B.MACE_FP32]["forces"]
+    assert s_err <= 2 * TOL[B.MACE_FP32]["forces"]
     # BF16-linear against FP32 at full size
     g16 = run_gpu(params, sysm, blob, prec=B.MACE_BF16_LINEAR)
     err = errors(g16, g32)

@@ -14,8 +14,9 @@ from synth.configs import CONFIGS, make_system, model_params
 pytestmark = pytest.mark.gpu
 
 B = pytest.importorskip("paper_2510_23621_amd.binding")
-from gpu_common import (STRESS, STRESS_GAINS, TOL, assert_parity, errors, lib_blob, oracle_blob,  # noqa: E402
-                        run_gpu, run_oracle)
+from gpu_common import (  # noqa: E402
+    STRESS, STRESS_GAINS, TOL, assert_parity, errors, lib_blob, oracle_blob, oracle_stress, run_gpu, run_oracle,
+    stress_error)
 
 
 @pytest.fixture(autouse=True, scope="module")
@@ -140,3 +141,34 @@ def test_forces_sum_to_zero_on_gpu():
     gpu = run_gpu(params, sysm, bl)
     F = gpu["forces"]
     assert np.abs(F.sum(0)).max() <= 1e-4 * np.abs(F).max() * np.sqrt(len(F))
+
+
+@pytest.mark.parametrize("case", ["water96_nominal", "water96_stress_inputs", "molecules12"])
+def test_stress_against_oracle(case):
+    """Per-graph stress sigma = (1/V) dE/d(epsilon) (the oracle by autograd
+    through a homogeneous strain) at the force tolerance; a batch of
+    molecules (no cell, V = 1) checks the per-graph segmentation. FP32 is
+    compared with the FP64 oracle; BF16-linear with the oracle's BF16
+    emulation (a pressure is a small residual of large edge terms, so the
+    model's own BF16 deviation from FP64 can exceed the force tolerance)."""
+    if case == "molecules12":
+        params = model_params(4, K=64, **STRESS)
+        sysm = synth.molecule_batch(12, seed=2)
+        gains = STRESS_GAINS
+    else:
+        params = model_params(0) if case == "water96_nominal" else model_params(0, **STRESS)
+        sysm = make_system(0, seed=0)
+        gains = None if case == "water96_nominal" else STRESS_GAINS
+    bo = oracle_blob(params, 6, gains)
+    bl = lib_blob(params, 6, gains)
+    ref64 = oracle_stress(params, sysm, bo)
+    ref16 = oracle_stress(params, sysm, bo, bf16=True)
+    for prec, ref in ((B.MACE_FP32, ref64), (B.MACE_BF16_LINEAR, ref16)):
+        gpu = run_gpu(params, sysm, bl, prec=prec, stress=True)
+        err = stress_error(gpu["stress"], ref)
+        print(f"[parity] stress {case} prec={prec} rel {err:.3e} (vs FP64 {stress_error(gpu['stress'], ref64):.3e}) "
+              f"|sigma| {np.abs(ref64).max():.3e}", flush=True)
+        assert gpu["stress"].shape == ref.shape
+        assert err <= TOL[prec]["forces"], (case, prec, err)
+    again = run_gpu(params, sysm, bl, stress=True)
+    assert np.array_equal(again["stress"], run_gpu(params, sysm, bl, stress=True)["stress"])

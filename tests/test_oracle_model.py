@@ -394,3 +394,56 @@ def test_no_edges_energy_constant_zero_force():
     assert np.all(out["forces"] == 0.0)
     moved = synth.System(sysm.positions + 1.0, sysm.species, None, sysm.graph_of_atom, 1)
     assert _energy(d, blob, moved) == out["energy"][0]
+
+
+# ------------------------------------------------------------------ stress
+
+def _strained(system, eps):
+    M = np.eye(3) + eps
+    cells = None if system.cells is None else np.asarray(system.cells) @ M
+    return synth.System(np.asarray(system.positions) @ M, system.species, cells, system.graph_of_atom,
+                        system.n_graphs)
+
+
+def test_stress_matches_strain_finite_differences():
+    """sigma = (1/V) dE/d(epsilon) against central differences of E under a
+    small homogeneous strain (positions and cell, neighbour list rebuilt)."""
+    d = _small_desc(hidden_lmax=1, K=6, rc=3.2)
+    blob = synth.weight_blob(mace.weight_layout(d), 11, {".radial.3": 4.0})
+    system = _cluster(14, seed=5, box=6.3)
+    sig = mace.stress(d, blob, system)[0]
+    V = abs(np.linalg.det(system.cells[0]))
+    h = 1e-5
+    for a, b in [(0, 0), (1, 2), (2, 1), (2, 2), (0, 1)]:
+        e = np.zeros((3, 3))
+        e[a, b] = h
+        fd = (_energy(d, blob, _strained(system, e)) - _energy(d, blob, _strained(system, -e))) / (2 * h * V)
+        assert abs(fd - sig[a, b]) <= 1e-6 * np.abs(sig).max() + 1e-12, (a, b, fd, sig[a, b])
+    # rotation invariance makes dE/d(epsilon) symmetric
+    assert np.abs(sig - sig.T).max() <= 1e-10 * np.abs(sig).max()
+
+
+def test_stress_of_isolated_cluster_is_the_position_force_moment():
+    """Without a cell every atom moves with the strain, so dE/d(epsilon)_ab =
+    sum_i x_ia dE/dx_ib = -sum_i x_ia F_ib (V = 1)."""
+    d = _small_desc(hidden_lmax=1, K=6, rc=3.2)
+    blob = synth.weight_blob(mace.weight_layout(d), 12, {".radial.3": 4.0})
+    system = _cluster(10, seed=9)
+    out = mace.energy_forces(d, blob, system)
+    ref = -np.asarray(system.positions).T @ out["forces"]
+    sig = mace.stress(d, blob, system)[0]
+    assert np.abs(sig - ref).max() <= 1e-10 * np.abs(ref).max()
+
+
+def test_stress_is_intensive_under_supercell():
+    """Doubling a periodic cell along x doubles E and V: sigma is unchanged."""
+    d = _small_desc(hidden_lmax=1, K=6, rc=3.2)
+    blob = synth.weight_blob(mace.weight_layout(d), 13, {".radial.3": 4.0})
+    system = _cluster(12, seed=3, box=6.5)
+    cell = system.cells[0]
+    pos2 = np.concatenate([system.positions, system.positions + cell[0]])
+    sup = synth.System(pos2, np.concatenate([system.species, system.species]),
+                       (np.diag([2.0, 1.0, 1.0]) @ cell)[None], np.zeros(24, np.int32), 1)
+    s1 = mace.stress(d, blob, system)[0]
+    s2 = mace.stress(d, blob, sup)[0]
+    assert np.abs(s1 - s2).max() <= 1e-9 * np.abs(s1).max()
