@@ -116,7 +116,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=1)
-    ap.add_argument("--prec", choices=["fp32", "bf16"], default="fp32")
+    ap.add_argument("--prec", choices=["fp32", "bf16", "fp16"], default="fp32")
     ap.add_argument("--kernel", default="auto", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -146,7 +146,7 @@ def main():
 
     cfg = args.config
     params = model_params(cfg)
-    prec = B.MACE_FP32 if args.prec == "fp32" else B.MACE_BF16_LINEAR
+    prec = {"fp32": B.MACE_FP32, "bf16": B.MACE_BF16_LINEAR, "fp16": B.MACE_FP16_LINEAR}[args.prec]
     sysm = make_system(cfg, seed=0)
     desc = B.make_desc(**params)
     lay, _ = B.mace_weight_layout(desc)
@@ -232,20 +232,25 @@ def main():
     f1.record(stream)
     torch.cuda.synchronize()
     fwd_ms = f0.elapsed_time(f1) / args.steps
-    other = B.MACE_BF16_LINEAR if prec == B.MACE_FP32 else B.MACE_FP32
-    g2 = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
-                   sh if periodic else None, sysm.cells if periodic else None,
-                   sysm.graph_of_atom.astype(np.int32) if sysm.n_graphs > 1 else None, sysm.n_graphs, other)
-    eps2, Eg2, F2 = g2.outputs(True)
-    for _ in range(args.warmup):
-        B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
-    f0.record(stream)
-    for _ in range(args.steps):
-        B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
-    f1.record(stream)
-    torch.cuda.synchronize()
-    other_ms = f0.elapsed_time(f1) / args.steps
-    g2.close()
+    others = {}
+    for other, oname in ((B.MACE_FP32, "fp32"), (B.MACE_BF16_LINEAR, "bf16_linear"), (B.MACE_FP16_LINEAR, "fp16_linear")):
+        if other == prec:
+            continue
+        g2 = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                       sh if periodic else None, sysm.cells if periodic else None,
+                       sysm.graph_of_atom.astype(np.int32) if sysm.n_graphs > 1 else None, sysm.n_graphs, other)
+        eps2, Eg2, F2 = g2.outputs(True)
+        for _ in range(args.warmup):
+            B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
+        f0.record(stream)
+        for _ in range(args.steps):
+            B.mace_forces(g2.handle, pos, eps2, Eg2, F2, stream)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        other_ms = f0.elapsed_time(f1) / args.steps
+        others[oname] = {"atoms_per_s": round(N / (other_ms * 1e-3), 1), "edges_per_s": round(E / (other_ms * 1e-3), 1),
+                         "ms_per_step": round(other_ms, 4)}
+        g2.close()
 
     out = {
         "metric": "atoms/s and edges/s for MACE energy+forces (FP32, BF16-linear); % roofline",
@@ -254,7 +259,7 @@ def main():
         "edges_per_s": round(E * args.steps / (total_ms * 1e-3), 1),
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if prec == B.MACE_FP32 else "f32+bf16-linear",
+        "dtype": {B.MACE_FP32: "f32", B.MACE_BF16_LINEAR: "f32+bf16-linear", B.MACE_FP16_LINEAR: "f32+f16-linear"}[prec],
         "data": "synthetic",
         "config": {"workload": CONFIGS[cfg]["name"], "n_atoms": N, "n_edges": E, "K": params["K"],
                    "hidden_lmax": params["hidden_lmax"], "r_cut": params["r_cut"], "correlation": 3,
@@ -262,9 +267,7 @@ def main():
         "roofline": roof,
         "step_ms_p10_p50_p90": [round(float(np.percentile(per_call, q)), 4) for q in (10, 50, 90)],
         "forward_only": {"atoms_per_s": round(N / (fwd_ms * 1e-3), 1), "ms": round(fwd_ms, 4)},
-        ("bf16_linear" if other == B.MACE_BF16_LINEAR else "fp32"): {
-            "atoms_per_s": round(N / (other_ms * 1e-3), 1), "edges_per_s": round(E / (other_ms * 1e-3), 1),
-            "ms_per_step": round(other_ms, 4)},
+        "other_precisions": others,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params)

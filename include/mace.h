@@ -39,8 +39,11 @@ typedef enum {
 
 typedef enum {
   MACE_FP32 = 0,          /* every step in FP32 */
-  MACE_BF16_LINEAR = 1    /* channel-mixing linears with BF16 inputs and weights,
+  MACE_BF16_LINEAR = 1,   /* channel-mixing linears with BF16 inputs and weights,
                              FP32 accumulation; everything else FP32 */
+  MACE_FP16_LINEAR = 2    /* the same with IEEE binary16 (round to nearest even;
+                             an input or weight beyond 65504 becomes infinite and
+                             the outputs then hold non-finite values) */
 } mace_precision;
 
 /* Model hyper-parameters (host).  Supported: sh_lmax = 3, correlation = 3,

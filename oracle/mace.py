@@ -40,7 +40,8 @@ R10 Every linear is y_k = sum_k' W[k', k] x_k'; weights are N(0,1)/sqrt(fan_in)
 R11 BF16-linear mode (emulation): inputs and weights of the channel-mixing
     linears (linear_up, path-merging linear, species linears, product linear,
     readout linears) rounded to bfloat16 (round to nearest even); all sums
-    and every other step in FP64.
+    and every other step in FP64. FP16-linear mode: the same with IEEE
+    binary16 (round to nearest even, overflow to infinity).
 R12 Stress: the NPT metrics paragraph takes the pressure as -tr(sigma)/3 and
     does not define sigma. Here sigma = (1/V) dE/d(epsilon) for a homogeneous
     strain acting on row vectors, x -> x (I + epsilon), on positions and cell
@@ -183,22 +184,28 @@ def _round_bf16(x: torch.Tensor) -> torch.Tensor:
     return x.to(torch.bfloat16).to(DT)
 
 
-class _Lin:
-    """Channel-mixing linear y = x @ W with optional BF16 emulation (R11)."""
+def _round_fp16(x: torch.Tensor) -> torch.Tensor:
+    return x.to(torch.float16).to(DT)
 
-    def __init__(self, bf16: bool):
-        self.bf16 = bf16
+
+class _Lin:
+    """Channel-mixing linear y = x @ W with optional BF16 or FP16 emulation
+    of its inputs and weights (R11)."""
+
+    def __init__(self, bf16: bool, fp16: bool = False):
+        assert not (bf16 and fp16)
+        self.round = _round_bf16 if bf16 else (_round_fp16 if fp16 else None)
 
     def __call__(self, x, W):
-        if self.bf16:
-            return _round_bf16(x) @ _round_bf16(W)
+        if self.round is not None:
+            return self.round(x) @ self.round(W)
         return x @ W
 
     def species(self, x, W, z):
         """x [N, c, K], W [S, K, K], z [N]: y[n] = x[n] @ W[z[n]]."""
         Wz = W[z]
-        if self.bf16:
-            return torch.bmm(_round_bf16(x), _round_bf16(Wz))
+        if self.round is not None:
+            return torch.bmm(self.round(x), self.round(Wz))
         return torch.bmm(x, Wz)
 
 
@@ -261,9 +268,9 @@ def build_graph(system, d: ModelDesc) -> Graph:
 
 def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
                   bf16_linear: bool = False, edge_chunk: int = 1 << 16,
-                  return_intermediates: bool = False):
+                  return_intermediates: bool = False, fp16_linear: bool = False):
     """Per-atom energies eps_i [N] for positions pos [N,3] (float64)."""
-    lin = _Lin(bf16_linear)
+    lin = _Lin(bf16_linear, fp16_linear)
     z = graph.species
     N = pos.shape[0]
     K = d.K
@@ -336,13 +343,13 @@ def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
 
 
 def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
-                  bf16_linear: bool = False, forces: bool = True):
+                  bf16_linear: bool = False, forces: bool = True, fp16_linear: bool = False):
     """Returns dict(eps [N], energy [G], forces [N,3] or None, graph)."""
     W = unpack_weights(d, blob)
     if graph is None:
         graph = build_graph(system, d)
     pos = torch.tensor(system.positions, dtype=DT, requires_grad=forces)
-    eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear)
+    eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear)
     Eg = graph_energies(eps, graph)
     F = None
     if forces:
@@ -356,7 +363,7 @@ def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = 
 
 
 def stress(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
-           bf16_linear: bool = False):
+           bf16_linear: bool = False, fp16_linear: bool = False):
     """Stress of every graph, sigma_g = (1/V_g) dE_g/d(epsilon_g) [G,3,3].
 
     The pressure of the NPT metrics paragraph is p = -tr(sigma)/3. A
@@ -377,7 +384,7 @@ def stress(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
     g_edge = graph.graph_of_atom[graph.receiver]
     shifted = Graph(graph.sender, graph.receiver, torch.einsum("ea,eab->eb", graph.shift_vec, Fm[g_edge]),
                     graph.species, graph.graph_of_atom, graph.n_graphs)
-    eps = node_energies(d, W, shifted, pos, bf16_linear=bf16_linear)
+    eps = node_energies(d, W, shifted, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear)
     Eg = graph_energies(eps, graph)
     dE = None
     if Eg.requires_grad:

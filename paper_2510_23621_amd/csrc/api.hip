@@ -157,7 +157,7 @@ struct Carver {
 
 struct Buffers {
   float *w = nullptr, *wT = nullptr, *sp_table = nullptr;
-  unsigned short *wbf = nullptr, *wbfT = nullptr;   // bf16 K-packed copies (BF16-linear mode)
+  unsigned short *wbf = nullptr, *wbfT = nullptr;   // 16-bit K-packed copies (BF16- / FP16-linear modes)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
       *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
       *tile_count = nullptr, *tile_species = nullptr, *quad_tile = nullptr, *quad_count = nullptr;
@@ -292,6 +292,9 @@ struct ProfScope {
 #define PROF(kid) ProfScope _prof_##__LINE__(h, kid, s)
 
 mace_status hip_ok(hipError_t e) { return e == hipSuccess ? MACE_OK : MACE_EHIP; }
+
+// rounding mode of the channel-mixing linears: 0 FP32, 1 bfloat16, 2 binary16
+int lowp_mode(mace_precision p) { return p == MACE_BF16_LINEAR ? 1 : (p == MACE_FP16_LINEAR ? 2 : 0); }
 
 LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, const Model& m, int cin, int cout,
                           bool species) {
@@ -438,7 +441,7 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.n_quads = h->n_quads;
   a.K = h->m.d.K;
   a.accumulate = accumulate;
-  a.bf16 = h->prec == MACE_BF16_LINEAR;
+  a.lowp = lowp_mode(h->prec);
   return a;
 }
 
@@ -459,7 +462,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
   const Model& m = h->m;
   Buffers& b = h->b;
   const int N = (int)h->N, E = (int)h->E, K = m.d.K;
-  const bool bf16 = h->prec == MACE_BF16_LINEAR;
+  const int lowp = lowp_mode(h->prec);
   {
     PROF(KID_EDGE_FEATURES);
     // geometry and the radial hidden layers of every interaction layer, in
@@ -498,10 +501,10 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"), b.Y,
                      src, inv_c, b.At);
     }
-    if (t == 0 && !bf16) {
+    if (t == 0 && !lowp) {
       PROF(KID_LINEAR);
       launch_linear(s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
-    } else if (t == 0) {   // BF16-linear: each linear rounds its own inputs and weights
+    } else if (t == 0) {   // 16-bit linears: each linear rounds its own inputs and weights
       {
         PROF(KID_LINEAR);
         launch_linear(s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
@@ -528,14 +531,14 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     if (!L.last)
       {
         PROF(KID_READOUT);
-        launch_readout_fwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, bf16,
+        launch_readout_fwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
                            t > 0, eps);
       }
     else
       {
         PROF(KID_READOUT);
         launch_readout_fwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, bf16, t > 0, eps);
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, t > 0, eps);
       }
   }
 }
@@ -544,7 +547,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
   const Model& m = h->m;
   Buffers& b = h->b;
   const int N = (int)h->N, E = (int)h->E, K = m.d.K, T = m.d.n_layers;
-  const bool bf16 = h->prec == MACE_BF16_LINEAR;
+  const int lowp = lowp_mode(h->prec);
   const float inv_c = (float)(1.0 / m.d.c_norm);
   float* dnext = b.dh0;
   float* dprev = b.dh1;
@@ -560,12 +563,12 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       {
         PROF(KID_READOUT);
         launch_readout_bwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, bf16, dnext);
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, dnext);
       }
     } else {
       {
         PROF(KID_READOUT);
-        launch_readout_bwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, bf16,
+        launch_readout_bwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
                            dnext);
       }
     }
@@ -577,7 +580,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
     }
-    if (t == 0 && !bf16) {
+    if (t == 0 && !lowp) {
       PROF(KID_LINEAR);
       launch_linear(s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
     } else {
@@ -691,7 +694,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   if (st != MACE_OK) return st;
   if (!weights || !species || !workspace || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return MACE_EINVAL;
   if (n_edges > 0 && !edge_index) return MACE_EINVAL;
-  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR) return MACE_EINVAL;
+  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR && prec != MACE_FP16_LINEAR) return MACE_EINVAL;
   if (weight_floats != m.total) return MACE_EINVAL;
   if (n_atoms > (1LL << 30) || n_edges > (1LL << 31) - 1) return MACE_EUNSUPPORTED;
   if (!graph_of_atom && n_graphs != 1) return MACE_EINVAL;
@@ -818,14 +821,22 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     }
   }
 
-  // bf16 copies of every K x K block, packed [K/8][K][8] (element (k, n) at
-  // ((k/8) K + n) 8 + k%8) for the MFMA B operand of the BF16 linears
+  // 16-bit copies (bf16 or binary16, by mode) of every K x K block, packed
+  // [K/8][K][8] (element (k, n) at ((k/8) K + n) 8 + k%8) for the MFMA B
+  // operand of the 16-bit linears
   std::vector<uint16_t> hbf(m.total, 0), hbfT(m.total, 0);
   auto to_bf16 = [](float x) -> uint16_t {
     uint32_t u;
     std::memcpy(&u, &x, 4);
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
+  };
+  auto to_16 = [&](float x) -> uint16_t {
+    if (prec != MACE_FP16_LINEAR) return to_bf16(x);
+    const _Float16 hx = (_Float16)x;   // round to nearest even, overflow to infinity
+    uint16_t u;
+    std::memcpy(&u, &hx, 2);
+    return u;
   };
   for (auto& t : m.tensors) {
     const auto& sh = t.shape;
@@ -836,8 +847,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       for (int64_t k = 0; k < K; ++k)
         for (int64_t n = 0; n < K; ++n) {
           const int64_t dst = base + ((k / 8) * K + n) * 8 + (k % 8);
-          hbf[dst] = to_bf16(hw[base + k * K + n]);
-          hbfT[dst] = to_bf16(hwT[base + k * K + n]);
+          hbf[dst] = to_16(hw[base + k * K + n]);
+          hbfT[dst] = to_16(hwT[base + k * K + n]);
         }
     }
   }
@@ -895,7 +906,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(up(b.quad_count, qcount.data(), qcount.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
-                       prec == MACE_BF16_LINEAR, b.sp_table);
+                       lowp_mode(prec), b.sp_table);
   chk(hipGetLastError());
   chk(hipStreamSynchronize(s));  // host vectors go out of scope below
   if (err != hipSuccess) {

@@ -15,12 +15,14 @@ namespace mace {
 // FP32: v_mfma_f32_16x16x4_f32 with A[l%16][l/16], B[l/16][l%16]; the K-long
 // reduction runs in the order k = 16 q + 4 s + c (s = l/16 the MFMA's k slot,
 // c the float4 component), so a lane's A values for four MFMAs are one float4.
-// BF16 (inputs and weights rounded to nearest even, FP32 accumulation):
-// v_mfma_f32_16x16x32_bf16 with A[l%16][8(l/16)+i], B[8(l/16)+i][l%16]; the
-// weights come pre-packed as [K/8][K][8] bf16, i.e. 16-byte runs along k.
+// BF16 / FP16 (inputs and weights rounded to nearest even, FP32 accumulation):
+// v_mfma_f32_16x16x32_bf16 / _f16 with A[l%16][8(l/16)+i], B[8(l/16)+i][l%16];
+// the weights come pre-packed as [K/8][K][8] 16-bit values, i.e. 16-byte runs
+// along k.
 // Result register r of lane l holds D[4(l/16)+r][l%16].
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef unsigned short us8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ unsigned short bf16_bits(float x) {
@@ -29,15 +31,24 @@ __device__ __forceinline__ unsigned short bf16_bits(float x) {
   __builtin_memcpy(&u, &r, 4);
   return (unsigned short)(u >> 16);
 }
+__device__ __forceinline__ unsigned short fp16_bits(float x) { return __builtin_bit_cast(unsigned short, (_Float16)x); }
+template <int LP>
+__device__ __forceinline__ unsigned short lowp_bits(float x) {
+  if constexpr (LP == 1) return bf16_bits(x);
+  else return fp16_bits(x);
+}
 
 constexpr int kLinCt = 4;   // column tiles per block
 
-template <int K, bool BF16>
+// LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
+// rounding and the MFMA instruction)
+template <int K, int LP>
 __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* __restrict__ Lp, LinArgs a) {
+  constexpr bool BF16 = LP != 0;   // any 16-bit path
   const LinLaunch& L = *Lp;
   static_assert(K % 32 == 0, "K is a multiple of 32");
   constexpr int PF = K + 4;    // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
-  constexpr int PB = K + 8;    // BF16 panel row pitch in bf16 (68 dwords at K = 128)
+  constexpr int PB = K + 8;    // 16-bit panel row pitch in elements (68 dwords at K = 128)
   constexpr int kPanel = BF16 ? (64 * PB + 1) / 2 : 64 * PF;
   __shared__ __align__(16) float sB[kPanel];
   unsigned short* sBb = reinterpret_cast<unsigned short*>(sB);
@@ -79,8 +90,8 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
         const f4 lo = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4)) * keep;
         const f4 hi = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4) + 4) * keep;
         us8 v;
-        v[0] = bf16_bits(lo[0]); v[1] = bf16_bits(lo[1]); v[2] = bf16_bits(lo[2]); v[3] = bf16_bits(lo[3]);
-        v[4] = bf16_bits(hi[0]); v[5] = bf16_bits(hi[1]); v[6] = bf16_bits(hi[2]); v[7] = bf16_bits(hi[3]);
+        v[0] = lowp_bits<LP>(lo[0]); v[1] = lowp_bits<LP>(lo[1]); v[2] = lowp_bits<LP>(lo[2]); v[3] = lowp_bits<LP>(lo[3]);
+        v[4] = lowp_bits<LP>(hi[0]); v[5] = lowp_bits<LP>(hi[1]); v[6] = lowp_bits<LP>(hi[2]); v[7] = lowp_bits<LP>(hi[3]);
         ab[ks] = v;
       }
     }
@@ -119,8 +130,12 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
 #pragma unroll
         for (int j = 0; j < kLinCt; ++j) {
           const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, ab[ks]), __builtin_bit_cast(bf8, b),
-                                                           acc[j], 0, 0, 0);
+          if constexpr (LP == 1)
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, ab[ks]), __builtin_bit_cast(bf8, b),
+                                                             acc[j], 0, 0, 0);
+          else
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, ab[ks]), __builtin_bit_cast(h8, b),
+                                                            acc[j], 0, 0, 0);
         }
     }
   }
@@ -166,8 +181,9 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
 #define MACE_LIN(KK)                                                        \
   case KK:                                                                 \
-    if (a.bf16) linear_kernel<KK, true><<<grid, block, 0, s>>>(L, a);      \
-    else linear_kernel<KK, false><<<grid, block, 0, s>>>(L, a);            \
+    if (a.lowp == 1) linear_kernel<KK, 1><<<grid, block, 0, s>>>(L, a);    \
+    else if (a.lowp == 2) linear_kernel<KK, 2><<<grid, block, 0, s>>>(L, a); \
+    else linear_kernel<KK, 0><<<grid, block, 0, s>>>(L, a);                \
     break;
   switch (a.K) {
     MACE_LIN(32)
@@ -184,17 +200,17 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
 // One block per node, threads = channels, fixed-order tree reduction in LDS.
 __global__ void __launch_bounds__(128) readout_fwd_kernel(int N, int K, const float* __restrict__ h, int h_stride,
                                                           const float* __restrict__ w, const float* __restrict__ w1,
-                                                          const float* __restrict__ w2, int hidden, int bf16,
+                                                          const float* __restrict__ w2, int hidden, int lowp,
                                                           int accumulate, float* __restrict__ eps) {
   __shared__ float red[16][128];
   const int n = blockIdx.x, k = threadIdx.x;
   float x = (k < K) ? h[(size_t)n * h_stride + k] : 0.f;
-  if (bf16) x = bf16_round(x);
+  x = lowp_round(x, lowp);
   const int nv = w ? 1 : hidden;
   for (int j = 0; j < nv; ++j) {
     float wv = 0.f;
     if (k < K) wv = w ? w[k] : w1[(size_t)k * hidden + j];
-    if (bf16) wv = bf16_round(wv);
+    wv = lowp_round(wv, lowp);
     red[j][k] = x * wv;
   }
   __syncthreads();
@@ -212,9 +228,9 @@ __global__ void __launch_bounds__(128) readout_fwd_kernel(int N, int K, const fl
       for (int j = 0; j < hidden; ++j) {
         float a = silu(red[j][0]);
         float v2 = w2[j];
-        if (bf16) {
-          a = bf16_round(a);
-          v2 = bf16_round(v2);
+        if (lowp) {
+          a = lowp_round(a, lowp);
+          v2 = lowp_round(v2, lowp);
         }
         out += a * v2;
       }
@@ -226,7 +242,7 @@ __global__ void __launch_bounds__(128) readout_fwd_kernel(int N, int K, const fl
 // dh[n][0][k] += dE/dh (energy = sum of eps).
 __global__ void __launch_bounds__(128) readout_bwd_kernel(int N, int K, const float* __restrict__ h, int h_stride,
                                                           const float* __restrict__ w, const float* __restrict__ w1,
-                                                          const float* __restrict__ w2, int hidden, int bf16,
+                                                          const float* __restrict__ w2, int hidden, int lowp,
                                                           float* __restrict__ dh) {
   __shared__ float red[16][128];
   __shared__ float gz[16];
@@ -234,17 +250,17 @@ __global__ void __launch_bounds__(128) readout_bwd_kernel(int N, int K, const fl
   if (w) {
     if (k < K) {
       float wv = w[k];
-      if (bf16) wv = bf16_round(wv);
+      wv = lowp_round(wv, lowp);
       dh[(size_t)n * h_stride + k] += wv;
     }
     return;
   }
   float x = (k < K) ? h[(size_t)n * h_stride + k] : 0.f;
-  if (bf16) x = bf16_round(x);
+  x = lowp_round(x, lowp);
   for (int j = 0; j < hidden; ++j) {
     float wv = 0.f;
     if (k < K) wv = w1[(size_t)k * hidden + j];
-    if (bf16) wv = bf16_round(wv);
+    wv = lowp_round(wv, lowp);
     red[j][k] = x * wv;
   }
   __syncthreads();
@@ -255,9 +271,9 @@ __global__ void __launch_bounds__(128) readout_bwd_kernel(int N, int K, const fl
   }
   if (k < hidden) {
     float v2 = w2[k];
-    if (bf16) v2 = bf16_round(v2);
+    v2 = lowp_round(v2, lowp);
     float gzj = v2 * silu_grad(red[k][0]);
-    if (bf16) gzj = bf16_round(gzj);
+    gzj = lowp_round(gzj, lowp);
     gz[k] = gzj;
   }
   __syncthreads();
@@ -265,7 +281,7 @@ __global__ void __launch_bounds__(128) readout_bwd_kernel(int N, int K, const fl
     float acc = 0.f;
     for (int j = 0; j < hidden; ++j) {
       float wv = w1[(size_t)k * hidden + j];
-      if (bf16) wv = bf16_round(wv);
+      wv = lowp_round(wv, lowp);
       acc += gz[j] * wv;
     }
     dh[(size_t)n * h_stride + k] += acc;
@@ -292,16 +308,16 @@ __global__ void __launch_bounds__(256) graph_energy_kernel(int G, const int* __r
 // species. Accumulated in FP64 (one rounding, once per graph setup): a
 // rounding error here is shared by every atom of the species.
 __global__ void species_table_kernel(int S, int K, const float* __restrict__ emb, const float* __restrict__ wup,
-                                     int bf16, float* __restrict__ table) {
+                                     int lowp, float* __restrict__ table) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= S * K) return;
   const int z = idx / K, k = idx % K;
   double acc = 0.0;
   for (int kk = 0; kk < K; ++kk) {
     float x = emb[(size_t)z * K + kk], w = wup[(size_t)kk * K + k];
-    if (bf16) {
-      x = bf16_round(x);
-      w = bf16_round(w);
+    if (lowp) {
+      x = lowp_round(x, lowp);
+      w = lowp_round(w, lowp);
     }
     acc += (double)x * (double)w;
   }
@@ -309,21 +325,21 @@ __global__ void species_table_kernel(int S, int K, const float* __restrict__ emb
 }
 
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int bf16, int accumulate, float* eps) {
+                        const float* w2, int hidden, int lowp, int accumulate, float* eps) {
   if (N <= 0) return;
-  readout_fwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, bf16, accumulate, eps);
+  readout_fwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps);
 }
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int bf16, float* dh) {
+                        const float* w2, int hidden, int lowp, float* dh) {
   if (N <= 0) return;
-  readout_bwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, bf16, dh);
+  readout_bwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, lowp, dh);
 }
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
   if (G <= 0) return;
   graph_energy_kernel<<<G, 256, 0, s>>>(G, graph_off, eps, E);
 }
-void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int bf16, float* table) {
-  species_table_kernel<<<(S * K + 127) / 128, 128, 0, s>>>(S, K, emb, wup, bf16, table);
+void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp, float* table) {
+  species_table_kernel<<<(S * K + 127) / 128, 128, 0, s>>>(S, K, emb, wup, lowp, table);
 }
 
 }  // namespace mace

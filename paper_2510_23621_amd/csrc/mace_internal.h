@@ -35,6 +35,16 @@ __host__ __device__ __forceinline__ float bf16_round(float x) {
   return r;
 }
 
+// Round-to-nearest-even float -> IEEE binary16 -> float (FP16-linear mode);
+// magnitudes beyond the binary16 range become infinite.
+__host__ __device__ __forceinline__ float fp16_round(float x) { return (float)(_Float16)x; }
+
+// Inputs and weights of the channel-mixing linears: lowp 0 keeps FP32, 1
+// rounds to bfloat16, 2 to binary16.
+__host__ __device__ __forceinline__ float lowp_round(float x, int lowp) {
+  return lowp == 1 ? bf16_round(x) : (lowp == 2 ? fp16_round(x) : x);
+}
+
 // Forward-mode dual number carrying d/d(vx, vy, vz) of an edge vector.
 template <class S>
 struct Dual3 {
@@ -261,7 +271,7 @@ struct LinArgs {
   const float* residual;    // [N][cout][K] or null, added to every comp written to y
   const float* w;           // weight base (FP32, row-major [in][out])
   const float* wt;          // the same blob with every K x K block transposed ([out][in])
-  const unsigned short* wbf;  // same tensors as bf16, each K x K block packed [K/8][K][8]
+  const unsigned short* wbf;  // same tensors in the low precision (bf16 or binary16 bits), each K x K block packed [K/8][K][8]
   const int* tile_start;    // [n_tiles] start in node_order
   const int* tile_count;    // [n_tiles]
   const int* tile_species;  // [n_tiles]
@@ -271,7 +281,7 @@ struct LinArgs {
   int n_tiles, n_quads;
   int K;
   int accumulate;           // y += instead of y =
-  int bf16;                 // round x and w to bf16 before multiplying
+  int lowp;                 // 0: FP32; round x and w to 1: bfloat16, 2: binary16 before multiplying
 };
 
 constexpr int kMaxRadialLayers = 4;
@@ -311,11 +321,11 @@ void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* spe
                        SymW w, const float* dB, float* dA);
 void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
-                        const float* w1, const float* w2, int hidden, int bf16, int accumulate, float* eps);
+                        const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
-                        const float* w1, const float* w2, int hidden, int bf16, float* dh);
+                        const float* w1, const float* w2, int hidden, int lowp, float* dh);
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E);
-void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int bf16,
+void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp,
                           float* table);
 void launch_fill(hipStream_t s, float* p, size_t n, float v);
 

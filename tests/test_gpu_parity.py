@@ -172,3 +172,29 @@ def test_stress_against_oracle(case):
         assert err <= TOL[prec]["forces"], (case, prec, err)
     again = run_gpu(params, sysm, bl, stress=True)
     assert np.array_equal(again["stress"], run_gpu(params, sysm, bl, stress=True)["stress"])
+
+
+@pytest.mark.parametrize("case", ["water96_stress_inputs", "molecules12_k64"])
+def test_fp16_linear_vs_fp64_and_emulation(case):
+    """FP16-linear mode (binary16 inputs and weights of every channel-mixing
+    linear, FP32 accumulation): against the FP64 oracle at the 16-bit
+    tolerances, and against the oracle's FP16 emulation."""
+    if case == "molecules12_k64":
+        params = model_params(4, K=64, **STRESS)
+        sysm = synth.molecule_batch(12, seed=2)
+    else:
+        params = model_params(0, **STRESS)
+        sysm = make_system(0, seed=0)
+    bo = oracle_blob(params, 7, STRESS_GAINS)
+    bl = lib_blob(params, 7, STRESS_GAINS)
+    ref = run_oracle(params, sysm, bo)
+    g16 = run_gpu(params, sysm, bl, prec=B.MACE_FP16_LINEAR)
+    assert_parity(g16, ref, B.MACE_FP16_LINEAR, f"{case} fp16 vs fp64")
+    emu = run_oracle(params, sysm, bo, fp16=True)
+    err = errors(g16, emu)
+    print(f"[parity] {case} fp16 gpu vs fp16-emulating oracle {err}", flush=True)
+    assert err["energy"] <= 5e-4 and err["forces"] <= 5e-3, err
+    # binary16 keeps three more significand bits than bfloat16
+    gb = run_gpu(params, sysm, bl, prec=B.MACE_BF16_LINEAR)
+    assert errors(g16, ref)["forces"] < errors(gb, ref)["forces"]
+

@@ -447,3 +447,40 @@ def test_stress_is_intensive_under_supercell():
     s1 = mace.stress(d, blob, system)[0]
     s2 = mace.stress(d, blob, sup)[0]
     assert np.abs(s1 - s2).max() <= 1e-9 * np.abs(s1).max()
+
+
+# ------------------------------------------------------------------ 16-bit linears
+
+def test_fp16_rounding_is_ieee_binary16_nearest_even():
+    """The FP16-linear emulation rounds to IEEE binary16 (10 fraction bits),
+    ties to even, overflow to infinity: values fixed by the format itself."""
+    u = 2.0 ** -10                                   # ulp of binary16 at 1
+    x = torch.tensor([1 + u / 2, 1 + 1.5 * u, 1 + 0.75 * u, 65504.0, 65519.0, 65520.0, -70000.0,
+                      2.0 ** -24, 2.0 ** -26, 3 * 2.0 ** -25], dtype=torch.float64)
+    want = [1.0, 1 + 2 * u, 1 + u, 65504.0, 65504.0, math.inf, -math.inf, 2.0 ** -24, 0.0, 2 * 2.0 ** -24]
+    got = mace._round_fp16(x).tolist()
+    assert got == want, got
+
+
+def test_bf16_rounding_is_bfloat16_nearest_even():
+    u = 2.0 ** -7                                    # ulp of bfloat16 at 1
+    x = torch.tensor([1 + u / 2, 1 + 1.5 * u, 1 + 0.25 * u, 3.0e38], dtype=torch.float64)
+    got = mace._round_bf16(x).tolist()
+    assert got[:3] == [1.0, 1 + 2 * u, 1.0], got
+    assert got[3] == float(np.float32(3.0e38)) or abs(got[3] / 3.0e38 - 1) < 2 ** -8
+
+
+def test_16bit_linear_modes_stay_close_to_fp64():
+    """Rounding the linears' inputs and weights moves energies and forces by
+    about the format's precision: FP16 (11 significant bits) less than BF16 (8)."""
+    d = _desc(0)
+    blob = synth.weight_blob(mace.weight_layout(d), 4)
+    system = make_system(0, seed=0)
+    ref = mace.energy_forces(d, blob, system)
+    dev = {}
+    for name, kw in (("bf16", dict(bf16_linear=True)), ("fp16", dict(fp16_linear=True))):
+        out = mace.energy_forces(d, blob, system, graph=ref["graph"], **kw)
+        dev[name] = (abs(out["energy"] - ref["energy"]).max() / np.abs(ref["eps"]).sum(),
+                     np.linalg.norm(out["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"]))
+    assert dev["fp16"][1] < dev["bf16"][1] and dev["fp16"][1] < 2e-3 and dev["bf16"][1] < 2e-2, dev
+    assert dev["fp16"][0] < dev["bf16"][0] + 1e-9, dev
