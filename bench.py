@@ -116,7 +116,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=1)
-    ap.add_argument("--prec", choices=["fp32", "bf16", "fp16"], default="fp32")
+    ap.add_argument("--prec", choices=["fp32", "bf16", "fp16", "bf16radial"], default="fp32")
     ap.add_argument("--kernel", default="auto", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -146,7 +146,8 @@ def main():
 
     cfg = args.config
     params = model_params(cfg)
-    prec = {"fp32": B.MACE_FP32, "bf16": B.MACE_BF16_LINEAR, "fp16": B.MACE_FP16_LINEAR}[args.prec]
+    prec = {"fp32": B.MACE_FP32, "bf16": B.MACE_BF16_LINEAR, "fp16": B.MACE_FP16_LINEAR,
+            "bf16radial": B.MACE_BF16_RADIAL}[args.prec]
     sysm = make_system(cfg, seed=0)
     desc = B.make_desc(**params)
     lay, _ = B.mace_weight_layout(desc)
@@ -233,7 +234,8 @@ def main():
     torch.cuda.synchronize()
     fwd_ms = f0.elapsed_time(f1) / args.steps
     others = {}
-    for other, oname in ((B.MACE_FP32, "fp32"), (B.MACE_BF16_LINEAR, "bf16_linear"), (B.MACE_FP16_LINEAR, "fp16_linear")):
+    for other, oname in ((B.MACE_FP32, "fp32"), (B.MACE_BF16_LINEAR, "bf16_linear"), (B.MACE_FP16_LINEAR, "fp16_linear"),
+                         (B.MACE_BF16_RADIAL, "bf16_linear_and_radial")):
         if other == prec:
             continue
         g2 = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
@@ -259,7 +261,8 @@ def main():
         "edges_per_s": round(E * args.steps / (total_ms * 1e-3), 1),
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": {B.MACE_FP32: "f32", B.MACE_BF16_LINEAR: "f32+bf16-linear", B.MACE_FP16_LINEAR: "f32+f16-linear"}[prec],
+        "dtype": {B.MACE_FP32: "f32", B.MACE_BF16_LINEAR: "f32+bf16-linear", B.MACE_FP16_LINEAR: "f32+f16-linear",
+                  B.MACE_BF16_RADIAL: "f32+bf16-linear+bf16-radial"}[prec],
         "data": "synthetic",
         "config": {"workload": CONFIGS[cfg]["name"], "n_atoms": N, "n_edges": E, "K": params["K"],
                    "hidden_lmax": params["hidden_lmax"], "r_cut": params["r_cut"], "correlation": 3,

@@ -41,9 +41,13 @@ typedef enum {
   MACE_FP32 = 0,          /* every step in FP32 */
   MACE_BF16_LINEAR = 1,   /* channel-mixing linears with BF16 inputs and weights,
                              FP32 accumulation; everything else FP32 */
-  MACE_FP16_LINEAR = 2    /* the same with IEEE binary16 (round to nearest even;
+  MACE_FP16_LINEAR = 2,   /* the same with IEEE binary16 (round to nearest even;
                              an input or weight beyond 65504 becomes infinite and
                              the outputs then hold non-finite values) */
+  MACE_BF16_RADIAL = 3    /* MACE_BF16_LINEAR, and the last layer of the radial
+                             MLP (the P*K-wide one) on BF16 operands with FP32
+                             accumulation: R = bf16(a3) bf16(W) forward and
+                             dE/da3 = bf16(dE/dR) bf16(W)^T backward */
 } mace_precision;
 
 /* Model hyper-parameters (host).  Supported: sh_lmax = 3, correlation = 3,

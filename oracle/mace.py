@@ -46,6 +46,13 @@ R12 Stress: the NPT metrics paragraph takes the pressure as -tr(sigma)/3 and
     does not define sigma. Here sigma = (1/V) dE/d(epsilon) for a homogeneous
     strain acting on row vectors, x -> x (I + epsilon), on positions and cell
     rows alike; V = |det cell|, or 1 for a graph without a cell.
+R13 BF16-radial mode (emulation): BF16-linear, and the last product of the
+    radial MLP takes bfloat16-rounded inputs and weights.
+    In both 16-bit emulations autograd differentiates the rounding as a cast:
+    the gradient that flows back into a rounded operand is itself rounded to
+    the same format (after the FP64 transposed product), whereas the library
+    rounds the incoming gradient before its transposed product. Both are
+    16-bit backward passes; they differ by rounding order only.
 """
 from __future__ import annotations
 
@@ -168,12 +175,16 @@ def silu(x):
     return x * torch.sigmoid(x)
 
 
-def radial_mlp(e: torch.Tensor, W: dict, t: int, n_hidden: int) -> torch.Tensor:
-    """Reading R5: e @ W0 -> SiLU -> ... -> @ W_last."""
+def radial_mlp(e: torch.Tensor, W: dict, t: int, n_hidden: int, bf16_last: bool = False) -> torch.Tensor:
+    """Reading R5: e @ W0 -> SiLU -> ... -> @ W_last (with bf16_last, the last
+    product takes bfloat16-rounded inputs and weights, R13)."""
     h = e
     for i in range(n_hidden):
         h = silu(h @ W[f"{t}.radial.{i}"])
-    return h @ W[f"{t}.radial.{n_hidden}"]
+    Wl = W[f"{t}.radial.{n_hidden}"]
+    if bf16_last:
+        return _round_bf16(h) @ _round_bf16(Wl)
+    return h @ Wl
 
 
 # --------------------------------------------------------------------------
@@ -268,7 +279,7 @@ def build_graph(system, d: ModelDesc) -> Graph:
 
 def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
                   bf16_linear: bool = False, edge_chunk: int = 1 << 16,
-                  return_intermediates: bool = False, fp16_linear: bool = False):
+                  return_intermediates: bool = False, fp16_linear: bool = False, bf16_radial: bool = False):
     """Per-atom energies eps_i [N] for positions pos [N,3] (float64)."""
     lin = _Lin(bf16_linear, fp16_linear)
     z = graph.species
@@ -299,7 +310,7 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
         At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
         for e0 in range(0, E, edge_chunk):
             sl = slice(e0, e0 + edge_chunk)
-            R = radial_mlp(rb[sl], W, t, nh).reshape(-1, len(paths), K)  # [e,P,K]
+            R = radial_mlp(rb[sl], W, t, nh, bf16_radial).reshape(-1, len(paths), K)  # [e,P,K]
             for p, (lh, ly, lo) in enumerate(paths):
                 C = torch.from_numpy(so3.real_cg(lh, ly, lo))
                 hs = ht[lh][snd[sl]]                                      # [e, 2lh+1, K]
@@ -343,13 +354,15 @@ def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
 
 
 def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
-                  bf16_linear: bool = False, forces: bool = True, fp16_linear: bool = False):
+                  bf16_linear: bool = False, forces: bool = True, fp16_linear: bool = False,
+                  bf16_radial: bool = False):
     """Returns dict(eps [N], energy [G], forces [N,3] or None, graph)."""
     W = unpack_weights(d, blob)
     if graph is None:
         graph = build_graph(system, d)
     pos = torch.tensor(system.positions, dtype=DT, requires_grad=forces)
-    eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear)
+    eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear,
+                        bf16_radial=bf16_radial)
     Eg = graph_energies(eps, graph)
     F = None
     if forces:
@@ -363,7 +376,7 @@ def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = 
 
 
 def stress(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
-           bf16_linear: bool = False, fp16_linear: bool = False):
+           bf16_linear: bool = False, fp16_linear: bool = False, bf16_radial: bool = False):
     """Stress of every graph, sigma_g = (1/V_g) dE_g/d(epsilon_g) [G,3,3].
 
     The pressure of the NPT metrics paragraph is p = -tr(sigma)/3. A
@@ -384,7 +397,8 @@ def stress(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
     g_edge = graph.graph_of_atom[graph.receiver]
     shifted = Graph(graph.sender, graph.receiver, torch.einsum("ea,eab->eb", graph.shift_vec, Fm[g_edge]),
                     graph.species, graph.graph_of_atom, graph.n_graphs)
-    eps = node_energies(d, W, shifted, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear)
+    eps = node_energies(d, W, shifted, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear,
+                        bf16_radial=bf16_radial)
     Eg = graph_energies(eps, graph)
     dE = None
     if Eg.requires_grad:

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libmace_amd.so")
 MACE_FP32 = 0
 MACE_BF16_LINEAR = 1
 MACE_FP16_LINEAR = 2
+MACE_BF16_RADIAL = 3
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 

@@ -294,7 +294,9 @@ struct ProfScope {
 mace_status hip_ok(hipError_t e) { return e == hipSuccess ? MACE_OK : MACE_EHIP; }
 
 // rounding mode of the channel-mixing linears: 0 FP32, 1 bfloat16, 2 binary16
-int lowp_mode(mace_precision p) { return p == MACE_BF16_LINEAR ? 1 : (p == MACE_FP16_LINEAR ? 2 : 0); }
+int lowp_mode(mace_precision p) {
+  return (p == MACE_BF16_LINEAR || p == MACE_BF16_RADIAL) ? 1 : (p == MACE_FP16_LINEAR ? 2 : 0);
+}
 
 LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, const Model& m, int cin, int cout,
                           bool species) {
@@ -499,7 +501,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     {
       PROF(KID_TP_FWD);
       launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"), b.Y,
-                     src, inv_c, b.At);
+                     src, inv_c, b.At, h->prec == MACE_BF16_RADIAL);
     }
     if (t == 0 && !lowp) {
       PROF(KID_LINEAR);
@@ -600,7 +602,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     {
       PROF(KID_TP_BWD);
       launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
-                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p);
+                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, h->prec == MACE_BF16_RADIAL);
     }
     {
       // right after the partials are written, while they are still in the
@@ -694,7 +696,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   if (st != MACE_OK) return st;
   if (!weights || !species || !workspace || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return MACE_EINVAL;
   if (n_edges > 0 && !edge_index) return MACE_EINVAL;
-  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR && prec != MACE_FP16_LINEAR) return MACE_EINVAL;
+  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR && prec != MACE_FP16_LINEAR && prec != MACE_BF16_RADIAL)
+    return MACE_EINVAL;
   if (weight_floats != m.total) return MACE_EINVAL;
   if (n_atoms > (1LL << 30) || n_edges > (1LL << 31) - 1) return MACE_EUNSUPPORTED;
   if (!graph_of_atom && n_graphs != 1) return MACE_EINVAL;

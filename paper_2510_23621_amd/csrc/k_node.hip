@@ -25,12 +25,6 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef unsigned short us8 __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ unsigned short bf16_bits(float x) {
-  float r = bf16_round(x);
-  unsigned int u;
-  __builtin_memcpy(&u, &r, 4);
-  return (unsigned short)(u >> 16);
-}
 __device__ __forceinline__ unsigned short fp16_bits(float x) { return __builtin_bit_cast(unsigned short, (_Float16)x); }
 template <int LP>
 __device__ __forceinline__ unsigned short lowp_bits(float x) {

@@ -92,6 +92,100 @@ __device__ __forceinline__ void tile_radial(const float* __restrict__ a3, int e0
   __builtin_amdgcn_s_setprio(0);
 }
 
+// ---- BF16 radial mode: R = bf16(a3) bf16(W3) and dE/da3 = bf16(dR) bf16(W3)^T
+// on v_mfma_f32_16x16x32_bf16 (FP32 accumulation); lane l supplies
+// A[l%16][8(l/16)+i] and B[8(l/16)+i][l%16], i = 0..7.
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+typedef unsigned short us8v __attribute__((ext_vector_type(8)));
+constexpr int kWbPitch = 72;   // bf16 per row of the forward slice: 64 + 8 (36 dwords, 4 mod 32)
+constexpr int kWtPitch = 24;   // bf16 per row of the transposed slice: 16 + 8 (16-byte aligned)
+constexpr int kT2Pitch = 20;   // floats per row of the two-path transpose tile (16-byte aligned)
+
+__device__ __forceinline__ f4 mfma_bf16(us8v a, us8v b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a), __builtin_bit_cast(bf8v, b), c, 0, 0,
+                                                 0);
+}
+__device__ __forceinline__ us8v to_bf16x8(f4 lo, f4 hi) {
+  us8v v;
+  v[0] = bf16_bits(lo[0]); v[1] = bf16_bits(lo[1]); v[2] = bf16_bits(lo[2]); v[3] = bf16_bits(lo[3]);
+  v[4] = bf16_bits(hi[0]); v[5] = bf16_bits(hi[1]); v[6] = bf16_bits(hi[2]); v[7] = bf16_bits(hi[3]);
+  return v;
+}
+
+// Forward slice sWb[(p*16 + kk)*kWbPitch + j] = bf16(W3[j][p K + 16 ct + kk]);
+// with `transposed`, also sWt[(p*64 + j)*kWtPitch + kk] (the dE/da3 operand).
+template <int P>
+__device__ __forceinline__ void load_w3_slice_bf16(const float* __restrict__ W3, int K, int ct,
+                                                   unsigned short* sWb, unsigned short* sWt) {
+  const int PK = P * K;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    const unsigned short v = bf16_bits(W3[(size_t)j * PK + p * K + 16 * ct + kk]);
+    sWb[(p * 16 + kk) * kWbPitch + j] = v;
+    if (sWt) sWt[(p * 64 + j) * kWtPitch + kk] = v;
+  }
+}
+
+// As tile_radial, on BF16 operands: two MFMAs (k = 32 each) per path.
+template <int P>
+__device__ __forceinline__ void tile_radial_bf16(const float* __restrict__ a3, int e0, int e_end,
+                                                 const unsigned short* __restrict__ sWb, f4* r) {
+  const int l = threadIdx.x & 63;
+  const int row = e0 + (l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+  us8v a[2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) a[ks] = to_bf16x8(arow[8 * ks] * keep, arow[8 * ks + 1] * keep);
+  const unsigned short* wb = sWb + (l & 15) * kWbPitch + 8 * (l >> 4);
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+      acc = mfma_bf16(a[ks], *reinterpret_cast<const us8v*>(wb + p * 16 * kWbPitch + 32 * ks), acc);
+    r[p] = acc;
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// dE/da3 partial on BF16 operands: D[e][j] = sum over (p, kk) of
+// bf16(dR[e][p][kk]) bf16(W3[j][p K + 16 ct + kk]); the reduction index
+// 32 ks + 8 (l/16) + i is path 2 ks + (l/16)/2, channel 8 ((l/16)%2) + i. Each
+// pair of dR tiles goes through the wave's transpose buffer tw (2 x 16 x
+// kT2Pitch floats) to put the edge on l%16.
+template <int P>
+__device__ __forceinline__ void tile_da3_bf16(const f4* r, const unsigned short* __restrict__ sWt, float* tw,
+                                              f4* d3) {
+  const int l = threadIdx.x & 63, g = l >> 4, kk = l & 15;
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < (P + 1) / 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int p = 2 * ks + pl;
+        tw[(pl * 16 + 4 * g + q) * kT2Pitch + kk] = (p < P) ? r[p < P ? p : 0][q] : 0.f;
+      }
+    __builtin_amdgcn_wave_barrier();
+    const float* src = tw + ((g >> 1) * 16 + kk) * kT2Pitch + 8 * (g & 1);
+    const us8v a = to_bf16x8(*reinterpret_cast<const f4*>(src), *reinterpret_cast<const f4*>(src + 4));
+    __builtin_amdgcn_wave_barrier();
+    const int p = min(2 * ks + (g >> 1), P - 1);   // a missing odd path reads a valid row; its A is zero
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+      const us8v b = *reinterpret_cast<const us8v*>(sWt + (p * 64 + 16 * jt + kk) * kWtPitch + 8 * (g & 1));
+      d3[jt] = mfma_bf16(a, b, d3[jt]);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
 // Y rows of the wave's 16-edge tile into LDS: sy[row][m], row pitch kYPitch.
 // Lane l moves float4 number l%4 of row l/4.
 __device__ __forceinline__ void stage_y(const float* __restrict__ Y, int e0, int e_end, float* sy) {
@@ -113,7 +207,7 @@ __device__ __forceinline__ void read_y(const float* sy, int row, float* y) {
   }
 }
 
-template <int LHMAX, int NW = TprShape<LHMAX, false>::waves>
+template <int LHMAX, bool RB, int NW = TprShape<LHMAX, false>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
 tpr_fwd_kernel(
@@ -123,10 +217,12 @@ tpr_fwd_kernel(
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
-  __shared__ float sW[P * 16 * kWPitch];
+  constexpr int kSlice = RB ? (P * 16 * kWbPitch + 1) / 2 : P * 16 * kWPitch;   // floats
+  __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
   const int ct = blockIdx.y;
-  load_w3_slice<P>(W3, K, ct, sW);
+  if constexpr (RB) load_w3_slice_bf16<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW), nullptr);
+  else load_w3_slice<P>(W3, K, ct, sW);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int g = l >> 4;
@@ -140,7 +236,8 @@ tpr_fwd_kernel(
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
       stage_y(Y, e0, e_end, sy);
       f4 r[P];
-      tile_radial<P>(a3, e0, e_end, sW, r);
+      if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      else tile_radial<P>(a3, e0, e_end, sW, r);
       // lane group 0 holds the tile's first edges, so nq covers every valid one;
       // the scheduling barrier keeps one edge's operands live at a time
       const int nq = min(4, e_end - e0);
@@ -215,7 +312,7 @@ __device__ __forceinline__ float group_reduce16(float* v, int lane) {
 //   da3[e][j]     += sum_{p,k} dR[e][p][k] W3[j][p K + k]           (channel-tile partial)
 // The partials of channel tile ct go to dYp[ct][e][16] and da3p[ct][e][64];
 // their sum over tiles (fixed order) is taken by the hidden-layer backward.
-template <int LHMAX, int NW = TprShape<LHMAX, true>::waves>
+template <int LHMAX, bool RB, int NW = TprShape<LHMAX, true>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true>::per_simd, TprShape<LHMAX, true>::per_simd)))
 tpr_bwd_kernel(
@@ -226,11 +323,15 @@ tpr_bwd_kernel(
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
-  __shared__ float sW[P * 16 * kWPitch];
+  constexpr int kSlice = RB ? (P * 16 * kWbPitch + P * 64 * kWtPitch + 1) / 2 : P * 16 * kWPitch;   // floats
+  __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
-  __shared__ float sT[NW][16 * kTPitch];
+  __shared__ __align__(16) float sT[NW][RB ? 2 * 16 * kT2Pitch : 16 * kTPitch];
+  unsigned short* sWb = reinterpret_cast<unsigned short*>(sW);
+  unsigned short* sWt = sWb + P * 16 * kWbPitch;
   const int ct = blockIdx.y;
-  load_w3_slice<P>(W3, K, ct, sW);
+  if constexpr (RB) load_w3_slice_bf16<P>(W3, K, ct, sWb, sWt);
+  else load_w3_slice<P>(W3, K, ct, sW);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int g = l >> 4, kk = l & 15;
@@ -247,7 +348,8 @@ tpr_bwd_kernel(
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
       stage_y(Y, e0, e_end, sy);
       f4 r[P];   // R on entry; dR (zero for edges past e_end) after the edge loop
-      tile_radial<P>(a3, e0, e_end, sW, r);
+      if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, sWb, r);
+      else tile_radial<P>(a3, e0, e_end, sW, r);
       const int nq = min(4, e_end - e0);
       static_for<0, 4>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
@@ -307,28 +409,32 @@ tpr_bwd_kernel(
       });
       // da3 partial: D[e][j] = sum_{p, k} dR[e][p][k] W3[j][p K + 16 ct + k]. The
       // A operand wants the edge on l%16, so each dR tile is transposed through LDS.
-      __builtin_amdgcn_s_setprio(1);
       f4 d3[4];
+      if constexpr (RB) {
+        tile_da3_bf16<P>(r, sWt, tw, d3);
+      } else {
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int p = 0; p < P; ++p) {
-        __builtin_amdgcn_sched_barrier(0);
+        for (int p = 0; p < P; ++p) {
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) tw[(4 * g + q) * kTPitch + kk] = r[p][q];
-        __builtin_amdgcn_wave_barrier();
-        float av[4];
+          for (int q = 0; q < 4; ++q) tw[(4 * g + q) * kTPitch + kk] = r[p][q];
+          __builtin_amdgcn_wave_barrier();
+          float av[4];
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) av[kq] = tw[kk * kTPitch + 4 * kq + g];
-        __builtin_amdgcn_wave_barrier();
+          for (int kq = 0; kq < 4; ++kq) av[kq] = tw[kk * kTPitch + 4 * kq + g];
+          __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int kq = 0; kq < 4; ++kq) {
-          const float* wrow = sW + (p * 16 + 4 * kq + g) * kWPitch + kk;
+          for (int kq = 0; kq < 4; ++kq) {
+            const float* wrow = sW + (p * 16 + 4 * kq + g) * kWPitch + kk;
 #pragma unroll
-          for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(av[kq], wrow[16 * jt], d3[jt]);
+            for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(av[kq], wrow[16 * jt], d3[jt]);
+          }
         }
+        __builtin_amdgcn_s_setprio(0);
       }
-      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int e = e0 + 4 * g + rr;
@@ -350,47 +456,61 @@ int tpr_grid_x(int N, int n_ct, int waves, int blocks_per_cu) {
   return std::max(1, std::min(want, (N + waves - 1) / waves));
 }
 
-template <int LH>
+template <int LH, bool RB>
 void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c, float* At) {
   using S = TprShape<LH, false>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
-  tpr_fwd_kernel<LH><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
+  tpr_fwd_kernel<LH, RB><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
 }
 
-template <int LH>
+template <int LH, bool RB>
 void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
                     const float* dAt, float* dYp, float* Q, float* da3p) {
   using S = TprShape<LH, true>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
-  tpr_bwd_kernel<LH><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
+  tpr_bwd_kernel<LH, RB><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
                                                     Q, da3p);
 }
 }  // namespace
 
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At) {
+                    float inv_c, float* At, int radial_bf16) {
   if (N <= 0) return;
+#define MACE_TPRF(LH)                                                                                  \
+  case LH:                                                                                             \
+    if (radial_bf16) tpr_fwd_launch<LH, true>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
+    else tpr_fwd_launch<LH, false>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);            \
+    break;
   switch (lh_max) {
-    case 0: tpr_fwd_launch<0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
-    case 1: tpr_fwd_launch<1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
-    case 2: tpr_fwd_launch<2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); break;
+    MACE_TPRF(0)
+    MACE_TPRF(1)
+    MACE_TPRF(2)
   }
+#undef MACE_TPRF
 }
 
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p) {
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_bf16) {
   if (N <= 0 || E <= 0) return;
+#define MACE_TPRB(LH)                                                                                       \
+  case LH:                                                                                                  \
+    if (radial_bf16)                                                                                        \
+      tpr_bwd_launch<LH, true>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p);  \
+    else                                                                                                    \
+      tpr_bwd_launch<LH, false>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); \
+    break;
   switch (lh_max) {
-    case 0: tpr_bwd_launch<0>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
-    case 1: tpr_bwd_launch<1>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
-    case 2: tpr_bwd_launch<2>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); break;
+    MACE_TPRB(0)
+    MACE_TPRB(1)
+    MACE_TPRB(2)
   }
+#undef MACE_TPRB
 }
 
 }  // namespace mace

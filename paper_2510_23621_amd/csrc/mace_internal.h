@@ -35,6 +35,14 @@ __host__ __device__ __forceinline__ float bf16_round(float x) {
   return r;
 }
 
+// bfloat16 bits of x rounded to nearest even (MFMA operands)
+__host__ __device__ __forceinline__ unsigned short bf16_bits(float x) {
+  const float r = bf16_round(x);
+  unsigned int u;
+  __builtin_memcpy(&u, &r, 4);
+  return (unsigned short)(u >> 16);
+}
+
 // Round-to-nearest-even float -> IEEE binary16 -> float (FP16-linear mode);
 // magnitudes beyond the binary16 range become infinite.
 __host__ __device__ __forceinline__ float fp16_round(float x) { return (float)(_Float16)x; }
@@ -306,10 +314,10 @@ void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, con
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At);
+                    float inv_c, float* At, int radial_bf16);
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p);
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_bf16);
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
 struct SymW {

@@ -16,7 +16,7 @@ STRESS = dict(c_norm=1.0)
 STRESS_GAINS = {".radial.3": 4.0}
 
 TOL = {B.MACE_FP32: dict(energy=1e-6, forces=1e-5), B.MACE_BF16_LINEAR: dict(energy=5e-3, forces=2e-2),
-       B.MACE_FP16_LINEAR: dict(energy=5e-3, forces=2e-2)}
+       B.MACE_FP16_LINEAR: dict(energy=5e-3, forces=2e-2), B.MACE_BF16_RADIAL: dict(energy=5e-3, forces=2e-2)}
 
 
 def lib_blob(params: dict, seed: int, gains=None) -> np.ndarray:
@@ -55,13 +55,14 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     return outs if repeats > 1 else outs[0]
 
 
-def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True, fp16=False):
-    return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16, forces=forces,
-                              fp16_linear=fp16)
+def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True, fp16=False, bf16_radial=False):
+    return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16 or bf16_radial,
+                              forces=forces, fp16_linear=fp16, bf16_radial=bf16_radial)
 
 
-def oracle_stress(params: dict, system, blob: np.ndarray, bf16=False, fp16=False):
-    return mace.stress(mace.ModelDesc(**params), blob, system, bf16_linear=bf16, fp16_linear=fp16)
+def oracle_stress(params: dict, system, blob: np.ndarray, bf16=False, fp16=False, bf16_radial=False):
+    return mace.stress(mace.ModelDesc(**params), blob, system, bf16_linear=bf16 or bf16_radial, fp16_linear=fp16,
+                       bf16_radial=bf16_radial)
 
 
 def stress_error(gpu_stress: np.ndarray, ref_stress: np.ndarray) -> float:

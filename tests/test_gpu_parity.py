@@ -198,3 +198,33 @@ def test_fp16_linear_vs_fp64_and_emulation(case):
     gb = run_gpu(params, sysm, bl, prec=B.MACE_BF16_LINEAR)
     assert errors(g16, ref)["forces"] < errors(gb, ref)["forces"]
 
+
+@pytest.mark.parametrize("case", ["water96_stress_inputs", "water102_k128_l2", "molecules12_k64"])
+def test_bf16_radial_vs_fp64_and_emulation(case):
+    """BF16-radial mode (BF16-linear, and the wide last radial layer on BF16
+    MFMA in both directions): against the FP64 oracle at the 16-bit
+    tolerances, and against the oracle's emulation (which does not round dE/dR
+    in the backward product, hence the looser force bound)."""
+    if case == "molecules12_k64":
+        params = model_params(4, K=64, **STRESS)
+        sysm = synth.molecule_batch(12, seed=2)
+    elif case == "water102_k128_l2":
+        params = model_params(0, K=128, hidden_lmax=2, **STRESS)
+        sysm = synth.water_box(34, seed=7, box=10.0)
+    else:
+        params = model_params(0, **STRESS)
+        sysm = make_system(0, seed=0)
+    bo = oracle_blob(params, 8, STRESS_GAINS)
+    bl = lib_blob(params, 8, STRESS_GAINS)
+    ref = run_oracle(params, sysm, bo)
+    gr = run_gpu(params, sysm, bl, prec=B.MACE_BF16_RADIAL, stress=True)
+    assert_parity(gr, ref, B.MACE_BF16_RADIAL, f"{case} bf16-radial vs fp64")
+    emu = run_oracle(params, sysm, bo, bf16_radial=True)
+    err = errors(gr, emu)
+    print(f"[parity] {case} bf16-radial gpu vs emulating oracle {err}", flush=True)
+    assert err["energy"] <= 1e-3 and err["forces"] <= 1e-2, err
+    if case == "water96_stress_inputs":
+        se = stress_error(gr["stress"], oracle_stress(params, sysm, bo, bf16_radial=True))
+        print(f"[parity] {case} bf16-radial stress vs emulating oracle {se:.3e}", flush=True)
+        assert se <= 2e-2, se
+

@@ -484,3 +484,19 @@ def test_16bit_linear_modes_stay_close_to_fp64():
                      np.linalg.norm(out["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"]))
     assert dev["fp16"][1] < dev["bf16"][1] and dev["fp16"][1] < 2e-3 and dev["bf16"][1] < 2e-2, dev
     assert dev["fp16"][0] < dev["bf16"][0] + 1e-9, dev
+
+
+def test_bf16_radial_mode_rounds_the_last_radial_product():
+    """R13: BF16-radial changes the result relative to BF16-linear (the
+    rounding of the last radial product takes effect) but stays within the
+    16-bit force tolerance of FP64 (the rounding itself is pinned by the
+    bfloat16 nearest-even values above)."""
+    d = _desc(0)
+    blob = synth.weight_blob(mace.weight_layout(d), 4)
+    system = make_system(0, seed=0)
+    ref = mace.energy_forces(d, blob, system)
+    lin = mace.energy_forces(d, blob, system, graph=ref["graph"], bf16_linear=True)
+    rad = mace.energy_forces(d, blob, system, graph=ref["graph"], bf16_linear=True, bf16_radial=True)
+    assert not np.array_equal(lin["forces"], rad["forces"])
+    fdev = np.linalg.norm(rad["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"])
+    assert fdev < 2e-2, fdev
