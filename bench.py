@@ -86,6 +86,28 @@ def kernel_work(name, model, N, E):
     return tot_b, tot_f
 
 
+def linear_roofline(B, g, pos, stream, steps, prec, kid):
+    """The channel-mixing linears (every linear_kernel launch of a step):
+    algorithmic flops and bytes (summed by the library from the launch plans)
+    over their HIP-event time, against the MFMA peak of the mode's operand
+    type and against HBM bandwidth."""
+    eps, Eg, F = g.outputs(True)
+    B.mace_profile_select(g.handle, kid)
+    for _ in range(steps):
+        B.mace_forces(g.handle, pos, eps, Eg, F, stream)
+    ms, launches = B.mace_profile_read(g.handle)
+    flops, byts = B.mace_profile_work(g.handle)
+    B.mace_profile_select(g.handle, -1)
+    peak = FP32_MFMA_PEAK_TFLOPS if prec == B.MACE_FP32 else BF16_MFMA_PEAK_TFLOPS
+    tfl = flops / (ms * 1e-3) / 1e12
+    gbs = byts / (ms * 1e-3) / 1e9
+    return {"launches_per_step": launches / steps, "avg_launch_ms": round(ms / max(launches, 1), 5),
+            "ms_per_step": round(ms / steps, 4), "flops_per_step": int(flops / steps),
+            "bytes_per_step": int(byts / steps), "achieved_tflops": round(tfl, 2),
+            "mfma_peak_tflops": peak, "mfma_frac": round(tfl / peak, 4),
+            "achieved_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def cpu_baseline(params, seconds_hint=15.0, max_reps=10):
     """FP64 oracle E+F on a 64-molecule periodic water box with the same
     model (a bounded sample of the workload; atoms/s scales with atoms),
@@ -113,8 +135,8 @@ def cpu_baseline(params, seconds_hint=15.0, max_reps=10):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--prec", choices=["fp32", "bf16", "fp16", "bf16radial"], default="fp32")
     ap.add_argument("--kernel", default="auto", help="kernel class whose roofline is reported")
@@ -214,8 +236,8 @@ def main():
                  "algorithmic_flops_per_launch": int(flops_per_launch),
                  "kernel_share_of_step": round(k_ms / total_ms, 4)})
 
-    # outside the timed region: per-call spread, the forward pass alone, and
-    # the other precision mode on the same workload
+    # outside the timed region: per-call spread, the linears' roofline, the
+    # forward pass alone, and the other precision modes on the same workload
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     for a, b in evs:
         a.record(stream)
@@ -223,6 +245,7 @@ def main():
         b.record(stream)
     torch.cuda.synchronize()
     per_call = np.array([a.elapsed_time(b) for a, b in evs])
+    linears = {prec: linear_roofline(B, g, pos, stream, args.steps, prec, kids["linear_kernel"])}
     f0 = torch.cuda.Event(enable_timing=True)
     f1 = torch.cuda.Event(enable_timing=True)
     for _ in range(args.warmup):
@@ -252,6 +275,7 @@ def main():
         other_ms = f0.elapsed_time(f1) / args.steps
         others[oname] = {"atoms_per_s": round(N / (other_ms * 1e-3), 1), "edges_per_s": round(E / (other_ms * 1e-3), 1),
                          "ms_per_step": round(other_ms, 4)}
+        linears[other] = linear_roofline(B, g2, pos, stream, args.steps, other, kids["linear_kernel"])
         g2.close()
 
     out = {
@@ -271,6 +295,8 @@ def main():
         "step_ms_p10_p50_p90": [round(float(np.percentile(per_call, q)), 4) for q in (10, 50, 90)],
         "forward_only": {"atoms_per_s": round(N / (fwd_ms * 1e-3), 1), "ms": round(fwd_ms, 4)},
         "other_precisions": others,
+        "linears": {name: linears[p] for p, name in ((B.MACE_FP32, "fp32"), (B.MACE_BF16_LINEAR, "bf16_linear"),
+                                                      (B.MACE_FP16_LINEAR, "fp16_linear")) if p in linears},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params)

@@ -138,6 +138,16 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
 mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                                float* forces, double* stress, void* stream);
 
+/* Device-detected errors of the calls enqueued since setup or the previous
+ * check: the edge kernels OR status bits into a word of the workspace,
+ * 1 = an edge vector with a non-finite component (NaN or infinite
+ * positions), 2 = an edge of length zero (coincident atoms).  After such a
+ * call the outputs are undefined but the handle stays valid.  Enqueues a
+ * read and a reset of the word on stream, waits for the stream, stores the
+ * bits in *device_flags (host, may be NULL) and returns MACE_ENONFINITE if
+ * flag 1 is set, else MACE_ERANGE if flag 2 is set, else MACE_OK. */
+mace_status mace_graph_check(mace_graph* g, int32_t* device_flags, void* stream);
+
 /* Releases the host handle (the workspace stays the caller's). */
 void mace_graph_destroy(mace_graph* g);
 
@@ -154,6 +164,13 @@ const char* mace_status_string(mace_status s);
 mace_status mace_profile_select(mace_graph* g, int32_t kernel);
 mace_status mace_profile_read(mace_graph* g, double* total_ms, int64_t* launches);
 const char* mace_kernel_name(int32_t kernel);
+/* Algorithmic work of the selected class's launches since the last select
+ * (host outputs; not reset by mace_profile_read).  Summed for the linear
+ * class only (0 for the others): flops = 2 K^2 per node and weight term
+ * component; bytes = each distinct input component, output component and
+ * weight block moved once (outputs read too when accumulated into or when a
+ * residual is added; 16-bit weights count 2 bytes). */
+mace_status mace_profile_work(mace_graph* g, double* flops, double* bytes);
 
 /* Table export for checking the library's couplings (host). */
 /* real CG C^{l3}_{l1 l2}[m1][m2][m3] into out (host) [(2l1+1)(2l2+1)(2l3+1)] */

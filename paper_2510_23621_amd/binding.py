@@ -25,7 +25,7 @@ STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE
 EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", "mace_graph_setup",
             "mace_forward_energy", "mace_forces", "mace_forces_stress", "mace_graph_destroy", "mace_status_string",
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
-            "mace_profile_read", "mace_kernel_name"]
+            "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work"]
 
 
 class MaceError(RuntimeError):
@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         L.mace_forces.argtypes = [P, P, P, P, P, P]
         L.mace_forces_stress.argtypes = [P, P, P, P, P, P, P]
         L.mace_graph_destroy.argtypes = [P]
+        L.mace_graph_check.argtypes = [P, P, P]
+        L.mace_profile_work.argtypes = [P, P, P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
         L.mace_status_string.restype = ctypes.c_char_p
@@ -184,6 +186,17 @@ def mace_forces_stress(handle, positions, node_energy, graph_energy, forces, str
                                     _ptr(stress), _stream(stream)), "mace_forces_stress")
 
 
+def mace_graph_check(handle, stream=None):
+    """(status, flags): the status code and the device status bits since setup
+    or the previous check (1 non-finite edge vector, 2 zero-length edge); the
+    word is reset. Returns the status instead of raising."""
+    flags = ctypes.c_int32(0)
+    code = lib().mace_graph_check(handle, ctypes.byref(flags), _stream(stream))
+    if code == -4 or code == -1:
+        _check(code, "mace_graph_check")
+    return code, flags.value
+
+
 def mace_graph_destroy(handle):
     if handle:
         lib().mace_graph_destroy(handle)
@@ -228,6 +241,13 @@ def mace_profile_read(handle):
     n = ctypes.c_int64()
     _check(lib().mace_profile_read(handle, ctypes.byref(ms), ctypes.byref(n)), "mace_profile_read")
     return ms.value, n.value
+
+
+def mace_profile_work(handle):
+    """(flops, bytes): algorithmic work of the selected class's launches."""
+    f, b = ctypes.c_double(0), ctypes.c_double(0)
+    _check(lib().mace_profile_work(handle, ctypes.byref(f), ctypes.byref(b)), "mace_profile_work")
+    return f.value, b.value
 
 
 def mace_kernel_name(kernel: int) -> str:

@@ -172,6 +172,7 @@ struct Buffers {
   float *da3p = nullptr, *dYp = nullptr;   // per-channel-tile partials [K/16][E][64], [K/16][E][16]
   float4* g = nullptr;
   double* inv_vol = nullptr;      // [G] 1/|det cell|, or 1 without cells
+  int* status = nullptr;          // device status word (kStatus* bits)
   LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 4
 };
 
@@ -236,6 +237,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.g = c.take<float4>(std::max<int64_t>(E, 1));
   b.inv_vol = c.take<double>(G);
   b.lin_dev = c.take<LinLaunch>(6 * T + 4);
+  b.status = c.take<int>(64);
 }
 
 }  // namespace
@@ -257,6 +259,7 @@ struct mace_graph {
   std::vector<hipEvent_t> prof_ev;   // 2 * kProfPairs
   int prof_used = 0;
   int64_t prof_dropped = 0;
+  double prof_flops = 0.0, prof_bytes = 0.0;   // algorithmic work of the profiled launches
   Model m;
   Buffers b;
   int64_t N = 0, E = 0;
@@ -290,6 +293,19 @@ struct ProfScope {
   }
 };
 #define PROF(kid) ProfScope _prof_##__LINE__(h, kid, s)
+
+// A linear launch, bracketed for profiling; while the linear class is
+// selected its algorithmic work is summed too.
+void run_linear(mace_graph* h, hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
+  ProfScope ps(h, KID_LINEAR, s);
+  if (ps.on && a.n_quads > 0 && P.host.plan.n_groups > 0) {
+    double f = 0.0, b = 0.0;
+    linear_work(P.host.plan, a, h->N, h->m.d.n_species, &f, &b);
+    h->prof_flops += f;
+    h->prof_bytes += b;
+  }
+  launch_linear(s, P, a);
+}
 
 mace_status hip_ok(hipError_t e) { return e == hipSuccess ? MACE_OK : MACE_EHIP; }
 
@@ -478,7 +494,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       }
       // (a later chunk recomputes the same Y and rbf)
       launch_edge_prologue(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf,
-                           rs);
+                           rs, b.status);
     }
   }
   const float inv_c = (float)(1.0 / m.d.c_norm);
@@ -492,8 +508,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       src_map = b.species;
     } else {
       {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->upskip[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0, nullptr, b.sc));
+        run_linear(h, s, h->upskip[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0, nullptr, b.sc));
       }
       src = b.ht[t];
       src_map = nullptr;
@@ -504,21 +519,17 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
                      src, inv_c, b.At, h->prec == MACE_BF16_RADIAL);
     }
     if (t == 0 && !lowp) {
-      PROF(KID_LINEAR);
-      launch_linear(s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
+      run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
     } else if (t == 0) {   // 16-bit linears: each linear rounds its own inputs and weights
       {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
+        run_linear(h, s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
       }
       {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->skip0, largs(h, b.Apre, b.A[t], nullptr, false, 0));
+        run_linear(h, s, h->skip0, largs(h, b.Apre, b.A[t], nullptr, false, 0));
       }
     } else {
       {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->lin[t], largs(h, b.At, b.A[t], nullptr, false, 0));
+        run_linear(h, s, h->lin[t], largs(h, b.At, b.A[t], nullptr, false, 0));
       }
     }
     {
@@ -527,8 +538,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     }
     float* hout = L.last ? b.hlast : b.hin[t + 1];
     {
-      PROF(KID_LINEAR);
-      launch_linear(s, h->prod[t], largs(h, b.B, hout, t > 0 ? b.sc : nullptr, false, 0));
+      run_linear(h, s, h->prod[t], largs(h, b.B, hout, t > 0 ? b.sc : nullptr, false, 0));
     }
     if (!L.last)
       {
@@ -575,27 +585,23 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       }
     }
     {
-      PROF(KID_LINEAR);
-      launch_linear(s, h->prodT[t], largs(h, dnext, b.dB, nullptr, true, 0));
+      run_linear(h, s, h->prodT[t], largs(h, dnext, b.dB, nullptr, true, 0));
     }
     {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
     }
     if (t == 0 && !lowp) {
-      PROF(KID_LINEAR);
-      launch_linear(s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
+      run_linear(h, s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
     } else {
       const float* dApre = b.dA;
       if (t == 0) {
         {
-          PROF(KID_LINEAR);
-          launch_linear(s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
+          run_linear(h, s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
         }
         dApre = b.dApre;
       }
-      PROF(KID_LINEAR);
-      launch_linear(s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
+      run_linear(h, s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
     }
     const float* src = t == 0 ? b.sp_table : b.ht[t];
     const int* src_map = t == 0 ? b.species : nullptr;
@@ -617,8 +623,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
         launch_sender_sum(s, N, L.din, K, b.snd_off, b.snd_perm, b.Q, b.dht);
       }
       {
-        PROF(KID_LINEAR);
-        launch_linear(s, h->upskipT[t], largs(h, b.dht, dprev, nullptr, true, 0, dnext));
+        run_linear(h, s, h->upskipT[t], largs(h, b.dht, dprev, nullptr, true, 0, dnext));
       }
       std::swap(dnext, dprev);
     }
@@ -908,6 +913,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(up(b.quad_tile, qtile.data(), qtile.size() * 4));
   chk(up(b.quad_count, qcount.data(), qcount.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
+  chk(hipMemsetAsync(b.status, 0, sizeof(int), s));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
                        lowp_mode(prec), b.sp_table);
   chk(hipGetLastError());
@@ -967,6 +973,19 @@ mace_status mace_forces_stress(mace_graph* g, const float* positions, float* nod
   return hip_ok(hipGetLastError());
 }
 
+mace_status mace_graph_check(mace_graph* g, int32_t* device_flags, void* stream) {
+  if (!g) return MACE_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  int flags = 0;
+  if (hipMemcpyAsync(&flags, g->b.status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipMemsetAsync(g->b.status, 0, sizeof(int), s) != hipSuccess || hipStreamSynchronize(s) != hipSuccess)
+    return MACE_EHIP;
+  if (device_flags) *device_flags = flags;
+  if (flags & kStatusNonFinite) return MACE_ENONFINITE;
+  if (flags & kStatusZeroLength) return MACE_ERANGE;
+  return MACE_OK;
+}
+
 void mace_graph_destroy(mace_graph* g) {
   if (!g) return;
   for (auto e : g->prof_ev) hipEventDestroy(e);
@@ -983,6 +1002,14 @@ mace_status mace_profile_select(mace_graph* g, int32_t kernel) {
   g->prof_kernel = kernel;
   g->prof_used = 0;
   g->prof_dropped = 0;
+  g->prof_flops = g->prof_bytes = 0.0;
+  return MACE_OK;
+}
+
+mace_status mace_profile_work(mace_graph* g, double* flops, double* bytes) {
+  if (!g || !flops || !bytes) return MACE_EINVAL;
+  *flops = g->prof_flops;
+  *bytes = g->prof_bytes;
   return MACE_OK;
 }
 

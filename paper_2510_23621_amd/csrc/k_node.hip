@@ -1,6 +1,9 @@
 // Node-level kernels: the channel-mixing linears (linear_up, path-merging
 // linear, species-dependent linears, product-basis linear and their
 // transposes), readouts, per-graph energy sums, the layer-0 species table.
+#include <set>
+#include <utility>
+
 #include "mace_internal.h"
 
 namespace mace {
@@ -166,6 +169,29 @@ LinLaunch make_lin_launch(const LinPlan& plan) {
     }
   L.n_gc = n;
   return L;
+}
+
+void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, double* flops, double* bytes) {
+  const double K = a.K, row = (double)N * K * 4.0;
+  const double wbytes = K * K * (a.lowp ? 2.0 : 4.0);
+  std::set<std::pair<int, int>> in_comp;
+  std::set<std::pair<int64_t, int>> wblk;
+  double f = 0.0, b = 0.0;
+  for (int gi = 0; gi < p.n_groups; ++gi) {
+    const LinGroup& g = p.g[gi];
+    for (int ti = g.t0; ti < g.t1; ++ti) {
+      const LinTerm& t = p.t[ti];
+      f += 2.0 * K * K * (double)N * g.ncomp;
+      for (int c = 0; c < g.ncomp; ++c) in_comp.insert({t.src, t.in_c0 + c});
+      wblk.insert({t.w_off, t.species});
+    }
+    const bool resid = a.residual && g.dst == 0;
+    b += g.ncomp * row * (1.0 + (a.accumulate ? 1.0 : 0.0) + (resid ? 1.0 : 0.0));
+  }
+  b += in_comp.size() * row;
+  for (const auto& w : wblk) b += wbytes * (w.second ? n_species : 1);
+  *flops = f;
+  *bytes = b;
 }
 
 void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {

@@ -111,7 +111,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
                                                             const int* __restrict__ snd, const int* __restrict__ rcv,
                                                             const double4* __restrict__ shift, double rc, int p,
                                                             int nb, float* __restrict__ Y, float* __restrict__ rbf,
-                                                            RadialSet rs) {
+                                                            RadialSet rs, int* __restrict__ status) {
   __shared__ float xs[kTE * kXPad];
   __shared__ float ha[kTE * kPad];
   __shared__ float hb[kTE * kPad];
@@ -127,7 +127,8 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
     for (int i = 0; i < kXPad; ++i) row[i] = 0.f;
     if (e < E) {
       float y[16];
-      edge_geometry(e, pos, snd, rcv, shift, rc, p, nb, y, row);
+      const int bad = edge_geometry(e, pos, snd, rcv, shift, rc, p, nb, y, row);
+      if (bad) atomicOr(status, bad);
       float4* Yv = reinterpret_cast<float4*>(Y + (size_t)e * 16);
 #pragma unroll
       for (int v = 0; v < 4; ++v) Yv[v] = make_float4(y[4 * v], y[4 * v + 1], y[4 * v + 2], y[4 * v + 3]);
@@ -266,11 +267,11 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
 
 void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
                           const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
-                          const RadialSet& rs) {
+                          const RadialSet& rs, int* status) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
-  if (nb <= 8) edge_prologue_kernel<8><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs);
-  else edge_prologue_kernel<16><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs);
+  if (nb <= 8) edge_prologue_kernel<8><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
+  else edge_prologue_kernel<16><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
 }
 
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,

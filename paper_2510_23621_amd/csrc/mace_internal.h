@@ -7,6 +7,11 @@
 
 namespace mace {
 
+// Device status bits, OR-ed into one word of the workspace by the kernels
+// that detect the condition and read back by mace_graph_check.
+constexpr int kStatusNonFinite = 1;    // an edge vector with a NaN or infinite component
+constexpr int kStatusZeroLength = 2;   // an edge of length 0 (coincident atoms)
+
 constexpr int kMaxTerms = 48;
 constexpr int kMaxGroups = 24;
 constexpr int kLinTileNodes = 16;   // nodes per MFMA tile of the channel-mixing linear
@@ -212,9 +217,11 @@ __device__ __forceinline__ float4 edge_geometry_vjp(int e, const float* __restri
 // shift, r = |d|, u = d / r; Y[16] (real harmonics of u) and eb[nb] (radial
 // basis times envelope). The periodic shift and the difference of wrapped
 // positions would otherwise carry FP32 rounding into every edge.
-__device__ __forceinline__ void edge_geometry(int e, const float* __restrict__ pos, const int* __restrict__ snd,
-                                              const int* __restrict__ rcv, const double4* __restrict__ shift,
-                                              double rc, int p, int nb, float* yout, float* ebout) {
+// Returns the edge's device status bits: kStatusNonFinite when d is not
+// finite, kStatusZeroLength when r = 0 (coincident atoms); 0 otherwise.
+__device__ __forceinline__ int edge_geometry(int e, const float* __restrict__ pos, const int* __restrict__ snd,
+                                             const int* __restrict__ rcv, const double4* __restrict__ shift,
+                                             double rc, int p, int nb, float* yout, float* ebout) {
   const int s = snd[e], r = rcv[e];
   const double4 sh = shift[e];
   const double dx = ((double)pos[3 * s + 0] - (double)pos[3 * r + 0]) + sh.x;
@@ -228,6 +235,7 @@ __device__ __forceinline__ void edge_geometry(int e, const float* __restrict__ p
   double eb[16];
   bessel_env<double>(rr, rc, p, nb, eb);
   for (int n = 0; n < nb; ++n) ebout[n] = (float)eb[n];
+  return !isfinite(rr) ? kStatusNonFinite : (rr == 0.0 ? kStatusZeroLength : 0);
 }
 
 // --------------------------------------------------------------- launchers
@@ -302,7 +310,7 @@ struct RadialSet {
 };
 void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
                           const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
-                          const RadialSet& rs);
+                          const RadialSet& rs, int* status);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
@@ -328,6 +336,11 @@ void launch_symcon_fwd(hipStream_t s, int lout_max, int N, int K, const int* spe
 void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
                        SymW w, const float* dB, float* dA);
 void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
+// Algorithmic work of one linear launch over N nodes: flops = 2 K^2 per
+// (node, term component); bytes = every distinct input component and weight
+// block read once, every output component written once (read too when
+// accumulating or adding the residual).
+void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, double* flops, double* bytes);
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
                         const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,

@@ -67,6 +67,10 @@ class MaceGraph:
         B.mace_forces_stress(self.handle, pos, eps, E, F, S, stream)
         return eps, E, F, S
 
+    def check(self, stream=None):
+        """(status, flags) of the device checks since setup or the last check."""
+        return B.mace_graph_check(self.handle, stream)
+
     def close(self):
         if getattr(self, "handle", None):
             B.mace_graph_destroy(self.handle)

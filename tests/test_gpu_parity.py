@@ -228,3 +228,39 @@ def test_bf16_radial_vs_fp64_and_emulation(case):
         print(f"[parity] {case} bf16-radial stress vs emulating oracle {se:.3e}", flush=True)
         assert se <= 2e-2, se
 
+
+def test_device_status_word_flags_bad_positions():
+    """Device-detected errors: a NaN coordinate sets flag 1 (MACE_ENONFINITE),
+    two atoms joined by an edge moved onto each other set flag 2
+    (MACE_ERANGE); the check resets the word and a later good call reads
+    clean, with the same outputs as before."""
+    from paper_2510_23621_amd.graph import MaceGraph
+    params = model_params(0)
+    sysm = make_system(0, seed=0)
+    bl = lib_blob(params, 8)
+    snd, rcv, sh = B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells)
+    g = MaceGraph(B.make_desc(**params), bl, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                  sh, sysm.cells, None, 1, B.MACE_FP32)
+    pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
+    _, E0, F0 = g.energy_forces(pos)
+    assert g.check() == (0, 0)
+    bad = pos.clone()
+    bad[5, 1] = float("nan")
+    g.energy_forces(bad)
+    code, flags = g.check()
+    print(f"[status] nan position -> {code} {flags}", flush=True)
+    assert flags & 1 and code == -5
+    assert g.check() == (0, 0)
+    # move the sender of an edge without periodic shift onto its receiver: d = 0
+    e0 = int(np.flatnonzero((sh == 0).all(axis=1))[0])
+    bad = pos.clone()
+    bad[int(snd[e0])] = bad[int(rcv[e0])]
+    g.energy(bad)
+    code, flags = g.check()
+    print(f"[status] coincident atoms -> {code} {flags}", flush=True)
+    assert flags == 2 and code == -2
+    _, E1, F1 = g.energy_forces(pos)
+    assert g.check() == (0, 0)
+    assert torch.equal(E0, E1) and torch.equal(F0, F1)
+    g.close()
+
