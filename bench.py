@@ -278,6 +278,23 @@ def main():
         linears[other] = linear_roofline(B, g2, pos, stream, args.steps, other, kids["linear_kernel"])
         g2.close()
 
+    # the device neighbour list of the same system (outside the timed region)
+    dpos = torch.from_numpy(np.ascontiguousarray(sysm.positions, dtype=np.float64)).cuda()
+    goff = None
+    if sysm.n_graphs > 1:
+        goff = np.concatenate([[0], np.cumsum(np.bincount(sysm.graph_of_atom, minlength=sysm.n_graphs))])
+    nl_ms = []
+    for _ in range(6):
+        torch.cuda.synchronize()
+        t_a = time.perf_counter()
+        s_d, _, _ = B.mace_neighbor_list_device(dpos, params["r_cut"], sysm.cells, goff, sysm.n_graphs, max_edges=E)
+        torch.cuda.synchronize()
+        nl_ms.append((time.perf_counter() - t_a) * 1e3)
+    t_a = time.perf_counter()
+    B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells, sysm.graph_of_atom, sysm.n_graphs)
+    host_nl_ms = (time.perf_counter() - t_a) * 1e3
+    assert len(s_d) == E
+
     out = {
         "metric": "atoms/s and edges/s for MACE energy+forces (FP32, BF16-linear); % roofline",
         "value": round(N * args.steps / (total_ms * 1e-3), 1),
@@ -295,6 +312,9 @@ def main():
         "step_ms_p10_p50_p90": [round(float(np.percentile(per_call, q)), 4) for q in (10, 50, 90)],
         "forward_only": {"atoms_per_s": round(N / (fwd_ms * 1e-3), 1), "ms": round(fwd_ms, 4)},
         "other_precisions": others,
+        "neighbor_list": {"device_ms_median": round(float(np.median(nl_ms[1:])), 3),
+                          "host_ms": round(host_nl_ms, 2), "edges": E,
+                          "note": "wall time of one call incl. workspace allocation and the edge-count read-back"},
         "linears": {name: linears[p] for p, name in ((B.MACE_FP32, "fp32"), (B.MACE_BF16_LINEAR, "bf16_linear"),
                                                       (B.MACE_FP16_LINEAR, "fp16_linear")) if p in linears},
     }

@@ -102,6 +102,27 @@ mace_status mace_neighbor_list(int64_t n_atoms, const double* positions, const d
                                const int32_t* graph_of_atom, int32_t n_graphs, double r_cut, int64_t max_edges,
                                int32_t* sender, int32_t* receiver, int32_t* shifts, int64_t* n_edges);
 
+/* The same neighbour list built on the device (FP64 hashed cell list; the
+ * same cutoff expression, evaluated without fused multiply-adds, so the
+ * output equals mace_neighbor_list's element for element).  positions (dev)
+ * [N][3] FP64, |coordinates| <= 1e9; cells (host) [G][3][3] rows = lattice
+ * vectors, or NULL; graph_offsets (host) [G+1] (atoms of graph g are
+ * [off[g], off[g+1]), off[0] = 0, off[G] = N) or NULL for one graph.
+ * Outputs (dev) of capacity max_edges: sender [E], receiver [E], shifts
+ * [E][3], sorted by (receiver, sender, S).  workspace (dev) of at least
+ * mace_neighbor_workspace_bytes.  Waits for the stream once, to read the
+ * edge count into *n_edges (host); the outputs are then written by work
+ * enqueued on stream.  MACE_ENOSPACE (with *n_edges = the count, outputs
+ * untouched) when max_edges is too small; MACE_ENONFINITE / MACE_ERANGE for
+ * non-finite / out-of-bound coordinates; MACE_EUNSUPPORTED beyond 2^30
+ * periodic-image candidates. */
+size_t mace_neighbor_workspace_bytes(int64_t n_atoms, const double* cells, const int32_t* graph_offsets,
+                                     int32_t n_graphs, double r_cut);
+mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, const double* cells,
+                                      const int32_t* graph_offsets, int32_t n_graphs, double r_cut,
+                                      int64_t max_edges, int32_t* sender, int32_t* receiver, int32_t* shifts,
+                                      int64_t* n_edges, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Validate and pack a graph and the weights into the workspace.
  * weights (dev) FP32 blob in mace_weight_layout order; species (dev) [N] in
  * 0..S-1; edge_index (dev) [2][E]: row 0 senders j, row 1 receivers i,

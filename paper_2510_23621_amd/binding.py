@@ -25,7 +25,8 @@ STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE
 EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", "mace_graph_setup",
             "mace_forward_energy", "mace_forces", "mace_forces_stress", "mace_graph_destroy", "mace_status_string",
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
-            "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work"]
+            "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
+            "mace_neighbor_workspace_bytes", "mace_neighbor_list_device"]
 
 
 class MaceError(RuntimeError):
@@ -68,6 +69,9 @@ def lib() -> ctypes.CDLL:
         L.mace_workspace_bytes.argtypes = [dp, I64, I64, I32, I32]
         L.mace_workspace_bytes.restype = Z
         L.mace_neighbor_list.argtypes = [I64, P, P, P, I32, D, I64, P, P, P, P]
+        L.mace_neighbor_workspace_bytes.argtypes = [I64, P, P, I32, D]
+        L.mace_neighbor_workspace_bytes.restype = Z
+        L.mace_neighbor_list_device.argtypes = [I64, P, P, P, I32, D, I64, P, P, P, P, P, Z, P]
         L.mace_graph_setup.argtypes = [dp, P, I64, I64, P, I64, P, P, P, P, I32, I32, P, Z, P, P]
         L.mace_forward_energy.argtypes = [P, P, P, P, P]
         L.mace_forces.argtypes = [P, P, P, P, P, P]
@@ -157,6 +161,46 @@ def mace_neighbor_list(positions: np.ndarray, r_cut: float, cells=None, graph_of
     _check(L.mace_neighbor_list(len(pos), _ptr(pos), _ptr(cl), _ptr(goa), n_graphs, float(r_cut), E,
                                 _ptr(snd), _ptr(rcv), _ptr(sh), ctypes.byref(ne)), "mace_neighbor_list")
     return snd, rcv, sh
+
+
+def mace_neighbor_workspace_bytes(n_atoms: int, r_cut: float, cells=None, graph_offsets=None, n_graphs: int = 1) -> int:
+    cl = None if cells is None else np.ascontiguousarray(cells, dtype=np.float64)
+    go = None if graph_offsets is None else np.ascontiguousarray(graph_offsets, dtype=np.int32)
+    return int(lib().mace_neighbor_workspace_bytes(int(n_atoms), _ptr(cl), _ptr(go), int(n_graphs), float(r_cut)))
+
+
+def mace_neighbor_list_device(positions, r_cut: float, cells=None, graph_offsets=None, n_graphs: int = 1,
+                              max_edges=None, stream=None):
+    """Device neighbour list. positions: float64 device tensor [N, 3]; cells
+    (host numpy [G, 3, 3]) or None; graph_offsets (host numpy int32 [G+1]) or
+    None. Returns (sender, receiver, shifts) int32 device tensors. With
+    max_edges None the count is taken first (one extra call)."""
+    import torch
+    N = int(positions.shape[0])
+    cl = None if cells is None else np.ascontiguousarray(cells, dtype=np.float64)
+    go = None if graph_offsets is None else np.ascontiguousarray(graph_offsets, dtype=np.int32)
+    nbytes = mace_neighbor_workspace_bytes(N, r_cut, cl, go, n_graphs)
+    if nbytes == 0:
+        raise MaceError(-1, "mace_neighbor_workspace_bytes")
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=positions.device)
+    ne = ctypes.c_int64()
+    L = lib()
+
+    def call(cap, snd, rcv, sh):
+        return L.mace_neighbor_list_device(N, _ptr(positions), _ptr(cl), _ptr(go), int(n_graphs), float(r_cut), cap,
+                                           _ptr(snd), _ptr(rcv), _ptr(sh), ctypes.byref(ne), _ptr(ws), nbytes,
+                                           _stream(stream))
+    if max_edges is None:
+        code = call(0, None, None, None)
+        if code not in (0, -3):
+            raise MaceError(code, "mace_neighbor_list_device")
+        max_edges = ne.value
+    snd = torch.empty(max(max_edges, 1), dtype=torch.int32, device=positions.device)
+    rcv = torch.empty_like(snd)
+    sh = torch.empty(max(max_edges, 1), 3, dtype=torch.int32, device=positions.device)
+    _check(call(max_edges, snd, rcv, sh), "mace_neighbor_list_device")
+    E = ne.value
+    return snd[:E], rcv[:E], sh[:E]
 
 
 def mace_graph_setup(desc, weights, n_atoms, species, n_edges, edge_index, unit_shifts, cells, graph_of_atom,

@@ -4,6 +4,7 @@
 2. compile the host neighbour list with g++ (-ffp-contract=off: its FP64
    arithmetic must round exactly as written)
 3. hipcc every kernel file and the host runtime for gfx950 -> libmace_amd.so
+   (the device neighbour list with -ffp-contract=off, like the host one)
 """
 from __future__ import annotations
 
@@ -16,7 +17,10 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmace_amd.so")
-HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip"]
+HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip",
+               "k_neighbors.hip"]
+# files whose FP64 arithmetic must round exactly as written (no fused multiply-adds)
+NO_CONTRACT = {"k_neighbors.hip"}
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall", "-Wno-unused-function",
     "-Wno-unused-variable", "-Wno-unused-but-set-variable",
@@ -48,7 +52,8 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     procs = []
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        cmd = [hipcc] + HIPCC_FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+        extra = ["-ffp-contract=off"] if src in NO_CONTRACT else []
+        cmd = [hipcc] + HIPCC_FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))

@@ -1,0 +1,477 @@
+// Device neighbour list for the graph problem statement: sender j -> receiver
+// i with image shift S is an edge iff
+//   0 < (d_x^2 + d_y^2) + d_z^2 < r_c^2,  d = (x_j - x_i) + ((S_0 a_0 + S_1 a_1) + S_2 a_2),
+// evaluated in FP64 with this operation order and no fused multiply-adds (the
+// same expression as the host list, so both produce the same edge set), every
+// periodic image enumerated, graphs never joined, output sorted by
+// (receiver, sender, S_0, S_1, S_2).
+//
+// Method (hashed cell list):
+//  1. every atom of a periodic graph is wrapped into its cell, x = x_w + n.cell
+//     with n = floor(fractional coordinates); the wrapped fractional
+//     coordinates lie in [0, 1), so images S' with |S'_a| <= floor(r_c |b_a| + 1)
+//     (b_a the reciprocal row) cover every pair within r_c;
+//  2. every image p = x_w + S'.cell of every atom (a candidate) is binned in
+//     Cartesian cubes of edge r_c + 1e-6, the cube (with the graph) hashed into
+//     a power-of-two slot table; a counting sort groups candidates by slot;
+//  3. one thread per receiver visits the 27 cubes around it, keeps the
+//     candidates of its own graph and cube, converts S' to the shift of the
+//     given (unwrapped) positions, S = S' - n_j + n_i, and applies the exact
+//     test above; a first pass counts, a scan gives each receiver its output
+//     segment, a second pass writes it and sorts it by (sender, S).
+// Binning only selects candidates; the cube edge exceeds r_c, so no pair
+// within r_c is missed, and every edge passes the exact FP64 test.
+#pragma clang fp contract(off)
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "../../include/mace.h"
+
+namespace {
+
+struct NlGraph {
+  double cell[9];   // rows = lattice vectors; zero without periodicity
+  double inv[9];    // cell^-1: fractional coordinate a = x . column a
+  int periodic;
+  int nr[3];        // wrapped-image range per lattice direction
+  int a0, a1;       // atoms [a0, a1)
+  int nimg;         // images per atom, prod (2 nr_a + 1)
+  int pad;
+  int64_t c0;       // first candidate of the graph
+};
+
+constexpr int kNlThreads = 256;
+constexpr int kScanPerThread = 16;
+constexpr int kScanTile = kNlThreads * kScanPerThread;
+constexpr double kCoordLimit = 1e9;   // |coordinate| bound (keeps cube indices in int32)
+constexpr int kFlagNonFinite = 1, kFlagRange = 2;
+
+__device__ __forceinline__ int graph_of(const NlGraph* gs, int G, int atom) {
+  int lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (gs[mid].a0 <= atom) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int graph_of_cand(const NlGraph* gs, int G, int64_t c) {
+  int lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (gs[mid].c0 <= c) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ uint32_t slot_of(int g, int bx, int by, int bz, uint32_t mask) {
+  uint64_t h = (uint64_t)(uint32_t)g;
+  h = h * 0x100000001B3ull + (uint32_t)bx;
+  h = h * 0x100000001B3ull + (uint32_t)by;
+  h = h * 0x100000001B3ull + (uint32_t)bz;
+  h ^= h >> 33;   // splitmix64 finaliser
+  h *= 0xFF51AFD7ED558CCDull;
+  h ^= h >> 33;
+  h *= 0xC4CEB9FE1A85EC53ull;
+  h ^= h >> 33;
+  return (uint32_t)h & mask;
+}
+
+__device__ __forceinline__ int cube(double p, double bs) { return (int)floor(p / bs); }
+
+// Wrap atoms of periodic graphs into the cell; flag non-finite or huge coordinates.
+__global__ void nl_wrap_kernel(int N, const double* __restrict__ pos, const NlGraph* __restrict__ gs, int G,
+                               double* __restrict__ xw, int4* __restrict__ nsh, int* __restrict__ flags) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const NlGraph& g = gs[graph_of(gs, G, i)];
+  const double x[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+  int bad = 0;
+  for (int c = 0; c < 3; ++c) {
+    if (!isfinite(x[c])) bad |= kFlagNonFinite;
+    else if (fabs(x[c]) > kCoordLimit) bad |= kFlagRange;
+  }
+  if (bad) atomicOr(flags, bad);
+  int n[3] = {0, 0, 0};
+  double w[3] = {x[0], x[1], x[2]};
+  if (g.periodic && !bad) {
+    for (int a = 0; a < 3; ++a) n[a] = (int)floor((x[0] * g.inv[0 * 3 + a] + x[1] * g.inv[1 * 3 + a]) + x[2] * g.inv[2 * 3 + a]);
+    for (int c = 0; c < 3; ++c)
+      w[c] = x[c] - (((double)n[0] * g.cell[0 * 3 + c] + (double)n[1] * g.cell[1 * 3 + c]) + (double)n[2] * g.cell[2 * 3 + c]);
+  }
+  for (int c = 0; c < 3; ++c) xw[3 * i + c] = bad ? 0.0 : w[c];
+  nsh[i] = make_int4(n[0], n[1], n[2], bad);
+}
+
+// Candidates: image S' of atom j, its cube and slot; slot populations counted.
+__global__ void nl_cand_kernel(int64_t C, const NlGraph* __restrict__ gs, int G, const double* __restrict__ xw,
+                               double bs, uint32_t mask, int* __restrict__ cand_j, int4* __restrict__ cand_s,
+                               int4* __restrict__ cand_b, int* __restrict__ slot_cnt) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  const int gi = graph_of_cand(gs, G, c);
+  const NlGraph& g = gs[gi];
+  const int64_t local = c - g.c0;
+  const int j = g.a0 + (int)(local / g.nimg);
+  int s = (int)(local % g.nimg);
+  const int w2 = 2 * g.nr[2] + 1, w1 = 2 * g.nr[1] + 1;
+  const int s2 = s % w2 - g.nr[2];
+  s /= w2;
+  const int s1 = s % w1 - g.nr[1];
+  const int s0 = s / w1 - g.nr[0];
+  int b[3];
+  for (int q = 0; q < 3; ++q) {
+    const double p = xw[3 * j + q] + (((double)s0 * g.cell[0 * 3 + q] + (double)s1 * g.cell[1 * 3 + q]) +
+                                      (double)s2 * g.cell[2 * 3 + q]);
+    b[q] = cube(p, bs);
+  }
+  cand_j[c] = j;
+  cand_s[c] = make_int4(s0, s1, s2, gi);
+  cand_b[c] = make_int4(b[0], b[1], b[2], 0);
+  atomicAdd(&slot_cnt[slot_of(gi, b[0], b[1], b[2], mask)], 1);
+}
+
+__global__ void nl_scatter_kernel(int64_t C, const int4* __restrict__ cand_s, const int4* __restrict__ cand_b,
+                                  uint32_t mask, const int64_t* __restrict__ slot_off, int* __restrict__ slot_fill,
+                                  int* __restrict__ order) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= C) return;
+  const int4 b = cand_b[c];
+  const uint32_t slot = slot_of(cand_s[c].w, b.x, b.y, b.z, mask);
+  order[slot_off[slot] + atomicAdd(&slot_fill[slot], 1)] = (int)c;
+}
+
+__device__ __forceinline__ bool key_less(int ja, const int* sa, int jb, const int* sb) {
+  if (ja != jb) return ja < jb;
+  if (sa[0] != sb[0]) return sa[0] < sb[0];
+  if (sa[1] != sb[1]) return sa[1] < sb[1];
+  return sa[2] < sb[2];
+}
+
+// Receiver pass: WRITE = false counts the edges of receiver i, WRITE = true
+// writes them to [off_i, off_i + count) and sorts that segment.
+template <bool WRITE>
+__global__ void nl_receiver_kernel(int N, const double* __restrict__ pos, const NlGraph* __restrict__ gs, int G,
+                                   const double* __restrict__ xw, const int4* __restrict__ nsh, double bs, double rc2,
+                                   uint32_t mask, const int64_t* __restrict__ slot_off, const int* __restrict__ order,
+                                   const int* __restrict__ cand_j, const int4* __restrict__ cand_s,
+                                   const int4* __restrict__ cand_b, int* __restrict__ count,
+                                   const int64_t* __restrict__ off, int32_t* __restrict__ sender,
+                                   int32_t* __restrict__ receiver, int32_t* __restrict__ shifts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int gi = graph_of(gs, G, i);
+  const NlGraph& g = gs[gi];
+  const int4 ni = nsh[i];
+  int n = 0;
+  const int64_t base = WRITE ? off[i] : 0;
+  if (!ni.w) {
+    const double xi[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+    const int bi[3] = {cube(xw[3 * i], bs), cube(xw[3 * i + 1], bs), cube(xw[3 * i + 2], bs)};
+    for (int dx = -1; dx <= 1; ++dx)
+      for (int dy = -1; dy <= 1; ++dy)
+        for (int dz = -1; dz <= 1; ++dz) {
+          const int bx = bi[0] + dx, by = bi[1] + dy, bz = bi[2] + dz;
+          const uint32_t slot = slot_of(gi, bx, by, bz, mask);
+          for (int64_t q = slot_off[slot]; q < slot_off[slot + 1]; ++q) {
+            const int c = order[q];
+            const int4 cs = cand_s[c];
+            const int4 cb = cand_b[c];
+            if (cs.w != gi || cb.x != bx || cb.y != by || cb.z != bz) continue;
+            const int j = cand_j[c];
+            const int4 nj = nsh[j];
+            if (nj.w) continue;
+            const int S[3] = {cs.x - nj.x + ni.x, cs.y - nj.y + ni.y, cs.z - nj.z + ni.z};
+            double d[3];
+            for (int q3 = 0; q3 < 3; ++q3) {
+              const double sv = g.periodic ? ((double)S[0] * g.cell[0 * 3 + q3] + (double)S[1] * g.cell[1 * 3 + q3]) +
+                                                 (double)S[2] * g.cell[2 * 3 + q3]
+                                           : 0.0;
+              d[q3] = (pos[3 * j + q3] - xi[q3]) + sv;
+            }
+            const double r2 = (d[0] * d[0] + d[1] * d[1]) + d[2] * d[2];
+            if (r2 < rc2 && r2 > 0.0) {
+              if (WRITE) {
+                const int64_t e = base + n;
+                sender[e] = j;
+                receiver[e] = i;
+                shifts[3 * e] = S[0];
+                shifts[3 * e + 1] = S[1];
+                shifts[3 * e + 2] = S[2];
+              }
+              ++n;
+            }
+          }
+        }
+  }
+  if (!WRITE) {
+    count[i] = n;
+    return;
+  }
+  // insertion sort of the segment by (sender, S)
+  for (int a = 1; a < n; ++a) {
+    const int64_t ea = base + a;
+    const int ja = sender[ea];
+    const int sa[3] = {shifts[3 * ea], shifts[3 * ea + 1], shifts[3 * ea + 2]};
+    int b = a - 1;
+    while (b >= 0) {
+      const int64_t eb = base + b;
+      const int sb[3] = {shifts[3 * eb], shifts[3 * eb + 1], shifts[3 * eb + 2]};
+      if (!key_less(ja, sa, sender[eb], sb)) break;
+      sender[eb + 1] = sender[eb];
+      shifts[3 * (eb + 1)] = sb[0];
+      shifts[3 * (eb + 1) + 1] = sb[1];
+      shifts[3 * (eb + 1) + 2] = sb[2];
+      --b;
+    }
+    const int64_t ed = base + b + 1;
+    sender[ed] = ja;
+    shifts[3 * ed] = sa[0];
+    shifts[3 * ed + 1] = sa[1];
+    shifts[3 * ed + 2] = sa[2];
+  }
+}
+
+// Exclusive scan of n int32 counts into out[0..n] (out[n] = total), int64.
+// Tile pass (kScanTile elements per block, tile totals to bsum), one-block
+// pass over the tile totals, then the tile offsets added.
+__device__ __forceinline__ int64_t block_exclusive_scan(int64_t v, int64_t* sh, int64_t* total) {
+  const int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+  for (int st = 1; st < kNlThreads; st <<= 1) {
+    const int64_t add = t >= st ? sh[t - st] : 0;
+    __syncthreads();
+    sh[t] += add;
+    __syncthreads();
+  }
+  const int64_t incl = sh[t];
+  *total = sh[kNlThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ void __launch_bounds__(kNlThreads) nl_scan_tile_kernel(int64_t n, const int* __restrict__ in,
+                                                                    int64_t* __restrict__ out,
+                                                                    int64_t* __restrict__ bsum) {
+  __shared__ int64_t sh[kNlThreads];
+  const int64_t t0 = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanPerThread;
+  int64_t s = 0;
+  for (int u = 0; u < kScanPerThread; ++u)
+    if (t0 + u < n) s += in[t0 + u];
+  int64_t total;
+  int64_t run = block_exclusive_scan(s, sh, &total);
+  for (int u = 0; u < kScanPerThread; ++u)
+    if (t0 + u < n) {
+      out[t0 + u] = run;
+      run += in[t0 + u];
+    }
+  if (threadIdx.x == 0) bsum[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(kNlThreads) nl_scan_top_kernel(int nb, int64_t* __restrict__ bsum) {
+  __shared__ int64_t sh[kNlThreads];
+  int64_t carry = 0;
+  for (int c0 = 0; c0 < nb; c0 += kNlThreads) {
+    const int idx = c0 + threadIdx.x;
+    const int64_t v = idx < nb ? bsum[idx] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan(v, sh, &total);
+    if (idx < nb) bsum[idx] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) bsum[nb] = carry;
+}
+
+__global__ void nl_scan_add_kernel(int64_t n, int64_t* __restrict__ out, const int64_t* __restrict__ bsum,
+                                   int nb) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] += bsum[i / kScanTile];
+  if (i == 0) out[n] = bsum[nb];
+}
+
+void scan(hipStream_t s, int64_t n, const int* in, int64_t* out, int64_t* bsum) {
+  const int nb = (int)((n + kScanTile - 1) / kScanTile);
+  if (nb > 0) nl_scan_tile_kernel<<<nb, kNlThreads, 0, s>>>(n, in, out, bsum);
+  nl_scan_top_kernel<<<1, kNlThreads, 0, s>>>(nb, bsum);
+  const int64_t blocks = std::max<int64_t>(1, (n + kNlThreads - 1) / kNlThreads);
+  nl_scan_add_kernel<<<(unsigned)blocks, kNlThreads, 0, s>>>(n, out, bsum, nb);
+}
+
+bool invert3(const double* c, double* inv) {
+  const double det = c[0] * (c[4] * c[8] - c[5] * c[7]) - c[1] * (c[3] * c[8] - c[5] * c[6]) +
+                     c[2] * (c[3] * c[7] - c[4] * c[6]);
+  if (!(std::fabs(det) > 0) || !std::isfinite(det)) return false;
+  inv[0] = (c[4] * c[8] - c[5] * c[7]) / det;
+  inv[1] = (c[2] * c[7] - c[1] * c[8]) / det;
+  inv[2] = (c[1] * c[5] - c[2] * c[4]) / det;
+  inv[3] = (c[5] * c[6] - c[3] * c[8]) / det;
+  inv[4] = (c[0] * c[8] - c[2] * c[6]) / det;
+  inv[5] = (c[2] * c[3] - c[0] * c[5]) / det;
+  inv[6] = (c[3] * c[7] - c[4] * c[6]) / det;
+  inv[7] = (c[1] * c[6] - c[0] * c[7]) / det;
+  inv[8] = (c[0] * c[4] - c[1] * c[3]) / det;
+  return true;
+}
+
+constexpr int64_t kMaxCandidates = int64_t(1) << 30;
+
+// Host plan: per-graph records, candidate count, slot table size and the
+// workspace layout (256-byte aligned pieces).
+struct NlPlan {
+  std::vector<NlGraph> gs;
+  int64_t C = 0;
+  uint32_t n_slots = 0;
+  size_t o_gs, o_xw, o_nsh, o_cj, o_cs, o_cb, o_scnt, o_sfill, o_soff, o_order, o_rcnt, o_roff, o_bsum, o_flags,
+      bytes;
+};
+
+mace_status plan_nl(int64_t N, const double* cells, const int32_t* goff, int32_t G, double r_cut, NlPlan& p) {
+  if (N < 0 || N > (int64_t(1) << 30) || !(r_cut > 0) || !std::isfinite(r_cut) || G < 1) return MACE_EINVAL;
+  if (!goff && G != 1) return MACE_EINVAL;
+  p.gs.assign(G, NlGraph{});
+  int64_t C = 0;
+  for (int g = 0; g < G; ++g) {
+    NlGraph& r = p.gs[g];
+    std::memset(&r, 0, sizeof(r));
+    r.a0 = goff ? goff[g] : 0;
+    r.a1 = goff ? goff[g + 1] : (int)N;
+    if (r.a0 < 0 || r.a1 < r.a0 || r.a1 > N || (g == 0 && r.a0 != 0)) return MACE_ERANGE;
+    if (g > 0 && r.a0 != p.gs[g - 1].a1) return MACE_ERANGE;
+    int64_t nimg = 1;
+    if (cells) {
+      r.periodic = 1;
+      std::memcpy(r.cell, cells + 9 * g, sizeof(r.cell));
+      if (!invert3(r.cell, r.inv)) return MACE_EINVAL;
+      for (int a = 0; a < 3; ++a) {
+        const double bn = std::sqrt(r.inv[0 * 3 + a] * r.inv[0 * 3 + a] + r.inv[1 * 3 + a] * r.inv[1 * 3 + a] +
+                                    r.inv[2 * 3 + a] * r.inv[2 * 3 + a]);
+        const double m = std::floor(r_cut * bn + 1.0 + 1e-6);
+        if (!(m < 1e4)) return MACE_EUNSUPPORTED;
+        r.nr[a] = (int)m;
+        nimg *= 2 * r.nr[a] + 1;
+      }
+    }
+    if (nimg > kMaxCandidates) return MACE_EUNSUPPORTED;
+    r.nimg = (int)nimg;
+    r.c0 = C;
+    C += (int64_t)(r.a1 - r.a0) * nimg;
+    if (C > kMaxCandidates) return MACE_EUNSUPPORTED;
+  }
+  if (!goff && p.gs[0].a1 != N) return MACE_ERANGE;
+  if (p.gs[G - 1].a1 != N) return MACE_ERANGE;
+  p.C = C;
+  uint32_t ns = 1024;
+  while ((int64_t)ns < 2 * C) ns <<= 1;
+  p.n_slots = ns;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += (bytes + 255) & ~size_t(255);
+    return at;
+  };
+  const size_t n1 = (size_t)std::max<int64_t>(N, 1), c1 = (size_t)std::max<int64_t>(C, 1);
+  p.o_gs = take(sizeof(NlGraph) * G);
+  p.o_xw = take(sizeof(double) * 3 * n1);
+  p.o_nsh = take(sizeof(int4) * n1);
+  p.o_cj = take(sizeof(int) * c1);
+  p.o_cs = take(sizeof(int4) * c1);
+  p.o_cb = take(sizeof(int4) * c1);
+  p.o_scnt = take(sizeof(int) * ns);
+  p.o_sfill = take(sizeof(int) * ns);
+  p.o_soff = take(sizeof(int64_t) * (ns + 1));
+  p.o_order = take(sizeof(int) * c1);
+  p.o_rcnt = take(sizeof(int) * n1);
+  p.o_roff = take(sizeof(int64_t) * (n1 + 1));
+  const int64_t tiles = (std::max<int64_t>(ns, n1) + kScanTile - 1) / kScanTile;
+  p.o_bsum = take(sizeof(int64_t) * (tiles + 1));
+  p.o_flags = take(sizeof(int));
+  p.bytes = o;
+  return MACE_OK;
+}
+
+}  // namespace
+
+extern "C" size_t mace_neighbor_workspace_bytes(int64_t n_atoms, const double* cells, const int32_t* graph_offsets,
+                                                int32_t n_graphs, double r_cut) {
+  NlPlan p;
+  if (plan_nl(n_atoms, cells, graph_offsets, n_graphs, r_cut, p) != MACE_OK) return 0;
+  return p.bytes;
+}
+
+extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, const double* cells,
+                                                 const int32_t* graph_offsets, int32_t n_graphs, double r_cut,
+                                                 int64_t max_edges, int32_t* sender, int32_t* receiver,
+                                                 int32_t* shifts, int64_t* n_edges, void* workspace,
+                                                 size_t workspace_bytes, void* stream) {
+  if (!n_edges || (n_atoms > 0 && !positions) || max_edges < 0) return MACE_EINVAL;
+  NlPlan p;
+  mace_status st = plan_nl(n_atoms, cells, graph_offsets, n_graphs, r_cut, p);
+  if (st != MACE_OK) return st;
+  if (!workspace || workspace_bytes < p.bytes) return MACE_ENOSPACE;
+  if (max_edges > 0 && (!sender || !receiver || !shifts)) return MACE_EINVAL;
+  *n_edges = 0;
+  if (n_atoms == 0) return MACE_OK;
+  hipStream_t s = (hipStream_t)stream;
+  char* w = reinterpret_cast<char*>(workspace);
+  auto* gs = reinterpret_cast<NlGraph*>(w + p.o_gs);
+  auto* xw = reinterpret_cast<double*>(w + p.o_xw);
+  auto* nsh = reinterpret_cast<int4*>(w + p.o_nsh);
+  auto* cj = reinterpret_cast<int*>(w + p.o_cj);
+  auto* cs = reinterpret_cast<int4*>(w + p.o_cs);
+  auto* cb = reinterpret_cast<int4*>(w + p.o_cb);
+  auto* scnt = reinterpret_cast<int*>(w + p.o_scnt);
+  auto* sfill = reinterpret_cast<int*>(w + p.o_sfill);
+  auto* soff = reinterpret_cast<int64_t*>(w + p.o_soff);
+  auto* order = reinterpret_cast<int*>(w + p.o_order);
+  auto* rcnt = reinterpret_cast<int*>(w + p.o_rcnt);
+  auto* roff = reinterpret_cast<int64_t*>(w + p.o_roff);
+  auto* bsum = reinterpret_cast<int64_t*>(w + p.o_bsum);
+  auto* flags = reinterpret_cast<int*>(w + p.o_flags);
+  const int N = (int)n_atoms, G = n_graphs;
+  const double bs = r_cut + 1e-6, rc2 = r_cut * r_cut;
+  const uint32_t mask = p.n_slots - 1;
+  hipError_t err = hipMemcpyAsync(gs, p.gs.data(), sizeof(NlGraph) * G, hipMemcpyHostToDevice, s);
+  if (err == hipSuccess) err = hipMemsetAsync(scnt, 0, sizeof(int) * p.n_slots, s);
+  if (err == hipSuccess) err = hipMemsetAsync(sfill, 0, sizeof(int) * p.n_slots, s);
+  if (err == hipSuccess) err = hipMemsetAsync(flags, 0, sizeof(int), s);
+  if (err != hipSuccess) {
+    hipStreamSynchronize(s);   // the plan's host copy must outlive the upload
+    return MACE_EHIP;
+  }
+  const unsigned nblk = (unsigned)((N + kNlThreads - 1) / kNlThreads);
+  const unsigned cblk = (unsigned)((p.C + kNlThreads - 1) / kNlThreads);
+  nl_wrap_kernel<<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, flags);
+  if (p.C > 0) {
+    nl_cand_kernel<<<cblk, kNlThreads, 0, s>>>(p.C, gs, G, xw, bs, mask, cj, cs, cb, scnt);
+  }
+  scan(s, p.n_slots, scnt, soff, bsum);
+  if (p.C > 0) nl_scatter_kernel<<<cblk, kNlThreads, 0, s>>>(p.C, cs, cb, mask, soff, sfill, order);
+  nl_receiver_kernel<false><<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order, cj,
+                                                         cs, cb, rcnt, nullptr, nullptr, nullptr, nullptr);
+  scan(s, N, rcnt, roff, bsum);
+  int64_t total = 0;
+  int hflags = 0;
+  err = hipGetLastError();
+  if (err == hipSuccess) err = hipMemcpyAsync(&total, roff + N, sizeof(int64_t), hipMemcpyDeviceToHost, s);
+  if (err == hipSuccess) err = hipMemcpyAsync(&hflags, flags, sizeof(int), hipMemcpyDeviceToHost, s);
+  const hipError_t serr = hipStreamSynchronize(s);
+  if (err == hipSuccess) err = serr;
+  if (err != hipSuccess) return MACE_EHIP;
+  if (hflags & kFlagNonFinite) return MACE_ENONFINITE;
+  if (hflags & kFlagRange) return MACE_ERANGE;
+  *n_edges = total;
+  if (total > max_edges) return MACE_ENOSPACE;
+  if (total > 0)
+    nl_receiver_kernel<true><<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order,
+                                                          cj, cs, cb, nullptr, roff, sender, receiver, shifts);
+  return hipGetLastError() == hipSuccess ? MACE_OK : MACE_EHIP;
+}

@@ -131,3 +131,18 @@ def test_status_codes_without_gpu():
                                     None, 0, None, ctypes.byref(h))
     assert code == -1
     assert B.mace_status_string(-3).startswith("workspace")
+
+
+def test_device_neighbor_workspace_size_without_gpu():
+    """The device list's workspace size is a host computation: positive for
+    valid input, 0 for a non-positive cutoff, a singular cell or offsets
+    that do not cover the atoms; larger with more periodic images."""
+    cell = np.eye(3)[None] * 10.0
+    n1 = B.mace_neighbor_workspace_bytes(100, 5.0, cell)
+    assert n1 > 0
+    assert B.mace_neighbor_workspace_bytes(100, 5.0, None) > 0
+    assert B.mace_neighbor_workspace_bytes(100, 12.0, cell) > n1     # more images per atom
+    assert B.mace_neighbor_workspace_bytes(100, 0.0, cell) == 0
+    assert B.mace_neighbor_workspace_bytes(100, 5.0, np.zeros((1, 3, 3))) == 0
+    assert B.mace_neighbor_workspace_bytes(100, 5.0, None, np.array([0, 50, 90], np.int32), 2) == 0
+    assert B.mace_neighbor_workspace_bytes(100, 5.0, None, np.array([0, 50, 100], np.int32), 2) > 0
