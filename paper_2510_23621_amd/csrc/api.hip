@@ -164,6 +164,7 @@ struct Buffers {
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
+  std::vector<float*> sg;   // per layer: [3][E][64] silu'(z) of the radial pre-activations
   std::vector<float*> A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
@@ -204,12 +205,14 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
   b.a3.resize(T);
+  b.sg.resize(T);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
   b.ht.assign(T, nullptr);
   for (int t = 0; t < T; ++t) {
     const LayerPlan& L = m.layers[t];
     b.a3[t] = c.take<float>(std::max<int64_t>(E, 1) * 64);
+    b.sg[t] = c.take<float>(std::max<int64_t>(E, 1) * 3 * 64);
     b.A[t] = c.take<float>(N * 16 * K);
     if (t > 0) {
       b.hin[t] = c.take<float>(N * L.din * K);
@@ -491,6 +494,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       for (int q = 0; q < rs.n; ++q) {
         rs.W[q] = b.w + m.off.at(std::to_string(t0 + q) + ".radial.0");
         rs.a3[q] = b.a3[t0 + q];
+        rs.sg[q] = b.sg[t0 + q];
       }
       // (a later chunk recomputes the same Y and rbf)
       launch_edge_prologue(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf,
@@ -568,20 +572,22 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     const std::string pre = std::to_string(t) + ".";
     float* hout = L.last ? b.hlast : b.hin[t + 1];
     if (L.last) {
-      {
+      // the energy reaches the last layer's output only through its readout:
+      // the readout's gradient is stored, the other components are zero
+      if (L.dout > 1) {
         PROF(KID_FILL);
         launch_fill(s, dnext, (size_t)N * L.dout * K, 0.f);
       }
       {
         PROF(KID_READOUT);
         launch_readout_bwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, dnext);
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, L.dout == 1, dnext);
       }
     } else {
       {
         PROF(KID_READOUT);
         launch_readout_bwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
-                           dnext);
+                           0, dnext);
       }
     }
     {
@@ -614,8 +620,8 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       // right after the partials are written, while they are still in the
       // last-level cache
       PROF(KID_RADIAL_BWD);
-      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, K / 16, b.dY,
-                        b.de, t < T - 1);
+      launch_radial_bwd(s, E, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.sg[t], b.da3p, b.dYp, K / 16,
+                        b.dY, b.de, t < T - 1);
     }
     if (t > 0) {
       {

@@ -215,96 +215,75 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
 }
 
 // ---------------------------------------------------------------- readouts
-// Non-last layers: eps[n] (+)= sum_k h[n][0][k] w[k].
-// Last layer:      eps[n] (+)= sum_j w2[j] silu(sum_k h[n][0][k] W1[k][j]).
-// One block per node, threads = channels, fixed-order tree reduction in LDS.
-__global__ void __launch_bounds__(128) readout_fwd_kernel(int N, int K, const float* __restrict__ h, int h_stride,
-                                                          const float* __restrict__ w, const float* __restrict__ w1,
-                                                          const float* __restrict__ w2, int hidden, int lowp,
-                                                          int accumulate, float* __restrict__ eps) {
-  __shared__ float red[16][128];
-  const int n = blockIdx.x, k = threadIdx.x;
-  float x = (k < K) ? h[(size_t)n * h_stride + k] : 0.f;
-  x = lowp_round(x, lowp);
-  const int nv = w ? 1 : hidden;
-  for (int j = 0; j < nv; ++j) {
-    float wv = 0.f;
-    if (k < K) wv = w ? w[k] : w1[(size_t)k * hidden + j];
-    wv = lowp_round(wv, lowp);
-    red[j][k] = x * wv;
-  }
-  __syncthreads();
-  for (int st = blockDim.x / 2; st > 0; st >>= 1) {
-    if (k < st)
-      for (int j = 0; j < nv; ++j) red[j][k] += red[j][k + st];
-    __syncthreads();
-  }
-  if (k == 0) {
-    float out;
-    if (w) {
-      out = red[0][0];
-    } else {
-      out = 0.f;
-      for (int j = 0; j < hidden; ++j) {
-        float a = silu(red[j][0]);
-        float v2 = w2[j];
-        if (lowp) {
-          a = lowp_round(a, lowp);
-          v2 = lowp_round(v2, lowp);
-        }
-        out += a * v2;
-      }
-    }
-    eps[n] = accumulate ? eps[n] + out : out;
-  }
+// One wave per node (4 per block). Non-last layers: eps[n] (+)= sum_k h[n][0][k] w[k].
+// Last layer: eps[n] (+)= sum_j w2[j] silu(z_j), z_j = sum_k h[n][0][k] W1[k][j]
+// (hidden <= 16): lane j + 16 q forms the part of z_j over the q-th quarter of
+// the channels, xor-butterflies sum the quarters and then the hidden units, in
+// a fixed order.
+constexpr int kReadoutNodes = 4;
+
+// z_j of the last-layer readout, in every lane whose hidden index is j
+__device__ __forceinline__ float readout_hidden_z(const float* __restrict__ hrow, int K,
+                                                  const float* __restrict__ w1, int hidden, int lowp, int lane) {
+  const int j = lane & 15, q = lane >> 4;
+  const int kq = K / 4;
+  float z = 0.f;
+  if (j < hidden)
+    for (int k = q * kq; k < (q + 1) * kq; ++k) z += lowp_round(hrow[k], lowp) * lowp_round(w1[(size_t)k * hidden + j], lowp);
+  z += __shfl_xor(z, 16);
+  z += __shfl_xor(z, 32);
+  return z;
 }
 
-// dh[n][0][k] += dE/dh (energy = sum of eps).
-__global__ void __launch_bounds__(128) readout_bwd_kernel(int N, int K, const float* __restrict__ h, int h_stride,
-                                                          const float* __restrict__ w, const float* __restrict__ w1,
-                                                          const float* __restrict__ w2, int hidden, int lowp,
-                                                          float* __restrict__ dh) {
-  __shared__ float red[16][128];
-  __shared__ float gz[16];
-  const int n = blockIdx.x, k = threadIdx.x;
+__global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, int K, const float* __restrict__ h,
+                                                                         int h_stride, const float* __restrict__ w,
+                                                                         const float* __restrict__ w1,
+                                                                         const float* __restrict__ w2, int hidden,
+                                                                         int lowp, int accumulate,
+                                                                         float* __restrict__ eps) {
+  const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const float* hrow = h + (size_t)n * h_stride;
+  float v = 0.f;
   if (w) {
-    if (k < K) {
-      float wv = w[k];
-      wv = lowp_round(wv, lowp);
-      dh[(size_t)n * h_stride + k] += wv;
+    for (int k = lane; k < K; k += 64) v += lowp_round(hrow[k], lowp) * lowp_round(w[k], lowp);
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m);
+  } else {
+    const float z = readout_hidden_z(hrow, K, w1, hidden, lowp, lane);
+    const int j = lane & 15;
+    if (j < hidden) v = lowp_round(silu(z), lowp) * lowp_round(w2[j], lowp);
+#pragma unroll
+    for (int m = 8; m > 0; m >>= 1) v += __shfl_xor(v, m);
+  }
+  if (lane == 0) eps[n] = accumulate ? eps[n] + v : v;
+}
+
+// dE/dh[n][0][k] from the readout (energy = sum of eps): added to dh, or
+// stored when overwrite is set.
+__global__ void __launch_bounds__(64 * kReadoutNodes) readout_bwd_kernel(int N, int K, const float* __restrict__ h,
+                                                                         int h_stride, const float* __restrict__ w,
+                                                                         const float* __restrict__ w1,
+                                                                         const float* __restrict__ w2, int hidden,
+                                                                         int lowp, int overwrite,
+                                                                         float* __restrict__ dh) {
+  const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (n >= N) return;
+  float* drow = dh + (size_t)n * h_stride;
+  if (w) {
+    for (int k = lane; k < K; k += 64) {
+      const float g = lowp_round(w[k], lowp);
+      drow[k] = overwrite ? g : drow[k] + g;
     }
     return;
   }
-  float x = (k < K) ? h[(size_t)n * h_stride + k] : 0.f;
-  x = lowp_round(x, lowp);
-  for (int j = 0; j < hidden; ++j) {
-    float wv = 0.f;
-    if (k < K) wv = w1[(size_t)k * hidden + j];
-    wv = lowp_round(wv, lowp);
-    red[j][k] = x * wv;
-  }
-  __syncthreads();
-  for (int st = blockDim.x / 2; st > 0; st >>= 1) {
-    if (k < st)
-      for (int j = 0; j < hidden; ++j) red[j][k] += red[j][k + st];
-    __syncthreads();
-  }
-  if (k < hidden) {
-    float v2 = w2[k];
-    v2 = lowp_round(v2, lowp);
-    float gzj = v2 * silu_grad(red[k][0]);
-    gzj = lowp_round(gzj, lowp);
-    gz[k] = gzj;
-  }
-  __syncthreads();
-  if (k < K) {
+  const float z = readout_hidden_z(h + (size_t)n * h_stride, K, w1, hidden, lowp, lane);
+  const int j = lane & 15;
+  const float gz = j < hidden ? lowp_round(lowp_round(w2[j], lowp) * silu_grad(z), lowp) : 0.f;
+  for (int k = lane; k < K; k += 64) {
     float acc = 0.f;
-    for (int j = 0; j < hidden; ++j) {
-      float wv = w1[(size_t)k * hidden + j];
-      wv = lowp_round(wv, lowp);
-      acc += gz[j] * wv;
-    }
-    dh[(size_t)n * h_stride + k] += acc;
+    for (int jj = 0; jj < hidden; ++jj) acc += __shfl(gz, jj) * lowp_round(w1[(size_t)k * hidden + jj], lowp);
+    drow[k] = overwrite ? acc : drow[k] + acc;
   }
 }
 
@@ -347,12 +326,14 @@ __global__ void species_table_kernel(int S, int K, const float* __restrict__ emb
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
                         const float* w2, int hidden, int lowp, int accumulate, float* eps) {
   if (N <= 0) return;
-  readout_fwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps);
+  readout_fwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
+      N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps);
 }
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int lowp, float* dh) {
+                        const float* w2, int hidden, int lowp, int overwrite, float* dh) {
   if (N <= 0) return;
-  readout_bwd_kernel<<<N, 128, 0, s>>>(N, K, h, h_stride, w, w1, w2, hidden, lowp, dh);
+  readout_bwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
+      N, K, h, h_stride, w, w1, w2, hidden, lowp, overwrite, dh);
 }
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
   if (G <= 0) return;

@@ -207,6 +207,23 @@ __device__ __forceinline__ void read_y(const float* sy, int row, float* y) {
   }
 }
 
+// Source rows in h of the edges e_first .. e_first + 3 (clamped to the last
+// valid edge): the sender itself, or its species-table row through src_map.
+__device__ __forceinline__ void sender_rows(const int* __restrict__ snd, const int* __restrict__ src_map,
+                                            int e_first, int e_end, int* srcq) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int s = snd[min(e_first + q, e_end - 1)];
+    srcq[q] = src_map ? src_map[s] : s;
+  }
+}
+
+template <int DIN>
+__device__ __forceinline__ void load_h_row(const float* __restrict__ h, int src, int K, int k, float* hv) {
+#pragma unroll
+  for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
+}
+
 template <int LHMAX, bool RB, int NW = TprShape<LHMAX, false>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
@@ -234,24 +251,27 @@ tpr_fwd_kernel(
     for (int c = 0; c < MID; ++c) acc[c] = 0.f;
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      // sender rows of the lane's four edges (edges past e_end carry R = 0),
+      // requested before the radial MFMAs so that their latency is hidden
+      int srcq[4];
+      sender_rows(snd, src_map, e0 + 4 * g, e_end, srcq);
       stage_y(Y, e0, e_end, sy);
       f4 r[P];
       if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
       // lane group 0 holds the tile's first edges, so nq covers every valid one;
-      // the scheduling barrier keeps one edge's operands live at a time
+      // the scheduling barrier keeps one edge's operands live at a time, and
+      // the next edge's h row is requested while this one is contracted
       const int nq = min(4, e_end - e0);
+      float hv[DIN];
+      load_h_row<DIN>(h, srcq[0], K, k, hv);
       static_for<0, 4>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
         __builtin_amdgcn_sched_barrier(0);
         if (q >= nq) return;
         const int row = 4 * g + q;
-        const int e = min(e0 + row, e_end - 1);   // edges past e_end carry R = 0
-        const int s = snd[e];
-        const int src = src_map ? src_map[s] : s;
-        float hv[DIN];
-#pragma unroll
-        for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
+        float hn[DIN];
+        if constexpr (q < 3) load_h_row<DIN>(h, srcq[q + 1], K, k, hn);
         float y[16];
         read_y(sy, row, y);
         for_paths<LHMAX>([&](auto tag) {
@@ -267,6 +287,10 @@ tpr_fwd_kernel(
 #pragma unroll
           for (int m = 0; m < 2 * lo + 1; ++m) acc[T::offset + m] += rv * t[m];
         });
+        if constexpr (q < 3) {
+#pragma unroll
+          for (int c = 0; c < DIN; ++c) hv[c] = hn[c];
+        }
       });
     }
     // lane groups 0+1 and 2+3, then the two pairs: every lane ends with the same sum
@@ -305,13 +329,21 @@ __device__ __forceinline__ float group_reduce16(float* v, int lane) {
 }
 
 // VJP of tpr_fwd. Given g = dE/dAt, per edge e (receiver i) and channel k,
-// with Bm_p[m2] = sum_{m1,m3} C h[m1] g[i][p][m3] and Dm_p[m1] = sum_{m2,m3} C Y[m2] g[i][p][m3]:
+// with G_p[m1][m2] = sum_m3 C g[i][p][m3] (per receiver and channel, kept in
+// LDS for the receiver's edges, one value per coupled (m1, m2) pair),
+// Bm_p[m2] = sum_m1 G_p[m1][m2] h[m1] and Dm_p[m1] = sum_m2 G_p[m1][m2] Y[m2]:
 //   dR[e][p][k]    = inv_c sum_m2 Bm_p[m2] Y[m2]
 //   dY[e][ly,m2]  += inv_c sum_k sum_p R Bm_p[m2]                    (channel-tile partial)
 //   Q[e][lh,m1][k] = inv_c sum_p R Dm_p[m1]                          (per-edge sender gradient)
 //   da3[e][j]     += sum_{p,k} dR[e][p][k] W3[j][p K + k]           (channel-tile partial)
 // The partials of channel tile ct go to dYp[ct][e][16] and da3p[ct][e][64];
 // their sum over tiles (fixed order) is taken by the hidden-layer backward.
+// G_p is formed once per receiver (GF) where its table fits beside the
+// weight slice at the kernel's occupancy; otherwise each edge contracts C
+// with g directly (product form C (g h), C (g Y)).
+template <int LHMAX, bool RB>
+constexpr bool tpr_bwd_gform() { return LHMAX == 0 || (LHMAX == 1 && !RB); }
+
 template <int LHMAX, bool RB, int NW = TprShape<LHMAX, true>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true>::per_simd, TprShape<LHMAX, true>::per_simd)))
@@ -327,6 +359,9 @@ tpr_bwd_kernel(
   __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
   __shared__ __align__(16) float sT[NW][RB ? 2 * 16 * kT2Pitch : 16 * kTPitch];
+  constexpr bool GF = tpr_bwd_gform<LHMAX, RB>();
+  constexpr int NPAIR = PairCount<LHMAX>::value;
+  __shared__ float sG[GF ? NW : 1][GF ? NPAIR * 16 : 1];   // [pair][channel]
   unsigned short* sWb = reinterpret_cast<unsigned short*>(sW);
   unsigned short* sWt = sWb + P * 16 * kWbPitch;
   const int ct = blockIdx.y;
@@ -338,6 +373,7 @@ tpr_bwd_kernel(
   const int k = 16 * ct + kk;
   float* sy = sY[w];
   float* tw = sT[w];
+  float* sg = sG[GF ? w : 0];
   float* dYc = dYp + (size_t)ct * E * 16;
   float* da3c = da3p + (size_t)ct * E * 64;
   for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
@@ -345,25 +381,46 @@ tpr_bwd_kernel(
 #pragma unroll
     for (int c = 0; c < MID; ++c) gv[c] = dAt[((size_t)i * MID + c) * K + k] * inv_c;
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+    if constexpr (GF) {
+      // G_p of this receiver and channel; the four lane groups hold the same
+      // channels, the first one stores
+      __builtin_amdgcn_wave_barrier();   // the previous receiver's reads come first
+      for_paths<LHMAX>([&](auto tag) {
+        using T = decltype(tag);
+        using C = mt::CG<T::lh, T::ly, T::lo>;
+        constexpr int goff = PathPairOffset<T::index>::value;
+        float Gp[C::npair];
+#pragma unroll
+        for (int u = 0; u < C::npair; ++u) Gp[u] = 0.f;
+        C::each_p([&](int m1, int m2, int m3, float cg, int pi) { Gp[pi] += cg * gv[T::offset + m3]; });
+        if (g == 0) {
+#pragma unroll
+          for (int u = 0; u < C::npair; ++u) sg[(goff + u) * 16 + kk] = Gp[u];
+        }
+      });
+      __builtin_amdgcn_wave_barrier();
+    }
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      int srcq[4];
+      sender_rows(snd, src_map, e0 + 4 * g, e_end, srcq);
       stage_y(Y, e0, e_end, sy);
       f4 r[P];   // R on entry; dR (zero for edges past e_end) after the edge loop
       if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, sWb, r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
       const int nq = min(4, e_end - e0);
+      float hv[DIN];
+      load_h_row<DIN>(h, srcq[0], K, k, hv);
       static_for<0, 4>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
         __builtin_amdgcn_sched_barrier(0);
         if (q >= nq) return;
+        if constexpr (GF) __asm__ volatile("" ::: "memory");   // G is read from LDS per edge, not held
         const int row = 4 * g + q;
         const int e_raw = e0 + row;
         const bool valid = e_raw < e_end;
         const int e = min(e_raw, e_end - 1);
-        const int s = snd[e];
-        const int src = src_map ? src_map[s] : s;
-        float hv[DIN];
-#pragma unroll
-        for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
+        float hn[DIN];
+        if constexpr (q < 3) load_h_row<DIN>(h, srcq[q + 1], K, k, hn);
         float y[16];
         read_y(sy, row, y);
         float dy[16], dh[DIN];
@@ -376,18 +433,28 @@ tpr_bwd_kernel(
           constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
           __builtin_amdgcn_sched_barrier(0);
           const float rv = r[T::index][q];
-          // Bm[m2] = sum C h[m1] g[m3], Dm[m1] = sum C Y[m2] g[m3]; then
-          // dR = Bm . Y, dY += R Bm, dh += R Dm. (C g is not formed on its own:
-          // it would be hoisted out of the edge loop as 86 live registers.)
+          // Bm[m2] = sum C h[m1] g[m3], Dm[m1] = sum C Y[m2] g[m3] (from the
+          // receiver's G table, or per coupling: C g held in registers would
+          // be 86 live values across the edge loop); then dR = Bm . Y,
+          // dY += R Bm, dh += R Dm.
           float Bm[2 * ly + 1], Dm[2 * lh + 1];
 #pragma unroll
           for (int m = 0; m < 2 * ly + 1; ++m) Bm[m] = 0.f;
 #pragma unroll
           for (int m = 0; m < 2 * lh + 1; ++m) Dm[m] = 0.f;
-          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
-            Bm[m2] += cg * (gv[T::offset + m3] * hv[lh * lh + m1]);
-            Dm[m1] += cg * (gv[T::offset + m3] * y[ly * ly + m2]);
-          });
+          if constexpr (GF) {
+            const float* gp = sg + PathPairOffset<T::index>::value * 16 + kk;
+            mt::CG<lh, ly, lo>::each_pair([&](int m1, int m2, int pi) {
+              const float gval = gp[pi * 16];
+              Bm[m2] += gval * hv[lh * lh + m1];
+              Dm[m1] += gval * y[ly * ly + m2];
+            });
+          } else {
+            mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
+              Bm[m2] += cg * (gv[T::offset + m3] * hv[lh * lh + m1]);
+              Dm[m1] += cg * (gv[T::offset + m3] * y[ly * ly + m2]);
+            });
+          }
           float d = 0.f;
 #pragma unroll
           for (int m = 0; m < 2 * ly + 1; ++m) {
@@ -405,6 +472,10 @@ tpr_bwd_kernel(
 #pragma unroll
             for (int c = 0; c < DIN; ++c) Q[((size_t)e * DIN + c) * K + k] = dh[c];
           }
+        }
+        if constexpr (q < 3) {
+#pragma unroll
+          for (int c = 0; c < DIN; ++c) hv[c] = hn[c];
         }
       });
       // da3 partial: D[e][j] = sum_{p, k} dR[e][p][k] W3[j][p K + 16 ct + k]. The

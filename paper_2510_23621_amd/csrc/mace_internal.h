@@ -306,6 +306,7 @@ constexpr int kMaxRadialLayers = 4;
 struct RadialSet {
   const float* W[kMaxRadialLayers];
   float* a3[kMaxRadialLayers];
+  float* sg[kMaxRadialLayers];   // [3][E][64] silu'(z) of the three pre-activations
   int n;
 };
 void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
@@ -313,7 +314,7 @@ void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd
                           const RadialSet& rs, int* status);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
-void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
+void launch_radial_bwd(hipStream_t s, int E, int nb, const float* W, const float* sg, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate);
 void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
                    const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
@@ -344,7 +345,7 @@ void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, d
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
                         const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
-                        const float* w1, const float* w2, int hidden, int lowp, float* dh);
+                        const float* w1, const float* w2, int hidden, int lowp, int overwrite, float* dh);
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E);
 void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp,
                           float* table);

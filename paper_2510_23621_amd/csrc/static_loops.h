@@ -94,4 +94,20 @@ __device__ __forceinline__ void for_paths(F&& f) {
 template <int I>
 using PathAt = PathTag<path_at(I, 0), path_at(I, 1), path_at(I, 2)>;
 
+// Offset of the I-th path's block in a per-channel table holding, path after
+// path, one value per (m1, m2) pair that carries a nonzero coupling.
+template <int I>
+struct PathPairOffset {
+  using Prev = PathAt<I - 1>;
+  static constexpr int value = PathPairOffset<I - 1>::value + mt::CG<Prev::lh, Prev::ly, Prev::lo>::npair;
+};
+template <>
+struct PathPairOffset<0> {
+  static constexpr int value = 0;
+};
+template <int LHMAX>
+struct PairCount {
+  static constexpr int value = PathPairOffset<path_count(LHMAX)>::value;
+};
+
 }  // namespace mace
