@@ -28,10 +28,12 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 KERNEL_SOURCES = {"edge_prologue_kernel": "k_radial.hip", "radial_bwd_kernel": "k_radial.hip",
-                  "tpr_fwd_kernel": "k_tpr.hip", "tpr_bwd_kernel": "k_tpr.hip", "linear_kernel": "k_node.hip"}
+                  "tpr_fwd_kernel": "k_tpr.hip", "tpr_bwd_kernel": "k_tpr.hip", "linear_kernel": "k_node.hip",
+                  "l0_gather_kernel": "k_layer0.hip", "l0_edge_bwd_kernel": "k_layer0.hip"}
 # kernel classes whose roofline is the FP32 MFMA peak (dense contractions);
 # the others are priced against HBM bandwidth
 MFMA_BOUND = ("edge_prologue_kernel", "radial_bwd_kernel", "tpr_fwd_kernel", "tpr_bwd_kernel")
+# (l0_gather_kernel and l0_edge_bwd_kernel are priced against HBM bandwidth)
 
 
 def source_hash(kname):
@@ -58,18 +60,30 @@ def measured_traffic(kname, workload):
     return rec["bytes_per_launch"]
 
 
-def kernel_work(name, model, N, E):
+def kernel_work(name, model, N, E, l0_factored=False, n_species=2):
     """Algorithmic (bytes, flops) of every launch of kernel class `name` in
     one step, summed.  Bytes count each compulsory HBM read/write once; flops
     of the MFMA-bound classes count the dense contractions only (the radial
     MLP layers, including the last one formed inside the tensor-product
-    kernels), not the Clebsch-Gordan arithmetic on the vector ALUs."""
+    kernels), not the Clebsch-Gordan arithmetic on the vector ALUs.  With
+    the first layer in factorised form its message comes from the l0_*
+    kernels and its radial backward reads one partial."""
     K, nb, layers = model["K"], model["n_bessel"], model["layers"]
     n_ct = K // 16
+    ki = 64 * n_species
     tot_b = tot_f = 0.0
     for t, L in enumerate(layers):
         P, mid, din = L["P"], L["mid"], L["din"]
-        if name == "tpr_fwd_kernel":
+        fact = l0_factored and t == 0
+        if fact and name in ("tpr_fwd_kernel", "tpr_bwd_kernel"):
+            continue
+        if name == "l0_gather_kernel" and fact:      # a3, Y, sender species in; U out
+            tot_b += E * (256 + 64 + 4) + (N + 1) * 4 + N * 16 * ki * 4
+            tot_f += E * 2 * 64 * 16
+        elif name == "l0_edge_bwd_kernel" and fact:  # gU, a3, Y, sender species in; dE/da3, dE/dY out
+            tot_b += N * 16 * ki * 4 + E * (256 + 64 + 4) + E * (256 + 64)
+            tot_f += E * 2 * 2 * 64 * 16
+        elif name == "tpr_fwd_kernel":
             tot_b += E * (256 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4 + 64 * P * K * 4
             tot_f += E * 2 * 64 * P * K
         elif name == "tpr_bwd_kernel":
@@ -77,11 +91,12 @@ def kernel_work(name, model, N, E):
             tot_b += E * (256 + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
             tot_f += E * 2 * 2 * 64 * P * K
         elif name == "edge_prologue_kernel":      # geometry once, hidden layers of every layer
-            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * 256
+            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * (256 + 3 * 256)   # a3, silu'
             tot_f += E * 2 * (nb * 64 + 2 * 64 * 64)
         elif name == "radial_bwd_kernel":
             acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
-            tot_b += E * (nb * 4 + n_ct * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
+            parts = 1 if fact else n_ct
+            tot_b += E * (3 * 256 + parts * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
             tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64)
     return tot_b, tot_f
 
@@ -217,7 +232,8 @@ def main():
 
     from paper_2510_23621_amd.csrc_info import layer_shapes
     model = layer_shapes(params)
-    byts, flops = kernel_work(kname, model, N, E)
+    l0_factored = B.mace_layer0_form(g.handle, -1) == B.MACE_L0_FACTORED
+    byts, flops = kernel_work(kname, model, N, E, l0_factored, params["n_species"])
     per_launch = k_launches / args.steps
     avg_launch_ms = k_ms / max(k_launches, 1)
     bytes_per_launch = byts / max(per_launch, 1)
@@ -307,7 +323,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": CONFIGS[cfg]["name"], "n_atoms": N, "n_edges": E, "K": params["K"],
                    "hidden_lmax": params["hidden_lmax"], "r_cut": params["r_cut"], "correlation": 3,
-                   "layers": 2, "precision": args.prec},
+                   "layers": 2, "precision": args.prec,
+                   "layer0_form": "factorised" if l0_factored else "per-edge"},
         "roofline": roof,
         "step_ms_p10_p50_p90": [round(float(np.percentile(per_call, q)), 4) for q in (10, 50, 90)],
         "forward_only": {"atoms_per_s": round(N / (fwd_ms * 1e-3), 1), "ms": round(fwd_ms, 4)},

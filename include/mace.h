@@ -159,6 +159,24 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
 mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                                float* forces, double* stress, void* stream);
 
+/* How the first interaction layer forms its message.  Its sender features
+ * depend on the species only (the embedding through linear_up) and its paths
+ * are (0, l, l), whose coupling is the identity, so Eq. 26 summed over a
+ * receiver's edges factorises: U[i][c][s][j] = sum over the edges into i
+ * from atoms of species s of a3[e][j] Y[e][c] (a3 the last hidden layer of
+ * the radial MLP, c = l^2 + m), then one node-level contraction of U with the
+ * last radial layer and the species table (in MACE_FP32, composed with the
+ * path-merging and species linears that follow it, in FP64 at setup).
+ *   MACE_L0_EDGE:     the per-edge product, as every other layer;
+ *   MACE_L0_FACTORED: the factorised form (S <= 4 only, else MACE_EUNSUPPORTED);
+ *   MACE_L0_AUTO:     setup's choice, factorised when S <= 4 and E >= 3 S N.
+ * Both forms compute the same function and differ only in FP32 rounding
+ * order.  request < 0 only queries; *in_use (host, may be NULL) receives
+ * MACE_L0_EDGE or MACE_L0_FACTORED.  Takes effect for calls enqueued after
+ * it returns; no device work. */
+typedef enum { MACE_L0_AUTO = 0, MACE_L0_EDGE = 1, MACE_L0_FACTORED = 2 } mace_l0_form;
+mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use);
+
 /* Device-detected errors of the calls enqueued since setup or the previous
  * check: the edge kernels OR status bits into a word of the workspace,
  * 1 = an edge vector with a non-finite component (NaN or infinite

@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmace_amd.so")
-HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip",
+HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_layer0.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip",
                "k_neighbors.hip"]
 # files whose FP64 arithmetic must round exactly as written (no fused multiply-adds)
 NO_CONTRACT = {"k_neighbors.hip"}

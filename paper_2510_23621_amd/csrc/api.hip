@@ -49,6 +49,8 @@ struct Model {
   std::map<std::string, int64_t> off;
   int64_t total = 0;       // floats of the weight blob
   int64_t comb_off = 0;    // after the blob: layer-0 path-merging x species weights [4][S][K][K]
+  int l0_ki = 0;           // channels of the factorised first layer's U (64 S), 0 when S > kL0MaxSpecies
+  int64_t l0_off = 0;      // after those: its weights [4][S][l0_ki][K] (transposed copy [4][S][K][l0_ki])
   int64_t total_ext = 0;   // blob + combined weights (FP32 copies only)
   int max_P = 0, max_mid = 0, max_din = 0, max_dout = 0;
 };
@@ -138,7 +140,9 @@ mace_status build_model(const mace_model_desc* desc, Model& m) {
   }
   m.total = o;
   m.comb_off = o;
-  m.total_ext = o + 4 * S * K * K;
+  m.l0_ki = S <= kL0MaxSpecies ? 64 * (int)S : 0;
+  m.l0_off = o + 4 * S * K * K;
+  m.total_ext = m.l0_off + 4 * S * (int64_t)m.l0_ki * K;
   return MACE_OK;
 }
 
@@ -171,10 +175,12 @@ struct Buffers {
   float *dh0 = nullptr, *dh1 = nullptr, *dB = nullptr, *dA = nullptr, *dApre = nullptr, *dAt = nullptr,
         *dY = nullptr, *de = nullptr, *Q = nullptr, *dht = nullptr;
   float *da3p = nullptr, *dYp = nullptr;   // per-channel-tile partials [K/16][E][64], [K/16][E][16]
+  float *U0 = nullptr, *gU0 = nullptr;     // factorised first layer: U and dE/dU, [N][16][l0_ki]
+  int* snd_z = nullptr;                    // [E] species of each edge's sender
   float4* g = nullptr;
   double* inv_vol = nullptr;      // [G] 1/|det cell|, or 1 without cells
   int* status = nullptr;          // device status word (kStatus* bits)
-  LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 4
+  LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 6
 };
 
 int64_t n_tiles_bound(int64_t N, int S) { return (N + kLinTileNodes - 1) / kLinTileNodes + S; }
@@ -239,7 +245,12 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.dht = c.take<float>(N * m.max_din * K);
   b.g = c.take<float4>(std::max<int64_t>(E, 1));
   b.inv_vol = c.take<double>(G);
-  b.lin_dev = c.take<LinLaunch>(6 * T + 4);
+  b.lin_dev = c.take<LinLaunch>(6 * T + 6);
+  b.snd_z = c.take<int>(std::max<int64_t>(E, 1));
+  if (m.l0_ki) {
+    b.U0 = c.take<float>(N * 16 * m.l0_ki);
+    b.gU0 = c.take<float>(N * 16 * m.l0_ki);
+  }
   b.status = c.take<int>(64);
 }
 
@@ -248,12 +259,13 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
 enum KernelId {
   KID_EDGE_FEATURES = 0, KID_TP_FWD, KID_LINEAR, KID_SYMCON_FWD, KID_READOUT,
   KID_TP_BWD, KID_RADIAL_BWD, KID_SYMCON_BWD, KID_SENDER_SUM, KID_EDGE_BWD, KID_FORCES, KID_GRAPH_ENERGY,
-  KID_FILL, KID_COUNT
+  KID_FILL, KID_L0_GATHER, KID_L0_BWD, KID_COUNT
 };
 const char* kKernelNames[KID_COUNT] = {
   "edge_prologue_kernel", "tpr_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
   "readout_kernel", "tpr_bwd_kernel", "radial_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
-  "edge_vjp_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel"};
+  "edge_vjp_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel", "l0_gather_kernel",
+  "l0_edge_bwd_kernel"};
 constexpr int kProfPairs = 4096;
 
 struct mace_graph {
@@ -272,6 +284,10 @@ struct mace_graph {
   // linear plans per layer (host copy for the grid, device copy for the kernel)
   std::vector<LinPlanRef> upskip, upskipT, lin, linT, prod, prodT;
   LinPlanRef skip0, skip0T, comb0, comb0T;
+  // first layer in factorised form: U -> A (FP32; composed with the
+  // path-merging and species linears) or U -> At (16-bit modes), and transposes
+  LinPlanRef l0f, l0fT;
+  bool l0_fact = false;
 };
 
 namespace {
@@ -296,6 +312,14 @@ struct ProfScope {
   }
 };
 #define PROF(kid) ProfScope _prof_##__LINE__(h, kid, s)
+
+// The first layer runs in factorised form where it has fewer multiply-adds:
+// per node 16 x 64 S x K (U to the message) against per edge 64 x P K (the
+// last radial layer), i.e. when the mean degree exceeds about 4 S (with a
+// margin for the per-edge passes of both forms).
+bool l0_auto(const Model& m, int64_t N, int64_t E) {
+  return m.l0_ki > 0 && E >= 3 * (int64_t)m.d.n_species * N;
+}
 
 // A linear launch, bracketed for profiling; while the linear class is
 // selected its algorithmic work is summed too.
@@ -421,6 +445,21 @@ void make_plans(mace_graph* h) {
     p.cout = m.layers[0].mid;
     h->comb0T.host = make_lin_launch(p);
   }
+  // factorised first layer: one term per l on components l^2 .. l^2 + 2l; the
+  // weights depend on the receiver's species where they include its species linear
+  if (m.l0_ki) {
+    const bool composed = lowp_mode(h->prec) == 0;
+    LinPlan p;
+    p.cin = 16;
+    p.cout = 16;
+    p.w_sstride = (int64_t)m.l0_ki * m.d.K;
+    for (int l = 0; l <= 3; ++l) {
+      p.g[p.n_groups++] = LinGroup{l * l, 2 * l + 1, p.n_terms, p.n_terms + 1, 0};
+      p.t[p.n_terms++] = LinTerm{l * l, 0, composed ? 1 : 0, m.l0_off + (int64_t)l * m.d.n_species * p.w_sstride};
+    }
+    h->l0f.host = make_lin_launch(p);
+    h->l0fT = h->l0f;
+  }
 }
 
 // copy every plan to the device buffer carved for them; the kernels read it there
@@ -430,7 +469,7 @@ hipError_t upload_plans(mace_graph* h, hipStream_t s) {
   for (int t = 0; t < T; ++t)
     for (auto* v : {&h->upskip, &h->upskipT, &h->lin, &h->linT, &h->prod, &h->prodT})
       refs.push_back(&(*v)[t]);
-  for (auto* r : {&h->skip0, &h->skip0T, &h->comb0, &h->comb0T}) refs.push_back(r);
+  for (auto* r : {&h->skip0, &h->skip0T, &h->comb0, &h->comb0T, &h->l0f, &h->l0fT}) refs.push_back(r);
   std::vector<LinLaunch> host(refs.size());
   for (size_t q = 0; q < refs.size(); ++q) {
     host[q] = refs[q]->host;
@@ -461,8 +500,19 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.quad_count = h->b.quad_count;
   a.n_quads = h->n_quads;
   a.K = h->m.d.K;
+  a.KI = 0;
   a.accumulate = accumulate;
   a.lowp = lowp_mode(h->prec);
+  return a;
+}
+
+// the factorised first layer's contraction (FP32 in every mode): U (l0_ki
+// channels) -> K channels, or its transpose
+LinArgs largs_l0(mace_graph* h, const float* x, float* y, bool transposed) {
+  LinArgs a = largs(h, x, y, nullptr, transposed, 0);
+  a.lowp = 0;
+  a.K = transposed ? h->m.l0_ki : h->m.d.K;
+  a.KI = transposed ? h->m.d.K : h->m.l0_ki;
   return a;
 }
 
@@ -505,34 +555,41 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
   for (int t = 0; t < m.d.n_layers; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
-    const float* src;
-    const int* src_map;
-    if (t == 0) {
-      src = b.sp_table;
-      src_map = b.species;
-    } else {
+    if (t == 0 && h->l0_fact) {
+      // factorised first layer: U per receiver, then one contraction (FP32
+      // mode: straight to A; 16-bit modes: to At, then their own linears)
       {
+        PROF(KID_L0_GATHER);
+        launch_l0_gather(s, N, m.d.n_species, b.rcv_off, b.snd_z, b.a3[0], b.Y, h->prec == MACE_BF16_RADIAL, b.U0);
+      }
+      if (!lowp) {
+        run_linear(h, s, h->l0f, largs_l0(h, b.U0, b.A[0], false));
+      } else {
+        run_linear(h, s, h->l0f, largs_l0(h, b.U0, b.At, false));
+        run_linear(h, s, h->lin[0], largs(h, b.At, b.Apre, nullptr, false, 0));
+        run_linear(h, s, h->skip0, largs(h, b.Apre, b.A[0], nullptr, false, 0));
+      }
+    } else {
+      // edge product with the sender features: the species table at layer 0,
+      // linear_up of h^t (with the residual species linear) after it
+      const float* src = b.sp_table;
+      const int* src_map = b.species;
+      if (t > 0) {
         run_linear(h, s, h->upskip[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0, nullptr, b.sc));
+        src = b.ht[t];
+        src_map = nullptr;
       }
-      src = b.ht[t];
-      src_map = nullptr;
-    }
-    {
-      PROF(KID_TP_FWD);
-      launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"), b.Y,
-                     src, inv_c, b.At, h->prec == MACE_BF16_RADIAL);
-    }
-    if (t == 0 && !lowp) {
-      run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
-    } else if (t == 0) {   // 16-bit linears: each linear rounds its own inputs and weights
       {
+        PROF(KID_TP_FWD);
+        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
+                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL);
+      }
+      if (t == 0 && !lowp) {
+        run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
+      } else if (t == 0) {   // 16-bit linears: each linear rounds its own inputs and weights
         run_linear(h, s, h->lin[t], largs(h, b.At, b.Apre, nullptr, false, 0));
-      }
-      {
         run_linear(h, s, h->skip0, largs(h, b.Apre, b.A[t], nullptr, false, 0));
-      }
-    } else {
-      {
+      } else {
         run_linear(h, s, h->lin[t], largs(h, b.At, b.A[t], nullptr, false, 0));
       }
     }
@@ -597,21 +654,32 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
     }
-    if (t == 0 && !lowp) {
+    const bool fact = t == 0 && h->l0_fact;
+    // dE/dAt (the transposes of the linears after the edge product); the
+    // factorised first layer ends in dE/dU instead
+    const float* dApre = b.dA;
+    if (t == 0 && lowp) {   // 16-bit modes: each linear's own transpose
+      run_linear(h, s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
+      dApre = b.dApre;
+    }
+    if (fact && !lowp) {
+      run_linear(h, s, h->l0fT, largs_l0(h, b.dA, b.gU0, true));
+    } else if (t == 0 && !lowp) {
       run_linear(h, s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
     } else {
-      const float* dApre = b.dA;
-      if (t == 0) {
-        {
-          run_linear(h, s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
-        }
-        dApre = b.dApre;
-      }
       run_linear(h, s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
+      if (fact) run_linear(h, s, h->l0fT, largs_l0(h, b.dAt, b.gU0, true));
     }
-    const float* src = t == 0 ? b.sp_table : b.ht[t];
-    const int* src_map = t == 0 ? b.species : nullptr;
-    {
+    int n_part = K / 16;
+    if (fact) {
+      // dE/da3 and dE/dY per edge, whole (one partial each)
+      PROF(KID_L0_BWD);
+      launch_l0_edge_bwd(s, N, m.d.n_species, b.rcv_off, b.snd_z, b.a3[0], b.Y, b.gU0, h->prec == MACE_BF16_RADIAL,
+                         b.da3p, b.dYp);
+      n_part = 1;
+    } else {
+      const float* src = t == 0 ? b.sp_table : b.ht[t];
+      const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
       launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, h->prec == MACE_BF16_RADIAL);
@@ -620,7 +688,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       // right after the partials are written, while they are still in the
       // last-level cache
       PROF(KID_RADIAL_BWD);
-      launch_radial_bwd(s, E, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.sg[t], b.da3p, b.dYp, K / 16,
+      launch_radial_bwd(s, E, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.sg[t], b.da3p, b.dYp, n_part,
                         b.dY, b.de, t < T - 1);
     }
     if (t > 0) {
@@ -835,6 +903,74 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     }
   }
 
+  // factorised first layer (S <= kL0MaxSpecies): U (64 S channels per
+  // component) to the layer's message, with c = l^2 + m, p(l) the path
+  // (0, l, l), table[s][k] = sum_k' emb[s][k'] Wup[k'][k] (the mode's rounding
+  // of emb and Wup, unrounded FP64 sums):
+  //   Wf[l][s, j][k] = inv_c W3[j][p(l) K + k] table[s][k]     (U -> At)
+  // and in FP32 mode composed with the path-merging and species linears,
+  //   Wtot[l][z][s, j][k] = sum_k' Wf[l][s, j][k'] (W_lin[p(l)] W_skip[l][z])[k'][k]   (U -> A)
+  // FP64 throughout, one rounding; stored [l][z][s, j][k] (16-bit modes: z = 0
+  // only) and transposed [l][z][k][s, j].
+  if (m.l0_ki) {
+    const LayerPlan& L0 = m.layers[0];
+    const int lowp = lowp_mode(prec);
+    const int64_t KI = m.l0_ki, PK = (int64_t)L0.P * K;
+    const double inv_c = 1.0 / m.d.c_norm;
+    std::vector<double> tab(S * K, 0.0);
+    const float* emb = hw.data() + m.off.at("embed");
+    const float* wup = hw.data() + m.off.at("0.up.0");
+    for (int64_t z = 0; z < S; ++z)
+      for (int64_t k = 0; k < K; ++k) {
+        double acc = 0.0;
+        for (int64_t q = 0; q < K; ++q)
+          acc += (double)lowp_round(emb[z * K + q], lowp) * (double)lowp_round(wup[q * K + k], lowp);
+        tab[z * K + k] = acc;
+      }
+    const float* w3 = hw.data() + m.off.at("0.radial.3");
+    std::vector<double> wf(KI * K), M(K * K);
+    for (int l = 0; l <= 3; ++l) {
+      int p = -1;
+      for (int q = 0; q < L0.P; ++q)
+        if (L0.paths[q].lo == l) p = q;
+      for (int64_t sj = 0; sj < KI; ++sj) {
+        const int64_t sp = sj / 64, j = sj % 64;
+        for (int64_t k = 0; k < K; ++k) {
+          double w = w3[j * PK + p * K + k];
+          if (prec == MACE_BF16_RADIAL) w = bf16_round((float)w);
+          wf[sj * K + k] = inv_c * w * tab[sp * K + k];
+        }
+      }
+      const int nz = lowp ? 1 : (int)S;
+      for (int z = 0; z < nz; ++z) {
+        const int64_t base = m.l0_off + ((int64_t)l * S + z) * KI * K;
+        if (lowp) {
+          for (int64_t sj = 0; sj < KI; ++sj)
+            for (int64_t k = 0; k < K; ++k) {
+              hw[base + sj * K + k] = (float)wf[sj * K + k];
+              hwT[base + k * KI + sj] = (float)wf[sj * K + k];
+            }
+          continue;
+        }
+        const float* wl = hw.data() + m.off.at("0.linear." + std::to_string(p));
+        const float* ws = hw.data() + m.off.at("0.skip." + std::to_string(l)) + (int64_t)z * K * K;
+        for (int64_t a = 0; a < K; ++a)
+          for (int64_t n = 0; n < K; ++n) {
+            double acc = 0.0;
+            for (int64_t q = 0; q < K; ++q) acc += (double)wl[a * K + q] * (double)ws[q * K + n];
+            M[a * K + n] = acc;
+          }
+        for (int64_t sj = 0; sj < KI; ++sj)
+          for (int64_t n = 0; n < K; ++n) {
+            double acc = 0.0;
+            for (int64_t q = 0; q < K; ++q) acc += wf[sj * K + q] * M[q * K + n];
+            hw[base + sj * K + n] = (float)acc;
+            hwT[base + n * KI + sj] = (float)acc;
+          }
+      }
+    }
+  }
+
   // 16-bit copies (bf16 or binary16, by mode) of every K x K block, packed
   // [K/8][K][8] (element (k, n) at ((k/8) K + n) 8 + k%8) for the MFMA B
   // operand of the 16-bit linears
@@ -902,6 +1038,9 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(up(b.rcv_off, rcv_off.data(), (N + 1) * 4));
   chk(up(b.snd_off, snd_off.data(), (N + 1) * 4));
   chk(up(b.snd_perm, snd_perm.data(), E * 4));
+  std::vector<int32_t> snd_z(std::max<int64_t>(E, 1), 0);
+  for (int64_t e = 0; e < E; ++e) snd_z[e] = hs[hsnd[e]];
+  chk(up(b.snd_z, snd_z.data(), E * 4));
   chk(up(b.graph_off, goff.data(), (G + 1) * 4));
   std::vector<double> inv_vol(G, 1.0);
   if (cells)
@@ -928,6 +1067,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     delete h;
     return MACE_EHIP;
   }
+  h->l0_fact = l0_auto(h->m, N, E);
   make_plans(h);
   if (upload_plans(h, s) != hipSuccess) {
     delete h;
@@ -996,6 +1136,16 @@ void mace_graph_destroy(mace_graph* g) {
   if (!g) return;
   for (auto e : g->prof_ev) hipEventDestroy(e);
   delete g;
+}
+
+mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
+  if (!g || request > MACE_L0_FACTORED) return MACE_EINVAL;
+  if (request == MACE_L0_FACTORED && !g->m.l0_ki) return MACE_EUNSUPPORTED;
+  if (request == MACE_L0_AUTO) g->l0_fact = l0_auto(g->m, g->N, g->E);
+  else if (request == MACE_L0_EDGE) g->l0_fact = false;
+  else if (request == MACE_L0_FACTORED) g->l0_fact = true;
+  if (in_use) *in_use = g->l0_fact ? MACE_L0_FACTORED : MACE_L0_EDGE;
+  return MACE_OK;
 }
 
 mace_status mace_profile_select(mace_graph* g, int32_t kernel) {

@@ -1,0 +1,188 @@
+// First interaction layer in factorised form.
+//
+// At layer 0 the sender features are the species table (h[j][k] =
+// table[z_j][k]) and every path is (0, l, l), whose coupling is the identity,
+// so the neighbour sum of Eq. 26 with the last radial layer written out is
+//   At[i][c][k] = inv_c sum_{e: rcv_e = i} (sum_j a3[e][j] W3[j][p(l) K + k]) table[z_e][k] Y[e][c]
+//               = sum_{s, j} U[i][c][s][j] Wf[l][s, j][k],
+//   U[i][c][s][j] = sum_{e: rcv_e = i, z_e = s} a3[e][j] Y[e][c],
+//   Wf[l][s, j][k] = inv_c W3[j][p(l) K + k] table[s][k],
+// with c = l^2 + m the component of Y and of At, p(l) the path (0, l, l) and
+// z_e the species of the edge's sender. The per-edge product is then 64 x 16
+// multiply-adds into U instead of the P K-wide radial layer, and the rest is
+// a node-level contraction over S * 64 channels that runs on the channel-mixing
+// linear kernel (where it can be composed with the path-merging and species
+// linears that follow it). The backward pass receives gU = dE/dU from the
+// transposed contraction and returns per edge
+//   dE/da3[e][j] = sum_c gU[i][c][z_e][j] Y[e][c],
+//   dE/dY[e][c]  = sum_j gU[i][c][z_e][j] a3[e][j].
+// In the BF16-radial mode a3 enters as its bfloat16 rounding (the weights
+// carry the rounded W3), which is the same product as the per-edge form.
+//
+// U and gU are [N][16][S * 64]. One block of four waves per receiver; lane
+// j = 0..63 is the radial hidden unit. Every sum runs over the receiver's
+// edges in CSR order within one lane, so results do not depend on scheduling.
+#include "mace_internal.h"
+
+namespace mace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kL0Edges = 4;   // edges whose loads are issued together
+
+// Wave w gathers components 4w .. 4w + 3 of U over every edge of the receiver.
+template <int S, bool RB>
+__global__ void __launch_bounds__(256) l0_gather_kernel(int N, const int* __restrict__ rcv_off,
+                                                        const int* __restrict__ snd_z, const float* __restrict__ a3,
+                                                        const float* __restrict__ Y, float* __restrict__ U) {
+  constexpr int KI = 64 * S;
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float acc[S][4];
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[s][c] = 0.f;
+  const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+  for (int e0 = e_beg; e0 < e_end; e0 += kL0Edges) {
+    float a[kL0Edges];
+    f4 y[kL0Edges];
+    int z[kL0Edges];
+#pragma unroll
+    for (int q = 0; q < kL0Edges; ++q) {
+      const int e = min(e0 + q, e_end - 1);
+      z[q] = snd_z[e];
+      a[q] = a3[(size_t)e * 64 + lane];
+      y[q] = *reinterpret_cast<const f4*>(Y + (size_t)e * 16 + 4 * w);
+    }
+#pragma unroll
+    for (int q = 0; q < kL0Edges; ++q) {
+      if (e0 + q >= e_end) break;
+      const float av = RB ? bf16_round(a[q]) : a[q];
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        if (z[q] == s) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[s][c] += av * y[q][c];
+        }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int s = 0; s < S; ++s) U[((size_t)i * 16 + 4 * w + c) * KI + 64 * s + lane] = acc[s][c];
+}
+
+// One halving step of a 64-lane reduce-scatter over v[0 .. 2 N_): lanes with
+// bit XOR set keep the upper half, the others the lower half, each adding the
+// partner lane's copy of the half it keeps.
+template <int N_, int XOR>
+__device__ __forceinline__ void halve(float* v, int lane) {
+  const bool hi = lane & XOR;
+#pragma unroll
+  for (int q = 0; q < N_; ++q) {
+    const float send = hi ? v[q] : v[q + N_];
+    const float keep = hi ? v[q + N_] : v[q];
+    v[q] = keep + __shfl_xor(send, XOR);
+  }
+}
+
+// Sum of v[0..15] over the 64 lanes of the wave: afterwards every lane l holds
+// the total of index (l >> 2) & 15 (fixed butterfly order).
+__device__ __forceinline__ float wave_reduce_scatter16(float* v, int lane) {
+  halve<8, 32>(v, lane);
+  halve<4, 16>(v, lane);
+  halve<2, 8>(v, lane);
+  halve<1, 4>(v, lane);
+  float t = v[0];
+  t += __shfl_xor(t, 2);
+  t += __shfl_xor(t, 1);
+  return t;
+}
+
+// Wave w takes the receiver's edges e_beg + w, e_beg + w + 4, ...; it holds
+// gU[i][c][s][lane] for every (s, c) in registers. dE/da3 goes to da3[e][64],
+// dE/dY to dY[e][16] (both overwritten).
+template <int S, bool RB>
+__global__ void __launch_bounds__(256) l0_edge_bwd_kernel(int N, const int* __restrict__ rcv_off,
+                                                          const int* __restrict__ snd_z,
+                                                          const float* __restrict__ a3, const float* __restrict__ Y,
+                                                          const float* __restrict__ gU, float* __restrict__ da3,
+                                                          float* __restrict__ dY) {
+  constexpr int KI = 64 * S;
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+  if (e_beg + w >= e_end) return;
+  float g[S][16];
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int c = 0; c < 16; ++c) g[s][c] = gU[((size_t)i * 16 + c) * KI + 64 * s + lane];
+  for (int e = e_beg + w; e < e_end; e += 4) {
+    const int z = snd_z[e];
+    float a = a3[(size_t)e * 64 + lane];
+    if (RB) a = bf16_round(a);
+    float y[16];
+#pragma unroll
+    for (int v4 = 0; v4 < 4; ++v4) {
+      const f4 t = *reinterpret_cast<const f4*>(Y + (size_t)e * 16 + 4 * v4);
+      y[4 * v4] = t[0];
+      y[4 * v4 + 1] = t[1];
+      y[4 * v4 + 2] = t[2];
+      y[4 * v4 + 3] = t[3];
+    }
+    float gs[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) gs[c] = g[0][c];
+#pragma unroll
+    for (int s = 1; s < S; ++s)
+      if (z == s) {
+#pragma unroll
+        for (int c = 0; c < 16; ++c) gs[c] = g[s][c];
+      }
+    float d = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) d += gs[c] * y[c];
+    da3[(size_t)e * 64 + lane] = d;
+    float v[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) v[c] = gs[c] * a;
+    const float t = wave_reduce_scatter16(v, lane);
+    if ((lane & 3) == 0) dY[(size_t)e * 16 + (lane >> 2)] = t;
+  }
+}
+
+void launch_l0_gather(hipStream_t s, int N, int S, const int* rcv_off, const int* snd_z, const float* a3,
+                      const float* Y, int rb, float* U) {
+  if (N <= 0) return;
+  auto go = [&](auto SS) {
+    constexpr int SV = decltype(SS)::value;
+    if (rb) l0_gather_kernel<SV, true><<<N, 256, 0, s>>>(N, rcv_off, snd_z, a3, Y, U);
+    else l0_gather_kernel<SV, false><<<N, 256, 0, s>>>(N, rcv_off, snd_z, a3, Y, U);
+  };
+  switch (S) {
+    case 1: go(std::integral_constant<int, 1>{}); break;
+    case 2: go(std::integral_constant<int, 2>{}); break;
+    case 3: go(std::integral_constant<int, 3>{}); break;
+    case 4: go(std::integral_constant<int, 4>{}); break;
+  }
+}
+
+void launch_l0_edge_bwd(hipStream_t s, int N, int S, const int* rcv_off, const int* snd_z, const float* a3,
+                        const float* Y, const float* gU, int rb, float* da3, float* dY) {
+  if (N <= 0) return;
+  auto go = [&](auto SS) {
+    constexpr int SV = decltype(SS)::value;
+    if (rb) l0_edge_bwd_kernel<SV, true><<<N, 256, 0, s>>>(N, rcv_off, snd_z, a3, Y, gU, da3, dY);
+    else l0_edge_bwd_kernel<SV, false><<<N, 256, 0, s>>>(N, rcv_off, snd_z, a3, Y, gU, da3, dY);
+  };
+  switch (S) {
+    case 1: go(std::integral_constant<int, 1>{}); break;
+    case 2: go(std::integral_constant<int, 2>{}); break;
+    case 3: go(std::integral_constant<int, 3>{}); break;
+    case 4: go(std::integral_constant<int, 4>{}); break;
+  }
+}
+
+}  // namespace mace

@@ -38,14 +38,16 @@ __device__ __forceinline__ unsigned short lowp_bits(float x) {
 constexpr int kLinCt = 4;   // column tiles per block
 
 // LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
-// rounding and the MFMA instruction)
-template <int K, int LP>
+// rounding and the MFMA instruction). K channels per output component, KI per
+// input component (KI != K only on the FP32 path).
+template <int K, int KI, int LP>
 __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* __restrict__ Lp, LinArgs a) {
   constexpr bool BF16 = LP != 0;   // any 16-bit path
   const LinLaunch& L = *Lp;
-  static_assert(K % 32 == 0, "K is a multiple of 32");
-  constexpr int PF = K + 4;    // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
-  constexpr int PB = K + 8;    // 16-bit panel row pitch in elements (68 dwords at K = 128)
+  static_assert(KI % 32 == 0 && K % 16 == 0, "KI is a multiple of 32, K of 16");
+  static_assert(!BF16 || KI == K, "16-bit linears are square");
+  constexpr int PF = KI + 4;   // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
+  constexpr int PB = KI + 8;   // 16-bit panel row pitch in elements (68 dwords at K = 128)
   constexpr int kPanel = BF16 ? (64 * PB + 1) / 2 : 64 * PF;
   __shared__ __align__(16) float sB[kPanel];
   unsigned short* sBb = reinterpret_cast<unsigned short*>(sB);
@@ -73,14 +75,14 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   for (int tm = grp.t0; tm < grp.t1; ++tm) {
     const LinTerm term = L.plan.t[tm];
     const int64_t zoff = term.species ? zstride : 0;
-    const float* xrow = term.src ? a.x2 + ((size_t)node * L.plan.cin2 + term.in_c0 + c) * K
-                                 : a.x + ((size_t)node * L.plan.cin + term.in_c0 + c) * K;
+    const float* xrow = term.src ? a.x2 + ((size_t)node * L.plan.cin2 + term.in_c0 + c) * KI
+                                 : a.x + ((size_t)node * L.plan.cin + term.in_c0 + c) * KI;
     // A operand first, so that its loads overlap the panel staging
-    f4 av[BF16 ? 1 : K / 16];
-    us8 ab[BF16 ? K / 32 : 1];
+    f4 av[BF16 ? 1 : KI / 16];
+    us8 ab[BF16 ? KI / 32 : 1];
     if constexpr (!BF16) {
 #pragma unroll
-      for (int q = 0; q < K / 16; ++q) av[q] = *reinterpret_cast<const f4*>(xrow + 16 * q + 4 * (l >> 4)) * keep;
+      for (int q = 0; q < KI / 16; ++q) av[q] = *reinterpret_cast<const f4*>(xrow + 16 * q + 4 * (l >> 4)) * keep;
     } else {
 #pragma unroll
       for (int ks = 0; ks < K / 32; ++ks) {
@@ -94,12 +96,12 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
     }
     __syncthreads();   // the previous term's MFMAs have read the panel
     if constexpr (!BF16) {
-      // panel row = output column n: the transposed blob holds W^T[n][0..K) contiguous
+      // panel row = output column n: the transposed blob holds W^T[n][0..KI) contiguous
       const float* Wt = a.wt + term.w_off + zoff;
-      for (int idx = tid; idx < 64 * (K / 4); idx += blockDim.x) {
-        const int col = idx / (K / 4), k4 = idx % (K / 4);
+      for (int idx = tid; idx < 64 * (KI / 4); idx += blockDim.x) {
+        const int col = idx / (KI / 4), k4 = idx % (KI / 4);
         const int n = 16 * ct0 + min(col, ncol - 1);
-        *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = *reinterpret_cast<const f4*>(Wt + (size_t)n * K + 4 * k4);
+        *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = *reinterpret_cast<const f4*>(Wt + (size_t)n * KI + 4 * k4);
       }
     } else {
       // packed [K/8][K][8]: 8 consecutive k of output column n are 16 contiguous bytes
@@ -114,7 +116,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
     __syncthreads();
     if constexpr (!BF16) {
 #pragma unroll
-      for (int q = 0; q < K / 16; ++q)
+      for (int q = 0; q < KI / 16; ++q)
 #pragma unroll
         for (int j = 0; j < kLinCt; ++j) {
           const f4 b = *reinterpret_cast<const f4*>(sB + (16 * j + (l & 15)) * PF + 16 * q + 4 * (l >> 4));
@@ -172,8 +174,9 @@ LinLaunch make_lin_launch(const LinPlan& plan) {
 }
 
 void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, double* flops, double* bytes) {
-  const double K = a.K, row = (double)N * K * 4.0;
-  const double wbytes = K * K * (a.lowp ? 2.0 : 4.0);
+  const double K = a.K, KI = a.KI > 0 ? a.KI : a.K;
+  const double row = (double)N * K * 4.0, row_in = (double)N * KI * 4.0;
+  const double wbytes = KI * K * (a.lowp ? 2.0 : 4.0);
   std::set<std::pair<int, int>> in_comp;
   std::set<std::pair<int64_t, int>> wblk;
   double f = 0.0, b = 0.0;
@@ -181,14 +184,14 @@ void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, d
     const LinGroup& g = p.g[gi];
     for (int ti = g.t0; ti < g.t1; ++ti) {
       const LinTerm& t = p.t[ti];
-      f += 2.0 * K * K * (double)N * g.ncomp;
+      f += 2.0 * KI * K * (double)N * g.ncomp;
       for (int c = 0; c < g.ncomp; ++c) in_comp.insert({t.src, t.in_c0 + c});
       wblk.insert({t.w_off, t.species});
     }
     const bool resid = a.residual && g.dst == 0;
     b += g.ncomp * row * (1.0 + (a.accumulate ? 1.0 : 0.0) + (resid ? 1.0 : 0.0));
   }
-  b += in_comp.size() * row;
+  b += in_comp.size() * row_in;
   for (const auto& w : wblk) b += wbytes * (w.second ? n_species : 1);
   *flops = f;
   *bytes = b;
@@ -199,11 +202,37 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   const LinLaunch* L = P.dev;
   const int halves = (a.K / 16 + kLinCt - 1) / kLinCt;
   dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
-#define MACE_LIN(KK)                                                        \
-  case KK:                                                                 \
-    if (a.lowp == 1) linear_kernel<KK, 1><<<grid, block, 0, s>>>(L, a);    \
-    else if (a.lowp == 2) linear_kernel<KK, 2><<<grid, block, 0, s>>>(L, a); \
-    else linear_kernel<KK, 0><<<grid, block, 0, s>>>(L, a);                \
+  const int KI = a.KI > 0 ? a.KI : a.K;
+  if (KI != a.K) {   // FP32 only: the factorised first-layer contraction and its transpose
+    if (a.lowp) return;
+    auto go = [&](auto KO, auto KIN) {
+      linear_kernel<decltype(KO)::value, decltype(KIN)::value, 0><<<grid, block, 0, s>>>(L, a);
+    };
+    auto in_w = [&](auto KO) {
+      switch (KI) {
+        case 32: go(KO, std::integral_constant<int, 32>{}); break;
+        case 64: go(KO, std::integral_constant<int, 64>{}); break;
+        case 96: go(KO, std::integral_constant<int, 96>{}); break;
+        case 128: go(KO, std::integral_constant<int, 128>{}); break;
+        case 192: go(KO, std::integral_constant<int, 192>{}); break;
+        case 256: go(KO, std::integral_constant<int, 256>{}); break;
+      }
+    };
+    switch (a.K) {
+      case 32: in_w(std::integral_constant<int, 32>{}); break;
+      case 64: in_w(std::integral_constant<int, 64>{}); break;
+      case 96: in_w(std::integral_constant<int, 96>{}); break;
+      case 128: in_w(std::integral_constant<int, 128>{}); break;
+      case 192: in_w(std::integral_constant<int, 192>{}); break;
+      case 256: in_w(std::integral_constant<int, 256>{}); break;
+    }
+    return;
+  }
+#define MACE_LIN(KK)                                                            \
+  case KK:                                                                     \
+    if (a.lowp == 1) linear_kernel<KK, KK, 1><<<grid, block, 0, s>>>(L, a);    \
+    else if (a.lowp == 2) linear_kernel<KK, KK, 2><<<grid, block, 0, s>>>(L, a); \
+    else linear_kernel<KK, KK, 0><<<grid, block, 0, s>>>(L, a);                \
     break;
   switch (a.K) {
     MACE_LIN(32)

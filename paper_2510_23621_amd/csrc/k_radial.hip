@@ -303,7 +303,8 @@ void launch_radial_bwd(hipStream_t s, int E, int nb, const float* W, const float
     constexpr int NPART = decltype(NP)::value;
     radial_bwd_kernel<NPART><<<g, 256, 0, s>>>(E, nb, W, sg, da3p, dYp, dY, de, accumulate);
   };
-  switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}
+  switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}, or 1 (whole values)
+    case 1: go(std::integral_constant<int, 1>{}); break;
     case 2: go(std::integral_constant<int, 2>{}); break;
     case 4: go(std::integral_constant<int, 4>{}); break;
     case 6: go(std::integral_constant<int, 6>{}); break;

@@ -295,7 +295,8 @@ struct LinArgs {
   const int* quad_tile;     // [n_quads] first tile of a run of <= kLinQuad tiles of one species
   const int* quad_count;    // [n_quads] tiles in the run
   int n_tiles, n_quads;
-  int K;
+  int K;                    // channels per component of y (and of x unless KI is set)
+  int KI;                   // channels per component of x (0: K)
   int accumulate;           // y += instead of y =
   int lowp;                 // 0: FP32; round x and w to 1: bfloat16, 2: binary16 before multiplying
 };
@@ -309,6 +310,12 @@ struct RadialSet {
   float* sg[kMaxRadialLayers];   // [3][E][64] silu'(z) of the three pre-activations
   int n;
 };
+// first interaction layer in factorised form (U, gU: [N][16][64 S], S <= 4)
+void launch_l0_gather(hipStream_t s, int N, int S, const int* rcv_off, const int* snd_z, const float* a3,
+                      const float* Y, int rb, float* U);
+void launch_l0_edge_bwd(hipStream_t s, int N, int S, const int* rcv_off, const int* snd_z, const float* a3,
+                        const float* Y, const float* gU, int rb, float* da3, float* dY);
+constexpr int kL0MaxSpecies = 4;
 void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
                           const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
                           const RadialSet& rs, int* status);

@@ -28,7 +28,8 @@ def oracle_blob(params: dict, seed: int, gains=None) -> np.ndarray:
     return synth.weight_blob(mace.weight_layout(mace.ModelDesc(**params)), seed, gains)
 
 
-def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1, stress=False):
+def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1, stress=False,
+            l0_form=None):
     desc = B.make_desc(**params)
     snd, rcv, sh = B.mace_neighbor_list(system.positions, params["r_cut"], system.cells, system.graph_of_atom,
                                         system.n_graphs)
@@ -37,6 +38,7 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     g = MaceGraph(desc, blob, system.species.astype(np.int32), ei, sh if periodic else None,
                   system.cells if periodic else None,
                   system.graph_of_atom.astype(np.int32) if system.n_graphs > 1 else None, system.n_graphs, prec)
+    form = B.mace_layer0_form(g.handle, -1 if l0_form is None else l0_form)
     pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
     outs = []
     for _ in range(repeats):
@@ -50,7 +52,7 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
         torch.cuda.synchronize()
         outs.append(dict(eps=eps.cpu().numpy().astype(np.float64), energy=E.cpu().numpy(),
                          forces=None if F is None else F.cpu().numpy().astype(np.float64), n_edges=len(snd),
-                         stress=None if S is None else S.cpu().numpy()))
+                         stress=None if S is None else S.cpu().numpy(), l0_form=form))
     g.close()
     return outs if repeats > 1 else outs[0]
 
