@@ -156,6 +156,9 @@ def main():
     ap.add_argument("--prec", choices=["fp32", "bf16", "fp16", "bf16radial"], default="fp32")
     ap.add_argument("--kernel", default="auto", help="kernel class whose roofline is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only-main", action="store_true",
+                    help="only the timed steps of the selected mode (for kernel traces): no per-call spread, "
+                         "linear roofline, forward-only, other modes or neighbour list")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB three times (reference kernel for scaling HBM counters)")
     args = ap.parse_args()
@@ -252,6 +255,12 @@ def main():
                  "algorithmic_flops_per_launch": int(flops_per_launch),
                  "kernel_share_of_step": round(k_ms / total_ms, 4)})
 
+    if args.only_main:
+        print(json.dumps({"metric": "atoms/s (timed steps only)", "value": round(N * args.steps / (total_ms * 1e-3), 1),
+                          "ms_per_step": round(ms_step, 4), "roofline": roof,
+                          "layer0_form": "factorised" if l0_factored else "per-edge"}), flush=True)
+        g.close()
+        return
     # outside the timed region: per-call spread, the linears' roofline, the
     # forward pass alone, and the other precision modes on the same workload
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
