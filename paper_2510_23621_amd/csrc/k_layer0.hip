@@ -28,7 +28,7 @@ namespace mace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kL0Edges = 4;   // edges whose loads are issued together
+constexpr int kL0Edges = 8;   // edges whose loads are issued together (gather)
 
 // Wave w gathers components 4w .. 4w + 3 of U over every edge of the receiver.
 template <int S, bool RB>
@@ -73,33 +73,6 @@ __global__ void __launch_bounds__(256) l0_gather_kernel(int N, const int* __rest
     for (int s = 0; s < S; ++s) U[((size_t)i * 16 + 4 * w + c) * KI + 64 * s + lane] = acc[s][c];
 }
 
-// One halving step of a 64-lane reduce-scatter over v[0 .. 2 N_): lanes with
-// bit XOR set keep the upper half, the others the lower half, each adding the
-// partner lane's copy of the half it keeps.
-template <int N_, int XOR>
-__device__ __forceinline__ void halve(float* v, int lane) {
-  const bool hi = lane & XOR;
-#pragma unroll
-  for (int q = 0; q < N_; ++q) {
-    const float send = hi ? v[q] : v[q + N_];
-    const float keep = hi ? v[q + N_] : v[q];
-    v[q] = keep + __shfl_xor(send, XOR);
-  }
-}
-
-// Sum of v[0..15] over the 64 lanes of the wave: afterwards every lane l holds
-// the total of index (l >> 2) & 15 (fixed butterfly order).
-__device__ __forceinline__ float wave_reduce_scatter16(float* v, int lane) {
-  halve<8, 32>(v, lane);
-  halve<4, 16>(v, lane);
-  halve<2, 8>(v, lane);
-  halve<1, 4>(v, lane);
-  float t = v[0];
-  t += __shfl_xor(t, 2);
-  t += __shfl_xor(t, 1);
-  return t;
-}
-
 // Wave w takes the receiver's edges e_beg + w, e_beg + w + 4, ...; it holds
 // gU[i][c][s][lane] for every (s, c) in registers. dE/da3 goes to da3[e][64],
 // dE/dY to dY[e][16] (both overwritten).
@@ -119,37 +92,47 @@ __global__ void __launch_bounds__(256) l0_edge_bwd_kernel(int N, const int* __re
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int c = 0; c < 16; ++c) g[s][c] = gU[((size_t)i * 16 + c) * KI + 64 * s + lane];
-  for (int e = e_beg + w; e < e_end; e += 4) {
-    const int z = snd_z[e];
-    float a = a3[(size_t)e * 64 + lane];
-    if (RB) a = bf16_round(a);
-    float y[16];
+  // two edges per iteration (e and e + 4), their loads issued together
+  for (int e = e_beg + w; e < e_end; e += 8) {
+    int ee[2], z[2];
+    float a[2], y[2][16];
 #pragma unroll
-    for (int v4 = 0; v4 < 4; ++v4) {
-      const f4 t = *reinterpret_cast<const f4*>(Y + (size_t)e * 16 + 4 * v4);
-      y[4 * v4] = t[0];
-      y[4 * v4 + 1] = t[1];
-      y[4 * v4 + 2] = t[2];
-      y[4 * v4 + 3] = t[3];
-    }
-    float gs[16];
+    for (int q = 0; q < 2; ++q) {
+      ee[q] = min(e + 4 * q, e_end - 1);   // a missing second edge repeats the first and stores nothing
+      z[q] = snd_z[ee[q]];
+      a[q] = a3[(size_t)ee[q] * 64 + lane];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) gs[c] = g[0][c];
-#pragma unroll
-    for (int s = 1; s < S; ++s)
-      if (z == s) {
-#pragma unroll
-        for (int c = 0; c < 16; ++c) gs[c] = g[s][c];
+      for (int v4 = 0; v4 < 4; ++v4) {
+        const f4 t = *reinterpret_cast<const f4*>(Y + (size_t)ee[q] * 16 + 4 * v4);
+        y[q][4 * v4] = t[0];
+        y[q][4 * v4 + 1] = t[1];
+        y[q][4 * v4 + 2] = t[2];
+        y[q][4 * v4 + 3] = t[3];
       }
-    float d = 0.f;
+    }
 #pragma unroll
-    for (int c = 0; c < 16; ++c) d += gs[c] * y[c];
-    da3[(size_t)e * 64 + lane] = d;
-    float v[16];
+    for (int q = 0; q < 2; ++q) {
+      if (q == 1 && e + 4 >= e_end) break;
+      const float av = RB ? bf16_round(a[q]) : a[q];
+      float gs[16];
 #pragma unroll
-    for (int c = 0; c < 16; ++c) v[c] = gs[c] * a;
-    const float t = wave_reduce_scatter16(v, lane);
-    if ((lane & 3) == 0) dY[(size_t)e * 16 + (lane >> 2)] = t;
+      for (int c = 0; c < 16; ++c) gs[c] = g[0][c];
+#pragma unroll
+      for (int s = 1; s < S; ++s)
+        if (z[q] == s) {
+#pragma unroll
+          for (int c = 0; c < 16; ++c) gs[c] = g[s][c];
+        }
+      float d = 0.f;
+#pragma unroll
+      for (int c = 0; c < 16; ++c) d += gs[c] * y[q][c];
+      da3[(size_t)ee[q] * 64 + lane] = d;
+      float v[16];
+#pragma unroll
+      for (int c = 0; c < 16; ++c) v[c] = gs[c] * av;
+      const float t = wave_reduce_scatter16(v, lane);
+      if ((lane & 3) == 0) dY[(size_t)ee[q] * 16 + (lane >> 2)] = t;
+    }
   }
 }
 

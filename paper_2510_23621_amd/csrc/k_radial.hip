@@ -266,14 +266,24 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, int nb, const fl
 #pragma unroll
     for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * g0[4 * rt + r];
   __syncthreads();
-  // de[e][i] = sum_j dz0[e][j] W0[i][j]
-  for (int idx = tid; idx < kTE * nb; idx += blockDim.x) {
-    int e = idx / nb, i = idx % nb;
-    if (e0 + e >= E) continue;
-    float sacc = 0.f;
-    for (int jj = 0; jj < kH; ++jj) sacc += ta[e * kPad + jj] * W0[i * kH + jj];
-    size_t o = (size_t)(e0 + e) * nb + i;
-    de[o] = accumulate ? de[o] + sacc : sacc;
+  // de[e][i] = sum_j dz0[e][j] W0[i][j] on MFMA: wave w takes the edge rows
+  // 16w .. 16w + 15, the 16 result columns are i (zero past nb <= 16)
+  {
+    const int i = l & 15;
+    f4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kH / 4; ++ks) {
+      const float bw = i < nb ? W0[i * kH + 4 * ks + (l >> 4)] : 0.f;
+      d = mfma4(ta[(16 * w + (l & 15)) * kPad + 4 * ks + (l >> 4)], bw, d);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int e = e0 + 16 * w + 4 * (l >> 4) + r;
+      if (e < E && i < nb) {
+        const size_t o = (size_t)e * nb + i;
+        de[o] = accumulate ? de[o] + d[r] : d[r];
+      }
+    }
   }
   for (int idx = tid; idx < kTE * 4; idx += blockDim.x) {
     const int e = e0 + (idx >> 2), c4 = idx & 3;

@@ -238,6 +238,33 @@ __device__ __forceinline__ int edge_geometry(int e, const float* __restrict__ po
   return !isfinite(rr) ? kStatusNonFinite : (rr == 0.0 ? kStatusZeroLength : 0);
 }
 
+// One halving step of a 64-lane reduce-scatter over v[0 .. 2 N_): lanes with
+// bit XOR set keep the upper half, the others the lower half, each adding the
+// partner lane's copy of the half it keeps.
+template <int N_, int XOR>
+__device__ __forceinline__ void halve(float* v, int lane) {
+  const bool hi = lane & XOR;
+#pragma unroll
+  for (int q = 0; q < N_; ++q) {
+    const float send = hi ? v[q] : v[q + N_];
+    const float keep = hi ? v[q + N_] : v[q];
+    v[q] = keep + __shfl_xor(send, XOR);
+  }
+}
+
+// Sum of v[0..15] over the 64 lanes of the wave: afterwards every lane l holds
+// the total of index (l >> 2) & 15 (fixed butterfly order).
+__device__ __forceinline__ float wave_reduce_scatter16(float* v, int lane) {
+  halve<8, 32>(v, lane);
+  halve<4, 16>(v, lane);
+  halve<2, 8>(v, lane);
+  halve<1, 4>(v, lane);
+  float t = v[0];
+  t += __shfl_xor(t, 2);
+  t += __shfl_xor(t, 1);
+  return t;
+}
+
 // --------------------------------------------------------------- launchers
 struct LinTerm {
   int in_c0;          // first input component of this term
