@@ -149,47 +149,92 @@ __global__ void nl_scatter_kernel(int64_t C, const int4* __restrict__ cand_s, co
   order[slot_off[slot] + atomicAdd(&slot_fill[slot], 1)] = (int)c;
 }
 
-__device__ __forceinline__ bool key_less(int ja, const int* sa, int jb, const int* sb) {
-  if (ja != jb) return ja < jb;
-  if (sa[0] != sb[0]) return sa[0] < sb[0];
-  if (sa[1] != sb[1]) return sa[1] < sb[1];
-  return sa[2] < sb[2];
+// Receiver pass, one wave per receiver: WRITE = false counts the edges of
+// receiver i, WRITE = true writes them to [off_i, off_{i+1}) sorted by
+// (sender, S). The candidates of the 27 cubes around the receiver form one
+// index range (cube after cube, slot order within a cube) that the lanes
+// take 64 at a time; an edge's place is the number of passing candidates
+// before it (ballot prefix). The segment is sorted by rank (each edge's
+// position = the number of keys below its own; keys are distinct) from a
+// per-wave LDS copy, or, beyond kNlSortCap edges, by one lane in place.
+constexpr int kNlWaves = 4;        // receivers per block
+constexpr int kNlSortCap = 256;    // edges per receiver sorted through LDS
+
+struct NlKey {
+  int j, s0, s1, s2;
+};
+
+__device__ __forceinline__ bool key_lt(const NlKey& a, const NlKey& b) {
+  if (a.j != b.j) return a.j < b.j;
+  if (a.s0 != b.s0) return a.s0 < b.s0;
+  if (a.s1 != b.s1) return a.s1 < b.s1;
+  return a.s2 < b.s2;
 }
 
-// Receiver pass: WRITE = false counts the edges of receiver i, WRITE = true
-// writes them to [off_i, off_i + count) and sorts that segment.
 template <bool WRITE>
-__global__ void nl_receiver_kernel(int N, const double* __restrict__ pos, const NlGraph* __restrict__ gs, int G,
-                                   const double* __restrict__ xw, const int4* __restrict__ nsh, double bs, double rc2,
-                                   uint32_t mask, const int64_t* __restrict__ slot_off, const int* __restrict__ order,
-                                   const int* __restrict__ cand_j, const int4* __restrict__ cand_s,
-                                   const int4* __restrict__ cand_b, int* __restrict__ count,
-                                   const int64_t* __restrict__ off, int32_t* __restrict__ sender,
-                                   int32_t* __restrict__ receiver, int32_t* __restrict__ shifts) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= N) return;
+__global__ void __launch_bounds__(64 * kNlWaves)
+nl_receiver_kernel(int N, const double* __restrict__ pos, const NlGraph* __restrict__ gs, int G,
+                   const double* __restrict__ xw, const int4* __restrict__ nsh, double bs, double rc2, uint32_t mask,
+                   const int64_t* __restrict__ slot_off, const int* __restrict__ order,
+                   const int* __restrict__ cand_j, const int4* __restrict__ cand_s, const int4* __restrict__ cand_b,
+                   int* __restrict__ count, const int64_t* __restrict__ off, int32_t* __restrict__ sender,
+                   int32_t* __restrict__ receiver, int32_t* __restrict__ shifts) {
+  __shared__ int64_t s_first[kNlWaves][27];
+  __shared__ int64_t s_end[kNlWaves][28];   // inclusive prefix of the cube ranges
+  __shared__ int s_cube[kNlWaves][27][3];
+  __shared__ NlKey s_key[WRITE ? kNlWaves : 1][WRITE ? kNlSortCap : 1];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int i = blockIdx.x * kNlWaves + w;
+  if (i >= N) return;   // whole wave; no block-wide barrier below
   const int gi = graph_of(gs, G, i);
   const NlGraph& g = gs[gi];
   const int4 ni = nsh[i];
-  int n = 0;
   const int64_t base = WRITE ? off[i] : 0;
+  const int64_t n_expect = WRITE ? off[i + 1] - off[i] : 0;
+  if (WRITE && n_expect == 0) return;
+  int64_t n = 0;
   if (!ni.w) {
     const double xi[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
     const int bi[3] = {cube(xw[3 * i], bs), cube(xw[3 * i + 1], bs), cube(xw[3 * i + 2], bs)};
-    for (int dx = -1; dx <= 1; ++dx)
-      for (int dy = -1; dy <= 1; ++dy)
-        for (int dz = -1; dz <= 1; ++dz) {
-          const int bx = bi[0] + dx, by = bi[1] + dy, bz = bi[2] + dz;
-          const uint32_t slot = slot_of(gi, bx, by, bz, mask);
-          for (int64_t q = slot_off[slot]; q < slot_off[slot + 1]; ++q) {
-            const int c = order[q];
-            const int4 cs = cand_s[c];
-            const int4 cb = cand_b[c];
-            if (cs.w != gi || cb.x != bx || cb.y != by || cb.z != bz) continue;
-            const int j = cand_j[c];
-            const int4 nj = nsh[j];
-            if (nj.w) continue;
-            const int S[3] = {cs.x - nj.x + ni.x, cs.y - nj.y + ni.y, cs.z - nj.z + ni.z};
+    // lanes 0..26: one neighbouring cube each, its slot range, then the prefix
+    int64_t len = 0;
+    if (lane < 27) {
+      const int bx = bi[0] + lane / 9 - 1, by = bi[1] + (lane / 3) % 3 - 1, bz = bi[2] + lane % 3 - 1;
+      const uint32_t slot = slot_of(gi, bx, by, bz, mask);
+      s_first[w][lane] = slot_off[slot];
+      len = slot_off[slot + 1] - slot_off[slot];
+      s_cube[w][lane][0] = bx;
+      s_cube[w][lane][1] = by;
+      s_cube[w][lane][2] = bz;
+    }
+    long long incl = len;
+#pragma unroll
+    for (int st = 1; st < 32; st <<= 1) {
+      const long long v = __shfl_up(incl, st);
+      if (lane >= st) incl += v;
+    }
+    if (lane < 27) s_end[w][lane] = incl;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    const int64_t total = s_end[w][26];
+    for (int64_t q0 = 0; q0 < total; q0 += 64) {
+      const int64_t q = q0 + lane;
+      bool hit = false;
+      int j = 0, S[3] = {0, 0, 0};
+      if (q < total) {
+        int c = 0;
+        while (s_end[w][c] <= q) ++c;   // the cube whose range holds q
+        const int64_t qs = s_first[w][c] + (q - (c ? s_end[w][c - 1] : 0));
+        const int cidx = order[qs];
+        const int4 cs = cand_s[cidx];
+        const int4 cb = cand_b[cidx];
+        if (cs.w == gi && cb.x == s_cube[w][c][0] && cb.y == s_cube[w][c][1] && cb.z == s_cube[w][c][2]) {
+          j = cand_j[cidx];
+          const int4 nj = nsh[j];
+          if (!nj.w) {
+            S[0] = cs.x - nj.x + ni.x;
+            S[1] = cs.y - nj.y + ni.y;
+            S[2] = cs.z - nj.z + ni.z;
             double d[3];
             for (int q3 = 0; q3 < 3; ++q3) {
               const double sv = g.periodic ? ((double)S[0] * g.cell[0 * 3 + q3] + (double)S[1] * g.cell[1 * 3 + q3]) +
@@ -198,45 +243,71 @@ __global__ void nl_receiver_kernel(int N, const double* __restrict__ pos, const 
               d[q3] = (pos[3 * j + q3] - xi[q3]) + sv;
             }
             const double r2 = (d[0] * d[0] + d[1] * d[1]) + d[2] * d[2];
-            if (r2 < rc2 && r2 > 0.0) {
-              if (WRITE) {
-                const int64_t e = base + n;
-                sender[e] = j;
-                receiver[e] = i;
-                shifts[3 * e] = S[0];
-                shifts[3 * e + 1] = S[1];
-                shifts[3 * e + 2] = S[2];
-              }
-              ++n;
-            }
+            hit = r2 < rc2 && r2 > 0.0;
           }
         }
+      }
+      const uint64_t bal = __ballot(hit);
+      if (WRITE && hit) {
+        const int64_t at = n + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+        if (n_expect <= kNlSortCap) {
+          if (at < kNlSortCap) s_key[w][at] = NlKey{j, S[0], S[1], S[2]};
+        } else {
+          const int64_t e = base + at;
+          sender[e] = j;
+          shifts[3 * e] = S[0];
+          shifts[3 * e + 1] = S[1];
+          shifts[3 * e + 2] = S[2];
+        }
+      }
+      n += __popcll(bal);
+    }
   }
   if (!WRITE) {
-    count[i] = n;
+    if (lane == 0) count[i] = (int)n;
     return;
   }
-  // insertion sort of the segment by (sender, S)
-  for (int a = 1; a < n; ++a) {
+  if (n_expect <= kNlSortCap) {
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    for (int a = lane; a < n_expect; a += 64) {
+      const NlKey ka = s_key[w][a];
+      int rank = 0;
+      for (int b = 0; b < n_expect; ++b) rank += key_lt(s_key[w][b], ka);
+      const int64_t e = base + rank;
+      sender[e] = ka.j;
+      receiver[e] = i;
+      shifts[3 * e] = ka.s0;
+      shifts[3 * e + 1] = ka.s1;
+      shifts[3 * e + 2] = ka.s2;
+    }
+    return;
+  }
+  // long segment: insertion sort in place by lane 0, after every lane's
+  // writes above are visible to it
+  for (int64_t a = lane; a < n_expect; a += 64) receiver[base + a] = i;
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  if (lane != 0) return;
+  for (int64_t a = 1; a < n_expect; ++a) {
     const int64_t ea = base + a;
-    const int ja = sender[ea];
-    const int sa[3] = {shifts[3 * ea], shifts[3 * ea + 1], shifts[3 * ea + 2]};
-    int b = a - 1;
+    const NlKey ka{sender[ea], shifts[3 * ea], shifts[3 * ea + 1], shifts[3 * ea + 2]};
+    int64_t b = a - 1;
     while (b >= 0) {
       const int64_t eb = base + b;
-      const int sb[3] = {shifts[3 * eb], shifts[3 * eb + 1], shifts[3 * eb + 2]};
-      if (!key_less(ja, sa, sender[eb], sb)) break;
-      sender[eb + 1] = sender[eb];
-      shifts[3 * (eb + 1)] = sb[0];
-      shifts[3 * (eb + 1) + 1] = sb[1];
-      shifts[3 * (eb + 1) + 2] = sb[2];
+      const NlKey kb{sender[eb], shifts[3 * eb], shifts[3 * eb + 1], shifts[3 * eb + 2]};
+      if (!key_lt(ka, kb)) break;
+      sender[eb + 1] = kb.j;
+      shifts[3 * (eb + 1)] = kb.s0;
+      shifts[3 * (eb + 1) + 1] = kb.s1;
+      shifts[3 * (eb + 1) + 2] = kb.s2;
       --b;
     }
     const int64_t ed = base + b + 1;
-    sender[ed] = ja;
-    shifts[3 * ed] = sa[0];
-    shifts[3 * ed + 1] = sa[1];
-    shifts[3 * ed + 2] = sa[2];
+    sender[ed] = ka.j;
+    shifts[3 * ed] = ka.s0;
+    shifts[3 * ed + 1] = ka.s1;
+    shifts[3 * ed + 2] = ka.s2;
   }
 }
 
@@ -455,7 +526,8 @@ extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* 
   }
   scan(s, p.n_slots, scnt, soff, bsum);
   if (p.C > 0) nl_scatter_kernel<<<cblk, kNlThreads, 0, s>>>(p.C, cs, cb, mask, soff, sfill, order);
-  nl_receiver_kernel<false><<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order, cj,
+  const unsigned rblk = (unsigned)((N + kNlWaves - 1) / kNlWaves);
+  nl_receiver_kernel<false><<<rblk, 64 * kNlWaves, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order, cj,
                                                          cs, cb, rcnt, nullptr, nullptr, nullptr, nullptr);
   scan(s, N, rcnt, roff, bsum);
   int64_t total = 0;
@@ -471,7 +543,7 @@ extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* 
   *n_edges = total;
   if (total > max_edges) return MACE_ENOSPACE;
   if (total > 0)
-    nl_receiver_kernel<true><<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order,
+    nl_receiver_kernel<true><<<rblk, 64 * kNlWaves, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order,
                                                           cj, cs, cb, nullptr, roff, sender, receiver, shifts);
   return hipGetLastError() == hipSuccess ? MACE_OK : MACE_EHIP;
 }

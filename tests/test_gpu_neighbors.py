@@ -63,6 +63,16 @@ def test_small_cell_many_images():
     assert E > 4 * 50
 
 
+def test_dense_images_long_segments():
+    """A 2.2 A cell with a 7 A cutoff: about 400 edges per receiver, beyond
+    the segment length the device list sorts through LDS."""
+    rng = np.random.default_rng(8)
+    cell = np.eye(3) * 2.2
+    pos = rng.uniform(0, 2.2, size=(3, 3))
+    E = _compare("2.2 A cell, 7 A cutoff", pos, 7.0, cell[None], None, 1, None)
+    assert E > 3 * 300
+
+
 def test_mixed_batch_and_no_edges():
     """Empty graphs and graphs without any pair in range inside a batch."""
     a = np.array([[0.0, 0, 0], [1.0, 0, 0], [0, 1.2, 0]])
