@@ -22,6 +22,8 @@ MACE_BF16_RADIAL = 3
 MACE_L0_AUTO = 0
 MACE_L0_EDGE = 1
 MACE_L0_FACTORED = 2
+MACE_RADIAL_FP32 = 0
+MACE_RADIAL_SPLIT_BF16 = 2
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 
@@ -29,7 +31,8 @@ EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", 
             "mace_forward_energy", "mace_forces", "mace_forces_stress", "mace_graph_destroy", "mace_status_string",
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
-            "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form"]
+            "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form",
+            "mace_radial_operands"]
 
 
 class MaceError(RuntimeError):
@@ -83,6 +86,7 @@ def lib() -> ctypes.CDLL:
         L.mace_graph_check.argtypes = [P, P, P]
         L.mace_profile_work.argtypes = [P, P, P]
         L.mace_layer0_form.argtypes = [P, I32, P]
+        L.mace_radial_operands.argtypes = [P, I32, P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
         L.mace_status_string.restype = ctypes.c_char_p
@@ -284,6 +288,14 @@ def mace_layer0_form(handle, request: int = -1) -> int:
     query the form of the first layer's message; returns the form in use."""
     used = ctypes.c_int32(0)
     _check(lib().mace_layer0_form(handle, request, ctypes.byref(used)), "mace_layer0_form")
+    return used.value
+
+
+def mace_radial_operands(handle, request: int = -1) -> int:
+    """Select (MACE_RADIAL_FP32 / MACE_RADIAL_SPLIT_BF16) or, with request < 0,
+    only query the operands of the last radial layer; returns the setting."""
+    used = ctypes.c_int32(0)
+    _check(lib().mace_radial_operands(handle, request, ctypes.byref(used)), "mace_radial_operands")
     return used.value
 
 

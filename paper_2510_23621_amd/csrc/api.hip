@@ -288,6 +288,7 @@ struct mace_graph {
   // path-merging and species linears) or U -> At (16-bit modes), and transposes
   LinPlanRef l0f, l0fT;
   bool l0_fact = false;
+  bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_radial_operands)
 };
 
 namespace {
@@ -582,7 +583,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       {
         PROF(KID_TP_FWD);
         launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
-                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL);
+                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0));
       }
       if (t == 0 && !lowp) {
         run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
@@ -1145,6 +1146,17 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
   else if (request == MACE_L0_EDGE) g->l0_fact = false;
   else if (request == MACE_L0_FACTORED) g->l0_fact = true;
   if (in_use) *in_use = g->l0_fact ? MACE_L0_FACTORED : MACE_L0_EDGE;
+  return MACE_OK;
+}
+
+mace_status mace_radial_operands(mace_graph* g, int32_t request, int32_t* in_use) {
+  if (!g) return MACE_EINVAL;
+  if (request >= 0) {
+    if (g->prec == MACE_BF16_RADIAL || (request != MACE_RADIAL_FP32 && request != MACE_RADIAL_SPLIT_BF16))
+      return MACE_EINVAL;
+    g->radial_split = request == MACE_RADIAL_SPLIT_BF16;
+  }
+  if (in_use) *in_use = g->prec == MACE_BF16_RADIAL ? 1 : (g->radial_split ? MACE_RADIAL_SPLIT_BF16 : MACE_RADIAL_FP32);
   return MACE_OK;
 }
 

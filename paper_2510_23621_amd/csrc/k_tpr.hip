@@ -150,6 +150,88 @@ __device__ __forceinline__ void tile_radial_bf16(const float* __restrict__ a3, i
   __builtin_amdgcn_s_setprio(0);
 }
 
+// ---- Split-BF16 radial layer (FP32-accurate): every FP32 operand x is carried
+// as x0 + x1 + x2 with x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1)
+// (each difference is exact in FP32, so the three parts hold all 24
+// significand bits), and a b = a0 b0 + (a0 b1 + a1 b0) + (a0 b2 + a1 b1 + a2 b0)
+// up to terms of relative size 2^-27, on v_mfma_f32_16x16x32_bf16 with FP32
+// accumulation: six BF16 MFMAs (16 cycles each) in place of eight FP32 ones
+// (32 cycles each) per 16 x 16 x 32 block.
+__device__ __forceinline__ void split3(float x, unsigned short& b0, unsigned short& b1, unsigned short& b2) {
+  const __bf16 h0 = (__bf16)x;
+  const float r1 = x - (float)h0;
+  const __bf16 h1 = (__bf16)r1;
+  const float r2 = r1 - (float)h1;
+  const __bf16 h2 = (__bf16)r2;
+  b0 = __builtin_bit_cast(unsigned short, h0);
+  b1 = __builtin_bit_cast(unsigned short, h1);
+  b2 = __builtin_bit_cast(unsigned short, h2);
+}
+
+// The three parts of the forward slice, part q at sWx + q P 16 kWbPitch, in the
+// layout of load_w3_slice_bf16.
+template <int P>
+__device__ __forceinline__ void load_w3_slice_x3(const float* __restrict__ W3, int K, int ct, unsigned short* sWx) {
+  const int PK = P * K;
+  constexpr int part = P * 16 * kWbPitch;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    const int o = (p * 16 + kk) * kWbPitch + j;
+    split3(W3[(size_t)j * PK + p * K + 16 * ct + kk], sWx[o], sWx[part + o], sWx[2 * part + o]);
+  }
+}
+
+// As tile_radial, FP32-accurate on split BF16 operands. The K steps are the
+// outer loop, so that only one step's A parts are live; within each step the
+// terms are added from the smallest to the largest.
+template <int P>
+__device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int e0, int e_end,
+                                               const unsigned short* __restrict__ sWx, f4* r) {
+  constexpr int part = P * 16 * kWbPitch;
+  const int l = threadIdx.x & 63;
+  const int row = e0 + (l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+  const unsigned short* wb = sWx + (l & 15) * kWbPitch + 8 * (l >> 4);
+#pragma unroll
+  for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+    const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+    us8v a0, a1, a2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned short x0, x1, x2;
+      split3(lo[i], x0, x1, x2);
+      a0[i] = x0;
+      a1[i] = x1;
+      a2[i] = x2;
+      split3(hi[i], x0, x1, x2);
+      a0[4 + i] = x0;
+      a1[4 + i] = x1;
+      a2[4 + i] = x2;
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      __builtin_amdgcn_sched_barrier(0);   // one path's B parts live at a time
+      const unsigned short* q = wb + p * 16 * kWbPitch + 32 * ks;
+      const us8v b0 = *reinterpret_cast<const us8v*>(q);
+      const us8v b1 = *reinterpret_cast<const us8v*>(q + part);
+      const us8v b2 = *reinterpret_cast<const us8v*>(q + 2 * part);
+      f4 acc = r[p];
+      acc = mfma_bf16(a2, b0, acc);
+      acc = mfma_bf16(a1, b1, acc);
+      acc = mfma_bf16(a0, b2, acc);
+      acc = mfma_bf16(a1, b0, acc);
+      acc = mfma_bf16(a0, b1, acc);
+      r[p] = mfma_bf16(a0, b0, acc);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
 // dE/da3 partial on BF16 operands: D[e][j] = sum over (p, kk) of
 // bf16(dR[e][p][kk]) bf16(W3[j][p K + 16 ct + kk]); the reduction index
 // 32 ks + 8 (l/16) + i is path 2 ks + (l/16)/2, channel 8 ((l/16)%2) + i. Each
@@ -224,7 +306,8 @@ __device__ __forceinline__ void load_h_row(const float* __restrict__ h, int src,
   for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
 }
 
-template <int LHMAX, bool RB, int NW = TprShape<LHMAX, false>::waves>
+// RM, the operands of the last radial layer: 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate)
+template <int LHMAX, int RM, int NW = TprShape<LHMAX, false>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
 tpr_fwd_kernel(
@@ -234,11 +317,13 @@ tpr_fwd_kernel(
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
-  constexpr int kSlice = RB ? (P * 16 * kWbPitch + 1) / 2 : P * 16 * kWPitch;   // floats
+  constexpr int kSlice = RM == 1 ? (P * 16 * kWbPitch + 1) / 2
+                        : (RM == 2 ? (3 * P * 16 * kWbPitch + 1) / 2 : P * 16 * kWPitch);   // floats
   __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
   const int ct = blockIdx.y;
-  if constexpr (RB) load_w3_slice_bf16<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW), nullptr);
+  if constexpr (RM == 1) load_w3_slice_bf16<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW), nullptr);
+  else if constexpr (RM == 2) load_w3_slice_x3<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW));
   else load_w3_slice<P>(W3, K, ct, sW);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -257,7 +342,8 @@ tpr_fwd_kernel(
       sender_rows(snd, src_map, e0 + 4 * g, e_end, srcq);
       stage_y(Y, e0, e_end, sy);
       f4 r[P];
-      if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      else if constexpr (RM == 2) tile_radial_x3<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
       // lane group 0 holds the tile's first edges, so nq covers every valid one;
       // the scheduling barrier keeps one edge's operands live at a time, and
@@ -527,13 +613,13 @@ int tpr_grid_x(int N, int n_ct, int waves, int blocks_per_cu) {
   return std::max(1, std::min(want, (N + waves - 1) / waves));
 }
 
-template <int LH, bool RB>
+template <int LH, int RM>
 void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c, float* At) {
   using S = TprShape<LH, false>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
-  tpr_fwd_kernel<LH, RB><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
+  tpr_fwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
 }
 
 template <int LH, bool RB>
@@ -550,12 +636,13 @@ void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, cons
 
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_bf16) {
+                    float inv_c, float* At, int radial_mode) {
   if (N <= 0) return;
-#define MACE_TPRF(LH)                                                                                  \
-  case LH:                                                                                             \
-    if (radial_bf16) tpr_fwd_launch<LH, true>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
-    else tpr_fwd_launch<LH, false>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);            \
+#define MACE_TPRF(LH)                                                                                    \
+  case LH:                                                                                               \
+    if (radial_mode == 1) tpr_fwd_launch<LH, 1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
+    else if (radial_mode == 2) tpr_fwd_launch<LH, 2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
+    else tpr_fwd_launch<LH, 0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);                  \
     break;
   switch (lh_max) {
     MACE_TPRF(0)

@@ -357,7 +357,7 @@ void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, con
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_bf16);
+                    float inv_c, float* At, int radial_mode);   // 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate)
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_bf16);

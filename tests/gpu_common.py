@@ -29,7 +29,7 @@ def oracle_blob(params: dict, seed: int, gains=None) -> np.ndarray:
 
 
 def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1, stress=False,
-            l0_form=None):
+            l0_form=None, radial=None):
     desc = B.make_desc(**params)
     snd, rcv, sh = B.mace_neighbor_list(system.positions, params["r_cut"], system.cells, system.graph_of_atom,
                                         system.n_graphs)
@@ -39,6 +39,8 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
                   system.cells if periodic else None,
                   system.graph_of_atom.astype(np.int32) if system.n_graphs > 1 else None, system.n_graphs, prec)
     form = B.mace_layer0_form(g.handle, -1 if l0_form is None else l0_form)
+    if radial is not None:
+        B.mace_radial_operands(g.handle, radial)
     pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
     outs = []
     for _ in range(repeats):
