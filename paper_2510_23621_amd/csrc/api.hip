@@ -683,7 +683,8 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
       launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
-                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, h->prec == MACE_BF16_RADIAL);
+                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p,
+                     h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0));
     }
     {
       // right after the partials are written, while they are still in the

@@ -38,9 +38,12 @@ constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
 // for l = 2 the W3 slice alone fills half the LDS. The MFMA phases raise
 // the wave's priority so that they issue ahead of the other waves' vector
 // work on the SIMD.
-template <int LHMAX, bool BWD>
+// The split-BF16 backward (RM = 2) keeps both layouts of the three W3 parts
+// in LDS (120 KB at P = 10): one 8-wave block per CU at l = 1.
+template <int LHMAX, bool BWD, int RM = 0>
 struct TprShape {
-  static constexpr int waves = (BWD && LHMAX == 1) ? 4 : 8;
+  static constexpr bool split_bwd = BWD && RM == 2;
+  static constexpr int waves = (BWD && LHMAX == 1 && !split_bwd) ? 4 : 8;
   static constexpr int per_simd = LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 2 : 4);
   static constexpr int blocks_per_cu = 4 * per_simd / waves;
 };
@@ -227,6 +230,138 @@ __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int
       acc = mfma_bf16(a1, b0, acc);
       acc = mfma_bf16(a0, b1, acc);
       r[p] = mfma_bf16(a0, b0, acc);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// Split parts in the backward, without row padding: a 16-byte chunk c of row r
+// sits at chunk c ^ s(r), so that the 16 lanes of an MFMA operand read hit 16
+// distinct 16-byte bank groups. Forward layout: row r = p 16 + kk of 64
+// elements (8 chunks of j), s(r) = (r >> 1) & 7. Transposed layout: row
+// r = p 64 + j of 16 elements (2 chunks of kk), s(r) = (r >> 3) & 1.
+__device__ __forceinline__ int swz_fwd(int r, int c) { return r * 64 + 8 * (c ^ ((r >> 1) & 7)); }
+__device__ __forceinline__ int swz_tr(int r, int c) { return r * 16 + 8 * (c ^ ((r >> 3) & 1)); }
+
+template <int P>
+__device__ __forceinline__ void load_w3_slices_x3_swz(const float* __restrict__ W3, int K, int ct,
+                                                      unsigned short* sWf, unsigned short* sWt) {
+  const int PK = P * K;
+  constexpr int part = P * 16 * 64;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    unsigned short x0, x1, x2;
+    split3(W3[(size_t)j * PK + p * K + 16 * ct + kk], x0, x1, x2);
+    const int of = swz_fwd(p * 16 + kk, j >> 3) + (j & 7);
+    const int ot = swz_tr(p * 64 + j, kk >> 3) + (kk & 7);
+    sWf[of] = x0;
+    sWf[part + of] = x1;
+    sWf[2 * part + of] = x2;
+    sWt[ot] = x0;
+    sWt[part + ot] = x1;
+    sWt[2 * part + ot] = x2;
+  }
+}
+
+// tile_radial_x3 on the swizzled forward layout
+template <int P>
+__device__ __forceinline__ void tile_radial_x3s(const float* __restrict__ a3, int e0, int e_end,
+                                                const unsigned short* __restrict__ sWf, f4* r) {
+  constexpr int part = P * 16 * 64;
+  const int l = threadIdx.x & 63;
+  const int row = e0 + (l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+#pragma unroll
+  for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+    const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+    us8v a0, a1, a2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned short x0, x1, x2;
+      split3(lo[i], x0, x1, x2);
+      a0[i] = x0;
+      a1[i] = x1;
+      a2[i] = x2;
+      split3(hi[i], x0, x1, x2);
+      a0[4 + i] = x0;
+      a1[4 + i] = x1;
+      a2[4 + i] = x2;
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      __builtin_amdgcn_sched_barrier(0);
+      const unsigned short* q = sWf + swz_fwd(p * 16 + (l & 15), 4 * ks + (l >> 4));
+      const us8v b0 = *reinterpret_cast<const us8v*>(q);
+      const us8v b1 = *reinterpret_cast<const us8v*>(q + part);
+      const us8v b2 = *reinterpret_cast<const us8v*>(q + 2 * part);
+      f4 acc = r[p];
+      acc = mfma_bf16(a2, b0, acc);
+      acc = mfma_bf16(a1, b1, acc);
+      acc = mfma_bf16(a0, b2, acc);
+      acc = mfma_bf16(a1, b0, acc);
+      acc = mfma_bf16(a0, b1, acc);
+      r[p] = mfma_bf16(a0, b0, acc);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// dE/da3 partial on split BF16 operands (dR split per tile, W3 parts from the
+// swizzled transposed layout); otherwise as tile_da3_bf16.
+template <int P>
+__device__ __forceinline__ void tile_da3_x3(const f4* r, const unsigned short* __restrict__ sWt, float* tw,
+                                            f4* d3) {
+  constexpr int part = P * 16 * 64;
+  const int l = threadIdx.x & 63, g = l >> 4, kk = l & 15;
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < (P + 1) / 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int p = 2 * ks + pl;
+        tw[(pl * 16 + 4 * g + q) * kT2Pitch + kk] = (p < P) ? r[p < P ? p : 0][q] : 0.f;
+      }
+    __builtin_amdgcn_wave_barrier();
+    const float* src = tw + ((g >> 1) * 16 + kk) * kT2Pitch + 8 * (g & 1);
+    const f4 lo = *reinterpret_cast<const f4*>(src), hi = *reinterpret_cast<const f4*>(src + 4);
+    __builtin_amdgcn_wave_barrier();
+    us8v a0, a1, a2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned short x0, x1, x2;
+      split3(lo[i], x0, x1, x2);
+      a0[i] = x0;
+      a1[i] = x1;
+      a2[i] = x2;
+      split3(hi[i], x0, x1, x2);
+      a0[4 + i] = x0;
+      a1[4 + i] = x1;
+      a2[4 + i] = x2;
+    }
+    const int p = min(2 * ks + (g >> 1), P - 1);   // a missing odd path reads a valid row; its A is zero
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+      const unsigned short* q = sWt + swz_tr(p * 64 + 16 * jt + kk, g & 1);
+      const us8v b0 = *reinterpret_cast<const us8v*>(q);
+      const us8v b1 = *reinterpret_cast<const us8v*>(q + part);
+      const us8v b2 = *reinterpret_cast<const us8v*>(q + 2 * part);
+      f4 acc = d3[jt];
+      acc = mfma_bf16(a2, b0, acc);
+      acc = mfma_bf16(a1, b1, acc);
+      acc = mfma_bf16(a0, b2, acc);
+      acc = mfma_bf16(a1, b0, acc);
+      acc = mfma_bf16(a0, b1, acc);
+      d3[jt] = mfma_bf16(a0, b0, acc);
     }
   }
   __builtin_amdgcn_s_setprio(0);
@@ -427,12 +562,14 @@ __device__ __forceinline__ float group_reduce16(float* v, int lane) {
 // G_p is formed once per receiver (GF) where its table fits beside the
 // weight slice at the kernel's occupancy; otherwise each edge contracts C
 // with g directly (product form C (g h), C (g Y)).
-template <int LHMAX, bool RB>
-constexpr bool tpr_bwd_gform() { return LHMAX == 0 || (LHMAX == 1 && !RB); }
+template <int LHMAX, int RM>
+constexpr bool tpr_bwd_gform() { return LHMAX == 0 || (LHMAX == 1 && RM == 0); }
 
-template <int LHMAX, bool RB, int NW = TprShape<LHMAX, true>::waves>
+// RM as in tpr_fwd_kernel (split BF16 for l <= 1 only: at l = 2 the two
+// layouts of the parts do not fit the LDS)
+template <int LHMAX, int RM, int NW = TprShape<LHMAX, true, RM>::waves>
 __global__ void __launch_bounds__(64 * NW)
-__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true>::per_simd, TprShape<LHMAX, true>::per_simd)))
+__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true, RM>::per_simd, TprShape<LHMAX, true, RM>::per_simd)))
 tpr_bwd_kernel(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
@@ -441,17 +578,21 @@ tpr_bwd_kernel(
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
-  constexpr int kSlice = RB ? (P * 16 * kWbPitch + P * 64 * kWtPitch + 1) / 2 : P * 16 * kWPitch;   // floats
+  static_assert(RM != 2 || LHMAX <= 1, "split-BF16 backward for l <= 1");
+  constexpr bool RB = RM == 1;
+  constexpr int kSlice = RM == 1 ? (P * 16 * kWbPitch + P * 64 * kWtPitch + 1) / 2
+                        : (RM == 2 ? 3 * P * 16 * 64 : P * 16 * kWPitch);   // floats
   __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
-  __shared__ __align__(16) float sT[NW][RB ? 2 * 16 * kT2Pitch : 16 * kTPitch];
-  constexpr bool GF = tpr_bwd_gform<LHMAX, RB>();
+  __shared__ __align__(16) float sT[NW][RM != 0 ? 2 * 16 * kT2Pitch : 16 * kTPitch];
+  constexpr bool GF = tpr_bwd_gform<LHMAX, RM>();
   constexpr int NPAIR = PairCount<LHMAX>::value;
   __shared__ float sG[GF ? NW : 1][GF ? NPAIR * 16 : 1];   // [pair][channel]
   unsigned short* sWb = reinterpret_cast<unsigned short*>(sW);
-  unsigned short* sWt = sWb + P * 16 * kWbPitch;
+  unsigned short* sWt = sWb + (RM == 2 ? 3 * P * 16 * 64 : P * 16 * kWbPitch);
   const int ct = blockIdx.y;
-  if constexpr (RB) load_w3_slice_bf16<P>(W3, K, ct, sWb, sWt);
+  if constexpr (RM == 1) load_w3_slice_bf16<P>(W3, K, ct, sWb, sWt);
+  else if constexpr (RM == 2) load_w3_slices_x3_swz<P>(W3, K, ct, sWb, sWt);
   else load_w3_slice<P>(W3, K, ct, sW);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -491,7 +632,8 @@ tpr_bwd_kernel(
       sender_rows(snd, src_map, e0 + 4 * g, e_end, srcq);
       stage_y(Y, e0, e_end, sy);
       f4 r[P];   // R on entry; dR (zero for edges past e_end) after the edge loop
-      if constexpr (RB) tile_radial_bf16<P>(a3, e0, e_end, sWb, r);
+      if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, sWb, r);
+      else if constexpr (RM == 2) tile_radial_x3s<P>(a3, e0, e_end, sWb, r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
       const int nq = min(4, e_end - e0);
       float hv[DIN];
@@ -567,8 +709,10 @@ tpr_bwd_kernel(
       // da3 partial: D[e][j] = sum_{p, k} dR[e][p][k] W3[j][p K + 16 ct + k]. The
       // A operand wants the edge on l%16, so each dR tile is transposed through LDS.
       f4 d3[4];
-      if constexpr (RB) {
+      if constexpr (RM == 1) {
         tile_da3_bf16<P>(r, sWt, tw, d3);
+      } else if constexpr (RM == 2) {
+        tile_da3_x3<P>(r, sWt, tw, d3);
       } else {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
@@ -622,14 +766,14 @@ void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* 
   tpr_fwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
 }
 
-template <int LH, bool RB>
+template <int LH, int RM>
 void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
                     const float* dAt, float* dYp, float* Q, float* da3p) {
-  using S = TprShape<LH, true>;
+  using S = TprShape<LH, true, RM>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
-  tpr_bwd_kernel<LH, RB><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
+  tpr_bwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
                                                     Q, da3p);
 }
 }  // namespace
@@ -654,19 +798,24 @@ void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
 
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_bf16) {
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode) {
   if (N <= 0 || E <= 0) return;
-#define MACE_TPRB(LH)                                                                                       \
-  case LH:                                                                                                  \
-    if (radial_bf16)                                                                                        \
-      tpr_bwd_launch<LH, true>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p);  \
-    else                                                                                                    \
-      tpr_bwd_launch<LH, false>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p); \
-    break;
+#define MACE_TPRB(LH, RM) tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p)
   switch (lh_max) {
-    MACE_TPRB(0)
-    MACE_TPRB(1)
-    MACE_TPRB(2)
+    case 0:
+      if (radial_mode == 1) MACE_TPRB(0, 1);
+      else if (radial_mode == 2) MACE_TPRB(0, 2);
+      else MACE_TPRB(0, 0);
+      break;
+    case 1:
+      if (radial_mode == 1) MACE_TPRB(1, 1);
+      else if (radial_mode == 2) MACE_TPRB(1, 2);
+      else MACE_TPRB(1, 0);
+      break;
+    case 2:   // split BF16 falls back to FP32 MFMA here
+      if (radial_mode == 1) MACE_TPRB(2, 1);
+      else MACE_TPRB(2, 0);
+      break;
   }
 #undef MACE_TPRB
 }

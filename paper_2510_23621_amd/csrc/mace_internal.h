@@ -360,7 +360,7 @@ void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
                     float inv_c, float* At, int radial_mode);   // 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate)
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_bf16);
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode);   // as launch_tpr_fwd; split BF16 runs on FP32 MFMA for l_h = 2
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
 struct SymW {
