@@ -246,6 +246,16 @@ def main():
     if kname in MFMA_BOUND:
         roof = {"bound": "mfma", "achieved": round(tfl, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tfl / FP32_MFMA_PEAK_TFLOPS, 4)}
+        split = (kname in ("tpr_fwd_kernel", "tpr_bwd_kernel") and prec != B.MACE_BF16_RADIAL
+                 and B.mace_radial_operands(g.handle, -1) == B.MACE_RADIAL_SPLIT_BF16
+                 and (kname == "tpr_fwd_kernel" or params["hidden_lmax"] <= 1))
+        if split:
+            # FP32-accurate products as six BF16 MFMA products each: the flops
+            # above are the FP32 products the algorithm needs; the BF16 MFMA
+            # pipe executes six times as many
+            roof.update({"operands": "split-bf16 (3 parts, 6 bf16 products per fp32 product, fp32 accumulation)",
+                         "executed_bf16_tflops": round(6 * tfl, 2), "bf16_peak": BF16_MFMA_PEAK_TFLOPS,
+                         "executed_frac_of_bf16_peak": round(6 * tfl / BF16_MFMA_PEAK_TFLOPS, 4)})
     else:
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(gbs / HBM_PEAK_GBS, 4)}
