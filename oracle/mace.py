@@ -199,6 +199,15 @@ def _round_fp16(x: torch.Tensor) -> torch.Tensor:
     return x.to(torch.float16).to(DT)
 
 
+def _rounding(fmt):
+    """Operand rounding of one block for the per-block precision study:
+    None (FP64), "bf16" or "fp16" (round to nearest even; the arithmetic and
+    every sum stay FP64). Gradients pass through the rounding unchanged."""
+    if fmt is None:
+        return lambda x: x
+    return {"bf16": _round_bf16, "fp16": _round_fp16}[fmt]
+
+
 class _Lin:
     """Channel-mixing linear y = x @ W with optional BF16 or FP16 emulation
     of its inputs and weights (R11)."""
@@ -221,12 +230,16 @@ class _Lin:
 
 
 def symmetric_contraction(A: torch.Tensor, W: dict, t: int, L: int, z: torch.Tensor,
-                          correlation: int, chunk: int = 64) -> torch.Tensor:
+                          correlation: int, chunk: int = 64, rnd=None) -> torch.Tensor:
     """Eq. 27 + message: B_{n,k,M} = sum_nu sum_eta W^{nu}_{z_n,L}[eta,k]
     sum_{a_1..a_nu} U^{nu,L}_eta[M, a_1..a_nu] prod_xi A_{n,k,a_xi}.
 
     A: [N, 16, K] -> [N, 2L+1, K].  Dense U, node chunks to bound memory.
+    rnd: optional rounding of the operands A and W (the U constants are not
+    rounded).
     """
+    rnd = rnd or (lambda x: x)
+    A = rnd(A)
     N, ncomp, K = A.shape
     outs = []
     Us = {}
@@ -246,7 +259,7 @@ def symmetric_contraction(A: torch.Tensor, W: dict, t: int, L: int, z: torch.Ten
                 continue
             ne = Us[nu].shape[0] // (2 * L + 1)
             Bnu = (mono @ Us[nu].T).reshape(n, K, ne, 2 * L + 1)   # [n,K,eta,M]
-            w = W[f"{t}.symc.{L}.{nu}"][zc]                          # [n, eta, K]
+            w = rnd(W[f"{t}.symc.{L}.{nu}"][zc])                     # [n, eta, K]
             acc = acc + torch.einsum("nkem,nek->nkm", Bnu, w)
         outs.append(acc.transpose(1, 2))
     return torch.cat(outs, dim=0)
@@ -279,9 +292,16 @@ def build_graph(system, d: ModelDesc) -> Graph:
 
 def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
                   bf16_linear: bool = False, edge_chunk: int = 1 << 16,
-                  return_intermediates: bool = False, fp16_linear: bool = False, bf16_radial: bool = False):
-    """Per-atom energies eps_i [N] for positions pos [N,3] (float64)."""
+                  return_intermediates: bool = False, fp16_linear: bool = False, bf16_radial: bool = False,
+                  tp_round=None, symcon_round=None):
+    """Per-atom energies eps_i [N] for positions pos [N,3] (float64).
+
+    tp_round / symcon_round ("bf16", "fp16" or None) round the operands of
+    one block for the per-block precision study: the edge product's sender
+    features, harmonics and radial weights (not the CG constants), or the
+    symmetric contraction's A and weights (not U)."""
     lin = _Lin(bf16_linear, fp16_linear)
+    rtp, rsc = _rounding(tp_round), _rounding(symcon_round)
     z = graph.species
     N = pos.shape[0]
     K = d.K
@@ -310,11 +330,11 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
         At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
         for e0 in range(0, E, edge_chunk):
             sl = slice(e0, e0 + edge_chunk)
-            R = radial_mlp(rb[sl], W, t, nh, bf16_radial).reshape(-1, len(paths), K)  # [e,P,K]
+            R = rtp(radial_mlp(rb[sl], W, t, nh, bf16_radial).reshape(-1, len(paths), K))  # [e,P,K]
             for p, (lh, ly, lo) in enumerate(paths):
                 C = torch.from_numpy(so3.real_cg(lh, ly, lo))
-                hs = ht[lh][snd[sl]]                                      # [e, 2lh+1, K]
-                Yl = Y[sl, ly * ly: ly * ly + 2 * ly + 1]                 # [e, 2ly+1]
+                hs = rtp(ht[lh][snd[sl]])                                 # [e, 2lh+1, K]
+                Yl = rtp(Y[sl, ly * ly: ly * ly + 2 * ly + 1])            # [e, 2ly+1]
                 msg = torch.einsum("abc,eak,eb->eck", C, hs, Yl) * R[:, p, None, :]
                 At[p] = At[p].index_add(0, rcv[sl], msg)
         At = [a / d.c_norm for a in At]                                   # R6
@@ -330,7 +350,7 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
         Afull = torch.cat(A, dim=1)                                        # [N,16,K]
         hn = {}
         for L in out_ls:
-            B = symmetric_contraction(Afull, W, t, L, z, d.correlation)
+            B = symmetric_contraction(Afull, W, t, L, z, d.correlation, rnd=rsc)
             hn[L] = lin(B, W[f"{t}.prod.{L}"])
             if L in sc:
                 hn[L] = hn[L] + sc[L]
@@ -355,14 +375,14 @@ def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
 
 def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
                   bf16_linear: bool = False, forces: bool = True, fp16_linear: bool = False,
-                  bf16_radial: bool = False):
+                  bf16_radial: bool = False, tp_round=None, symcon_round=None):
     """Returns dict(eps [N], energy [G], forces [N,3] or None, graph)."""
     W = unpack_weights(d, blob)
     if graph is None:
         graph = build_graph(system, d)
     pos = torch.tensor(system.positions, dtype=DT, requires_grad=forces)
     eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear,
-                        bf16_radial=bf16_radial)
+                        bf16_radial=bf16_radial, tp_round=tp_round, symcon_round=symcon_round)
     Eg = graph_energies(eps, graph)
     F = None
     if forces:

@@ -500,3 +500,74 @@ def test_bf16_radial_mode_rounds_the_last_radial_product():
     assert not np.array_equal(lin["forces"], rad["forces"])
     fdev = np.linalg.norm(rad["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"])
     assert fdev < 2e-2, fdev
+
+
+# ------------------------------------------------------- per-block precision study
+
+def _np_round16(x, fmt):
+    """Round to nearest even through FP32, written with numpy only: bfloat16
+    by the 16-bit truncation of the FP32 pattern with a nearest-even bias,
+    binary16 by numpy's half type."""
+    x32 = np.asarray(x, dtype=np.float64).astype(np.float32)
+    if fmt == "fp16":
+        return x32.astype(np.float16).astype(np.float64)
+    u = x32.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_edge_product_rounding_rounds_features_harmonics_and_radial_weights(fmt):
+    """The edge-product rounding of the precision study rounds exactly the
+    sender features, the harmonics and the radial weights (brute-force loops
+    on independently rounded operands), not the CG constants."""
+    d = _small_desc(hidden_lmax=1, K=3, rc=3.5, c_norm=1.7)
+    sysm = _cluster(5, seed=5, radius=1.6)
+    W = mace.unpack_weights(d, synth.weight_blob(mace.weight_layout(d), 1, STRESS_GAINS))
+    g = mace.build_graph(sysm, d)
+    pos = torch.tensor(sysm.positions)
+    _, ref = mace.node_energies(d, W, g, pos, return_intermediates=True)
+    _, inter = mace.node_energies(d, W, g, pos, return_intermediates=True, tp_round=fmt)
+    # layer 0 of the rounded run: A from rounded table, harmonics and radial weights
+    t = 0
+    paths = mace.tp_paths(d, t)
+    ht = {0: _np_round16((W["embed"][g.species][:, None, :] @ W["0.up.0"]).numpy(), fmt)}
+    Rall = _np_round16(mace.radial_mlp(inter["rbf"], W, t, 3).reshape(-1, len(paths), d.K).numpy(), fmt)
+    At = _edge_sum_loops(d, W, g, _np_round16(inter["Y"].numpy(), fmt), Rall, ht, t)
+    A = [sum(At[p] @ W[f"0.linear.{p}"].numpy() for p, (_, _, lo) in enumerate(paths) if lo == l) for l in range(4)]
+    z = g.species.numpy()
+    A = np.concatenate([np.einsum("nck,nkj->ncj", A[l], W[f"0.skip.{l}"].numpy()[z]) for l in range(4)], axis=1)
+    np.testing.assert_allclose(inter["0.A"].numpy(), A, rtol=1e-12, atol=1e-12)
+    assert not np.allclose(inter["0.A"].numpy(), ref["0.A"].numpy(), rtol=1e-7, atol=0)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_symmetric_contraction_rounding_rounds_a_and_weights(fmt):
+    """The contraction's rounding rounds A and the weights W (not U): the
+    unrounded contraction of independently rounded A and W."""
+    rng = np.random.default_rng(1)
+    K, S = 3, 2
+    A = torch.from_numpy(rng.standard_normal((4, 16, K)))
+    z = torch.tensor([0, 1, 1, 0])
+    for L in (0, 1, 2):
+        W = {f"0.symc.{L}.{nu}": torch.from_numpy(rng.standard_normal((S, so3.n_eta(nu, L), K))) for nu in (1, 2, 3)}
+        Wr = {k: torch.from_numpy(_np_round16(v.numpy(), fmt)) for k, v in W.items()}
+        got = mace.symmetric_contraction(A, W, 0, L, z, 3, rnd=mace._rounding(fmt)).numpy()
+        want = mace.symmetric_contraction(torch.from_numpy(_np_round16(A.numpy(), fmt)), Wr, 0, L, z, 3).numpy()
+        np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+
+
+def test_block_rounding_moves_the_result_by_about_the_format_precision():
+    """Rounding the edge product's or the contraction's operands moves
+    energies and forces away from FP64 by about the format's precision:
+    binary16 (11 significant bits) less than bfloat16 (8)."""
+    d = _desc(0)
+    blob = synth.weight_blob(mace.weight_layout(d), 4)
+    system = make_system(0, seed=0)
+    ref = mace.energy_forces(d, blob, system)
+    for key in ("tp_round", "symcon_round"):
+        dev = {}
+        for fmt in ("bf16", "fp16"):
+            out = mace.energy_forces(d, blob, system, graph=ref["graph"], **{key: fmt})
+            dev[fmt] = np.linalg.norm(out["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"])
+        assert 0 < dev["fp16"] < dev["bf16"] < 5e-2, (key, dev)
