@@ -193,6 +193,24 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use);
 typedef enum { MACE_RADIAL_FP32 = 0, MACE_RADIAL_SPLIT_BF16 = 2 } mace_radial_operands_kind;
 mace_status mace_radial_operands(mace_graph* g, int32_t request, int32_t* in_use);
 
+/* Per-block precision study (the paper's per-block low-precision experiments,
+ * run on the whole model): the operands of one block are rounded to nearest
+ * even as they are loaded, all arithmetic and sums staying FP32, on top of
+ * the handle's precision mode.
+ *   block MACE_BLOCK_EDGE_PRODUCT: the sender features, the harmonics and the
+ *     radial weights R of every edge product (the CG constants stay FP32);
+ *     the first layer then runs in per-edge form (its factorised form never
+ *     forms R);
+ *   block MACE_BLOCK_SYMMETRIC_CONTRACTION: A and the contraction weights (the
+ *     coupling constants stay FP32).
+ *   format 0 none (the default), 1 bfloat16, 2 IEEE binary16 (magnitudes
+ *     beyond 65504 become infinite); format < 0 only queries.
+ * Gradients pass through the rounding unchanged.  *in_use (host, may be
+ * NULL) receives the setting.  Takes effect for calls enqueued after it
+ * returns; no device work. */
+typedef enum { MACE_BLOCK_EDGE_PRODUCT = 0, MACE_BLOCK_SYMMETRIC_CONTRACTION = 1 } mace_block;
+mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, int32_t* in_use);
+
 /* Device-detected errors of the calls enqueued since setup or the previous
  * check: the edge kernels OR status bits into a word of the workspace,
  * 1 = an edge vector with a non-finite component (NaN or infinite

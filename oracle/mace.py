@@ -202,10 +202,13 @@ def _round_fp16(x: torch.Tensor) -> torch.Tensor:
 def _rounding(fmt):
     """Operand rounding of one block for the per-block precision study:
     None (FP64), "bf16" or "fp16" (round to nearest even; the arithmetic and
-    every sum stay FP64). Gradients pass through the rounding unchanged."""
+    every sum stay FP64). Gradients pass through the rounding unchanged
+    (x + (round(x) - x) with the difference held constant: the value is
+    round(x) exactly, the derivative 1)."""
     if fmt is None:
         return lambda x: x
-    return {"bf16": _round_bf16, "fp16": _round_fp16}[fmt]
+    r = {"bf16": _round_bf16, "fp16": _round_fp16}[fmt]
+    return lambda x: x + (r(x) - x).detach()
 
 
 class _Lin:

@@ -24,6 +24,8 @@ MACE_L0_EDGE = 1
 MACE_L0_FACTORED = 2
 MACE_RADIAL_FP32 = 0
 MACE_RADIAL_SPLIT_BF16 = 2
+MACE_BLOCK_EDGE_PRODUCT = 0
+MACE_BLOCK_SYMMETRIC_CONTRACTION = 1
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 
@@ -32,7 +34,7 @@ EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", 
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
             "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form",
-            "mace_radial_operands"]
+            "mace_radial_operands", "mace_block_rounding"]
 
 
 class MaceError(RuntimeError):
@@ -87,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.mace_profile_work.argtypes = [P, P, P]
         L.mace_layer0_form.argtypes = [P, I32, P]
         L.mace_radial_operands.argtypes = [P, I32, P]
+        L.mace_block_rounding.argtypes = [P, I32, I32, P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
         L.mace_status_string.restype = ctypes.c_char_p
@@ -296,6 +299,14 @@ def mace_radial_operands(handle, request: int = -1) -> int:
     only query the operands of the last radial layer; returns the setting."""
     used = ctypes.c_int32(0)
     _check(lib().mace_radial_operands(handle, request, ctypes.byref(used)), "mace_radial_operands")
+    return used.value
+
+
+def mace_block_rounding(handle, block: int, fmt: int = -1) -> int:
+    """Precision study: set (0 none, 1 bfloat16, 2 binary16) or, with
+    fmt < 0, only query the operand rounding of one block; returns it."""
+    used = ctypes.c_int32(0)
+    _check(lib().mace_block_rounding(handle, block, fmt, ctypes.byref(used)), "mace_block_rounding")
     return used.value
 
 

@@ -160,7 +160,7 @@ struct Carver {
 };
 
 struct Buffers {
-  float *w = nullptr, *wT = nullptr, *sp_table = nullptr;
+  float *w = nullptr, *wT = nullptr, *sp_table = nullptr, *sp_round = nullptr;   // (rounded copy: precision study)
   unsigned short *wbf = nullptr, *wbfT = nullptr;   // 16-bit K-packed copies (BF16- / FP16-linear modes)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
       *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
@@ -193,6 +193,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.wbf = c.take<unsigned short>(m.total);
   b.wbfT = c.take<unsigned short>(m.total);
   b.sp_table = c.take<float>(S * K);
+  b.sp_round = c.take<float>(S * K);
   b.species = c.take<int>(N);
   b.snd = c.take<int>(std::max<int64_t>(E, 1));
   b.rcv = c.take<int>(std::max<int64_t>(E, 1));
@@ -289,6 +290,7 @@ struct mace_graph {
   LinPlanRef l0f, l0fT;
   bool l0_fact = false;
   bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_radial_operands)
+  int tp_round = 0, sc_round = 0;   // precision study: operand rounding of the edge product / contraction
 };
 
 namespace {
@@ -552,11 +554,16 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
                            rs, b.status);
     }
   }
+  if (h->tp_round) {
+    // precision study: the edge products read rounded harmonics and sender features
+    launch_round(s, b.Y, b.Y, (size_t)E * 16, h->tp_round);
+    launch_round(s, b.sp_round, b.sp_table, (size_t)m.d.n_species * K, h->tp_round);
+  }
   const float inv_c = (float)(1.0 / m.d.c_norm);
   for (int t = 0; t < m.d.n_layers; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
-    if (t == 0 && h->l0_fact) {
+    if (t == 0 && h->l0_fact && !h->tp_round) {
       // factorised first layer: U per receiver, then one contraction (FP32
       // mode: straight to A; 16-bit modes: to At, then their own linears)
       {
@@ -573,17 +580,19 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     } else {
       // edge product with the sender features: the species table at layer 0,
       // linear_up of h^t (with the residual species linear) after it
-      const float* src = b.sp_table;
+      const float* src = h->tp_round ? b.sp_round : b.sp_table;
       const int* src_map = b.species;
       if (t > 0) {
         run_linear(h, s, h->upskip[t], largs(h, b.hin[t], b.ht[t], nullptr, false, 0, nullptr, b.sc));
+        launch_round(s, b.ht[t], b.ht[t], (size_t)N * L.din * K, h->tp_round);
         src = b.ht[t];
         src_map = nullptr;
       }
       {
         PROF(KID_TP_FWD);
         launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
-                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0));
+                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0),
+                       h->tp_round);
       }
       if (t == 0 && !lowp) {
         run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
@@ -596,7 +605,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     }
     {
       PROF(KID_SYMCON_FWD);
-      launch_symcon_fwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.B);
+      launch_symcon_fwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.B, h->sc_round);
     }
     float* hout = L.last ? b.hlast : b.hin[t + 1];
     {
@@ -653,9 +662,9 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     }
     {
       PROF(KID_SYMCON_BWD);
-      launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA);
+      launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA, h->sc_round);
     }
-    const bool fact = t == 0 && h->l0_fact;
+    const bool fact = t == 0 && h->l0_fact && !h->tp_round;
     // dE/dAt (the transposes of the linears after the edge product); the
     // factorised first layer ends in dE/dU instead
     const float* dApre = b.dA;
@@ -679,12 +688,12 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
                          b.da3p, b.dYp);
       n_part = 1;
     } else {
-      const float* src = t == 0 ? b.sp_table : b.ht[t];
+      const float* src = t == 0 ? (h->tp_round ? b.sp_round : b.sp_table) : b.ht[t];
       const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
       launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p,
-                     h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0));
+                     h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0), h->tp_round);
     }
     {
       // right after the partials are written, while they are still in the
@@ -1158,6 +1167,15 @@ mace_status mace_radial_operands(mace_graph* g, int32_t request, int32_t* in_use
     g->radial_split = request == MACE_RADIAL_SPLIT_BF16;
   }
   if (in_use) *in_use = g->prec == MACE_BF16_RADIAL ? 1 : (g->radial_split ? MACE_RADIAL_SPLIT_BF16 : MACE_RADIAL_FP32);
+  return MACE_OK;
+}
+
+mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, int32_t* in_use) {
+  if (!g || (block != MACE_BLOCK_EDGE_PRODUCT && block != MACE_BLOCK_SYMMETRIC_CONTRACTION) || format > 2)
+    return MACE_EINVAL;
+  int& r = block == MACE_BLOCK_EDGE_PRODUCT ? g->tp_round : g->sc_round;
+  if (format >= 0) r = format;
+  if (in_use) *in_use = r;
   return MACE_OK;
 }
 

@@ -127,6 +127,20 @@ void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off,
   forces_kernel<<<(N + 3) / 4, 256, 0, s>>>(N, rcv_off, snd_off, snd_perm, g, F);
 }
 
+// dst[i] = src[i] rounded to nearest even (rnd 1: bfloat16, 2: binary16); in
+// place when dst = src (the precision study's operand rounding of buffers)
+__global__ void round_kernel(float* dst, const float* src, size_t n, int rnd) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = lowp_round(src[i], rnd);
+}
+
+void launch_round(hipStream_t s, float* dst, const float* src, size_t n, int rnd) {
+  if (n == 0 || !rnd) return;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  round_kernel<<<(unsigned)blocks, 256, 0, s>>>(dst, src, n, rnd);
+}
+
 void launch_fill(hipStream_t s, float* p, size_t n, float v) {
   if (n == 0) return;
   size_t blocks = (n + 255) / 256;

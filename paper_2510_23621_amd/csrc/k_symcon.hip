@@ -4,7 +4,9 @@
 // where Tree_eta is the eta-th selected coupling tree and s_eta its scale
 // (the generalised-CG tensor U_eta = s_eta * Sym(Tree_eta); contracting a
 // symmetric power of A with the unsymmetrised tree gives the same value).
-// One thread per (node, channel); all coupling constants are immediates.
+// One thread per (node, channel); all coupling constants are immediates. The
+// precision study's rounding (rnd: 0 none, 1 bfloat16, 2 binary16) applies to
+// A and the weights as they are loaded; the coupling constants stay FP32.
 #include "mace_internal.h"
 #include "static_loops.h"
 
@@ -62,7 +64,7 @@ __device__ __forceinline__ void tree_vjp(const float* a, const float* gB, float 
   }
 }
 
-template <int LOUT>
+template <int LOUT, int RND>
 __global__ void __launch_bounds__(256) symcon_fwd_kernel(int N, int K, const int* __restrict__ species,
                                                          const float* __restrict__ A, SymW w,
                                                          float* __restrict__ B) {
@@ -73,7 +75,7 @@ __global__ void __launch_bounds__(256) symcon_fwd_kernel(int N, int K, const int
   const int z = species[n];
   float a[16];
 #pragma unroll
-  for (int c = 0; c < 16; ++c) a[c] = A[((size_t)n * 16 + c) * K + k];
+  for (int c = 0; c < 16; ++c) a[c] = lowp_round(A[((size_t)n * 16 + c) * K + k], RND);
   float b[DOUT];
 #pragma unroll
   for (int c = 0; c < DOUT; ++c) b[c] = 0.f;
@@ -85,7 +87,7 @@ __global__ void __launch_bounds__(256) symcon_fwd_kernel(int N, int K, const int
       if constexpr (ne > 0) {
         const float* W = w.w[L][nu] + (size_t)z * ne * K + k;
         mt::Trees<nu, L>::each([&](auto tree, int eta, float scale) {
-          float coef = W[(size_t)eta * K] * scale;
+          float coef = lowp_round(W[(size_t)eta * K], RND) * scale;
           float t[2 * L + 1];
           tree_eval<decltype(tree), L>(a, t);
 #pragma unroll
@@ -98,7 +100,7 @@ __global__ void __launch_bounds__(256) symcon_fwd_kernel(int N, int K, const int
   for (int c = 0; c < DOUT; ++c) B[((size_t)n * DOUT + c) * K + k] = b[c];
 }
 
-template <int LOUT>
+template <int LOUT, int RND>
 __global__ void __launch_bounds__(256) symcon_bwd_kernel(int N, int K, const int* __restrict__ species,
                                                          const float* __restrict__ A, SymW w,
                                                          const float* __restrict__ dB, float* __restrict__ dA) {
@@ -110,7 +112,7 @@ __global__ void __launch_bounds__(256) symcon_bwd_kernel(int N, int K, const int
   float a[16], da[16];
 #pragma unroll
   for (int c = 0; c < 16; ++c) {
-    a[c] = A[((size_t)n * 16 + c) * K + k];
+    a[c] = lowp_round(A[((size_t)n * 16 + c) * K + k], RND);
     da[c] = 0.f;
   }
   float gb[DOUT];
@@ -124,7 +126,7 @@ __global__ void __launch_bounds__(256) symcon_bwd_kernel(int N, int K, const int
       if constexpr (ne > 0) {
         const float* W = w.w[L][nu] + (size_t)z * ne * K + k;
         mt::Trees<nu, L>::each([&](auto tree, int eta, float scale) {
-          float coef = W[(size_t)eta * K] * scale;
+          float coef = lowp_round(W[(size_t)eta * K], RND) * scale;
           tree_vjp<decltype(tree), L>(a, gb + L * L, coef, da);
         });
       }
@@ -135,26 +137,42 @@ __global__ void __launch_bounds__(256) symcon_bwd_kernel(int N, int K, const int
 }
 
 void launch_symcon_fwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A, SymW w,
-                       float* B) {
+                       float* B, int rnd) {
   if (N <= 0) return;
   int tot = N * K;
   dim3 grid((tot + 255) / 256), block(256);
+  auto go = [&](auto LO, auto RD) {
+    symcon_fwd_kernel<decltype(LO)::value, decltype(RD)::value><<<grid, block, 0, s>>>(N, K, species, A, w, B);
+  };
+  auto pick = [&](auto LO) {
+    if (rnd == 1) go(LO, std::integral_constant<int, 1>{});
+    else if (rnd == 2) go(LO, std::integral_constant<int, 2>{});
+    else go(LO, std::integral_constant<int, 0>{});
+  };
   switch (lout_max) {
-    case 0: symcon_fwd_kernel<0><<<grid, block, 0, s>>>(N, K, species, A, w, B); break;
-    case 1: symcon_fwd_kernel<1><<<grid, block, 0, s>>>(N, K, species, A, w, B); break;
-    case 2: symcon_fwd_kernel<2><<<grid, block, 0, s>>>(N, K, species, A, w, B); break;
+    case 0: pick(std::integral_constant<int, 0>{}); break;
+    case 1: pick(std::integral_constant<int, 1>{}); break;
+    case 2: pick(std::integral_constant<int, 2>{}); break;
   }
 }
 
 void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A, SymW w,
-                       const float* dB, float* dA) {
+                       const float* dB, float* dA, int rnd) {
   if (N <= 0) return;
   int tot = N * K;
   dim3 grid((tot + 255) / 256), block(256);
+  auto go = [&](auto LO, auto RD) {
+    symcon_bwd_kernel<decltype(LO)::value, decltype(RD)::value><<<grid, block, 0, s>>>(N, K, species, A, w, dB, dA);
+  };
+  auto pick = [&](auto LO) {
+    if (rnd == 1) go(LO, std::integral_constant<int, 1>{});
+    else if (rnd == 2) go(LO, std::integral_constant<int, 2>{});
+    else go(LO, std::integral_constant<int, 0>{});
+  };
   switch (lout_max) {
-    case 0: symcon_bwd_kernel<0><<<grid, block, 0, s>>>(N, K, species, A, w, dB, dA); break;
-    case 1: symcon_bwd_kernel<1><<<grid, block, 0, s>>>(N, K, species, A, w, dB, dA); break;
-    case 2: symcon_bwd_kernel<2><<<grid, block, 0, s>>>(N, K, species, A, w, dB, dA); break;
+    case 0: pick(std::integral_constant<int, 0>{}); break;
+    case 1: pick(std::integral_constant<int, 1>{}); break;
+    case 2: pick(std::integral_constant<int, 2>{}); break;
   }
 }
 

@@ -405,6 +405,19 @@ __device__ __forceinline__ void tile_da3_bf16(const f4* r, const unsigned short*
 
 // Y rows of the wave's 16-edge tile into LDS: sy[row][m], row pitch kYPitch.
 // Lane l moves float4 number l%4 of row l/4.
+// The precision study's operand rounding of the edge product (rnd: 0 none,
+// 1 bfloat16, 2 binary16, round to nearest even) of the radial weights of a
+// tile; the harmonics and the sender features arrive rounded (the host runtime
+// rounds those buffers in place).
+template <int P>
+__device__ __forceinline__ void round_tile(f4* r, int rnd) {
+  if (!rnd) return;
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[p][q] = lowp_round(r[p][q], rnd);
+}
+
 __device__ __forceinline__ void stage_y(const float* __restrict__ Y, int e0, int e_end, float* sy) {
   const int l = threadIdx.x & 63;
   const int row = l >> 2, ch = l & 3;
@@ -448,7 +461,7 @@ __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LH
 tpr_fwd_kernel(
     int N, int K, const int* __restrict__ rcv_off, const int* __restrict__ snd, const int* __restrict__ src_map,
     const float* __restrict__ a3, const float* __restrict__ W3, const float* __restrict__ Y,
-    const float* __restrict__ h, float inv_c, float* __restrict__ At) {
+    const float* __restrict__ h, float inv_c, float* __restrict__ At, int rnd) {
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
@@ -480,6 +493,7 @@ tpr_fwd_kernel(
       if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else if constexpr (RM == 2) tile_radial_x3<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
+      round_tile<P>(r, rnd);
       // lane group 0 holds the tile's first edges, so nq covers every valid one;
       // the scheduling barrier keeps one edge's operands live at a time, and
       // the next edge's h row is requested while this one is contracted
@@ -574,7 +588,7 @@ tpr_bwd_kernel(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
-    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p) {
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
@@ -635,6 +649,7 @@ tpr_bwd_kernel(
       if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, sWb, r);
       else if constexpr (RM == 2) tile_radial_x3s<P>(a3, e0, e_end, sWb, r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
+      round_tile<P>(r, rnd);
       const int nq = min(4, e_end - e0);
       float hv[DIN];
       load_h_row<DIN>(h, srcq[0], K, k, hv);
@@ -759,34 +774,35 @@ int tpr_grid_x(int N, int n_ct, int waves, int blocks_per_cu) {
 
 template <int LH, int RM>
 void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* snd, const int* src_map,
-                    const float* a3, const float* W3, const float* Y, const float* h, float inv_c, float* At) {
+                    const float* a3, const float* W3, const float* Y, const float* h, float inv_c, float* At,
+                    int rnd) {
   using S = TprShape<LH, false>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
-  tpr_fwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);
+  tpr_fwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, rnd);
 }
 
 template <int LH, int RM>
 void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
-                    const float* dAt, float* dYp, float* Q, float* da3p) {
+                    const float* dAt, float* dYp, float* Q, float* da3p, int rnd) {
   using S = TprShape<LH, true, RM>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
   tpr_bwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
-                                                    Q, da3p);
+                                                    Q, da3p, rnd);
 }
 }  // namespace
 
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_mode) {
+                    float inv_c, float* At, int radial_mode, int tp_round) {
   if (N <= 0) return;
 #define MACE_TPRF(LH)                                                                                    \
   case LH:                                                                                               \
-    if (radial_mode == 1) tpr_fwd_launch<LH, 1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
-    else if (radial_mode == 2) tpr_fwd_launch<LH, 2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At); \
-    else tpr_fwd_launch<LH, 0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At);                  \
+    if (radial_mode == 1) tpr_fwd_launch<LH, 1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round); \
+    else if (radial_mode == 2) tpr_fwd_launch<LH, 2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round); \
+    else tpr_fwd_launch<LH, 0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round);                  \
     break;
   switch (lh_max) {
     MACE_TPRF(0)
@@ -798,9 +814,11 @@ void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
 
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode) {
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
+                    int tp_round) {
   if (N <= 0 || E <= 0) return;
-#define MACE_TPRB(LH, RM) tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p)
+#define MACE_TPRB(LH, RM) \
+  tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
   switch (lh_max) {
     case 0:
       if (radial_mode == 1) MACE_TPRB(0, 1);

@@ -357,19 +357,20 @@ void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, con
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_mode);   // 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate)
+                    float inv_c, float* At, int radial_mode, int tp_round);   // radial 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate); tp_round 0/1/2 none/bf16/fp16
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode);   // as launch_tpr_fwd; split BF16 runs on FP32 MFMA for l_h = 2
+                    float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
+                    int tp_round);   // as launch_tpr_fwd; split BF16 runs on FP32 MFMA for l_h = 2
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
 struct SymW {
   const float* w[4][4];     // [L][nu] -> [S][n_eta][K] or null
 };
 void launch_symcon_fwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
-                       SymW w, float* B);
+                       SymW w, float* B, int rnd);
 void launch_symcon_bwd(hipStream_t s, int lout_max, int N, int K, const int* species, const float* A,
-                       SymW w, const float* dB, float* dA);
+                       SymW w, const float* dB, float* dA, int rnd);
 void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
 // Algorithmic work of one linear launch over N nodes: flops = 2 K^2 per
 // (node, term component); bytes = every distinct input component and weight
@@ -384,5 +385,6 @@ void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float
 void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp,
                           float* table);
 void launch_fill(hipStream_t s, float* p, size_t n, float v);
+void launch_round(hipStream_t s, float* dst, const float* src, size_t n, int rnd);   // no-op for rnd = 0
 
 }  // namespace mace

@@ -29,7 +29,7 @@ def oracle_blob(params: dict, seed: int, gains=None) -> np.ndarray:
 
 
 def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=True, repeats=1, stress=False,
-            l0_form=None, radial=None):
+            l0_form=None, radial=None, rounding=None):
     desc = B.make_desc(**params)
     snd, rcv, sh = B.mace_neighbor_list(system.positions, params["r_cut"], system.cells, system.graph_of_atom,
                                         system.n_graphs)
@@ -41,6 +41,8 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     form = B.mace_layer0_form(g.handle, -1 if l0_form is None else l0_form)
     if radial is not None:
         B.mace_radial_operands(g.handle, radial)
+    for blk, fmt in (rounding or {}).items():
+        B.mace_block_rounding(g.handle, blk, fmt)
     pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
     outs = []
     for _ in range(repeats):
@@ -59,9 +61,11 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     return outs if repeats > 1 else outs[0]
 
 
-def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True, fp16=False, bf16_radial=False):
+def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True, fp16=False, bf16_radial=False,
+               tp_round=None, symcon_round=None):
     return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16 or bf16_radial,
-                              forces=forces, fp16_linear=fp16, bf16_radial=bf16_radial)
+                              forces=forces, fp16_linear=fp16, bf16_radial=bf16_radial, tp_round=tp_round,
+                              symcon_round=symcon_round)
 
 
 def oracle_stress(params: dict, system, blob: np.ndarray, bf16=False, fp16=False, bf16_radial=False):

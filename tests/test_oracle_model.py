@@ -571,3 +571,13 @@ def test_block_rounding_moves_the_result_by_about_the_format_precision():
             out = mace.energy_forces(d, blob, system, graph=ref["graph"], **{key: fmt})
             dev[fmt] = np.linalg.norm(out["forces"] - ref["forces"]) / np.linalg.norm(ref["forces"])
         assert 0 < dev["fp16"] < dev["bf16"] < 5e-2, (key, dev)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_block_rounding_value_is_the_rounding_and_gradient_passes_through(fmt):
+    x = torch.tensor(np.random.default_rng(3).standard_normal(64) * 3.0, requires_grad=True)
+    w = torch.tensor(np.random.default_rng(4).standard_normal(64))
+    y = mace._rounding(fmt)(x)
+    np.testing.assert_array_equal(y.detach().numpy(), _np_round16(x.detach().numpy(), fmt))
+    (g,) = torch.autograd.grad((w * y).sum(), x)
+    np.testing.assert_array_equal(g.numpy(), w.numpy())
