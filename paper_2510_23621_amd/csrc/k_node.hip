@@ -35,12 +35,14 @@ __device__ __forceinline__ unsigned short lowp_bits(float x) {
   else return fp16_bits(x);
 }
 
-constexpr int kLinCt = 4;   // column tiles per block
+constexpr int kLinCt = 4;        // column tiles per block
+constexpr int kLinSmallGrid = 512;   // blocks below which a square linear takes one column tile per block
 
 // LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
 // rounding and the MFMA instruction). K channels per output component, KI per
-// input component (KI != K only on the FP32 path).
-template <int K, int KI, int LP>
+// input component (KI != K only on the FP32 path). CT column tiles of 16
+// per block: kLinCt, or 1 for launches too small to fill the chip otherwise.
+template <int K, int KI, int LP, int CT>
 __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* __restrict__ Lp, LinArgs a) {
   constexpr bool BF16 = LP != 0;   // any 16-bit path
   const LinLaunch& L = *Lp;
@@ -48,15 +50,15 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   static_assert(!BF16 || KI == K, "16-bit linears are square");
   constexpr int PF = KI + 4;   // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
   constexpr int PB = KI + 8;   // 16-bit panel row pitch in elements (68 dwords at K = 128)
-  constexpr int kPanel = BF16 ? (64 * PB + 1) / 2 : 64 * PF;
+  constexpr int kPanel = BF16 ? (16 * CT * PB + 1) / 2 : 16 * CT * PF;
   __shared__ __align__(16) float sB[kPanel];
   unsigned short* sBb = reinterpret_cast<unsigned short*>(sB);
   const LinGC gcx = L.gc[blockIdx.y];
   const LinGroup grp = L.plan.g[gcx.g];
   const int c = gcx.c;
-  const int ct0 = blockIdx.z * kLinCt;
+  const int ct0 = blockIdx.z * CT;
   constexpr int nct = K / 16;
-  const int ncol = min(64, K - 16 * ct0);   // valid panel columns (K = 32 or 96: the last 64 are partial)
+  const int ncol = min(16 * CT, K - 16 * ct0);   // valid panel columns (K = 32 or 96: the last 64 are partial)
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int quad = blockIdx.x;
   const int tile0 = a.quad_tile[quad], ntile = a.quad_count[quad];
@@ -69,9 +71,9 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   // last node and are zeroed)
   const int node = a.node_order[t0 + min(l & 15, cnt - 1)];
   const float keep = (l & 15) < cnt ? 1.f : 0.f;
-  f4 acc[kLinCt];
+  f4 acc[CT];
 #pragma unroll
-  for (int j = 0; j < kLinCt; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < CT; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
   for (int tm = grp.t0; tm < grp.t1; ++tm) {
     const LinTerm term = L.plan.t[tm];
     const int64_t zoff = term.species ? zstride : 0;
@@ -98,7 +100,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
     if constexpr (!BF16) {
       // panel row = output column n: the transposed blob holds W^T[n][0..KI) contiguous
       const float* Wt = a.wt + term.w_off + zoff;
-      for (int idx = tid; idx < 64 * (KI / 4); idx += blockDim.x) {
+      for (int idx = tid; idx < 16 * CT * (KI / 4); idx += blockDim.x) {
         const int col = idx / (KI / 4), k4 = idx % (KI / 4);
         const int n = 16 * ct0 + min(col, ncol - 1);
         *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = *reinterpret_cast<const f4*>(Wt + (size_t)n * KI + 4 * k4);
@@ -106,7 +108,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
     } else {
       // packed [K/8][K][8]: 8 consecutive k of output column n are 16 contiguous bytes
       const unsigned short* Wp = a.wbf + term.w_off + zoff;
-      for (int idx = tid; idx < 64 * (K / 8); idx += blockDim.x) {
+      for (int idx = tid; idx < 16 * CT * (K / 8); idx += blockDim.x) {
         const int col = idx / (K / 8), kc = idx % (K / 8);
         const int n = 16 * ct0 + min(col, ncol - 1);
         *reinterpret_cast<us8*>(sBb + col * PB + 8 * kc) =
@@ -118,7 +120,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
 #pragma unroll
       for (int q = 0; q < KI / 16; ++q)
 #pragma unroll
-        for (int j = 0; j < kLinCt; ++j) {
+        for (int j = 0; j < CT; ++j) {
           const f4 b = *reinterpret_cast<const f4*>(sB + (16 * j + (l & 15)) * PF + 16 * q + 4 * (l >> 4));
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[q][cc], b[cc], acc[j], 0, 0, 0);
@@ -127,7 +129,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
 #pragma unroll
       for (int ks = 0; ks < K / 32; ++ks)
 #pragma unroll
-        for (int j = 0; j < kLinCt; ++j) {
+        for (int j = 0; j < CT; ++j) {
           const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));
           if constexpr (LP == 1)
             acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, ab[ks]), __builtin_bit_cast(bf8, b),
@@ -143,7 +145,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   const int cout = grp.dst ? L.plan.cout2 : L.plan.cout;
   const float* residual = grp.dst ? nullptr : a.residual;
 #pragma unroll
-  for (int j = 0; j < kLinCt; ++j) {
+  for (int j = 0; j < CT; ++j) {
     const int ct = ct0 + j;
     if (ct >= nct) continue;
 #pragma unroll
@@ -202,11 +204,29 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   const LinLaunch* L = P.dev;
   const int halves = (a.K / 16 + kLinCt - 1) / kLinCt;
   dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
+  const int KI0 = a.KI > 0 ? a.KI : a.K;
+  if (KI0 == a.K && (int64_t)a.n_quads * P.host.n_gc * halves < kLinSmallGrid) {
+    // small launch: one column tile per block, four times the blocks
+    dim3 g1(a.n_quads, P.host.n_gc, a.K / 16);
+    auto sq1 = [&](auto KK) {
+      constexpr int k = decltype(KK)::value;
+      if (a.lowp == 1) linear_kernel<k, k, 1, 1><<<g1, block, 0, s>>>(L, a);
+      else if (a.lowp == 2) linear_kernel<k, k, 2, 1><<<g1, block, 0, s>>>(L, a);
+      else linear_kernel<k, k, 0, 1><<<g1, block, 0, s>>>(L, a);
+    };
+    switch (a.K) {
+      case 32: sq1(std::integral_constant<int, 32>{}); break;
+      case 64: sq1(std::integral_constant<int, 64>{}); break;
+      case 96: sq1(std::integral_constant<int, 96>{}); break;
+      case 128: sq1(std::integral_constant<int, 128>{}); break;
+    }
+    return;
+  }
   const int KI = a.KI > 0 ? a.KI : a.K;
   if (KI != a.K) {   // FP32 only: the factorised first-layer contraction and its transpose
     if (a.lowp) return;
     auto go = [&](auto KO, auto KIN) {
-      linear_kernel<decltype(KO)::value, decltype(KIN)::value, 0><<<grid, block, 0, s>>>(L, a);
+      linear_kernel<decltype(KO)::value, decltype(KIN)::value, 0, kLinCt><<<grid, block, 0, s>>>(L, a);
     };
     auto in_w = [&](auto KO) {
       switch (KI) {
@@ -230,9 +250,9 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   }
 #define MACE_LIN(KK)                                                            \
   case KK:                                                                     \
-    if (a.lowp == 1) linear_kernel<KK, KK, 1><<<grid, block, 0, s>>>(L, a);    \
-    else if (a.lowp == 2) linear_kernel<KK, KK, 2><<<grid, block, 0, s>>>(L, a); \
-    else linear_kernel<KK, KK, 0><<<grid, block, 0, s>>>(L, a);                \
+    if (a.lowp == 1) linear_kernel<KK, KK, 1, kLinCt><<<grid, block, 0, s>>>(L, a);    \
+    else if (a.lowp == 2) linear_kernel<KK, KK, 2, kLinCt><<<grid, block, 0, s>>>(L, a); \
+    else linear_kernel<KK, KK, 0, kLinCt><<<grid, block, 0, s>>>(L, a);                \
     break;
   switch (a.K) {
     MACE_LIN(32)

@@ -81,3 +81,25 @@ def test_block_rounding_setting_and_combination(case):
     with pytest.raises(B.MaceError):
         B.mace_block_rounding(g.handle, B.MACE_BLOCK_EDGE_PRODUCT, 3)
     g.close()
+
+
+def test_study_table_on_one_case(case):
+    """Every precision arm on the same case, against FP64 (the study's table):
+    each 16-bit arm is further from FP64 than FP32 and within the 16-bit
+    tolerances."""
+    params, bo, bl, sysm = case
+    ref = run_oracle(params, sysm, bo)
+    arms = [("fp32", B.MACE_FP32, None), ("bf16 linears", B.MACE_BF16_LINEAR, None),
+            ("fp16 linears", B.MACE_FP16_LINEAR, None), ("bf16 linears + radial", B.MACE_BF16_RADIAL, None)]
+    for blk, key in BLOCKS.items():
+        for fmt, name in FORMATS.items():
+            arms.append((f"{key[:-6]} {name}", B.MACE_FP32, {blk: fmt}))
+    base = None
+    for label, prec, rounding in arms:
+        err = errors(run_gpu(params, sysm, bl, prec, rounding=rounding), ref)
+        print(f"[study-table] {label:24s} energy {err['energy']:.2e} eps_l2 {err['eps_l2']:.2e} "
+              f"forces {err['forces']:.2e}", flush=True)
+        if base is None:
+            base = err
+            continue
+        assert base["forces"] < err["forces"] <= 2e-2 and err["energy"] <= 5e-3, (label, err)
