@@ -91,13 +91,13 @@ def kernel_work(name, model, N, E, l0_factored=False, n_species=2):
             tot_b += E * (256 + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
             tot_f += E * 2 * 2 * 64 * P * K
         elif name == "edge_prologue_kernel":      # geometry once, hidden layers of every layer
-            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * (256 + 3 * 256)   # a3, silu'
+            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * 256   # a3
             tot_f += E * 2 * (nb * 64 + 2 * 64 * 64)
         elif name == "radial_bwd_kernel":
             acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
             parts = 1 if fact else n_ct
-            tot_b += E * (3 * 256 + parts * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
-            tot_f += E * 2 * (2 * nb * 64 + 4 * 64 * 64)
+            tot_b += E * (nb * 4 + parts * (256 + 64) + 64 * (1 + acc) + nb * 4 * (1 + acc))
+            tot_f += E * 2 * (3 * nb * 64 + 6 * 64 * 64)   # hidden layers again, then their VJP
     return tot_b, tot_f
 
 

@@ -168,7 +168,6 @@ struct Buffers {
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
-  std::vector<float*> sg;   // per layer: [3][E][64] silu'(z) of the radial pre-activations
   std::vector<float*> A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
@@ -212,14 +211,12 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
   b.a3.resize(T);
-  b.sg.resize(T);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
   b.ht.assign(T, nullptr);
   for (int t = 0; t < T; ++t) {
     const LayerPlan& L = m.layers[t];
     b.a3[t] = c.take<float>(std::max<int64_t>(E, 1) * 64);
-    b.sg[t] = c.take<float>(std::max<int64_t>(E, 1) * 3 * 64);
     b.A[t] = c.take<float>(N * 16 * K);
     if (t > 0) {
       b.hin[t] = c.take<float>(N * L.din * K);
@@ -547,7 +544,6 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       for (int q = 0; q < rs.n; ++q) {
         rs.W[q] = b.w + m.off.at(std::to_string(t0 + q) + ".radial.0");
         rs.a3[q] = b.a3[t0 + q];
-        rs.sg[q] = b.sg[t0 + q];
       }
       // (a later chunk recomputes the same Y and rbf)
       launch_edge_prologue(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf,
@@ -699,7 +695,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       // right after the partials are written, while they are still in the
       // last-level cache
       PROF(KID_RADIAL_BWD);
-      launch_radial_bwd(s, E, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.sg[t], b.da3p, b.dYp, n_part,
+      launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, n_part,
                         b.dY, b.de, t < T - 1);
     }
     if (t > 0) {

@@ -102,24 +102,10 @@ __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __re
   }
 }
 
-// silu'(z) of a hidden layer's result tile (result layout) to sg[E][64].
-__device__ __forceinline__ void store_silu_grad(int E, int e0, const f4* z, float* __restrict__ sg) {
-  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int col = 16 * w + (l & 15);
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int e = e0 + 16 * rt + 4 * (l >> 4) + r;
-      if (e < E) sg[(size_t)e * kH + col] = silu_grad(z[rt][r]);
-    }
-}
-
 // Edge prologue for a 64-edge tile: geometry of every edge (Y and the radial
 // basis e, written out; the first wave computes one edge per lane in FP64),
 // then the hidden layers a3 = SiLU(SiLU(SiLU(e W0) W1) W2) of the radial MLP
-// of every interaction layer in rs, all from the same e, keeping silu'(z) of
-// the three pre-activations for the backward pass.
+// of every interaction layer in rs, all from the same e.
 template <int NBP>
 __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* __restrict__ pos,
                                                             const int* __restrict__ snd, const int* __restrict__ rcv,
@@ -157,18 +143,14 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
     const float* W1 = W0 + nb * kH;
     const float* W2 = W1 + kH * kH;
     f4 z[4];
-    float* sg = rs.sg[t];
     load_b_frag<kH>(W1, kH, bn);
     hidden_mma<NBP>(xs, kXPad, bc, ha, z);
-    store_silu_grad(E, e0, z, sg);
     __syncthreads();
     load_b_frag<kH>(W2, kH, bc);
     hidden_mma<kH>(ha, kPad, bn, hb, z);
-    store_silu_grad(E, e0, z, sg + (size_t)E * kH);
     __syncthreads();
     if (t + 1 < rs.n) load_b_frag<NBP>(rs.W[t + 1], nb, bn);
     hidden_mma<kH>(hb, kPad, bc, ha, z);
-    store_silu_grad(E, e0, z, sg + (size_t)2 * E * kH);
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
@@ -184,63 +166,70 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 }
 
 // de = VJP of the hidden layers given dE/da3, which arrives as n_part partials
-// da3p[part][E][64] summed here in part order; silu'(z) of the three
-// pre-activations comes from the forward prologue (sg[3][E][64]), so the
-// pass is dz2 = da3 silu'(z2), dz1 = (dz2 W2^T) silu'(z1), dz0 = (dz1 W1^T)
-// silu'(z0), de = dz0 W0^T. The same pass folds the partials dYp[part][E][16]
-// of dE/dY into dY. With accumulate set, de and dY are added to instead of
-// overwritten.
-template <int NPART>
-__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, int nb, const float* __restrict__ W,
-                                                         const float* __restrict__ sg,
+// da3p[part][E][64] summed here in part order. The pre-activations z0, z1, z2
+// are recomputed from the radial basis (three FP32 MFMA layers per 64-edge
+// tile; cheaper than storing silu'(z) for every edge and reading it back), so
+// the pass is dz2 = da3 silu'(z2), dz1 = (dz2 W2^T) silu'(z1),
+// dz0 = (dz1 W1^T) silu'(z0), de = dz0 W0^T. The same pass folds the partials
+// dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
+// to instead of overwritten.
+template <int NBP, int NPART>
+__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+                                                         const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
                                                          float* __restrict__ dY, float* __restrict__ de,
                                                          int accumulate) {
+  __shared__ float xs[kTE * kXPad];
   __shared__ float ta[kTE * kPad];
   __shared__ float tb[kTE * kPad];
   const int e0 = blockIdx.x * kTE;
   const float* W0 = W;
   const float* W1 = W0 + nb * kH;
   const float* W2 = W1 + kH * kH;
-  const float* sg0 = sg;
-  const float* sg1 = sg + (size_t)E * kH;
-  const float* sg2 = sg + (size_t)2 * E * kH;
   const int tid = threadIdx.x;
   const int l = tid & 63, w = tid >> 6;
   const int col = 16 * w + (l & 15);
-  // operands of the two MFMA stages, requested before the partial sums:
-  // B[k = j][col = i] = W[i][j] (the transposed products), and silu'(z1),
-  // silu'(z0) in the result layout
-  float b2[kH / 4], b1[kH / 4], g1[16], g0[16];
+  // forward fragments, then the hidden layers again
+  float bc[kH / 4], bn[kH / 4];
+  load_b_frag<NBP>(W0, nb, bc);
+  load_basis_tile(E, e0, rbf, nb, (nb + 3) & ~3, xs);
+  __syncthreads();
+  f4 z0[4], z1[4], z2[4];
+  load_b_frag<kH>(W1, kH, bn);
+  hidden_mma<NBP>(xs, kXPad, bc, ta, z0);
+  __syncthreads();
+  load_b_frag<kH>(W2, kH, bc);
+  hidden_mma<kH>(ta, kPad, bn, tb, z1);
+  __syncthreads();
+  hidden_mma<kH>(tb, kPad, bc, ta, z2);   // (a3 itself is not needed)
+  // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
+  float b2[kH / 4];
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) {
-    b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
-    b1[ks] = W1[col * kH + 4 * ks + (l >> 4)];
-  }
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int e = e0 + 16 * rt + 4 * (l >> 4) + r;
-      const bool ok = e < E;
-      g1[4 * rt + r] = ok ? sg1[(size_t)e * kH + col] : 0.f;
-      g0[4 * rt + r] = ok ? sg0[(size_t)e * kH + col] : 0.f;
-    }
-  // dz2 = (partials summed in part order) * silu'(z2), as float4 rows into ta
+  for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
+  __syncthreads();   // every wave is done with ta (a3)
+  // the partials summed in part order, as float4 rows into ta
   for (int idx = tid; idx < kTE * kH / 4; idx += blockDim.x) {
     const int row = idx >> 4, c4 = idx & 15;
     const int e = min(e0 + row, E - 1);
     f4 v = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(da3p + ((size_t)q * E + e) * kH + 4 * c4);
-    v *= *reinterpret_cast<const f4*>(sg2 + (size_t)e * kH + 4 * c4);
     if (e0 + row >= E) v = f4{0.f, 0.f, 0.f, 0.f};
     *reinterpret_cast<f4*>(ta + row * kPad + 4 * c4) = v;
   }
   __syncthreads();
+  // dz2 = da3 silu'(z2), in place (result layout)
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] *= silu_grad(z2[rt][r]);
+  __syncthreads();
   f4 acc[4];
-  // dz1 = (dz2 W2^T) silu'(z1) into tb
+  // dz1 = (dz2 W2^T) silu'(z1) into tb; the next stage's B = W1^T requested meanwhile
+  float b1[kH / 4];
+#pragma unroll
+  for (int ks = 0; ks < kH / 4; ++ks) b1[ks] = W1[col * kH + 4 * ks + (l >> 4)];
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -251,7 +240,7 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, int nb, const fl
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) tb[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * g1[4 * rt + r];
+    for (int r = 0; r < 4; ++r) tb[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z1[rt][r]);
   __syncthreads();
   // dz0 = (dz1 W1^T) silu'(z0) into ta (every wave has read ta before the barrier above)
 #pragma unroll
@@ -264,7 +253,7 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, int nb, const fl
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * g0[4 * rt + r];
+    for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z0[rt][r]);
   __syncthreads();
   // de[e][i] = sum_j dz0[e][j] W0[i][j] on MFMA: wave w takes the edge rows
   // 16w .. 16w + 15, the 16 result columns are i (zero past nb <= 16)
@@ -305,13 +294,14 @@ void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd
   else edge_prologue_kernel<16><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
 }
 
-void launch_radial_bwd(hipStream_t s, int E, int nb, const float* W, const float* sg, const float* da3p,
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
   auto go = [&](auto NP) {
     constexpr int NPART = decltype(NP)::value;
-    radial_bwd_kernel<NPART><<<g, 256, 0, s>>>(E, nb, W, sg, da3p, dYp, dY, de, accumulate);
+    if (nb <= 8) radial_bwd_kernel<8, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+    else radial_bwd_kernel<16, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
   };
   switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}, or 1 (whole values)
     case 1: go(std::integral_constant<int, 1>{}); break;

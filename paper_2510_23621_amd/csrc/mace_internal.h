@@ -334,7 +334,6 @@ constexpr int kMaxRadialLayers = 4;
 struct RadialSet {
   const float* W[kMaxRadialLayers];
   float* a3[kMaxRadialLayers];
-  float* sg[kMaxRadialLayers];   // [3][E][64] silu'(z) of the three pre-activations
   int n;
 };
 // first interaction layer in factorised form (U, gU: [N][16][64 S], S <= 4)
@@ -348,7 +347,7 @@ void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd
                           const RadialSet& rs, int* status);
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
-void launch_radial_bwd(hipStream_t s, int E, int nb, const float* W, const float* sg, const float* da3p,
+void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate);
 void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
                    const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
