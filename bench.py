@@ -247,7 +247,7 @@ def main():
         roof = {"bound": "mfma", "achieved": round(tfl, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(tfl / FP32_MFMA_PEAK_TFLOPS, 4)}
         split = (kname in ("tpr_fwd_kernel", "tpr_bwd_kernel") and prec != B.MACE_BF16_RADIAL
-                 and B.mace_radial_operands(g.handle, -1) == B.MACE_RADIAL_SPLIT_BF16
+                 and B.mace_fp32_products(g.handle, -1) == B.MACE_PRODUCTS_SPLIT_BF16
                  and (kname == "tpr_fwd_kernel" or params["hidden_lmax"] <= 1))
         if split:
             # FP32-accurate products as six BF16 MFMA products each: the flops

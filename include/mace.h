@@ -179,19 +179,20 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use);
 
 /* Operands of the P*K-wide last radial layer (formed inside the edge-product
  * kernels of the layers in per-edge form) in the modes other than
- * MACE_BF16_RADIAL:
- *   MACE_RADIAL_FP32:       FP32 MFMA (v_mfma_f32_16x16x4_f32);
- *   MACE_RADIAL_SPLIT_BF16: every FP32 operand x carried as x0 + x1 + x2, the
- *     bfloat16 roundings of x, x - x0 and x - x0 - x1 (together exact), and
- *     each product formed from the six partial products down to relative
- *     size 2^-18 on BF16 MFMA with FP32 accumulation: as accurate as FP32
- *     products (the dropped terms are below 2^-26 relative), at a fraction of
- *     the FP32 MFMA time.  The default.
+ * MACE_BF16_RADIAL.  (The channel-mixing linears stay on FP32 MFMA: split
+ * products were measured slower there, where the MFMA is not the bound.)
+ *   MACE_PRODUCTS_FP32:       FP32 MFMA (v_mfma_f32_16x16x4_f32);
+ *   MACE_PRODUCTS_SPLIT_BF16: every FP32 operand x carried as x0 + x1 + x2,
+ *     the bfloat16 roundings of x, x - x0 and x - x0 - x1 (together exact),
+ *     and each product formed from the six partial products down to
+ *     relative size 2^-18 on BF16 MFMA with FP32 accumulation: as accurate
+ *     as FP32 products (the dropped terms are below 2^-26 relative), at a
+ *     fraction of the FP32 MFMA time.  The default.
  * request < 0 only queries; *in_use (host, may be NULL) receives the setting
  * (MACE_BF16_RADIAL handles report 1 and refuse a change with MACE_EINVAL).
  * Takes effect for calls enqueued after it returns; no device work. */
-typedef enum { MACE_RADIAL_FP32 = 0, MACE_RADIAL_SPLIT_BF16 = 2 } mace_radial_operands_kind;
-mace_status mace_radial_operands(mace_graph* g, int32_t request, int32_t* in_use);
+typedef enum { MACE_PRODUCTS_FP32 = 0, MACE_PRODUCTS_SPLIT_BF16 = 2 } mace_fp32_products_kind;
+mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use);
 
 /* Per-block precision study (the paper's per-block low-precision experiments,
  * run on the whole model): the operands of one block are rounded to nearest

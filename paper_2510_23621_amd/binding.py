@@ -22,8 +22,8 @@ MACE_BF16_RADIAL = 3
 MACE_L0_AUTO = 0
 MACE_L0_EDGE = 1
 MACE_L0_FACTORED = 2
-MACE_RADIAL_FP32 = 0
-MACE_RADIAL_SPLIT_BF16 = 2
+MACE_PRODUCTS_FP32 = 0
+MACE_PRODUCTS_SPLIT_BF16 = 2
 MACE_BLOCK_EDGE_PRODUCT = 0
 MACE_BLOCK_SYMMETRIC_CONTRACTION = 1
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
@@ -34,7 +34,7 @@ EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", 
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
             "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form",
-            "mace_radial_operands", "mace_block_rounding"]
+            "mace_fp32_products", "mace_block_rounding"]
 
 
 class MaceError(RuntimeError):
@@ -88,7 +88,7 @@ def lib() -> ctypes.CDLL:
         L.mace_graph_check.argtypes = [P, P, P]
         L.mace_profile_work.argtypes = [P, P, P]
         L.mace_layer0_form.argtypes = [P, I32, P]
-        L.mace_radial_operands.argtypes = [P, I32, P]
+        L.mace_fp32_products.argtypes = [P, I32, P]
         L.mace_block_rounding.argtypes = [P, I32, I32, P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
@@ -294,11 +294,11 @@ def mace_layer0_form(handle, request: int = -1) -> int:
     return used.value
 
 
-def mace_radial_operands(handle, request: int = -1) -> int:
-    """Select (MACE_RADIAL_FP32 / MACE_RADIAL_SPLIT_BF16) or, with request < 0,
+def mace_fp32_products(handle, request: int = -1) -> int:
+    """Select (MACE_PRODUCTS_FP32 / MACE_PRODUCTS_SPLIT_BF16) or, with request < 0,
     only query the operands of the last radial layer; returns the setting."""
     used = ctypes.c_int32(0)
-    _check(lib().mace_radial_operands(handle, request, ctypes.byref(used)), "mace_radial_operands")
+    _check(lib().mace_fp32_products(handle, request, ctypes.byref(used)), "mace_fp32_products")
     return used.value
 
 

@@ -286,7 +286,7 @@ struct mace_graph {
   // path-merging and species linears) or U -> At (16-bit modes), and transposes
   LinPlanRef l0f, l0fT;
   bool l0_fact = false;
-  bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_radial_operands)
+  bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_fp32_products)
   int tp_round = 0, sc_round = 0;   // precision study: operand rounding of the edge product / contraction
 };
 
@@ -1155,14 +1155,14 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
   return MACE_OK;
 }
 
-mace_status mace_radial_operands(mace_graph* g, int32_t request, int32_t* in_use) {
+mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use) {
   if (!g) return MACE_EINVAL;
   if (request >= 0) {
-    if (g->prec == MACE_BF16_RADIAL || (request != MACE_RADIAL_FP32 && request != MACE_RADIAL_SPLIT_BF16))
+    if (g->prec == MACE_BF16_RADIAL || (request != MACE_PRODUCTS_FP32 && request != MACE_PRODUCTS_SPLIT_BF16))
       return MACE_EINVAL;
-    g->radial_split = request == MACE_RADIAL_SPLIT_BF16;
+    g->radial_split = request == MACE_PRODUCTS_SPLIT_BF16;
   }
-  if (in_use) *in_use = g->prec == MACE_BF16_RADIAL ? 1 : (g->radial_split ? MACE_RADIAL_SPLIT_BF16 : MACE_RADIAL_FP32);
+  if (in_use) *in_use = g->prec == MACE_BF16_RADIAL ? 1 : (g->radial_split ? MACE_PRODUCTS_SPLIT_BF16 : MACE_PRODUCTS_FP32);
   return MACE_OK;
 }
 

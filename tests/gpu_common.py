@@ -40,7 +40,7 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
                   system.graph_of_atom.astype(np.int32) if system.n_graphs > 1 else None, system.n_graphs, prec)
     form = B.mace_layer0_form(g.handle, -1 if l0_form is None else l0_form)
     if radial is not None:
-        B.mace_radial_operands(g.handle, radial)
+        B.mace_fp32_products(g.handle, radial)
     for blk, fmt in (rounding or {}).items():
         B.mace_block_rounding(g.handle, blk, fmt)
     pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()

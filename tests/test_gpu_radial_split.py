@@ -30,8 +30,8 @@ def test_split_bf16_matches_fp32_and_oracle(K, hl):
     ref = run_oracle(params, sysm, bo)
     # both forms of layer 0, so that layer 0's edge product (P = 4) runs too
     for form in (B.MACE_L0_EDGE, B.MACE_L0_FACTORED):
-        plain = run_gpu(params, sysm, bl, B.MACE_FP32, l0_form=form, radial=B.MACE_RADIAL_FP32)
-        split = run_gpu(params, sysm, bl, B.MACE_FP32, l0_form=form, radial=B.MACE_RADIAL_SPLIT_BF16)
+        plain = run_gpu(params, sysm, bl, B.MACE_FP32, l0_form=form, radial=B.MACE_PRODUCTS_FP32)
+        split = run_gpu(params, sysm, bl, B.MACE_FP32, l0_form=form, radial=B.MACE_PRODUCTS_SPLIT_BF16)
         assert_parity(plain, ref, B.MACE_FP32, f"radial fp32 K={K} hl={hl} form={form}")
         assert_parity(split, ref, B.MACE_FP32, f"radial split-bf16 K={K} hl={hl} form={form}")
         err = errors(split, plain)
@@ -49,14 +49,14 @@ def test_split_bf16_default_and_modes():
     for prec, want in ((B.MACE_FP32, 2), (B.MACE_BF16_LINEAR, 2), (B.MACE_FP16_LINEAR, 2), (B.MACE_BF16_RADIAL, 1)):
         g = MaceGraph(B.make_desc(**params), bl, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
                       sh, sysm.cells, None, 1, prec)
-        assert B.mace_radial_operands(g.handle, -1) == want
+        assert B.mace_fp32_products(g.handle, -1) == want
         if prec == B.MACE_BF16_RADIAL:
             with pytest.raises(B.MaceError):
-                B.mace_radial_operands(g.handle, B.MACE_RADIAL_FP32)
+                B.mace_fp32_products(g.handle, B.MACE_PRODUCTS_FP32)
         g.close()
     # 16-bit-linear mode with the split radial layer against the mode's emulation
     emu = run_oracle(params, sysm, bo, bf16=True)
-    for radial in (B.MACE_RADIAL_FP32, B.MACE_RADIAL_SPLIT_BF16):
+    for radial in (B.MACE_PRODUCTS_FP32, B.MACE_PRODUCTS_SPLIT_BF16):
         g = run_gpu(params, sysm, bl, B.MACE_BF16_LINEAR, l0_form=B.MACE_L0_EDGE, radial=radial)
         err = errors(g, emu)
         print(f"[parity] bf16-linear radial={radial} vs emulation {err}", flush=True)
