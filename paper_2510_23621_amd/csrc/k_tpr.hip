@@ -580,11 +580,11 @@ template <int LHMAX, int RM>
 constexpr bool tpr_bwd_gform() { return LHMAX == 0 || (LHMAX == 1 && RM == 0); }
 
 // RM as in tpr_fwd_kernel (split BF16 for l <= 1 only: at l = 2 the two
-// layouts of the parts do not fit the LDS)
-template <int LHMAX, int RM, int NW = TprShape<LHMAX, true, RM>::waves>
-__global__ void __launch_bounds__(64 * NW)
-__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true, RM>::per_simd, TprShape<LHMAX, true, RM>::per_simd)))
-tpr_bwd_kernel(
+// layouts of the parts do not fit the LDS). This body keeps the forward's lane
+// layout (one channel, four edges per lane); the split-BF16 backward at
+// l_h <= 1 uses tpr_bwd_edge_lanes below.
+template <int LHMAX, int RM, int NW>
+__device__ __forceinline__ void tpr_bwd_channel_lanes(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
@@ -761,6 +761,307 @@ tpr_bwd_kernel(
       }
     }
   }
+}
+
+// ---- Split-BF16 backward at l_h <= 1 in the edge-lane layout.
+//
+// The radial MFMAs take the weight slice as the A operand and a3 as B, so the
+// result puts the edge on l%16: lane l holds R for edge e0 + l%16 and the four
+// channels 16 ct + 4(l/16) .. +3. Each lane then contracts one edge over four
+// channels:
+//   - the Y row and the sender's h rows are the lane's own (float4 loads);
+//   - the couplings come from the receiver's G table in LDS, one float4 over
+//     the four channels per (m1, m2) pair: Dm[m1] += G Y[m2] and
+//     dY[m2] += G (R h[m1]), two multiply-adds per pair and channel in place of
+//     two products and two multiply-adds per coupling coefficient;
+//   - dE/dY is summed over the lane's four channels in registers and over the
+//     four lane groups by two halving exchange steps;
+//   - dR is the A operand of the dE/da3 MFMA as it stands: in K step ks the
+//     reduction index 8(l/16) + i stands for path 2 ks + i/4 and channel
+//     4(l/16) + i%4, and W3's parts sit in LDS in that order, so no transpose
+//     through LDS is needed.
+// LDS: both layouts of the three W3 parts (120 KB at P = 10) and a G table of
+// PairCount x 16 floats per wave (38 KB for eight waves).
+
+// Edge-lane layout of a W3 part for the dE/da3 product:
+// element (((ks 64 + j) 4 + q) 2 + pl) 4 + c of the part is W3[j][p K + 16 ct + 4 q + c]
+// with p = 2 ks + pl, so that lane (l/16 = q, l%16) of K step ks reads its
+// eight reduction values as one 16-byte row.
+__device__ __forceinline__ int el_tr(int ks, int j, int q) { return ((ks * 64 + j) * 4 + q) * 8; }
+
+template <int P>
+__device__ __forceinline__ void load_w3_slices_x3_el(const float* __restrict__ W3, int K, int ct,
+                                                     unsigned short* sWf, unsigned short* sWe) {
+  static_assert(P % 2 == 0, "paths come in pairs per K step");
+  const int PK = P * K;
+  constexpr int part = P * 16 * 64;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    unsigned short x0, x1, x2;
+    split3(W3[(size_t)j * PK + p * K + 16 * ct + kk], x0, x1, x2);
+    const int of = swz_fwd(p * 16 + kk, j >> 3) + (j & 7);
+    const int oe = el_tr(p >> 1, j, kk >> 2) + 4 * (p & 1) + (kk & 3);
+    sWf[of] = x0;
+    sWf[part + of] = x1;
+    sWf[2 * part + of] = x2;
+    sWe[oe] = x0;
+    sWe[part + oe] = x1;
+    sWe[2 * part + oe] = x2;
+  }
+}
+
+// R in the edge-lane layout: r[p][c] = R[e0 + l%16][p][16 ct + 4(l/16) + c]
+// (zero for edges past e_end), split-BF16 products as in tile_radial_x3s with
+// the operands exchanged.
+template <int P>
+__device__ __forceinline__ void tile_radial_x3_el(const float* __restrict__ a3, int e0, int e_end,
+                                                  const unsigned short* __restrict__ sWf, f4* r) {
+  constexpr int part = P * 16 * 64;
+  const int l = threadIdx.x & 63;
+  const int row = e0 + (l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+#pragma unroll
+  for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+    const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+    us8v a0, a1, a2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned short x0, x1, x2;
+      split3(lo[i], x0, x1, x2);
+      a0[i] = x0;
+      a1[i] = x1;
+      a2[i] = x2;
+      split3(hi[i], x0, x1, x2);
+      a0[4 + i] = x0;
+      a1[4 + i] = x1;
+      a2[4 + i] = x2;
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      __builtin_amdgcn_sched_barrier(0);
+      const unsigned short* q = sWf + swz_fwd(p * 16 + (l & 15), 4 * ks + (l >> 4));
+      const us8v b0 = *reinterpret_cast<const us8v*>(q);
+      const us8v b1 = *reinterpret_cast<const us8v*>(q + part);
+      const us8v b2 = *reinterpret_cast<const us8v*>(q + 2 * part);
+      f4 acc = r[p];
+      acc = mfma_bf16(b0, a2, acc);
+      acc = mfma_bf16(b1, a1, acc);
+      acc = mfma_bf16(b2, a0, acc);
+      acc = mfma_bf16(b0, a1, acc);
+      acc = mfma_bf16(b1, a0, acc);
+      r[p] = mfma_bf16(b0, a0, acc);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// dE/da3 partial from dR in the edge-lane layout: d3[jt][rr] = D[e0 + 4(l/16) + rr][16 jt + l%16].
+template <int P>
+__device__ __forceinline__ void tile_da3_x3_el(const f4* r, const unsigned short* __restrict__ sWe, f4* d3) {
+  constexpr int part = P * 16 * 64;
+  const int l = threadIdx.x & 63, g = l >> 4, kk = l & 15;
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+  for (int ks = 0; ks < P / 2; ++ks) {
+    __builtin_amdgcn_sched_barrier(0);
+    us8v a0, a1, a2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      unsigned short x0, x1, x2;
+      split3(r[2 * ks][i], x0, x1, x2);
+      a0[i] = x0;
+      a1[i] = x1;
+      a2[i] = x2;
+      split3(r[2 * ks + 1][i], x0, x1, x2);
+      a0[4 + i] = x0;
+      a1[4 + i] = x1;
+      a2[4 + i] = x2;
+    }
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+      const unsigned short* q = sWe + el_tr(ks, 16 * jt + kk, g);
+      const us8v b0 = *reinterpret_cast<const us8v*>(q);
+      const us8v b1 = *reinterpret_cast<const us8v*>(q + part);
+      const us8v b2 = *reinterpret_cast<const us8v*>(q + 2 * part);
+      f4 acc = d3[jt];
+      acc = mfma_bf16(a2, b0, acc);
+      acc = mfma_bf16(a1, b1, acc);
+      acc = mfma_bf16(a0, b2, acc);
+      acc = mfma_bf16(a1, b0, acc);
+      acc = mfma_bf16(a0, b1, acc);
+      d3[jt] = mfma_bf16(a0, b0, acc);
+    }
+  }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+template <int LHMAX, int RM>
+constexpr bool tpr_bwd_edge_lanes() { return RM == 2 && LHMAX == 1; }
+
+template <int LHMAX, int NW>
+__device__ __forceinline__ void tpr_bwd_edge_lanes_body(
+    int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
+    const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
+    const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
+  constexpr int P = path_count(LHMAX);
+  constexpr int MID = mid_count(LHMAX);
+  constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
+  constexpr int NPAIR = PairCount<LHMAX>::value;
+  constexpr int part = P * 16 * 64;
+  __shared__ __align__(16) unsigned short sWx[6 * part];
+  __shared__ __align__(16) float sG[NW][NPAIR * 16];   // [pair][channel]
+  unsigned short* sWf = sWx;
+  unsigned short* sWe = sWx + 3 * part;
+  const int ct = blockIdx.y;
+  load_w3_slices_x3_el<P>(W3, K, ct, sWf, sWe);
+  __syncthreads();
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int g = l >> 4, kk = l & 15;
+  const int kb = 16 * ct + 4 * g;   // the lane's four channels in the edge loop
+  float* sg = sG[w];
+  float* dYc = dYp + (size_t)ct * E * 16;
+  float* da3c = da3p + (size_t)ct * E * 64;
+  for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
+    const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+    {
+      // G_p of this receiver for channel 16 ct + l%16; the four lane groups
+      // compute the same values and the first one stores
+      float gv[MID];
+#pragma unroll
+      for (int c = 0; c < MID; ++c) gv[c] = dAt[((size_t)i * MID + c) * K + 16 * ct + kk] * inv_c;
+      __builtin_amdgcn_wave_barrier();   // the previous receiver's reads come first
+      for_paths<LHMAX>([&](auto tag) {
+        using T = decltype(tag);
+        using C = mt::CG<T::lh, T::ly, T::lo>;
+        constexpr int goff = PathPairOffset<T::index>::value;
+        float Gp[C::npair];
+#pragma unroll
+        for (int u = 0; u < C::npair; ++u) Gp[u] = 0.f;
+        C::each_p([&](int m1, int m2, int m3, float cg, int pi) { Gp[pi] += cg * gv[T::offset + m3]; });
+        if (g == 0) {
+#pragma unroll
+          for (int u = 0; u < C::npair; ++u) sg[(goff + u) * 16 + kk] = Gp[u];
+        }
+      });
+      __builtin_amdgcn_wave_barrier();
+    }
+    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      __asm__ volatile("" ::: "memory");   // the G table is read per tile, not held in registers
+      const int e_raw = e0 + kk;
+      const bool valid = e_raw < e_end;
+      const int e = min(e_raw, e_end - 1);
+      int src = snd[e];
+      if (src_map) src = src_map[src];
+      f4 hv[DIN];
+#pragma unroll
+      for (int c = 0; c < DIN; ++c) hv[c] = *reinterpret_cast<const f4*>(h + ((size_t)src * DIN + c) * K + kb);
+      float y[16];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const f4 t4 = reinterpret_cast<const f4*>(Y + (size_t)e * 16)[v];
+        y[4 * v] = t4[0];
+        y[4 * v + 1] = t4[1];
+        y[4 * v + 2] = t4[2];
+        y[4 * v + 3] = t4[3];
+      }
+      f4 r[P];   // R on entry; dR (zero for edges past e_end) after the path loop
+      tile_radial_x3_el<P>(a3, e0, e_end, sWf, r);
+      round_tile<P>(r, rnd);
+      float dy[16];
+#pragma unroll
+      for (int m = 0; m < 16; ++m) dy[m] = 0.f;
+      f4 dh[DIN];
+#pragma unroll
+      for (int c = 0; c < DIN; ++c) dh[c] = f4{0.f, 0.f, 0.f, 0.f};
+      for_paths<LHMAX>([&](auto tag) {
+        using T = decltype(tag);
+        constexpr int lh = T::lh, ly = T::ly;
+        const f4 rv = r[T::index];
+        f4 Dm[2 * lh + 1], Rh[2 * lh + 1];
+#pragma unroll
+        for (int m = 0; m < 2 * lh + 1; ++m) {
+          Dm[m] = f4{0.f, 0.f, 0.f, 0.f};
+          Rh[m] = rv * hv[lh * lh + m];
+        }
+        const float* gp = sg + PathPairOffset<T::index>::value * 16 + 4 * g;
+        mt::CG<lh, ly, T::lo>::each_pair([&](int m1, int m2, int pi) {
+          const f4 G = *reinterpret_cast<const f4*>(gp + pi * 16);
+          const float yv = y[ly * ly + m2];
+          Dm[m1] += G * yv;
+          float t = dy[ly * ly + m2];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) t += G[c] * Rh[m1][c];
+          dy[ly * ly + m2] = t;
+        });
+        f4 d = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int m = 0; m < 2 * lh + 1; ++m) {
+          d += hv[lh * lh + m] * Dm[m];
+          dh[lh * lh + m] += rv * Dm[m];
+        }
+        r[T::index] = valid ? d : f4{0.f, 0.f, 0.f, 0.f};
+      });
+      // dE/dY over the tile's 16 channels: halve over lane bit 5 (l/16 >= 2
+      // keeps m2 8..15), then over lane bit 4; lane group q ends with m2 = 4q .. 4q + 3
+      {
+        const bool hi5 = g >= 2;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+          const float send = hi5 ? dy[m] : dy[m + 8];
+          const float keep = hi5 ? dy[m + 8] : dy[m];
+          dy[m] = keep + __shfl_xor(send, 32);
+        }
+        const bool hi4 = g & 1;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const float send = hi4 ? dy[m] : dy[m + 4];
+          const float keep = hi4 ? dy[m + 4] : dy[m];
+          dy[m] = keep + __shfl_xor(send, 16);
+        }
+      }
+      if (valid) {
+        *reinterpret_cast<f4*>(dYc + (size_t)e * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
+        if (Q) {
+#pragma unroll
+          for (int c = 0; c < DIN; ++c) *reinterpret_cast<f4*>(Q + ((size_t)e * DIN + c) * K + kb) = dh[c];
+        }
+      }
+      f4 d3[4];
+      tile_da3_x3_el<P>(r, sWe, d3);
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int ed = e0 + 4 * g + rr;
+        if (ed < e_end) {
+#pragma unroll
+          for (int jt = 0; jt < 4; ++jt) da3c[(size_t)ed * 64 + 16 * jt + kk] = d3[jt][rr];
+        }
+      }
+    }
+  }
+}
+
+template <int LHMAX, int RM, int NW = TprShape<LHMAX, true, RM>::waves>
+__global__ void __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true, RM>::per_simd, TprShape<LHMAX, true, RM>::per_simd)))
+tpr_bwd_kernel(
+    int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
+    const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
+    const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
+  if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
+    tpr_bwd_edge_lanes_body<LHMAX, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
+                                        rnd);
+  else
+    tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
+                                         rnd);
 }
 
 namespace {
