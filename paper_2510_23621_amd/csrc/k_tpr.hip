@@ -171,6 +171,35 @@ __device__ __forceinline__ void split3(float x, unsigned short& b0, unsigned sho
   b2 = __builtin_bit_cast(unsigned short, h2);
 }
 
+// split3 of eight values (lo, hi) into the three MFMA operands of their
+// parts, two values per conversion: v_cvt_pk_bf16_f32 rounds a pair to nearest
+// even and packs it as one operand word (first value in the low half), and the
+// rounded values are unpacked by shifts and masks to form the next remainder.
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef unsigned u4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ unsigned bf16_pack2(f2v x) { return __builtin_bit_cast(unsigned, __builtin_convertvector(x, bf2v)); }
+__device__ __forceinline__ f2v bf16_unpack2(unsigned w) {
+  return f2v{__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xffff0000u)};
+}
+__device__ __forceinline__ void split3_x8(f4 lo, f4 hi, us8v& a0, us8v& a1, us8v& a2) {
+  u4v w0, w1, w2;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const f2v x = h < 2 ? f2v{lo[2 * h], lo[2 * h + 1]} : f2v{hi[2 * h - 4], hi[2 * h - 3]};
+    const unsigned p0 = bf16_pack2(x);
+    const f2v r1 = x - bf16_unpack2(p0);
+    const unsigned p1 = bf16_pack2(r1);
+    const f2v r2 = r1 - bf16_unpack2(p1);
+    w0[h] = p0;
+    w1[h] = p1;
+    w2[h] = bf16_pack2(r2);
+  }
+  a0 = __builtin_bit_cast(us8v, w0);
+  a1 = __builtin_bit_cast(us8v, w1);
+  a2 = __builtin_bit_cast(us8v, w2);
+}
+
 // The three parts of the forward slice, part q at sWx + q P 16 kWbPitch, in the
 // layout of load_w3_slice_bf16.
 template <int P>
@@ -204,18 +233,7 @@ __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int
     __builtin_amdgcn_sched_barrier(0);
     const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
     us8v a0, a1, a2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      unsigned short x0, x1, x2;
-      split3(lo[i], x0, x1, x2);
-      a0[i] = x0;
-      a1[i] = x1;
-      a2[i] = x2;
-      split3(hi[i], x0, x1, x2);
-      a0[4 + i] = x0;
-      a1[4 + i] = x1;
-      a2[4 + i] = x2;
-    }
+    split3_x8(lo, hi, a0, a1, a2);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       __builtin_amdgcn_sched_barrier(0);   // one path's B parts live at a time
@@ -280,18 +298,7 @@ __device__ __forceinline__ void tile_radial_x3s(const float* __restrict__ a3, in
     __builtin_amdgcn_sched_barrier(0);
     const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
     us8v a0, a1, a2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      unsigned short x0, x1, x2;
-      split3(lo[i], x0, x1, x2);
-      a0[i] = x0;
-      a1[i] = x1;
-      a2[i] = x2;
-      split3(hi[i], x0, x1, x2);
-      a0[4 + i] = x0;
-      a1[4 + i] = x1;
-      a2[4 + i] = x2;
-    }
+    split3_x8(lo, hi, a0, a1, a2);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       __builtin_amdgcn_sched_barrier(0);
@@ -336,18 +343,7 @@ __device__ __forceinline__ void tile_da3_x3(const f4* r, const unsigned short* _
     const f4 lo = *reinterpret_cast<const f4*>(src), hi = *reinterpret_cast<const f4*>(src + 4);
     __builtin_amdgcn_wave_barrier();
     us8v a0, a1, a2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      unsigned short x0, x1, x2;
-      split3(lo[i], x0, x1, x2);
-      a0[i] = x0;
-      a1[i] = x1;
-      a2[i] = x2;
-      split3(hi[i], x0, x1, x2);
-      a0[4 + i] = x0;
-      a1[4 + i] = x1;
-      a2[4 + i] = x2;
-    }
+    split3_x8(lo, hi, a0, a1, a2);
     const int p = min(2 * ks + (g >> 1), P - 1);   // a missing odd path reads a valid row; its A is zero
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
@@ -829,18 +825,7 @@ __device__ __forceinline__ void tile_radial_x3_el(const float* __restrict__ a3, 
     __builtin_amdgcn_sched_barrier(0);
     const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
     us8v a0, a1, a2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      unsigned short x0, x1, x2;
-      split3(lo[i], x0, x1, x2);
-      a0[i] = x0;
-      a1[i] = x1;
-      a2[i] = x2;
-      split3(hi[i], x0, x1, x2);
-      a0[4 + i] = x0;
-      a1[4 + i] = x1;
-      a2[4 + i] = x2;
-    }
+    split3_x8(lo, hi, a0, a1, a2);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       __builtin_amdgcn_sched_barrier(0);
@@ -872,18 +857,7 @@ __device__ __forceinline__ void tile_da3_x3_el(const f4* r, const unsigned short
   for (int ks = 0; ks < P / 2; ++ks) {
     __builtin_amdgcn_sched_barrier(0);
     us8v a0, a1, a2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      unsigned short x0, x1, x2;
-      split3(r[2 * ks][i], x0, x1, x2);
-      a0[i] = x0;
-      a1[i] = x1;
-      a2[i] = x2;
-      split3(r[2 * ks + 1][i], x0, x1, x2);
-      a0[4 + i] = x0;
-      a1[4 + i] = x1;
-      a2[4 + i] = x2;
-    }
+    split3_x8(r[2 * ks], r[2 * ks + 1], a0, a1, a2);
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
       const unsigned short* q = sWe + el_tr(ks, 16 * jt + kk, g);
