@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 // dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
 // to instead of overwritten.
 template <int NBP, int NPART>
-__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                          const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
@@ -203,10 +203,6 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   hidden_mma<kH>(ta, kPad, bn, tb, z1);
   __syncthreads();
   hidden_mma<kH>(tb, kPad, bc, ta, z2);   // (a3 itself is not needed)
-  // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
-  float b2[kH / 4];
-#pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
   __syncthreads();   // every wave is done with ta (a3)
   // the partials summed in part order, as float4 rows into ta
   for (int idx = tid; idx < kTE * kH / 4; idx += blockDim.x) {
@@ -218,6 +214,11 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
     if (e0 + row >= E) v = f4{0.f, 0.f, 0.f, 0.f};
     *reinterpret_cast<f4*>(ta + row * kPad + 4 * c4) = v;
   }
+  // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
+  // (requested after the partials, which need the registers more)
+  float b2[kH / 4];
+#pragma unroll
+  for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
   __syncthreads();
   // dz2 = da3 silu'(z2), in place (result layout)
 #pragma unroll
