@@ -72,7 +72,7 @@ __device__ __forceinline__ void load_b_frag(const float* __restrict__ W, int nin
   }
 }
 
-template <int NIN_PAD>
+template <int NIN_PAD, bool STORE = true>
 __device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldin, const float* b,
                                            float* __restrict__ out, f4* z) {
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -89,8 +89,10 @@ __device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldi
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) {
     z[rt] = acc[rt];
+    if constexpr (STORE) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(acc[rt][r]);
+      for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(acc[rt][r]);
+    }
   }
 }
 
@@ -174,7 +176,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 // dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
 // to instead of overwritten.
 template <int NBP, int NPART>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                          const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
@@ -190,6 +192,37 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))
   const int tid = threadIdx.x;
   const int l = tid & 63, w = tid >> 6;
   const int col = 16 * w + (l & 15);
+  // The partial sums of dE/da3 (thread t holds rows (t + 256 s) / 16, s = 0..3,
+  // float4 column (t % 16), summed in part order) and of dE/dY (written out
+  // here). Even blocks take them before the forward recompute and odd blocks
+  // after it, so that the blocks that start together on a CU are not all in
+  // their memory phase, or all in their MFMA phase, at the same time.
+  f4 pacc[4];
+  auto sum_partials = [&]() {
+#pragma unroll
+    for (int sr = 0; sr < 4; ++sr) {
+      const int idx = tid + 256 * sr;
+      const int row = idx >> 4, c4 = idx & 15;
+      const int e = min(e0 + row, E - 1);
+      f4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(da3p + ((size_t)q * E + e) * kH + 4 * c4);
+      pacc[sr] = e0 + row < E ? v : f4{0.f, 0.f, 0.f, 0.f};
+      __builtin_amdgcn_sched_barrier(0);   // one row's loads in flight at a time
+    }
+    {
+      const int e = e0 + (tid >> 2), c4 = tid & 3;
+      if (e < E) {
+        f4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(dYp + ((size_t)q * E + e) * 16 + 4 * c4);
+        f4* o = reinterpret_cast<f4*>(dY + (size_t)e * 16 + 4 * c4);
+        *o = accumulate ? *o + v : v;
+      }
+    }
+  };
+  const bool parts_first = (blockIdx.x & 1) == 0;
+  if (parts_first) sum_partials();
   // forward fragments, then the hidden layers again
   float bc[kH / 4], bn[kH / 4];
   load_b_frag<NBP>(W0, nb, bc);
@@ -201,21 +234,21 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))
   __syncthreads();
   load_b_frag<kH>(W2, kH, bc);
   hidden_mma<kH>(ta, kPad, bn, tb, z1);
-  __syncthreads();
-  hidden_mma<kH>(tb, kPad, bc, ta, z2);   // (a3 itself is not needed)
-  __syncthreads();   // every wave is done with ta (a3)
-  // the partials summed in part order, as float4 rows into ta
-  for (int idx = tid; idx < kTE * kH / 4; idx += blockDim.x) {
-    const int row = idx >> 4, c4 = idx & 15;
-    const int e = min(e0 + row, E - 1);
-    f4 v = {0.f, 0.f, 0.f, 0.f};
+  __syncthreads();   // every wave is done with ta
+  auto store_partials = [&]() {
 #pragma unroll
-    for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(da3p + ((size_t)q * E + e) * kH + 4 * c4);
-    if (e0 + row >= E) v = f4{0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<f4*>(ta + row * kPad + 4 * c4) = v;
+    for (int sr = 0; sr < 4; ++sr) {
+      const int idx = tid + 256 * sr;
+      *reinterpret_cast<f4*>(ta + (idx >> 4) * kPad + 4 * (idx & 15)) = pacc[sr];
+    }
+  };
+  if (parts_first) store_partials();
+  hidden_mma<kH, false>(tb, kPad, bc, nullptr, z2);   // z2 only (a3 itself is not needed)
+  if (!parts_first) {
+    sum_partials();
+    store_partials();
   }
   // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
-  // (requested after the partials, which need the registers more)
   float b2[kH / 4];
 #pragma unroll
   for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
@@ -274,15 +307,6 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4))
         de[o] = accumulate ? de[o] + d[r] : d[r];
       }
     }
-  }
-  for (int idx = tid; idx < kTE * 4; idx += blockDim.x) {
-    const int e = e0 + (idx >> 2), c4 = idx & 3;
-    if (e >= E) continue;
-    f4 v = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(dYp + ((size_t)q * E + e) * 16 + 4 * c4);
-    f4* o = reinterpret_cast<f4*>(dY + (size_t)e * 16 + 4 * c4);
-    *o = accumulate ? *o + v : v;
   }
 }
 
