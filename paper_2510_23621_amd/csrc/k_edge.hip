@@ -14,7 +14,7 @@ __global__ void __launch_bounds__(256) edge_vjp_kernel(int E, const float* __res
                                                        float4* __restrict__ g) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= E) return;
-  float dyv[16], dev[16];
+  float dyv[16];
   const float4* dYv = reinterpret_cast<const float4*>(dY + (size_t)e * 16);
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
@@ -24,8 +24,7 @@ __global__ void __launch_bounds__(256) edge_vjp_kernel(int E, const float* __res
     dyv[4 * v + 2] = x.z;
     dyv[4 * v + 3] = x.w;
   }
-  for (int n = 0; n < nb; ++n) dev[n] = de[(size_t)e * nb + n];
-  g[e] = edge_geometry_vjp(e, pos, snd, rcv, shift, rc, p, nb, dyv, dev);
+  g[e] = edge_geometry_vjp(e, pos, snd, rcv, shift, rc, p, nb, dyv, de + (size_t)e * nb);
 }
 
 // One wave per atom: lanes take the atom's receiver edges and sender edges

@@ -229,13 +229,24 @@ __device__ __forceinline__ float4 edge_geometry_vjp(int e, const float* __restri
     gy += (double)dy[m] * y[m].y;
     gz += (double)dy[m] * y[m].z;
   }
-  D3 eb[16];
-  bessel_env<D3>(rr, rc, p, nb, eb);
+  // radial basis: the terms of bessel_env, each added as it is formed (no
+  // array indexed by the run-time basis size, which would live in scratch)
+  const D3 xr = rr * (1.0 / rc);
+  D3 q = D3(0.5 * p * (p + 1));
+  for (int j = p - 2; j >= 0; --j) q = q * xr + 0.5 * (j + 1) * (j + 2);
+  const D3 om = D3(1.0) - xr;
+  D3 env = (om * om) * (om * q);
+  if (!lt(xr, 1.0)) env = D3(0.0);
+  const D3 pre = (sqrt(2.0 / rc) * env) / rr;
+  const double pi = 3.14159265358979323846;
   for (int n = 0; n < nb; ++n) {
+    D3 sn, cn;
+    dsincos(rr * ((n + 1) * pi / rc), &sn, &cn);
+    const D3 en = pre * sn;
     const double w = de[n];
-    gx += w * eb[n].x;
-    gy += w * eb[n].y;
-    gz += w * eb[n].z;
+    gx += w * en.x;
+    gy += w * en.y;
+    gz += w * en.z;
   }
   return make_float4((float)gx, (float)gy, (float)gz, 0.f);
 }
