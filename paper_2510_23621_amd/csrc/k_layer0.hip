@@ -28,7 +28,8 @@ namespace mace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kL0Edges = 8;   // edges whose loads are issued together (gather)
+constexpr int kL0Edges = 16;     // edges whose loads are issued together (gather)
+constexpr int kL0BwdEdges = 4;   // edges per wave and iteration (backward), loads issued together
 
 // Wave w gathers components 4w .. 4w + 3 of U over every edge of the receiver.
 template <int S, bool RB>
@@ -57,11 +58,11 @@ __global__ void __launch_bounds__(256) l0_gather_kernel(int N, const int* __rest
     }
 #pragma unroll
     for (int q = 0; q < kL0Edges; ++q) {
-      if (e0 + q >= e_end) break;
-      const float av = RB ? bf16_round(a[q]) : a[q];
+      const float av = e0 + q < e_end ? (RB ? bf16_round(a[q]) : a[q]) : 0.f;   // past e_end: adds zero
+      const int zq = e0 + q < e_end ? z[q] : -1;
 #pragma unroll
       for (int s = 0; s < S; ++s)
-        if (z[q] == s) {
+        if (zq == s) {
 #pragma unroll
           for (int c = 0; c < 4; ++c) acc[s][c] += av * y[q][c];
         }
@@ -92,13 +93,13 @@ __global__ void __launch_bounds__(256) l0_edge_bwd_kernel(int N, const int* __re
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int c = 0; c < 16; ++c) g[s][c] = gU[((size_t)i * 16 + c) * KI + 64 * s + lane];
-  // two edges per iteration (e and e + 4), their loads issued together
-  for (int e = e_beg + w; e < e_end; e += 8) {
-    int ee[2], z[2];
-    float a[2], y[2][16];
+  // kL0BwdEdges edges per iteration (e, e + 4, ...), their loads issued together
+  for (int e = e_beg + w; e < e_end; e += 4 * kL0BwdEdges) {
+    int ee[kL0BwdEdges], z[kL0BwdEdges];
+    float a[kL0BwdEdges], y[kL0BwdEdges][16];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      ee[q] = min(e + 4 * q, e_end - 1);   // a missing second edge repeats the first and stores nothing
+    for (int q = 0; q < kL0BwdEdges; ++q) {
+      ee[q] = min(e + 4 * q, e_end - 1);   // a missing edge repeats the last one and stores nothing
       z[q] = snd_z[ee[q]];
       a[q] = a3[(size_t)ee[q] * 64 + lane];
 #pragma unroll
@@ -111,8 +112,8 @@ __global__ void __launch_bounds__(256) l0_edge_bwd_kernel(int N, const int* __re
       }
     }
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      if (q == 1 && e + 4 >= e_end) break;
+    for (int q = 0; q < kL0BwdEdges; ++q) {
+      if (e + 4 * q >= e_end) break;
       const float av = RB ? bf16_round(a[q]) : a[q];
       float gs[16];
 #pragma unroll
