@@ -691,18 +691,19 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p,
                      h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0), h->tp_round);
     }
+    // The edge backward wrote Q and the partials (about 390 MB at K = 128,
+    // more than the last-level cache holds); the sender sum reads Q first
+    // (measured faster than the radial backward first).
+    if (t > 0) {
+      PROF(KID_SENDER_SUM);
+      launch_sender_sum(s, N, L.din, K, b.snd_off, b.snd_perm, b.Q, b.dht);
+    }
     {
-      // right after the partials are written, while they are still in the
-      // last-level cache
       PROF(KID_RADIAL_BWD);
       launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, n_part,
                         b.dY, b.de, t < T - 1);
     }
     if (t > 0) {
-      {
-        PROF(KID_SENDER_SUM);
-        launch_sender_sum(s, N, L.din, K, b.snd_off, b.snd_perm, b.Q, b.dht);
-      }
       {
         run_linear(h, s, h->upskipT[t], largs(h, b.dht, dprev, nullptr, true, 0, dnext));
       }
