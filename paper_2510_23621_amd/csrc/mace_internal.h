@@ -187,7 +187,10 @@ __host__ __device__ __forceinline__ void sh16(T x, T y, T z, T* Y) {
 //   u(x) = 1 - (p+1)(p+2)/2 x^p + p(p+2) x^(p+1) - p(p+1)/2 x^(p+2), x < 1,
 // evaluated as u(x) = (1-x)^3 sum_{j<p} (j+1)(j+2)/2 x^j (the same polynomial,
 // free of the cancellation the expanded form suffers near the cutoff), and
-// every sin(n theta) evaluated directly.
+// sin(n theta) from one sine and cosine of theta = pi r / rc by the three-term
+// recurrence sin((n+1) theta) = 2 cos(theta) sin(n theta) - sin((n-1) theta)
+// (in FP64 within 1.1e-14 of the direct values for n <= 16, theta in (0, pi);
+// on dual numbers it carries the derivatives with it).
 template <class T>
 __host__ __device__ __forceinline__ void bessel_env(T r, double rc, int p, int nb, T* e) {
   using S = typename ScalarOf<T>::type;
@@ -199,10 +202,15 @@ __host__ __device__ __forceinline__ void bessel_env(T r, double rc, int p, int n
   T env = (om * om) * (om * q);
   if (!lt(xr, 1.0)) env = T(S(0));
   T pre = (S(sqrt(2.0 / rc)) * env) / r;
+  T s1, c1;
+  dsincos(r * S(pi / rc), &s1, &c1);
+  const T c2 = S(2) * c1;
+  T sp = T(S(0)), sn = s1;   // sin((n-1) theta), sin(n theta) for n = 1
   for (int n = 0; n < nb; ++n) {
-    T s, c;
-    dsincos(r * S((n + 1) * pi / rc), &s, &c);
-    e[n] = pre * s;
+    e[n] = pre * sn;
+    const T nx = c2 * sn - sp;
+    sp = sn;
+    sn = nx;
   }
 }
 
@@ -239,14 +247,19 @@ __device__ __forceinline__ float4 edge_geometry_vjp(int e, const float* __restri
   if (!lt(xr, 1.0)) env = D3(0.0);
   const D3 pre = (sqrt(2.0 / rc) * env) / rr;
   const double pi = 3.14159265358979323846;
+  D3 s1, c1;
+  dsincos(rr * (pi / rc), &s1, &c1);
+  const D3 c2 = 2.0 * c1;
+  D3 sp = D3(0.0), sn = s1;   // the recurrence of bessel_env
   for (int n = 0; n < nb; ++n) {
-    D3 sn, cn;
-    dsincos(rr * ((n + 1) * pi / rc), &sn, &cn);
     const D3 en = pre * sn;
     const double w = de[n];
     gx += w * en.x;
     gy += w * en.y;
     gz += w * en.z;
+    const D3 nx = c2 * sn - sp;
+    sp = sn;
+    sn = nx;
   }
   return make_float4((float)gx, (float)gy, (float)gz, 0.f);
 }
