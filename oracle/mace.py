@@ -175,16 +175,20 @@ def silu(x):
     return x * torch.sigmoid(x)
 
 
-def radial_mlp(e: torch.Tensor, W: dict, t: int, n_hidden: int, bf16_last: bool = False) -> torch.Tensor:
+def radial_mlp(e: torch.Tensor, W: dict, t: int, n_hidden: int, bf16_last: bool = False,
+               rnd=None) -> torch.Tensor:
     """Reading R5: e @ W0 -> SiLU -> ... -> @ W_last (with bf16_last, the last
-    product takes bfloat16-rounded inputs and weights, R13)."""
+    product takes bfloat16-rounded inputs and weights, R13). rnd (a rounding
+    from _rounding: the per-block precision study's radial-MLP block) rounds
+    the input and the weights of every layer, the basis e included."""
+    r = rnd if rnd is not None else (lambda x: x)
     h = e
     for i in range(n_hidden):
-        h = silu(h @ W[f"{t}.radial.{i}"])
+        h = silu(r(h) @ r(W[f"{t}.radial.{i}"]))
     Wl = W[f"{t}.radial.{n_hidden}"]
     if bf16_last:
-        return _round_bf16(h) @ _round_bf16(Wl)
-    return h @ Wl
+        return _round_bf16(r(h)) @ _round_bf16(r(Wl))
+    return r(h) @ r(Wl)
 
 
 # --------------------------------------------------------------------------
@@ -296,15 +300,16 @@ def build_graph(system, d: ModelDesc) -> Graph:
 def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
                   bf16_linear: bool = False, edge_chunk: int = 1 << 16,
                   return_intermediates: bool = False, fp16_linear: bool = False, bf16_radial: bool = False,
-                  tp_round=None, symcon_round=None):
+                  tp_round=None, symcon_round=None, radial_round=None):
     """Per-atom energies eps_i [N] for positions pos [N,3] (float64).
 
-    tp_round / symcon_round ("bf16", "fp16" or None) round the operands of
-    one block for the per-block precision study: the edge product's sender
-    features, harmonics and radial weights (not the CG constants), or the
-    symmetric contraction's A and weights (not U)."""
+    tp_round / symcon_round / radial_round ("bf16", "fp16" or None) round the
+    operands of one block for the per-block precision study: the edge
+    product's sender features, harmonics and radial weights (not the CG
+    constants), the symmetric contraction's A and weights (not U), or every
+    radial-MLP layer's input and weights."""
     lin = _Lin(bf16_linear, fp16_linear)
-    rtp, rsc = _rounding(tp_round), _rounding(symcon_round)
+    rtp, rsc, rrad = _rounding(tp_round), _rounding(symcon_round), _rounding(radial_round)
     z = graph.species
     N = pos.shape[0]
     K = d.K
@@ -333,7 +338,7 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
         At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
         for e0 in range(0, E, edge_chunk):
             sl = slice(e0, e0 + edge_chunk)
-            R = rtp(radial_mlp(rb[sl], W, t, nh, bf16_radial).reshape(-1, len(paths), K))  # [e,P,K]
+            R = rtp(radial_mlp(rb[sl], W, t, nh, bf16_radial, rnd=rrad).reshape(-1, len(paths), K))  # [e,P,K]
             for p, (lh, ly, lo) in enumerate(paths):
                 C = torch.from_numpy(so3.real_cg(lh, ly, lo))
                 hs = rtp(ht[lh][snd[sl]])                                 # [e, 2lh+1, K]
@@ -378,14 +383,15 @@ def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
 
 def energy_forces(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
                   bf16_linear: bool = False, forces: bool = True, fp16_linear: bool = False,
-                  bf16_radial: bool = False, tp_round=None, symcon_round=None):
+                  bf16_radial: bool = False, tp_round=None, symcon_round=None, radial_round=None):
     """Returns dict(eps [N], energy [G], forces [N,3] or None, graph)."""
     W = unpack_weights(d, blob)
     if graph is None:
         graph = build_graph(system, d)
     pos = torch.tensor(system.positions, dtype=DT, requires_grad=forces)
     eps = node_energies(d, W, graph, pos, bf16_linear=bf16_linear, fp16_linear=fp16_linear,
-                        bf16_radial=bf16_radial, tp_round=tp_round, symcon_round=symcon_round)
+                        bf16_radial=bf16_radial, tp_round=tp_round, symcon_round=symcon_round,
+                        radial_round=radial_round)
     Eg = graph_energies(eps, graph)
     F = None
     if forces:

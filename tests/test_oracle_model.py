@@ -557,15 +557,40 @@ def test_symmetric_contraction_rounding_rounds_a_and_weights(fmt):
         np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
 
 
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_radial_mlp_rounding_rounds_every_layers_input_and_weights(fmt):
+    """The radial-MLP rounding of the precision study rounds the input of
+    every layer (the basis, then each SiLU output) and every layer's weights:
+    a numpy MLP on independently rounded operands; leaving out any one of
+    those roundings gives a different result."""
+    d = _desc(0)
+    W = mace.unpack_weights(d, synth.weight_blob(mace.weight_layout(d), 2))
+    rng = np.random.default_rng(7)
+    e = rng.uniform(-0.5, 1.5, (40, d.n_bessel))
+    t, nh = 0, len(d.radial_hidden)
+    got = mace.radial_mlp(torch.from_numpy(e), W, t, nh, rnd=mace._rounding(fmt)).numpy()
+
+    def np_mlp(skip=None):
+        r = lambda x, tag: x if tag == skip else _np_round16(x, fmt)  # noqa: E731
+        h = e
+        for i in range(nh + 1):
+            z = r(h, ("in", i)) @ r(W[f"{t}.radial.{i}"].numpy(), ("w", i))
+            h = z / (1.0 + np.exp(-z)) if i < nh else z
+        return h
+    np.testing.assert_allclose(got, np_mlp(), rtol=1e-12, atol=1e-13)
+    for skip in [("in", i) for i in range(nh + 1)] + [("w", i) for i in range(nh + 1)]:
+        assert not np.allclose(got, np_mlp(skip), rtol=1e-9, atol=0), skip
+
+
 def test_block_rounding_moves_the_result_by_about_the_format_precision():
-    """Rounding the edge product's or the contraction's operands moves
+    """Rounding the edge product's, the contraction's or the radial MLP's operands moves
     energies and forces away from FP64 by about the format's precision:
     binary16 (11 significant bits) less than bfloat16 (8)."""
     d = _desc(0)
     blob = synth.weight_blob(mace.weight_layout(d), 4)
     system = make_system(0, seed=0)
     ref = mace.energy_forces(d, blob, system)
-    for key in ("tp_round", "symcon_round"):
+    for key in ("tp_round", "symcon_round", "radial_round"):
         dev = {}
         for fmt in ("bf16", "fp16"):
             out = mace.energy_forces(d, blob, system, graph=ref["graph"], **{key: fmt})
