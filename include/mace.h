@@ -203,13 +203,20 @@ mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use);
  *     the first layer then runs in per-edge form (its factorised form never
  *     forms R);
  *   block MACE_BLOCK_SYMMETRIC_CONTRACTION: A and the contraction weights (the
- *     coupling constants stay FP32).
+ *     coupling constants stay FP32);
+ *   block MACE_BLOCK_RADIAL_MLP: the input and the weights of every layer of
+ *     the radial MLP (the radial basis, each SiLU output, W0..W3); the first
+ *     layer then runs in per-edge form.
  *   format 0 none (the default), 1 bfloat16, 2 IEEE binary16 (magnitudes
  *     beyond 65504 become infinite); format < 0 only queries.
  * Gradients pass through the rounding unchanged.  *in_use (host, may be
  * NULL) receives the setting.  Takes effect for calls enqueued after it
  * returns; no device work. */
-typedef enum { MACE_BLOCK_EDGE_PRODUCT = 0, MACE_BLOCK_SYMMETRIC_CONTRACTION = 1 } mace_block;
+typedef enum {
+  MACE_BLOCK_EDGE_PRODUCT = 0,
+  MACE_BLOCK_SYMMETRIC_CONTRACTION = 1,
+  MACE_BLOCK_RADIAL_MLP = 2
+} mace_block;
 mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, int32_t* in_use);
 
 /* Device-detected errors of the calls enqueued since setup or the previous

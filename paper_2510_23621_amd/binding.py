@@ -26,6 +26,7 @@ MACE_PRODUCTS_FP32 = 0
 MACE_PRODUCTS_SPLIT_BF16 = 2
 MACE_BLOCK_EDGE_PRODUCT = 0
 MACE_BLOCK_SYMMETRIC_CONTRACTION = 1
+MACE_BLOCK_RADIAL_MLP = 2
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 

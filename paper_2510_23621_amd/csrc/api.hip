@@ -161,6 +161,7 @@ struct Carver {
 
 struct Buffers {
   float *w = nullptr, *wT = nullptr, *sp_table = nullptr, *sp_round = nullptr;   // (rounded copy: precision study)
+  float* w_round = nullptr;   // precision study: rounded copies of the last radial layers' weights
   unsigned short *wbf = nullptr, *wbfT = nullptr;   // 16-bit K-packed copies (BF16- / FP16-linear modes)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
       *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
@@ -193,6 +194,7 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.wbfT = c.take<unsigned short>(m.total);
   b.sp_table = c.take<float>(S * K);
   b.sp_round = c.take<float>(S * K);
+  b.w_round = c.take<float>(m.total_ext);
   b.species = c.take<int>(N);
   b.snd = c.take<int>(std::max<int64_t>(E, 1));
   b.rcv = c.take<int>(std::max<int64_t>(E, 1));
@@ -287,7 +289,8 @@ struct mace_graph {
   LinPlanRef l0f, l0fT;
   bool l0_fact = false;
   bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_fp32_products)
-  int tp_round = 0, sc_round = 0;   // precision study: operand rounding of the edge product / contraction
+  // precision study: operand rounding of the edge product / contraction / radial MLP
+  int tp_round = 0, sc_round = 0, rad_round = 0;
 };
 
 namespace {
@@ -541,6 +544,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
     for (int t0 = 0; t0 < m.d.n_layers; t0 += kMaxRadialLayers) {
       RadialSet rs;
       rs.n = std::min(kMaxRadialLayers, m.d.n_layers - t0);
+      rs.rnd = h->rad_round;
       for (int q = 0; q < rs.n; ++q) {
         rs.W[q] = b.w + m.off.at(std::to_string(t0 + q) + ".radial.0");
         rs.a3[q] = b.a3[t0 + q];
@@ -550,6 +554,14 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
                            rs, b.status);
     }
   }
+  if (h->rad_round) {
+    // precision study: the last radial layer (inside the edge products) reads rounded weights
+    for (int t = 0; t < m.d.n_layers; ++t) {
+      const int64_t o = m.off.at(std::to_string(t) + ".radial.3");
+      launch_round(s, b.w_round + o, b.w + o, (size_t)64 * m.layers[t].P * K, h->rad_round);
+    }
+  }
+  const float* wr3 = h->rad_round ? b.w_round : b.w;
   if (h->tp_round) {
     // precision study: the edge products read rounded harmonics and sender features
     launch_round(s, b.Y, b.Y, (size_t)E * 16, h->tp_round);
@@ -559,7 +571,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
   for (int t = 0; t < m.d.n_layers; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
-    if (t == 0 && h->l0_fact && !h->tp_round) {
+    if (t == 0 && h->l0_fact && !h->tp_round && !h->rad_round) {
       // factorised first layer: U per receiver, then one contraction (FP32
       // mode: straight to A; 16-bit modes: to At, then their own linears)
       {
@@ -586,7 +598,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       }
       {
         PROF(KID_TP_FWD);
-        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
+        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], wr3 + m.off.at(pre + "radial.3"),
                        b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0),
                        h->tp_round);
       }
@@ -660,7 +672,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA, h->sc_round);
     }
-    const bool fact = t == 0 && h->l0_fact && !h->tp_round;
+    const bool fact = t == 0 && h->l0_fact && !h->tp_round && !h->rad_round;
     // dE/dAt (the transposes of the linears after the edge product); the
     // factorised first layer ends in dE/dU instead
     const float* dApre = b.dA;
@@ -687,7 +699,8 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       const float* src = t == 0 ? (h->tp_round ? b.sp_round : b.sp_table) : b.ht[t];
       const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
-      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t], b.w + m.off.at(pre + "radial.3"),
+      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t],
+                     (h->rad_round ? b.w_round : b.w) + m.off.at(pre + "radial.3"),
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p,
                      h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0), h->tp_round);
     }
@@ -701,7 +714,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     {
       PROF(KID_RADIAL_BWD);
       launch_radial_bwd(s, E, b.rbf, m.d.n_bessel, b.w + m.off.at(pre + "radial.0"), b.da3p, b.dYp, n_part,
-                        b.dY, b.de, t < T - 1);
+                        b.dY, b.de, t < T - 1, h->rad_round);
     }
     if (t > 0) {
       {
@@ -1168,9 +1181,11 @@ mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use) 
 }
 
 mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, int32_t* in_use) {
-  if (!g || (block != MACE_BLOCK_EDGE_PRODUCT && block != MACE_BLOCK_SYMMETRIC_CONTRACTION) || format > 2)
+  if (!g || (block != MACE_BLOCK_EDGE_PRODUCT && block != MACE_BLOCK_SYMMETRIC_CONTRACTION &&
+             block != MACE_BLOCK_RADIAL_MLP) || format > 2)
     return MACE_EINVAL;
-  int& r = block == MACE_BLOCK_EDGE_PRODUCT ? g->tp_round : g->sc_round;
+  int& r = block == MACE_BLOCK_EDGE_PRODUCT ? g->tp_round
+                                            : (block == MACE_BLOCK_SYMMETRIC_CONTRACTION ? g->sc_round : g->rad_round);
   if (format >= 0) r = format;
   if (in_use) *in_use = r;
   return MACE_OK;

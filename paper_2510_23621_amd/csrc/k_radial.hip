@@ -61,20 +61,21 @@ __device__ __forceinline__ void hidden_layer(const float* __restrict__ in, int l
 
 // The two halves of hidden_layer, so that the next layer's B fragments can
 // be in flight while the current layer's MFMAs run.
-template <int NIN_PAD>
-__device__ __forceinline__ void load_b_frag(const float* __restrict__ W, int nin, float* b) {
+template <int NIN_PAD, bool RND = false>
+__device__ __forceinline__ void load_b_frag(const float* __restrict__ W, int nin, float* b, int rnd = 0) {
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = 16 * w + (l & 15);
 #pragma unroll
   for (int ks = 0; ks < NIN_PAD / 4; ++ks) {
     const int k = 4 * ks + (l >> 4);
     b[ks] = (k < nin) ? W[k * kH + col] : 0.f;
+    if constexpr (RND) b[ks] = lowp_round(b[ks], rnd);
   }
 }
 
-template <int NIN_PAD, bool STORE = true>
+template <int NIN_PAD, bool STORE = true, bool RND = false>
 __device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldin, const float* b,
-                                           float* __restrict__ out, f4* z) {
+                                           float* __restrict__ out, f4* z, int rnd = 0) {
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = 16 * w + (l & 15);
   f4 acc[4];
@@ -91,24 +92,31 @@ __device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldi
     z[rt] = acc[rt];
     if constexpr (STORE) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(acc[rt][r]);
+      for (int r = 0; r < 4; ++r) {
+        const float a = silu(acc[rt][r]);
+        out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = RND ? lowp_round(a, rnd) : a;
+      }
     }
   }
 }
 
+template <bool RND = false>
 __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __restrict__ rbf, int nb, int nb_pad,
-                                                float* xs) {
+                                                float* xs, int rnd = 0) {
   for (int idx = threadIdx.x; idx < kTE * kXPad; idx += blockDim.x) {
     int e = idx / kXPad, i = idx % kXPad;
-    xs[idx] = (e0 + e < E && i < nb) ? rbf[(size_t)(e0 + e) * nb + i] : 0.f;
+    const float v = (e0 + e < E && i < nb) ? rbf[(size_t)(e0 + e) * nb + i] : 0.f;
+    xs[idx] = RND ? lowp_round(v, rnd) : v;
   }
 }
 
 // Edge prologue for a 64-edge tile: geometry of every edge (Y and the radial
 // basis e, written out; the first wave computes one edge per lane in FP64),
 // then the hidden layers a3 = SiLU(SiLU(SiLU(e W0) W1) W2) of the radial MLP
-// of every interaction layer in rs, all from the same e.
-template <int NBP>
+// of every interaction layer in rs, all from the same e. RND: the precision
+// study's rounding of every layer's input and weights (rs.rnd: 1 bfloat16,
+// 2 binary16); the basis is written out unrounded.
+template <int NBP, bool RND>
 __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* __restrict__ pos,
                                                             const int* __restrict__ snd, const int* __restrict__ rcv,
                                                             const double4* __restrict__ shift, double rc, int p,
@@ -121,7 +129,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
   // B fragments: bc for the layer being computed, bn for the next one (in
   // flight meanwhile); the first is requested before the geometry
   float bc[kH / 4], bn[kH / 4];
-  load_b_frag<NBP>(rs.W[0], nb, bc);
+  load_b_frag<NBP, RND>(rs.W[0], nb, bc, rs.rnd);
   if (threadIdx.x < kTE) {
     const int e = e0 + threadIdx.x;
     float row[kXPad];
@@ -137,7 +145,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
       for (int n = 0; n < nb; ++n) rbf[(size_t)e * nb + n] = row[n];
     }
 #pragma unroll
-    for (int i = 0; i < kXPad; ++i) xs[threadIdx.x * kXPad + i] = row[i];
+    for (int i = 0; i < kXPad; ++i) xs[threadIdx.x * kXPad + i] = RND ? lowp_round(row[i], rs.rnd) : row[i];
   }
   __syncthreads();
   for (int t = 0; t < rs.n; ++t) {
@@ -145,14 +153,14 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
     const float* W1 = W0 + nb * kH;
     const float* W2 = W1 + kH * kH;
     f4 z[4];
-    load_b_frag<kH>(W1, kH, bn);
-    hidden_mma<NBP>(xs, kXPad, bc, ha, z);
+    load_b_frag<kH, RND>(W1, kH, bn, rs.rnd);
+    hidden_mma<NBP, true, RND>(xs, kXPad, bc, ha, z, rs.rnd);
     __syncthreads();
-    load_b_frag<kH>(W2, kH, bc);
-    hidden_mma<kH>(ha, kPad, bn, hb, z);
+    load_b_frag<kH, RND>(W2, kH, bc, rs.rnd);
+    hidden_mma<kH, true, RND>(ha, kPad, bn, hb, z, rs.rnd);
     __syncthreads();
-    if (t + 1 < rs.n) load_b_frag<NBP>(rs.W[t + 1], nb, bn);
-    hidden_mma<kH>(hb, kPad, bc, ha, z);
+    if (t + 1 < rs.n) load_b_frag<NBP, RND>(rs.W[t + 1], nb, bn, rs.rnd);
+    hidden_mma<kH, true, RND>(hb, kPad, bc, ha, z, rs.rnd);
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
@@ -175,13 +183,13 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 // dz0 = (dz1 W1^T) silu'(z0), de = dz0 W0^T. The same pass folds the partials
 // dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
 // to instead of overwritten.
-template <int NBP, int NPART>
+template <int NBP, int NPART, bool RND>
 __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                          const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
                                                          float* __restrict__ dY, float* __restrict__ de,
-                                                         int accumulate) {
+                                                         int accumulate, int rnd) {
   __shared__ float xs[kTE * kXPad];
   __shared__ float ta[kTE * kPad];
   __shared__ float tb[kTE * kPad];
@@ -225,15 +233,15 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   if (parts_first) sum_partials();
   // forward fragments, then the hidden layers again
   float bc[kH / 4], bn[kH / 4];
-  load_b_frag<NBP>(W0, nb, bc);
-  load_basis_tile(E, e0, rbf, nb, (nb + 3) & ~3, xs);
+  load_b_frag<NBP, RND>(W0, nb, bc, rnd);
+  load_basis_tile<RND>(E, e0, rbf, nb, (nb + 3) & ~3, xs, rnd);
   __syncthreads();
   f4 z0[4], z1[4], z2[4];
-  load_b_frag<kH>(W1, kH, bn);
-  hidden_mma<NBP>(xs, kXPad, bc, ta, z0);
+  load_b_frag<kH, RND>(W1, kH, bn, rnd);
+  hidden_mma<NBP, true, RND>(xs, kXPad, bc, ta, z0, rnd);
   __syncthreads();
-  load_b_frag<kH>(W2, kH, bc);
-  hidden_mma<kH>(ta, kPad, bn, tb, z1);
+  load_b_frag<kH, RND>(W2, kH, bc, rnd);
+  hidden_mma<kH, true, RND>(ta, kPad, bn, tb, z1, rnd);
   __syncthreads();   // every wave is done with ta
   auto store_partials = [&]() {
 #pragma unroll
@@ -243,7 +251,7 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
     }
   };
   if (parts_first) store_partials();
-  hidden_mma<kH, false>(tb, kPad, bc, nullptr, z2);   // z2 only (a3 itself is not needed)
+  hidden_mma<kH, false, RND>(tb, kPad, bc, nullptr, z2, rnd);   // z2 only (a3 itself is not needed)
   if (!parts_first) {
     sum_partials();
     store_partials();
@@ -251,7 +259,10 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
   float b2[kH / 4];
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
+  for (int ks = 0; ks < kH / 4; ++ks) {
+    b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
+    if constexpr (RND) b2[ks] = lowp_round(b2[ks], rnd);
+  }
   __syncthreads();
   // dz2 = da3 silu'(z2), in place (result layout)
 #pragma unroll
@@ -263,7 +274,10 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   // dz1 = (dz2 W2^T) silu'(z1) into tb; the next stage's B = W1^T requested meanwhile
   float b1[kH / 4];
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) b1[ks] = W1[col * kH + 4 * ks + (l >> 4)];
+  for (int ks = 0; ks < kH / 4; ++ks) {
+    b1[ks] = W1[col * kH + 4 * ks + (l >> 4)];
+    if constexpr (RND) b1[ks] = lowp_round(b1[ks], rnd);
+  }
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -296,7 +310,8 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
     f4 d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < kH / 4; ++ks) {
-      const float bw = i < nb ? W0[i * kH + 4 * ks + (l >> 4)] : 0.f;
+      float bw = i < nb ? W0[i * kH + 4 * ks + (l >> 4)] : 0.f;
+      if constexpr (RND) bw = lowp_round(bw, rnd);
       d = mfma4(ta[(16 * w + (l & 15)) * kPad + 4 * ks + (l >> 4)], bw, d);
     }
 #pragma unroll
@@ -315,18 +330,28 @@ void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd
                           const RadialSet& rs, int* status) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
-  if (nb <= 8) edge_prologue_kernel<8><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
-  else edge_prologue_kernel<16><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
+  auto go = [&](auto R) {
+    constexpr bool RND = decltype(R)::value;
+    if (nb <= 8) edge_prologue_kernel<8, RND><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
+    else edge_prologue_kernel<16, RND><<<g, 256, 0, s>>>(E, pos, snd, rcv, shift, rc, p, nb, Y, rbf, rs, status);
+  };
+  if (rs.rnd) go(std::true_type{});
+  else go(std::false_type{});
 }
 
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
-                       const float* dYp, int n_part, float* dY, float* de, int accumulate) {
+                       const float* dYp, int n_part, float* dY, float* de, int accumulate, int rnd) {
   if (E <= 0) return;
   const int g = (E + kTE - 1) / kTE;
   auto go = [&](auto NP) {
     constexpr int NPART = decltype(NP)::value;
-    if (nb <= 8) radial_bwd_kernel<8, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
-    else radial_bwd_kernel<16, NPART><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate);
+    if (rnd) {
+      if (nb <= 8) radial_bwd_kernel<8, NPART, true><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate, rnd);
+      else radial_bwd_kernel<16, NPART, true><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate, rnd);
+    } else {
+      if (nb <= 8) radial_bwd_kernel<8, NPART, false><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate, 0);
+      else radial_bwd_kernel<16, NPART, false><<<g, 256, 0, s>>>(E, rbf, nb, W, da3p, dYp, dY, de, accumulate, 0);
+    }
   };
   switch (n_part) {   // K / 16 for K in {32, 64, 96, 128}, or 1 (whole values)
     case 1: go(std::integral_constant<int, 1>{}); break;

@@ -386,6 +386,7 @@ struct RadialSet {
   const float* W[kMaxRadialLayers];
   float* a3[kMaxRadialLayers];
   int n;
+  int rnd;   // precision study: rounding of every hidden layer's input and weights (0 none, 1 bf16, 2 fp16)
 };
 // first interaction layer in factorised form (U, gU: [N][16][64 S], S <= 4)
 void launch_l0_gather(hipStream_t s, int N, int S, const int* rcv_off, const int* snd_z, const float* a3,
@@ -399,7 +400,7 @@ void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
                    const float4* g, float* F);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
-                       const float* dYp, int n_part, float* dY, float* de, int accumulate);
+                       const float* dYp, int n_part, float* dY, float* de, int accumulate, int rnd);
 void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
                    const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
                    double* stress);

@@ -62,10 +62,10 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
 
 
 def run_oracle(params: dict, system, blob: np.ndarray, bf16=False, forces=True, fp16=False, bf16_radial=False,
-               tp_round=None, symcon_round=None):
+               tp_round=None, symcon_round=None, radial_round=None):
     return mace.energy_forces(mace.ModelDesc(**params), blob, system, bf16_linear=bf16 or bf16_radial,
                               forces=forces, fp16_linear=fp16, bf16_radial=bf16_radial, tp_round=tp_round,
-                              symcon_round=symcon_round)
+                              symcon_round=symcon_round, radial_round=radial_round)
 
 
 def oracle_stress(params: dict, system, blob: np.ndarray, bf16=False, fp16=False, bf16_radial=False):

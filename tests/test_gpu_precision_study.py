@@ -1,6 +1,6 @@
 """Per-block precision study on the GPU (the paper's per-block low-precision
 experiments, run on the whole model through the C ABI): the operands of the
-edge product or of the symmetric contraction rounded to bfloat16 or binary16
+edge product, of the symmetric contraction or of the radial MLP rounded to bfloat16 or binary16
 (FP32 arithmetic), each against the oracle's emulation of the same rounding
 and against FP64.  The printed deviations from FP64 are the study's result."""
 import numpy as np
@@ -14,11 +14,13 @@ pytestmark = pytest.mark.gpu
 B = pytest.importorskip("paper_2510_23621_amd.binding")
 from gpu_common import errors, lib_blob, oracle_blob, run_gpu, run_oracle  # noqa: E402
 
-BLOCKS = {B.MACE_BLOCK_EDGE_PRODUCT: "tp_round", B.MACE_BLOCK_SYMMETRIC_CONTRACTION: "symcon_round"}
+BLOCKS = {B.MACE_BLOCK_EDGE_PRODUCT: "tp_round", B.MACE_BLOCK_SYMMETRIC_CONTRACTION: "symcon_round",
+          B.MACE_BLOCK_RADIAL_MLP: "radial_round"}
 FORMATS = {1: "bf16", 2: "fp16"}
 # GPU (FP32 arithmetic on rounded FP32 values) against the FP64 emulation: the
 # same roundings up to a value that sits within FP32 rounding of a 16-bit
-# rounding boundary (measured: 1e-9 to 3e-7 on energies, 4e-7 on forces)
+# rounding boundary (measured: 1e-9 to 3e-7 on energies, up to 2e-6 for the
+# radial MLP's binary16 arm, 5e-7 on forces)
 EMU_TOL = {1: (1e-5, 1e-4), 2: (1e-5, 1e-4)}
 
 
@@ -76,6 +78,8 @@ def test_block_rounding_setting_and_combination(case):
     assert B.mace_block_rounding(g.handle, B.MACE_BLOCK_EDGE_PRODUCT) == 0
     assert B.mace_block_rounding(g.handle, B.MACE_BLOCK_EDGE_PRODUCT, 2) == 2
     assert B.mace_block_rounding(g.handle, B.MACE_BLOCK_SYMMETRIC_CONTRACTION) == 0
+    assert B.mace_block_rounding(g.handle, B.MACE_BLOCK_RADIAL_MLP, 1) == 1
+    assert B.mace_block_rounding(g.handle, B.MACE_BLOCK_RADIAL_MLP) == 1
     with pytest.raises(B.MaceError):
         B.mace_block_rounding(g.handle, 7, 1)
     with pytest.raises(B.MaceError):
