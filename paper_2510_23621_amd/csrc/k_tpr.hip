@@ -508,15 +508,15 @@ tpr_fwd_kernel(
         for_paths<LHMAX>([&](auto tag) {
           using T = decltype(tag);
           constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
-          float t[2 * lo + 1];
-#pragma unroll
-          for (int m = 0; m < 2 * lo + 1; ++m) t[m] = 0.f;
-          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
-            t[m3] += cg * (hv[lh * lh + m1] * y[ly * ly + m2]);
-          });
+          // R folded into the sender features first: acc += C (R h[m1]) Y[m2],
+          // one product per coupled pair and one multiply-add per coefficient
           const float rv = r[T::index][q];
+          float hr[2 * lh + 1];
 #pragma unroll
-          for (int m = 0; m < 2 * lo + 1; ++m) acc[T::offset + m] += rv * t[m];
+          for (int m = 0; m < 2 * lh + 1; ++m) hr[m] = rv * hv[lh * lh + m];
+          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
+            acc[T::offset + m3] += cg * (hr[m1] * y[ly * ly + m2]);
+          });
         });
         if constexpr (q < 3) {
 #pragma unroll
