@@ -35,7 +35,10 @@ constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
 // blocks per CU fit the LDS below l = 2 and give four waves per SIMD at 128
 // VGPRs; the l = 1 backward needs more registers (dE/dAt of the receiver
 // stays live) and runs two 4-wave blocks per CU at 256 (at 168 it spills);
-// for l = 2 the W3 slice alone fills half the LDS. The MFMA phases raise
+// for l = 2 the W3 slice alone fills half the LDS, and the l = 2 backward
+// runs one 4-wave block per CU, one wave per SIMD, so that its state fits the
+// whole register file (VGPRs and AGPRs; at two waves per SIMD it spilled
+// about 300 bytes per lane to scratch, 1.3x slower). The MFMA phases raise
 // the wave's priority so that they issue ahead of the other waves' vector
 // work on the SIMD.
 // The split-BF16 backward (RM = 2) keeps both layouts of the three W3 parts
@@ -43,8 +46,8 @@ constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
 template <int LHMAX, bool BWD, int RM = 0>
 struct TprShape {
   static constexpr bool split_bwd = BWD && RM == 2;
-  static constexpr int waves = (BWD && LHMAX == 1 && !split_bwd) ? 4 : 8;
-  static constexpr int per_simd = LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 2 : 4);
+  static constexpr int waves = ((BWD && LHMAX == 1 && !split_bwd) || (BWD && LHMAX == 2)) ? 4 : 8;
+  static constexpr int per_simd = (BWD && LHMAX == 2) ? 1 : (LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 2 : 4));
   static constexpr int blocks_per_cu = 4 * per_simd / waves;
 };
 
