@@ -20,58 +20,75 @@
 // carry the rounded W3), which is the same product as the per-edge form.
 //
 // U and gU are [N][16][S * 64]. One block of four waves per receiver; lane
-// j = 0..63 is the radial hidden unit. Every sum runs over the receiver's
-// edges in CSR order within one lane, so results do not depend on scheduling.
+// j = 0..63 is the radial hidden unit. Every sum has a fixed order (the
+// gather's: each wave over its edges in CSR order, then the four waves in
+// order), so results do not depend on scheduling.
 #include "mace_internal.h"
 
 namespace mace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kL0Edges = 16;     // edges whose loads are issued together (gather)
-constexpr int kL0BwdEdges = 4;   // edges per wave and iteration (backward), loads issued together
+constexpr int kL0BwdEdges = 4;   // edges per wave and iteration, their loads issued together
 
-// Wave w gathers components 4w .. 4w + 3 of U over every edge of the receiver.
+// Wave w takes the receiver's edges e_beg + w, e_beg + w + 4, ... (four per
+// iteration, their loads issued together) for all 16 components; the waves'
+// sums are added in wave order through LDS (waves 1-3 store, wave 0 adds).
 template <int S, bool RB>
 __global__ void __launch_bounds__(256) l0_gather_kernel(int N, const int* __restrict__ rcv_off,
                                                         const int* __restrict__ snd_z, const float* __restrict__ a3,
                                                         const float* __restrict__ Y, float* __restrict__ U) {
   constexpr int KI = 64 * S;
+  __shared__ float part[3][16][KI];
   const int i = blockIdx.x;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  float acc[S][4];
+  float acc[S][16];
 #pragma unroll
   for (int s = 0; s < S; ++s)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[s][c] = 0.f;
+    for (int c = 0; c < 16; ++c) acc[s][c] = 0.f;
   const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
-  for (int e0 = e_beg; e0 < e_end; e0 += kL0Edges) {
-    float a[kL0Edges];
-    f4 y[kL0Edges];
-    int z[kL0Edges];
+  for (int e = e_beg + w; e < e_end; e += 4 * kL0BwdEdges) {
+    float a[kL0BwdEdges];
+    f4 y[kL0BwdEdges][4];
+    int z[kL0BwdEdges];
 #pragma unroll
-    for (int q = 0; q < kL0Edges; ++q) {
-      const int e = min(e0 + q, e_end - 1);
-      z[q] = snd_z[e];
-      a[q] = a3[(size_t)e * 64 + lane];
-      y[q] = *reinterpret_cast<const f4*>(Y + (size_t)e * 16 + 4 * w);
+    for (int q = 0; q < kL0BwdEdges; ++q) {
+      const int eq = min(e + 4 * q, e_end - 1);
+      z[q] = snd_z[eq];
+      a[q] = a3[(size_t)eq * 64 + lane];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) y[q][v] = reinterpret_cast<const f4*>(Y + (size_t)eq * 16)[v];
     }
 #pragma unroll
-    for (int q = 0; q < kL0Edges; ++q) {
-      const float av = e0 + q < e_end ? (RB ? bf16_round(a[q]) : a[q]) : 0.f;   // past e_end: adds zero
-      const int zq = e0 + q < e_end ? z[q] : -1;
+    for (int q = 0; q < kL0BwdEdges; ++q) {
+      const bool valid = e + 4 * q < e_end;
+      const float av = valid ? (RB ? bf16_round(a[q]) : a[q]) : 0.f;   // past e_end: adds zero
+      const int zq = valid ? z[q] : -1;
 #pragma unroll
       for (int s = 0; s < S; ++s)
         if (zq == s) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) acc[s][c] += av * y[q][c];
+          for (int c = 0; c < 16; ++c) acc[s][c] += av * y[q][c >> 2][c & 3];
         }
     }
   }
+  if (w > 0) {
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
+    for (int c = 0; c < 16; ++c)
 #pragma unroll
-    for (int s = 0; s < S; ++s) U[((size_t)i * 16 + 4 * w + c) * KI + 64 * s + lane] = acc[s][c];
+      for (int s = 0; s < S; ++s) part[w - 1][c][64 * s + lane] = acc[s][c];
+  }
+  __syncthreads();
+  if (w == 0) {
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const int o = 64 * s + lane;
+        U[((size_t)i * 16 + c) * KI + o] = ((acc[s][c] + part[0][c][o]) + part[1][c][o]) + part[2][c][o];
+      }
+  }
 }
 
 // Wave w takes the receiver's edges e_beg + w, e_beg + w + 4, ...; it holds
