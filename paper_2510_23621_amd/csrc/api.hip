@@ -169,6 +169,7 @@ struct Buffers {
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
+  std::vector<unsigned short*> a3x;   // per layer: its three bfloat16 parts [E][3][64] (split-BF16 products)
   std::vector<float*> A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
@@ -213,12 +214,14 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
   b.a3.resize(T);
+  b.a3x.resize(T);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
   b.ht.assign(T, nullptr);
   for (int t = 0; t < T; ++t) {
     const LayerPlan& L = m.layers[t];
     b.a3[t] = c.take<float>(std::max<int64_t>(E, 1) * 64);
+    b.a3x[t] = c.take<unsigned short>(std::max<int64_t>(E, 1) * 3 * 64);
     b.A[t] = c.take<float>(N * 16 * K);
     if (t > 0) {
       b.hin[t] = c.take<float>(N * L.din * K);
@@ -322,6 +325,19 @@ struct ProfScope {
 // margin for the per-edge passes of both forms).
 bool l0_auto(const Model& m, int64_t N, int64_t E) {
   return m.l0_ki > 0 && E >= 3 * (int64_t)m.d.n_species * N;
+}
+
+// The edge products of layer t run their last radial layer on split-BF16
+// operands, and both read a3 as the three parts the prologue writes (radial
+// mode 3; l_h = 1 only, the edge-lane backward), or split it per tile (2).
+bool layer_factorised(const mace_graph* h, int t) {
+  return t == 0 && h->l0_fact && !h->tp_round && !h->rad_round;
+}
+bool a3_presplit(const mace_graph* h, int t) {
+  return h->radial_split && h->prec != MACE_BF16_RADIAL && h->m.layers[t].lh_max == 1 && !layer_factorised(h, t);
+}
+int radial_mode(const mace_graph* h, int t) {
+  return h->prec == MACE_BF16_RADIAL ? 1 : (!h->radial_split ? 0 : (a3_presplit(h, t) ? 3 : 2));
 }
 
 // A linear launch, bracketed for profiling; while the linear class is
@@ -548,6 +564,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       for (int q = 0; q < rs.n; ++q) {
         rs.W[q] = b.w + m.off.at(std::to_string(t0 + q) + ".radial.0");
         rs.a3[q] = b.a3[t0 + q];
+        rs.a3x[q] = a3_presplit(h, t0 + q) ? b.a3x[t0 + q] : nullptr;
       }
       // (a later chunk recomputes the same Y and rbf)
       launch_edge_prologue(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, m.d.n_bessel, b.Y, b.rbf,
@@ -571,7 +588,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
   for (int t = 0; t < m.d.n_layers; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
-    if (t == 0 && h->l0_fact && !h->tp_round && !h->rad_round) {
+    if (layer_factorised(h, t)) {
       // factorised first layer: U per receiver, then one contraction (FP32
       // mode: straight to A; 16-bit modes: to At, then their own linears)
       {
@@ -598,9 +615,9 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       }
       {
         PROF(KID_TP_FWD);
-        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, b.a3[t], wr3 + m.off.at(pre + "radial.3"),
-                       b.Y, src, inv_c, b.At, h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0),
-                       h->tp_round);
+        const float* a3t = a3_presplit(h, t) ? reinterpret_cast<const float*>(b.a3x[t]) : b.a3[t];
+        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, a3t, wr3 + m.off.at(pre + "radial.3"),
+                       b.Y, src, inv_c, b.At, radial_mode(h, t), h->tp_round);
       }
       if (t == 0 && !lowp) {
         run_linear(h, s, h->comb0, largs(h, b.At, b.A[t], nullptr, false, 0));
@@ -672,7 +689,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       PROF(KID_SYMCON_BWD);
       launch_symcon_bwd(s, L.lout_max, N, K, b.species, b.A[t], symw(h, t), b.dB, b.dA, h->sc_round);
     }
-    const bool fact = t == 0 && h->l0_fact && !h->tp_round && !h->rad_round;
+    const bool fact = layer_factorised(h, t);
     // dE/dAt (the transposes of the linears after the edge product); the
     // factorised first layer ends in dE/dU instead
     const float* dApre = b.dA;
@@ -699,10 +716,10 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
       const float* src = t == 0 ? (h->tp_round ? b.sp_round : b.sp_table) : b.ht[t];
       const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
-      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map, b.a3[t],
+      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map,
+                     a3_presplit(h, t) ? reinterpret_cast<const float*>(b.a3x[t]) : b.a3[t],
                      (h->rad_round ? b.w_round : b.w) + m.off.at(pre + "radial.3"),
-                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p,
-                     h->prec == MACE_BF16_RADIAL ? 1 : (h->radial_split ? 2 : 0), h->tp_round);
+                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, radial_mode(h, t), h->tp_round);
     }
     // The edge backward wrote Q and the partials (about 390 MB at K = 128,
     // more than the last-level cache holds); the sender sum reads Q first

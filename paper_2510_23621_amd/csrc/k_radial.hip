@@ -165,11 +165,22 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 #pragma unroll
     for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
     float* a3 = rs.a3[t];
+    unsigned short* a3x = rs.a3x[t];
     for (int idx = threadIdx.x; idx < kTE * kH / 4; idx += blockDim.x) {
       const int e = idx >> 4, c4 = idx & 15;
-      if (e0 + e < E)
-        *reinterpret_cast<f4*>(a3 + (size_t)(e0 + e) * kH + 4 * c4) =
-            *reinterpret_cast<const f4*>(ha + e * kPad + 4 * c4);
+      if (e0 + e >= E) continue;
+      const f4 v = *reinterpret_cast<const f4*>(ha + e * kPad + 4 * c4);
+      if (a3x) {   // the three bfloat16 parts, [E][3][64]
+        unsigned p0[2], p1[2], p2[2];
+        split3_pair(f2v{v[0], v[1]}, p0[0], p1[0], p2[0]);
+        split3_pair(f2v{v[2], v[3]}, p0[1], p1[1], p2[1]);
+        unsigned short* row = a3x + (size_t)(e0 + e) * 3 * kH + 4 * c4;
+        *reinterpret_cast<uint2*>(row) = make_uint2(p0[0], p0[1]);
+        *reinterpret_cast<uint2*>(row + kH) = make_uint2(p1[0], p1[1]);
+        *reinterpret_cast<uint2*>(row + 2 * kH) = make_uint2(p2[0], p2[1]);
+      } else {
+        *reinterpret_cast<f4*>(a3 + (size_t)(e0 + e) * kH + 4 * c4) = v;
+      }
     }
     __syncthreads();   // ha is rewritten by the next layer's MLP
   }

@@ -45,7 +45,7 @@ constexpr int kYPitch = 20;   // Y tile row: 16 floats + 4 (float4-aligned)
 // in LDS (120 KB at P = 10): one 8-wave block per CU at l = 1.
 template <int LHMAX, bool BWD, int RM = 0>
 struct TprShape {
-  static constexpr bool split_bwd = BWD && RM == 2;
+  static constexpr bool split_bwd = BWD && (RM == 2 || RM == 3);
   static constexpr int waves = ((BWD && LHMAX == 1 && !split_bwd) || (BWD && LHMAX == 2)) ? 4 : 8;
   static constexpr int per_simd = (BWD && LHMAX == 2) ? 1 : (LHMAX == 2 ? 2 : ((BWD && LHMAX == 1) ? 2 : 4));
   static constexpr int blocks_per_cu = 4 * per_simd / waves;
@@ -178,29 +178,33 @@ __device__ __forceinline__ void split3(float x, unsigned short& b0, unsigned sho
 // parts, two values per conversion: v_cvt_pk_bf16_f32 rounds a pair to nearest
 // even and packs it as one operand word (first value in the low half), and the
 // rounded values are unpacked by shifts and masks to form the next remainder.
-typedef float f2v __attribute__((ext_vector_type(2)));
-typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
 typedef unsigned u4v __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ unsigned bf16_pack2(f2v x) { return __builtin_bit_cast(unsigned, __builtin_convertvector(x, bf2v)); }
-__device__ __forceinline__ f2v bf16_unpack2(unsigned w) {
-  return f2v{__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xffff0000u)};
-}
 __device__ __forceinline__ void split3_x8(f4 lo, f4 hi, us8v& a0, us8v& a1, us8v& a2) {
   u4v w0, w1, w2;
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
     const f2v x = h < 2 ? f2v{lo[2 * h], lo[2 * h + 1]} : f2v{hi[2 * h - 4], hi[2 * h - 3]};
-    const unsigned p0 = bf16_pack2(x);
-    const f2v r1 = x - bf16_unpack2(p0);
-    const unsigned p1 = bf16_pack2(r1);
-    const f2v r2 = r1 - bf16_unpack2(p1);
+    unsigned p0, p1, p2;
+    split3_pair(x, p0, p1, p2);
     w0[h] = p0;
     w1[h] = p1;
-    w2[h] = bf16_pack2(r2);
+    w2[h] = p2;
   }
   a0 = __builtin_bit_cast(us8v, w0);
   a1 = __builtin_bit_cast(us8v, w1);
   a2 = __builtin_bit_cast(us8v, w2);
+}
+
+// The parts of a3[row][32 ks + 8 (l/16) .. +7] from the pre-split rows
+// ([E][3][64] bfloat16), zero where keep is false (rows past the tile's end).
+__device__ __forceinline__ void load_a3_parts(const unsigned short* __restrict__ a3x, int row, bool keep, int ks,
+                                              us8v& a0, us8v& a1, us8v& a2) {
+  const int l = threadIdx.x & 63;
+  const unsigned short* base = a3x + (size_t)row * 192 + 32 * ks + 8 * (l >> 4);
+  const us8v z = {0, 0, 0, 0, 0, 0, 0, 0};
+  a0 = keep ? *reinterpret_cast<const us8v*>(base) : z;
+  a1 = keep ? *reinterpret_cast<const us8v*>(base + 64) : z;
+  a2 = keep ? *reinterpret_cast<const us8v*>(base + 128) : z;
 }
 
 // The three parts of the forward slice, part q at sWx + q P 16 kWbPitch, in the
@@ -219,14 +223,16 @@ __device__ __forceinline__ void load_w3_slice_x3(const float* __restrict__ W3, i
 // As tile_radial, FP32-accurate on split BF16 operands. The K steps are the
 // outer loop, so that only one step's A parts are live; within each step the
 // terms are added from the smallest to the largest.
-template <int P>
+// PRE: a3 points at the pre-split parts ([E][3][64] bfloat16) instead.
+template <int P, bool PRE = false>
 __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int e0, int e_end,
                                                const unsigned short* __restrict__ sWx, f4* r) {
   constexpr int part = P * 16 * kWbPitch;
   const int l = threadIdx.x & 63;
   const int row = e0 + (l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
-  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+  const int crow = min(row, e_end - 1);
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)crow * 64 + 8 * (l >> 4));
   const unsigned short* wb = sWx + (l & 15) * kWbPitch + 8 * (l >> 4);
 #pragma unroll
   for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
@@ -234,9 +240,13 @@ __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     __builtin_amdgcn_sched_barrier(0);
-    const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
     us8v a0, a1, a2;
-    split3_x8(lo, hi, a0, a1, a2);
+    if constexpr (PRE) {
+      load_a3_parts(reinterpret_cast<const unsigned short*>(a3), crow, row < e_end, ks, a0, a1, a2);
+    } else {
+      const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+      split3_x8(lo, hi, a0, a1, a2);
+    }
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       __builtin_amdgcn_sched_barrier(0);   // one path's B parts live at a time
@@ -453,7 +463,9 @@ __device__ __forceinline__ void load_h_row(const float* __restrict__ h, int src,
   for (int c = 0; c < DIN; ++c) hv[c] = h[((size_t)src * DIN + c) * K + k];
 }
 
-// RM, the operands of the last radial layer: 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate)
+// RM, the operands of the last radial layer: 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate),
+// 3 split BF16 with a3 arriving as its three parts (the a3 argument then points at
+// [E][3][64] bfloat16 written by the edge prologue)
 template <int LHMAX, int RM, int NW = TprShape<LHMAX, false>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
@@ -464,13 +476,14 @@ tpr_fwd_kernel(
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
+  constexpr bool SPLIT = RM == 2 || RM == 3;
   constexpr int kSlice = RM == 1 ? (P * 16 * kWbPitch + 1) / 2
-                        : (RM == 2 ? (3 * P * 16 * kWbPitch + 1) / 2 : P * 16 * kWPitch);   // floats
+                        : (SPLIT ? (3 * P * 16 * kWbPitch + 1) / 2 : P * 16 * kWPitch);   // floats
   __shared__ __align__(16) float sW[kSlice];
   __shared__ float sY[NW][16 * kYPitch];
   const int ct = blockIdx.y;
   if constexpr (RM == 1) load_w3_slice_bf16<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW), nullptr);
-  else if constexpr (RM == 2) load_w3_slice_x3<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW));
+  else if constexpr (SPLIT) load_w3_slice_x3<P>(W3, K, ct, reinterpret_cast<unsigned short*>(sW));
   else load_w3_slice<P>(W3, K, ct, sW);
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -490,7 +503,8 @@ tpr_fwd_kernel(
       stage_y(Y, e0, e_end, sy);
       f4 r[P];
       if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
-      else if constexpr (RM == 2) tile_radial_x3<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      else if constexpr (SPLIT)
+        tile_radial_x3<P, RM == 3>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else tile_radial<P>(a3, e0, e_end, sW, r);
       round_tile<P>(r, rnd);
       // lane group 0 holds the tile's first edges, so nq covers every valid one;
@@ -592,6 +606,7 @@ __device__ __forceinline__ void tpr_bwd_channel_lanes(
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
   static_assert(RM != 2 || LHMAX <= 1, "split-BF16 backward for l <= 1");
+  static_assert(RM != 3, "pre-split a3: edge-lane backward only");
   constexpr bool RB = RM == 1;
   constexpr int kSlice = RM == 1 ? (P * 16 * kWbPitch + P * 64 * kWtPitch + 1) / 2
                         : (RM == 2 ? 3 * P * 16 * 64 : P * 16 * kWPitch);   // floats
@@ -812,23 +827,28 @@ __device__ __forceinline__ void load_w3_slices_x3_el(const float* __restrict__ W
 // R in the edge-lane layout: r[p][c] = R[e0 + l%16][p][16 ct + 4(l/16) + c]
 // (zero for edges past e_end), split-BF16 products as in tile_radial_x3s with
 // the operands exchanged.
-template <int P>
+template <int P, bool PRE = false>
 __device__ __forceinline__ void tile_radial_x3_el(const float* __restrict__ a3, int e0, int e_end,
                                                   const unsigned short* __restrict__ sWf, f4* r) {
   constexpr int part = P * 16 * 64;
   const int l = threadIdx.x & 63;
   const int row = e0 + (l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
-  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+  const int crow = min(row, e_end - 1);
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)crow * 64 + 8 * (l >> 4));
 #pragma unroll
   for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
   __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     __builtin_amdgcn_sched_barrier(0);
-    const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
     us8v a0, a1, a2;
-    split3_x8(lo, hi, a0, a1, a2);
+    if constexpr (PRE) {
+      load_a3_parts(reinterpret_cast<const unsigned short*>(a3), crow, row < e_end, ks, a0, a1, a2);
+    } else {
+      const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+      split3_x8(lo, hi, a0, a1, a2);
+    }
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       __builtin_amdgcn_sched_barrier(0);
@@ -880,9 +900,10 @@ __device__ __forceinline__ void tile_da3_x3_el(const f4* r, const unsigned short
 }
 
 template <int LHMAX, int RM>
-constexpr bool tpr_bwd_edge_lanes() { return RM == 2 && LHMAX == 1; }
+constexpr bool tpr_bwd_edge_lanes() { return (RM == 2 || RM == 3) && LHMAX == 1; }
 
-template <int LHMAX, int NW>
+// PRE: a3 arrives as its three parts (RM = 3).
+template <int LHMAX, int NW, bool PRE>
 __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
@@ -950,7 +971,7 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
         y[4 * v + 3] = t4[3];
       }
       f4 r[P];   // R on entry; dR (zero for edges past e_end) after the path loop
-      tile_radial_x3_el<P>(a3, e0, e_end, sWf, r);
+      tile_radial_x3_el<P, PRE>(a3, e0, e_end, sWf, r);
       round_tile<P>(r, rnd);
       float dy[16];
 #pragma unroll
@@ -1034,7 +1055,7 @@ tpr_bwd_kernel(
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
     float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
-    tpr_bwd_edge_lanes_body<LHMAX, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
+    tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
@@ -1076,16 +1097,25 @@ void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, float* At, int radial_mode, int tp_round) {
   if (N <= 0) return;
-#define MACE_TPRF(LH)                                                                                    \
-  case LH:                                                                                               \
-    if (radial_mode == 1) tpr_fwd_launch<LH, 1>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round); \
-    else if (radial_mode == 2) tpr_fwd_launch<LH, 2>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round); \
-    else tpr_fwd_launch<LH, 0>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round);                  \
-    break;
+#define MACE_TPRF(LH, RM) tpr_fwd_launch<LH, RM>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round)
+  // radial_mode 3 (pre-split a3) is requested for l_h = 1 only
   switch (lh_max) {
-    MACE_TPRF(0)
-    MACE_TPRF(1)
-    MACE_TPRF(2)
+    case 0:
+      if (radial_mode == 1) MACE_TPRF(0, 1);
+      else if (radial_mode == 2) MACE_TPRF(0, 2);
+      else if (radial_mode == 0) MACE_TPRF(0, 0);
+      break;
+    case 1:
+      if (radial_mode == 1) MACE_TPRF(1, 1);
+      else if (radial_mode == 2) MACE_TPRF(1, 2);
+      else if (radial_mode == 3) MACE_TPRF(1, 3);
+      else MACE_TPRF(1, 0);
+      break;
+    case 2:
+      if (radial_mode == 1) MACE_TPRF(2, 1);
+      else if (radial_mode == 2) MACE_TPRF(2, 2);
+      else if (radial_mode == 0) MACE_TPRF(2, 0);
+      break;
   }
 #undef MACE_TPRF
 }
@@ -1106,6 +1136,7 @@ void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
     case 1:
       if (radial_mode == 1) MACE_TPRB(1, 1);
       else if (radial_mode == 2) MACE_TPRB(1, 2);
+      else if (radial_mode == 3) MACE_TPRB(1, 3);
       else MACE_TPRB(1, 0);
       break;
     case 2:   // split BF16 falls back to FP32 MFMA here

@@ -75,6 +75,24 @@ __host__ __device__ __forceinline__ unsigned short bf16_bits(float x) {
   return (unsigned short)(u >> 16);
 }
 
+// Split-BF16 operands (FP32-accurate products on the BF16 MFMA pipe): a pair of
+// FP32 values x is carried as three packed bfloat16 words p0, p1, p2 with
+// p0 = bf16(x), p1 = bf16(x - p0), p2 = bf16(x - p0 - p1) per element (each
+// difference exact in FP32); v_cvt_pk_bf16_f32 rounds a pair to nearest even
+// and packs it (first value in the low half), shifts and masks unpack it.
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ unsigned bf16_pack2(f2v x) { return __builtin_bit_cast(unsigned, __builtin_convertvector(x, bf2v)); }
+__device__ __forceinline__ f2v bf16_unpack2(unsigned w) {
+  return f2v{__builtin_bit_cast(float, w << 16), __builtin_bit_cast(float, w & 0xffff0000u)};
+}
+__device__ __forceinline__ void split3_pair(f2v x, unsigned& p0, unsigned& p1, unsigned& p2) {
+  p0 = bf16_pack2(x);
+  const f2v r1 = x - bf16_unpack2(p0);
+  p1 = bf16_pack2(r1);
+  p2 = bf16_pack2(r1 - bf16_unpack2(p1));
+}
+
 // Round-to-nearest-even float -> IEEE binary16 -> float (FP16-linear mode);
 // magnitudes beyond the binary16 range become infinite.
 __host__ __device__ __forceinline__ float fp16_round(float x) { return (float)(_Float16)x; }
@@ -385,6 +403,10 @@ constexpr int kMaxRadialLayers = 4;
 struct RadialSet {
   const float* W[kMaxRadialLayers];
   float* a3[kMaxRadialLayers];
+  // where set, the layer's a3 is written as its three bfloat16 parts instead,
+  // [E][3][64] (part q of edge e at a3x + (3 e + q) 64): the split-BF16 edge
+  // products then read them rather than splitting a3 per channel tile
+  unsigned short* a3x[kMaxRadialLayers];
   int n;
   int rnd;   // precision study: rounding of every hidden layer's input and weights (0 none, 1 bf16, 2 fp16)
 };
