@@ -60,14 +60,16 @@ def measured_traffic(kname, workload):
     return rec["bytes_per_launch"]
 
 
-def kernel_work(name, model, N, E, l0_factored=False, n_species=2):
+def kernel_work(name, model, N, E, l0_factored=False, n_species=2, presplit=False):
     """Algorithmic (bytes, flops) of every launch of kernel class `name` in
     one step, summed.  Bytes count each compulsory HBM read/write once; flops
     of the MFMA-bound classes count the dense contractions only (the radial
     MLP layers, including the last one formed inside the tensor-product
     kernels), not the Clebsch-Gordan arithmetic on the vector ALUs.  With
     the first layer in factorised form its message comes from the l0_*
-    kernels and its radial backward reads one partial."""
+    kernels and its radial backward reads one partial.  With presplit
+    (split-BF16 products), a3 of the per-edge l_h = 1 layers is stored as its
+    three bfloat16 parts, 384 bytes per edge instead of 256."""
     K, nb, layers = model["K"], model["n_bessel"], model["layers"]
     n_ct = K // 16
     ki = 64 * n_species
@@ -75,6 +77,7 @@ def kernel_work(name, model, N, E, l0_factored=False, n_species=2):
     for t, L in enumerate(layers):
         P, mid, din = L["P"], L["mid"], L["din"]
         fact = l0_factored and t == 0
+        a3b = 384 if (presplit and din == 4 and not fact) else 256
         if fact and name in ("tpr_fwd_kernel", "tpr_bwd_kernel"):
             continue
         if name == "l0_gather_kernel" and fact:      # a3, Y, sender species in; U out
@@ -84,14 +87,14 @@ def kernel_work(name, model, N, E, l0_factored=False, n_species=2):
             tot_b += N * 16 * ki * 4 + E * (256 + 64 + 4) + E * (256 + 64)
             tot_f += E * 2 * 2 * 64 * 16
         elif name == "tpr_fwd_kernel":
-            tot_b += E * (256 + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4 + 64 * P * K * 4
+            tot_b += E * (a3b + 64 + 4) + N * (din + mid) * K * 4 + (N + 1) * 4 + 64 * P * K * 4
             tot_f += E * 2 * 64 * P * K
         elif name == "tpr_bwd_kernel":
             q = din * K * 4 if t > 0 else 0
-            tot_b += E * (256 + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
+            tot_b += E * (a3b + 64 + 4 + n_ct * (64 + 256) + q) + N * (din + mid) * K * 4 + 64 * P * K * 4
             tot_f += E * 2 * 2 * 64 * P * K
         elif name == "edge_prologue_kernel":      # geometry once, hidden layers of every layer
-            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * 256   # a3
+            tot_b += E * ((12 + 8 + 32 + 64 + nb * 4) if t == 0 else 0) + E * a3b   # a3
             tot_f += E * 2 * (nb * 64 + 2 * 64 * 64)
         elif name == "radial_bwd_kernel":
             acc = t < len(layers) - 1          # de and dY accumulate into the later layer's values
@@ -236,7 +239,8 @@ def main():
     from paper_2510_23621_amd.csrc_info import layer_shapes
     model = layer_shapes(params)
     l0_factored = B.mace_layer0_form(g.handle, -1) == B.MACE_L0_FACTORED
-    byts, flops = kernel_work(kname, model, N, E, l0_factored, params["n_species"])
+    presplit = prec != B.MACE_BF16_RADIAL and B.mace_fp32_products(g.handle, -1) == B.MACE_PRODUCTS_SPLIT_BF16
+    byts, flops = kernel_work(kname, model, N, E, l0_factored, params["n_species"], presplit)
     per_launch = k_launches / args.steps
     avg_launch_ms = k_ms / max(k_launches, 1)
     bytes_per_launch = byts / max(per_launch, 1)
