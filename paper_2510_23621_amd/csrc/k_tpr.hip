@@ -65,15 +65,23 @@ __device__ __forceinline__ void load_w3_slice(const float* __restrict__ W3, int 
   }
 }
 
+// MFMA row of the tile that carries edge e0 + rho: rho itself, or with TRP the
+// transposed order 4 (rho % 4) + rho / 4, which puts edge e0 + 4 q + (l/16) in
+// result register q of lane l (a tile of n edges then needs ceil(n / 4) edge
+// iterations per lane instead of min(n, 4)).
+template <bool TRP>
+__device__ __forceinline__ int tile_edge(int rho) { return TRP ? 4 * (rho & 3) + (rho >> 2) : rho; }
+
 // R of the 16 edges e0 .. e0+15 (edges at or past e_end get R = 0) for the
-// wave's channel tile: r[p][q] = R[e0 + 4(l/16) + q][p][16 ct + l%16].
+// wave's channel tile: r[p][q] = R[e0 + 4(l/16) + q][p][16 ct + l%16]
+// (R[e0 + 4 q + l/16] with TRP).
 // The 64-long reduction runs in the order j = 16 qq + 4 s + c so that every
 // lane reads its A operand as four float4.
-template <int P>
+template <int P, bool TRP = false>
 __device__ __forceinline__ void tile_radial(const float* __restrict__ a3, int e0, int e_end,
                                             const float* __restrict__ sW, f4* r) {
   const int l = threadIdx.x & 63;
-  const int row = e0 + (l & 15);
+  const int row = e0 + tile_edge<TRP>(l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
   const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 4 * (l >> 4));
   f4 a[4];
@@ -133,11 +141,11 @@ __device__ __forceinline__ void load_w3_slice_bf16(const float* __restrict__ W3,
 }
 
 // As tile_radial, on BF16 operands: two MFMAs (k = 32 each) per path.
-template <int P>
+template <int P, bool TRP = false>
 __device__ __forceinline__ void tile_radial_bf16(const float* __restrict__ a3, int e0, int e_end,
                                                  const unsigned short* __restrict__ sWb, f4* r) {
   const int l = threadIdx.x & 63;
-  const int row = e0 + (l & 15);
+  const int row = e0 + tile_edge<TRP>(l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
   const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
   us8v a[2];
@@ -224,12 +232,12 @@ __device__ __forceinline__ void load_w3_slice_x3(const float* __restrict__ W3, i
 // outer loop, so that only one step's A parts are live; within each step the
 // terms are added from the smallest to the largest.
 // PRE: a3 points at the pre-split parts ([E][3][64] bfloat16) instead.
-template <int P, bool PRE = false>
+template <int P, bool PRE = false, bool TRP = false>
 __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int e0, int e_end,
                                                const unsigned short* __restrict__ sWx, f4* r) {
   constexpr int part = P * 16 * kWbPitch;
   const int l = threadIdx.x & 63;
-  const int row = e0 + (l & 15);
+  const int row = e0 + tile_edge<TRP>(l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
   const int crow = min(row, e_end - 1);
   const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)crow * 64 + 8 * (l >> 4));
@@ -498,26 +506,31 @@ tpr_fwd_kernel(
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
       // sender rows of the lane's four edges (edges past e_end carry R = 0),
       // requested before the radial MFMAs so that their latency is hidden
+      // edge e0 + 4 q + g is the lane's q-th (transposed tile rows)
       int srcq[4];
-      sender_rows(snd, src_map, e0 + 4 * g, e_end, srcq);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int sq = snd[min(e0 + 4 * q + g, e_end - 1)];
+        srcq[q] = src_map ? src_map[sq] : sq;
+      }
       stage_y(Y, e0, e_end, sy);
       f4 r[P];
-      if constexpr (RM == 1) tile_radial_bf16<P>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      if constexpr (RM == 1) tile_radial_bf16<P, true>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
       else if constexpr (SPLIT)
-        tile_radial_x3<P, RM == 3>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
-      else tile_radial<P>(a3, e0, e_end, sW, r);
+        tile_radial_x3<P, RM == 3, true>(a3, e0, e_end, reinterpret_cast<const unsigned short*>(sW), r);
+      else tile_radial<P, true>(a3, e0, e_end, sW, r);
       round_tile<P>(r, rnd);
-      // lane group 0 holds the tile's first edges, so nq covers every valid one;
-      // the scheduling barrier keeps one edge's operands live at a time, and
-      // the next edge's h row is requested while this one is contracted
-      const int nq = min(4, e_end - e0);
+      // a tile of n edges fills registers q < ceil(n / 4) (edges past e_end
+      // carry R = 0); the scheduling barrier keeps one edge's operands live at
+      // a time, and the next edge's h row is requested while this one is contracted
+      const int nq = min(4, (e_end - e0 + 3) >> 2);
       float hv[DIN];
       load_h_row<DIN>(h, srcq[0], K, k, hv);
       static_for<0, 4>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
         __builtin_amdgcn_sched_barrier(0);
         if (q >= nq) return;
-        const int row = 4 * g + q;
+        const int row = 4 * q + g;   // the lane's edge e0 + row
         float hn[DIN];
         if constexpr (q < 3) load_h_row<DIN>(h, srcq[q + 1], K, k, hn);
         float y[16];
