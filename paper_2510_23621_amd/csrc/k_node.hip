@@ -10,9 +10,9 @@ namespace mace {
 
 // Channel-mixing linear on MFMA. A block of kLinQuad waves owns up to four
 // 16-node tiles of one species (one per wave, the 16 MFMA rows), one output
-// component of one group and up to 64 output channels (4 column tiles of 16;
-// blockIdx.z picks which 64). For every term of the group the block stages the
-// term's weight panel (64 output columns x K inputs, stored [col][k]) in LDS
+// component of one group and up to 32 output channels (kLinCt = 2 column tiles
+// of 16; blockIdx.z picks which 32). For every term of the group the block
+// stages the term's weight panel (32 output columns x K inputs, stored [col][k]) in LDS
 // once for its four tiles; each wave reads its A operand straight from memory
 // as float4 rows and its B operand from LDS as 16-byte reads.
 // FP32: v_mfma_f32_16x16x4_f32 with A[l%16][l/16], B[l/16][l%16]; the K-long
@@ -35,7 +35,7 @@ __device__ __forceinline__ unsigned short lowp_bits(float x) {
   else return fp16_bits(x);
 }
 
-constexpr int kLinCt = 4;        // column tiles per block
+constexpr int kLinCt = 2;        // column tiles per block (measured: 2 < 4 < 1 < 8 in time per step)
 constexpr int kLinSmallGrid = 512;   // blocks below which a square linear takes one column tile per block
 
 // LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
@@ -206,7 +206,7 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
   const int KI0 = a.KI > 0 ? a.KI : a.K;
   if (KI0 == a.K && (int64_t)a.n_quads * P.host.n_gc * halves < kLinSmallGrid) {
-    // small launch: one column tile per block, four times the blocks
+    // small launch: one column tile per block, kLinCt times the blocks
     dim3 g1(a.n_quads, P.host.n_gc, a.K / 16);
     auto sq1 = [&](auto KK) {
       constexpr int k = decltype(KK)::value;
