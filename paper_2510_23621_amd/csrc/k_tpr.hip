@@ -983,7 +983,7 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
         y[4 * v + 2] = t4[2];
         y[4 * v + 3] = t4[3];
       }
-      f4 r[P];   // R on entry; dR (zero for edges past e_end) after the path loop
+      f4 r[P];   // R on entry (zero for edges past e_end); dR after the path loop
       tile_radial_x3_el<P, PRE>(a3, e0, e_end, sWf, r);
       round_tile<P>(r, rnd);
       float dy[16];
@@ -1018,7 +1018,9 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
           d += hv[lh * lh + m] * Dm[m];
           dh[lh * lh + m] += rv * Dm[m];
         }
-        r[T::index] = valid ? d : f4{0.f, 0.f, 0.f, 0.f};
+        // (rows past e_end keep their finite dR: a row of the dE/da3 product
+        // depends on its own edge only, and those rows are not stored)
+        r[T::index] = d;
       });
       // dE/dY over the tile's 16 channels: halve over lane bit 5 (l/16 >= 2
       // keeps m2 8..15), then over lane bit 4; lane group q ends with m2 = 4q .. 4q + 3
