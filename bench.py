@@ -176,7 +176,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on one GPU only (asked for {max(args.gpus, world)}): this build has no multi-GPU path",
+        print(f"bench.py runs on one GPU only (asked for {max(args.gpus, world)}): the library has no multi-GPU path",
               file=sys.stderr)
         sys.exit(2)
 

@@ -430,7 +430,7 @@ void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, con
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
 void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_mode, int tp_round);   // radial 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate); tp_round 0/1/2 none/bf16/fp16
+                    float inv_c, float* At, int radial_mode, int tp_round);   // radial 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate), 3 split BF16 with a3 pre-split (l_h = 1); tp_round 0/1/2 none/bf16/fp16
 void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
