@@ -74,17 +74,31 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   f4 acc[CT];
 #pragma unroll
   for (int j = 0; j < CT; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-  for (int tm = grp.t0; tm < grp.t1; ++tm) {
+  // Terms are software-pipelined: the next term's A rows and weight panel are
+  // requested into registers while the current term's MFMAs run.
+  constexpr int kPanelVec = BF16 ? 16 * CT * (K / 8) : 16 * CT * (KI / 4);   // 16-byte vectors per panel
+  constexpr int kPanelPer = (kPanelVec + 64 * kLinQuad - 1) / (64 * kLinQuad);   // per thread
+  f4 av[BF16 ? 1 : KI / 16];
+  us8 ab[BF16 ? KI / 32 : 1];
+  f4 pv[BF16 ? 1 : kPanelPer];
+  us8 pb[BF16 ? kPanelPer : 1];
+  auto load_term = [&](int tm) {
     const LinTerm term = L.plan.t[tm];
     const int64_t zoff = term.species ? zstride : 0;
     const float* xrow = term.src ? a.x2 + ((size_t)node * L.plan.cin2 + term.in_c0 + c) * KI
                                  : a.x + ((size_t)node * L.plan.cin + term.in_c0 + c) * KI;
-    // A operand first, so that its loads overlap the panel staging
-    f4 av[BF16 ? 1 : KI / 16];
-    us8 ab[BF16 ? KI / 32 : 1];
     if constexpr (!BF16) {
 #pragma unroll
       for (int q = 0; q < KI / 16; ++q) av[q] = *reinterpret_cast<const f4*>(xrow + 16 * q + 4 * (l >> 4)) * keep;
+      // panel row = output column n: the transposed blob holds W^T[n][0..KI) contiguous
+      const float* Wt = a.wt + term.w_off + zoff;
+#pragma unroll
+      for (int u = 0; u < kPanelPer; ++u) {
+        const int idx = min(tid + 64 * kLinQuad * u, kPanelVec - 1);
+        const int col = idx / (KI / 4), k4 = idx % (KI / 4);
+        const int n = 16 * ct0 + min(col, ncol - 1);
+        pv[u] = *reinterpret_cast<const f4*>(Wt + (size_t)n * KI + 4 * k4);
+      }
     } else {
 #pragma unroll
       for (int ks = 0; ks < K / 32; ++ks) {
@@ -95,27 +109,44 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
         v[4] = lowp_bits<LP>(hi[0]); v[5] = lowp_bits<LP>(hi[1]); v[6] = lowp_bits<LP>(hi[2]); v[7] = lowp_bits<LP>(hi[3]);
         ab[ks] = v;
       }
-    }
-    __syncthreads();   // the previous term's MFMAs have read the panel
-    if constexpr (!BF16) {
-      // panel row = output column n: the transposed blob holds W^T[n][0..KI) contiguous
-      const float* Wt = a.wt + term.w_off + zoff;
-      for (int idx = tid; idx < 16 * CT * (KI / 4); idx += blockDim.x) {
-        const int col = idx / (KI / 4), k4 = idx % (KI / 4);
-        const int n = 16 * ct0 + min(col, ncol - 1);
-        *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = *reinterpret_cast<const f4*>(Wt + (size_t)n * KI + 4 * k4);
-      }
-    } else {
       // packed [K/8][K][8]: 8 consecutive k of output column n are 16 contiguous bytes
       const unsigned short* Wp = a.wbf + term.w_off + zoff;
-      for (int idx = tid; idx < 16 * CT * (K / 8); idx += blockDim.x) {
+#pragma unroll
+      for (int u = 0; u < kPanelPer; ++u) {
+        const int idx = min(tid + 64 * kLinQuad * u, kPanelVec - 1);
         const int col = idx / (K / 8), kc = idx % (K / 8);
         const int n = 16 * ct0 + min(col, ncol - 1);
-        *reinterpret_cast<us8*>(sBb + col * PB + 8 * kc) =
-            *reinterpret_cast<const us8*>(Wp + ((size_t)kc * K + n) * 8);
+        pb[u] = *reinterpret_cast<const us8*>(Wp + ((size_t)kc * K + n) * 8);
+      }
+    }
+  };
+  if (grp.t0 < grp.t1) load_term(grp.t0);
+  for (int tm = grp.t0; tm < grp.t1; ++tm) {
+    __syncthreads();   // the previous term's MFMAs have read the panel
+#pragma unroll
+    for (int u = 0; u < kPanelPer; ++u) {
+      const int idx = tid + 64 * kLinQuad * u;
+      if (idx < kPanelVec) {
+        if constexpr (!BF16) {
+          const int col = idx / (KI / 4), k4 = idx % (KI / 4);
+          *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) = pv[u];
+        } else {
+          const int col = idx / (K / 8), kc = idx % (K / 8);
+          *reinterpret_cast<us8*>(sBb + col * PB + 8 * kc) = pb[u];
+        }
       }
     }
     __syncthreads();
+    f4 avc[BF16 ? 1 : KI / 16];
+    us8 abc[BF16 ? KI / 32 : 1];
+    if constexpr (!BF16) {
+#pragma unroll
+      for (int q = 0; q < KI / 16; ++q) avc[q] = av[q];
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KI / 32; ++ks) abc[ks] = ab[ks];
+    }
+    if (tm + 1 < grp.t1) load_term(tm + 1);   // in flight during this term's MFMAs
     if constexpr (!BF16) {
 #pragma unroll
       for (int q = 0; q < KI / 16; ++q)
@@ -123,7 +154,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
         for (int j = 0; j < CT; ++j) {
           const f4 b = *reinterpret_cast<const f4*>(sB + (16 * j + (l & 15)) * PF + 16 * q + 4 * (l >> 4));
 #pragma unroll
-          for (int cc = 0; cc < 4; ++cc) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[q][cc], b[cc], acc[j], 0, 0, 0);
+          for (int cc = 0; cc < 4; ++cc) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(avc[q][cc], b[cc], acc[j], 0, 0, 0);
         }
     } else {
 #pragma unroll
@@ -132,10 +163,10 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
         for (int j = 0; j < CT; ++j) {
           const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));
           if constexpr (LP == 1)
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, ab[ks]), __builtin_bit_cast(bf8, b),
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, abc[ks]), __builtin_bit_cast(bf8, b),
                                                              acc[j], 0, 0, 0);
           else
-            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, ab[ks]), __builtin_bit_cast(h8, b),
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, abc[ks]), __builtin_bit_cast(h8, b),
                                                             acc[j], 0, 0, 0);
         }
     }
