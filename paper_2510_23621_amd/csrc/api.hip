@@ -522,6 +522,7 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.KI = 0;
   a.accumulate = accumulate;
   a.lowp = lowp_mode(h->prec);
+  a.bias0 = nullptr;
   return a;
 }
 
@@ -548,7 +549,9 @@ SymW symw(mace_graph* h, int t) {
 }
 
 // Forward pass; keeps every intermediate the backward pass reads.
-void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
+// seed_grad: the last layer's readout also stores the backward pass's
+// starting gradient (dE/dh of the last layer's output, in b.dh0).
+void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, bool seed_grad) {
   const Model& m = h->m;
   Buffers& b = h->b;
   const int N = (int)h->N, E = (int)h->E, K = m.d.K;
@@ -640,13 +643,14 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps) {
       {
         PROF(KID_READOUT);
         launch_readout_fwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
-                           t > 0, eps);
+                           t > 0, eps, nullptr);
       }
     else
       {
         PROF(KID_READOUT);
         launch_readout_fwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, t > 0, eps);
+                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, t > 0, eps,
+                           seed_grad && L.dout == 1 ? b.dh0 : nullptr);
       }
   }
 }
@@ -663,7 +667,9 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
     float* hout = L.last ? b.hlast : b.hin[t + 1];
-    if (L.last) {
+    if (L.last && L.dout == 1) {
+      // the forward's readout stored its gradient in dnext (b.dh0)
+    } else if (L.last) {
       // the energy reaches the last layer's output only through its readout:
       // the readout's gradient is stored, the other components are zero
       if (L.dout > 1) {
@@ -675,13 +681,9 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
         launch_readout_bwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
                            b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, L.dout == 1, dnext);
       }
-    } else {
-      {
-        PROF(KID_READOUT);
-        launch_readout_bwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
-                           0, dnext);
-      }
     }
+    // a layer below the last: its readout's gradient (the readout weights) was
+    // added to dnext by the epilogue of the transposed linear that wrote it
     {
       run_linear(h, s, h->prodT[t], largs(h, dnext, b.dB, nullptr, true, 0));
     }
@@ -735,7 +737,9 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     }
     if (t > 0) {
       {
-        run_linear(h, s, h->upskipT[t], largs(h, b.dht, dprev, nullptr, true, 0, dnext));
+        LinArgs la = largs(h, b.dht, dprev, nullptr, true, 0, dnext);
+        la.bias0 = b.w + m.off.at(std::to_string(t - 1) + ".readout");   // layer t - 1 is not the last
+        run_linear(h, s, h->upskipT[t], la);
       }
       std::swap(dnext, dprev);
     }
@@ -1119,7 +1123,7 @@ mace_status mace_forward_energy(mace_graph* g, const float* positions, float* no
                                 void* stream) {
   if (!g || !positions || !node_energy || !graph_energy) return MACE_EINVAL;
   hipStream_t s = (hipStream_t)stream;
-  run_forward(g, s, positions, node_energy);
+  run_forward(g, s, positions, node_energy, false);
   {
     mace_graph* h = g;
     PROF(KID_GRAPH_ENERGY);
@@ -1132,7 +1136,7 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
                         float* forces, void* stream) {
   if (!g || !positions || !node_energy || !graph_energy || !forces) return MACE_EINVAL;
   hipStream_t s = (hipStream_t)stream;
-  run_forward(g, s, positions, node_energy);
+  run_forward(g, s, positions, node_energy, true);
   {
     mace_graph* h = g;
     PROF(KID_GRAPH_ENERGY);

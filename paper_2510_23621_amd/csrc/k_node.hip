@@ -187,6 +187,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
       float v = acc[j][r];
       if (residual) v += residual[o];
       if (a.accumulate) v += y[o];
+      if (a.bias0 && grp.out_c0 + c == 0 && !grp.dst) v += lowp_round(a.bias0[16 * ct + (l & 15)], a.lowp);
       y[o] = v;
     }
   }
@@ -315,12 +316,29 @@ __device__ __forceinline__ float readout_hidden_z(const float* __restrict__ hrow
   return z;
 }
 
+// dE/dh[n][0][k] = sum_j W1[k][j] w2[j] silu'(z_j) of the last-layer readout,
+// stored to drow or added to it
+__device__ __forceinline__ void readout_mlp_grad(float z, int K, const float* __restrict__ w1,
+                                                 const float* __restrict__ w2, int hidden, int lowp, int lane,
+                                                 int overwrite, float* __restrict__ drow) {
+  const int j = lane & 15;
+  const float gz = j < hidden ? lowp_round(lowp_round(w2[j], lowp) * silu_grad(z), lowp) : 0.f;
+  for (int k = lane; k < K; k += 64) {
+    float acc = 0.f;
+    for (int jj = 0; jj < hidden; ++jj) acc += __shfl(gz, jj) * lowp_round(w1[(size_t)k * hidden + jj], lowp);
+    drow[k] = overwrite ? acc : drow[k] + acc;
+  }
+}
+
+// dh (the last-layer readout only, null otherwise): the readout's gradient is
+// stored there as well, so that the backward pass starts from it.
 __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, int K, const float* __restrict__ h,
                                                                          int h_stride, const float* __restrict__ w,
                                                                          const float* __restrict__ w1,
                                                                          const float* __restrict__ w2, int hidden,
                                                                          int lowp, int accumulate,
-                                                                         float* __restrict__ eps) {
+                                                                         float* __restrict__ eps,
+                                                                         float* __restrict__ dh) {
   const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (n >= N) return;
   const float* hrow = h + (size_t)n * h_stride;
@@ -335,6 +353,7 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, 
     if (j < hidden) v = lowp_round(silu(z), lowp) * lowp_round(w2[j], lowp);
 #pragma unroll
     for (int m = 8; m > 0; m >>= 1) v += __shfl_xor(v, m);
+    if (dh) readout_mlp_grad(z, K, w1, w2, hidden, lowp, lane, 1, dh + (size_t)n * h_stride);
   }
   if (lane == 0) eps[n] = accumulate ? eps[n] + v : v;
 }
@@ -358,13 +377,7 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_bwd_kernel(int N, 
     return;
   }
   const float z = readout_hidden_z(h + (size_t)n * h_stride, K, w1, hidden, lowp, lane);
-  const int j = lane & 15;
-  const float gz = j < hidden ? lowp_round(lowp_round(w2[j], lowp) * silu_grad(z), lowp) : 0.f;
-  for (int k = lane; k < K; k += 64) {
-    float acc = 0.f;
-    for (int jj = 0; jj < hidden; ++jj) acc += __shfl(gz, jj) * lowp_round(w1[(size_t)k * hidden + jj], lowp);
-    drow[k] = overwrite ? acc : drow[k] + acc;
-  }
+  readout_mlp_grad(z, K, w1, w2, hidden, lowp, lane, overwrite, drow);
 }
 
 // Per-graph energy in FP64, fixed order: strided partial sums, then a tree.
@@ -404,10 +417,10 @@ __global__ void species_table_kernel(int S, int K, const float* __restrict__ emb
 }
 
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int lowp, int accumulate, float* eps) {
+                        const float* w2, int hidden, int lowp, int accumulate, float* eps, float* dh) {
   if (N <= 0) return;
   readout_fwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
-      N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps);
+      N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps, w ? nullptr : dh);
 }
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
                         const float* w2, int hidden, int lowp, int overwrite, float* dh) {

@@ -395,6 +395,7 @@ struct LinArgs {
   int KI;                   // channels per component of x (0: K)
   int accumulate;           // y += instead of y =
   int lowp;                 // 0: FP32; round x and w to 1: bfloat16, 2: binary16 before multiplying
+  const float* bias0;       // [K] or null: rounded like the weights and added last to component 0 of y
 };
 
 constexpr int kMaxRadialLayers = 4;
@@ -450,8 +451,11 @@ void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
 // block read once, every output component written once (read too when
 // accumulating or adding the residual).
 void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, double* flops, double* bytes);
+// dh: for the MLP readout (w null), also store its gradient dE/dh[n][0][k] there
+// (null: not wanted).
 void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
-                        const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps);
+                        const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps,
+                        float* dh);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
                         const float* w1, const float* w2, int hidden, int lowp, int overwrite, float* dh);
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E);
