@@ -588,6 +588,8 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
     launch_round(s, b.sp_round, b.sp_table, (size_t)m.d.n_species * K, h->tp_round);
   }
   const float inv_c = (float)(1.0 / m.d.c_norm);
+  ReadoutLin ro{};   // linear readouts not yet evaluated
+  int ro_acc = 0;     // eps already holds earlier readouts
   for (int t = 0; t < m.d.n_layers; ++t) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
@@ -639,19 +641,24 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
     {
       run_linear(h, s, h->prod[t], largs(h, b.B, hout, t > 0 ? b.sc : nullptr, false, 0));
     }
-    if (!L.last)
-      {
+    if (!L.last) {
+      // evaluated with the last layer's readout (or earlier, kMaxReadoutLin at a time)
+      if (ro.n == kMaxReadoutLin) {
         PROF(KID_READOUT);
-        launch_readout_fwd(s, N, K, hout, L.dout * K, b.w + m.off.at(pre + "readout"), nullptr, nullptr, 0, lowp,
-                           t > 0, eps, nullptr);
+        launch_readout_fwd(s, N, K, ro, nullptr, 0, nullptr, nullptr, 0, lowp, ro_acc, eps, nullptr);
+        ro_acc = 1;
+        ro.n = 0;
       }
-    else
-      {
-        PROF(KID_READOUT);
-        launch_readout_fwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, t > 0, eps,
-                           seed_grad && L.dout == 1 ? b.dh0 : nullptr);
-      }
+      ro.h[ro.n] = hout;
+      ro.w[ro.n] = b.w + m.off.at(pre + "readout");
+      ro.stride[ro.n] = L.dout * K;
+      ++ro.n;
+    } else {
+      PROF(KID_READOUT);
+      launch_readout_fwd(s, N, K, ro, hout, L.dout * K, b.w + m.off.at(pre + "readout.0"),
+                         b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, ro_acc, eps,
+                         seed_grad && L.dout == 1 ? b.dh0 : nullptr);
+    }
   }
 }
 

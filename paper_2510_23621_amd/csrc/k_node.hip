@@ -330,10 +330,24 @@ __device__ __forceinline__ void readout_mlp_grad(float z, int K, const float* __
   }
 }
 
-// dh (the last-layer readout only, null otherwise): the readout's gradient is
-// stored there as well, so that the backward pass starts from it.
-__global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, int K, const float* __restrict__ h,
-                                                                         int h_stride, const float* __restrict__ w,
+// sum_k h[k] w[k] of a linear readout, in every lane (fixed order: strided
+// partial sums, then an xor-butterfly)
+__device__ __forceinline__ float readout_linear(const float* __restrict__ hrow, int K, const float* __restrict__ w,
+                                                int lowp, int lane) {
+  float v = 0.f;
+  for (int k = lane; k < K; k += 64) v += lowp_round(hrow[k], lowp) * lowp_round(w[k], lowp);
+#pragma unroll
+  for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+
+// eps[n] = (prior) + lin readout 0 + lin readout 1 + ... + MLP readout, added
+// left to right: the prior is eps[n] itself when accumulate is set, and the MLP
+// readout (h non-null, the last layer) reads h. dh (MLP readout only, null
+// otherwise): its gradient is stored there as well, so that the backward pass
+// starts from it.
+__global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, int K, ReadoutLin lin,
+                                                                         const float* __restrict__ h, int h_stride,
                                                                          const float* __restrict__ w1,
                                                                          const float* __restrict__ w2, int hidden,
                                                                          int lowp, int accumulate,
@@ -341,21 +355,23 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, 
                                                                          float* __restrict__ dh) {
   const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (n >= N) return;
-  const float* hrow = h + (size_t)n * h_stride;
-  float v = 0.f;
-  if (w) {
-    for (int k = lane; k < K; k += 64) v += lowp_round(hrow[k], lowp) * lowp_round(w[k], lowp);
-#pragma unroll
-    for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m);
-  } else {
-    const float z = readout_hidden_z(hrow, K, w1, hidden, lowp, lane);
+  bool have = accumulate != 0;
+  float v = have ? eps[n] : 0.f;
+  for (int i = 0; i < lin.n; ++i) {
+    const float r = readout_linear(lin.h[i] + (size_t)n * lin.stride[i], K, lin.w[i], lowp, lane);
+    v = have ? v + r : r;
+    have = true;
+  }
+  if (h) {
+    const float z = readout_hidden_z(h + (size_t)n * h_stride, K, w1, hidden, lowp, lane);
     const int j = lane & 15;
-    if (j < hidden) v = lowp_round(silu(z), lowp) * lowp_round(w2[j], lowp);
+    float r = j < hidden ? lowp_round(silu(z), lowp) * lowp_round(w2[j], lowp) : 0.f;
 #pragma unroll
-    for (int m = 8; m > 0; m >>= 1) v += __shfl_xor(v, m);
+    for (int m = 8; m > 0; m >>= 1) r += __shfl_xor(r, m);
+    v = have ? v + r : r;
     if (dh) readout_mlp_grad(z, K, w1, w2, hidden, lowp, lane, 1, dh + (size_t)n * h_stride);
   }
-  if (lane == 0) eps[n] = accumulate ? eps[n] + v : v;
+  if (lane == 0) eps[n] = v;
 }
 
 // dE/dh[n][0][k] from the readout (energy = sum of eps): added to dh, or
@@ -416,11 +432,12 @@ __global__ void species_table_kernel(int S, int K, const float* __restrict__ emb
   table[idx] = (float)acc;
 }
 
-void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int lowp, int accumulate, float* eps, float* dh) {
-  if (N <= 0) return;
+void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, const float* h, int h_stride,
+                        const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps,
+                        float* dh) {
+  if (N <= 0 || (lin.n == 0 && !h)) return;
   readout_fwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
-      N, K, h, h_stride, w, w1, w2, hidden, lowp, accumulate, eps, w ? nullptr : dh);
+      N, K, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, h ? dh : nullptr);
 }
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
                         const float* w2, int hidden, int lowp, int overwrite, float* dh) {

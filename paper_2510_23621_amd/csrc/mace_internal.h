@@ -451,9 +451,19 @@ void launch_linear(hipStream_t s, const LinPlanRef& plan, const LinArgs& a);
 // block read once, every output component written once (read too when
 // accumulating or adding the residual).
 void linear_work(const LinPlan& p, const LinArgs& a, int64_t N, int n_species, double* flops, double* bytes);
-// dh: for the MLP readout (w null), also store its gradient dE/dh[n][0][k] there
-// (null: not wanted).
-void launch_readout_fwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
+// Linear readouts (sum_k h[n][0][k] w[k]) of layers below the last, evaluated
+// together with the last layer's
+constexpr int kMaxReadoutLin = 4;
+struct ReadoutLin {
+  const float* h[kMaxReadoutLin];   // [N][stride] layer outputs
+  const float* w[kMaxReadoutLin];   // [K] readout weights
+  int stride[kMaxReadoutLin];
+  int n;
+};
+// eps[n] = (eps[n] if accumulate) + the linear readouts in order + the MLP
+// readout of h (null: none), added left to right. dh: for the MLP readout, also
+// store its gradient dE/dh[n][0][k] there (null: not wanted).
+void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, const float* h, int h_stride,
                         const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps,
                         float* dh);
 void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,

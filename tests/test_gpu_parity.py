@@ -63,17 +63,18 @@ def test_small_water_variants_fp32(K, hl):
 
 
 def test_many_layers_fp32():
-    """Five interaction layers: more than the four layers one launch of the
+    """Six interaction layers: more than the four layers one launch of the
     edge prologue (geometry plus the radial hidden layers) takes, so the
-    chunked launches are exercised; the backward accumulates dE/dY and dE/de
-    over five layers."""
-    params = model_params(0, K=32, hidden_lmax=1, n_layers=5, **STRESS)
+    chunked launches are exercised; five linear readouts below the last layer,
+    more than one readout launch takes, so the node energies are built over two
+    launches; the backward accumulates dE/dY and dE/de over six layers."""
+    params = model_params(0, K=32, hidden_lmax=1, n_layers=6, **STRESS)
     bo = oracle_blob(params, 5, STRESS_GAINS)
     bl = lib_blob(params, 5, STRESS_GAINS)
     sysm = synth.water_box(12, seed=11, box=7.5)
     ref = run_oracle(params, sysm, bo)
     gpu = run_gpu(params, sysm, bl)
-    assert_parity(gpu, ref, B.MACE_FP32, "water36 five layers")
+    assert_parity(gpu, ref, B.MACE_FP32, "water36 six layers")
 
 
 def test_molecule_batch_fp32_and_bf16():
