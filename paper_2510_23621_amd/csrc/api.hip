@@ -262,12 +262,12 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
 enum KernelId {
   KID_EDGE_FEATURES = 0, KID_TP_FWD, KID_LINEAR, KID_SYMCON_FWD, KID_READOUT,
   KID_TP_BWD, KID_RADIAL_BWD, KID_SYMCON_BWD, KID_SENDER_SUM, KID_EDGE_BWD, KID_FORCES, KID_GRAPH_ENERGY,
-  KID_FILL, KID_L0_GATHER, KID_L0_BWD, KID_COUNT
+  KID_L0_GATHER, KID_L0_BWD, KID_COUNT
 };
 const char* kKernelNames[KID_COUNT] = {
   "edge_prologue_kernel", "tpr_fwd_kernel", "linear_kernel", "symcon_fwd_kernel",
   "readout_kernel", "tpr_bwd_kernel", "radial_bwd_kernel", "symcon_bwd_kernel", "sender_sum_kernel",
-  "edge_vjp_kernel", "forces_kernel", "graph_energy_kernel", "fill_kernel", "l0_gather_kernel",
+  "edge_vjp_kernel", "forces_kernel", "graph_energy_kernel", "l0_gather_kernel",
   "l0_edge_bwd_kernel"};
 constexpr int kProfPairs = 4096;
 
@@ -657,7 +657,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
       PROF(KID_READOUT);
       launch_readout_fwd(s, N, K, ro, hout, L.dout * K, b.w + m.off.at(pre + "readout.0"),
                          b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, ro_acc, eps,
-                         seed_grad && L.dout == 1 ? b.dh0 : nullptr);
+                         seed_grad ? b.dh0 : nullptr);
     }
   }
 }
@@ -674,23 +674,10 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
     const LayerPlan& L = m.layers[t];
     const std::string pre = std::to_string(t) + ".";
     float* hout = L.last ? b.hlast : b.hin[t + 1];
-    if (L.last && L.dout == 1) {
-      // the forward's readout stored its gradient in dnext (b.dh0)
-    } else if (L.last) {
-      // the energy reaches the last layer's output only through its readout:
-      // the readout's gradient is stored, the other components are zero
-      if (L.dout > 1) {
-        PROF(KID_FILL);
-        launch_fill(s, dnext, (size_t)N * L.dout * K, 0.f);
-      }
-      {
-        PROF(KID_READOUT);
-        launch_readout_bwd(s, N, K, hout, L.dout * K, nullptr, b.w + m.off.at(pre + "readout.0"),
-                           b.w + m.off.at(pre + "readout.1"), m.d.readout_hidden, lowp, L.dout == 1, dnext);
-      }
-    }
-    // a layer below the last: its readout's gradient (the readout weights) was
-    // added to dnext by the epilogue of the transposed linear that wrote it
+    // dnext already holds dE/d(output of layer t): for the last layer (one
+    // scalar component) its forward readout stored it; for a layer below the
+    // last, the transposed linear that wrote dnext added that layer's readout
+    // gradient (the readout weights) in its epilogue.
     {
       run_linear(h, s, h->prodT[t], largs(h, dnext, b.dB, nullptr, true, 0));
     }

@@ -1,6 +1,6 @@
 // Per-edge geometry backward (g_e = dE/dd_e from dE/dY_e and dE/de_e), the
-// deterministic force assembly F_i = sum_{e: rcv=i} g_e - sum_{e: snd=i} g_e,
-// and a fill kernel. (The forward geometry runs in the edge prologue of
+// deterministic force assembly F_i = sum_{e: rcv=i} g_e - sum_{e: snd=i} g_e.
+// (The forward geometry runs in the edge prologue of
 // k_radial.hip.)
 #include "mace_internal.h"
 
@@ -57,12 +57,6 @@ __global__ void __launch_bounds__(256) forces_kernel(int N, const int* __restric
     F[3 * i + 1] = (float)fy;
     F[3 * i + 2] = (float)fz;
   }
-}
-
-__global__ void fill_kernel(float* p, size_t n, float v) {
-  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (; i < n; i += stride) p[i] = v;
 }
 
 // stress[gi][a][b] = inv_vol[gi] * sum over the graph's edges of d_e[a] g_e[b]
@@ -138,13 +132,6 @@ void launch_round(hipStream_t s, float* dst, const float* src, size_t n, int rnd
   size_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   round_kernel<<<(unsigned)blocks, 256, 0, s>>>(dst, src, n, rnd);
-}
-
-void launch_fill(hipStream_t s, float* p, size_t n, float v) {
-  if (n == 0) return;
-  size_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  fill_kernel<<<(unsigned)blocks, 256, 0, s>>>(p, n, v);
 }
 
 }  // namespace mace

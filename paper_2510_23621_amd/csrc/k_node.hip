@@ -317,7 +317,8 @@ __device__ __forceinline__ float readout_hidden_z(const float* __restrict__ hrow
 }
 
 // dE/dh[n][0][k] = sum_j W1[k][j] w2[j] silu'(z_j) of the last-layer readout,
-// stored to drow or added to it
+// stored to drow or added to it (the energy reaches the last layer's output, a
+// single scalar component, only through this readout)
 __device__ __forceinline__ void readout_mlp_grad(float z, int K, const float* __restrict__ w1,
                                                  const float* __restrict__ w2, int hidden, int lowp, int lane,
                                                  int overwrite, float* __restrict__ drow) {
@@ -374,28 +375,6 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, 
   if (lane == 0) eps[n] = v;
 }
 
-// dE/dh[n][0][k] from the readout (energy = sum of eps): added to dh, or
-// stored when overwrite is set.
-__global__ void __launch_bounds__(64 * kReadoutNodes) readout_bwd_kernel(int N, int K, const float* __restrict__ h,
-                                                                         int h_stride, const float* __restrict__ w,
-                                                                         const float* __restrict__ w1,
-                                                                         const float* __restrict__ w2, int hidden,
-                                                                         int lowp, int overwrite,
-                                                                         float* __restrict__ dh) {
-  const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (n >= N) return;
-  float* drow = dh + (size_t)n * h_stride;
-  if (w) {
-    for (int k = lane; k < K; k += 64) {
-      const float g = lowp_round(w[k], lowp);
-      drow[k] = overwrite ? g : drow[k] + g;
-    }
-    return;
-  }
-  const float z = readout_hidden_z(h + (size_t)n * h_stride, K, w1, hidden, lowp, lane);
-  readout_mlp_grad(z, K, w1, w2, hidden, lowp, lane, overwrite, drow);
-}
-
 // Per-graph energy in FP64, fixed order: strided partial sums, then a tree.
 __global__ void __launch_bounds__(256) graph_energy_kernel(int G, const int* __restrict__ off,
                                                            const float* __restrict__ eps, double* __restrict__ E) {
@@ -438,12 +417,6 @@ void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, cons
   if (N <= 0 || (lin.n == 0 && !h)) return;
   readout_fwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
       N, K, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, h ? dh : nullptr);
-}
-void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w, const float* w1,
-                        const float* w2, int hidden, int lowp, int overwrite, float* dh) {
-  if (N <= 0) return;
-  readout_bwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
-      N, K, h, h_stride, w, w1, w2, hidden, lowp, overwrite, dh);
 }
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
   if (G <= 0) return;

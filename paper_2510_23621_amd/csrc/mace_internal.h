@@ -466,12 +466,9 @@ struct ReadoutLin {
 void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, const float* h, int h_stride,
                         const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps,
                         float* dh);
-void launch_readout_bwd(hipStream_t s, int N, int K, const float* h, int h_stride, const float* w,
-                        const float* w1, const float* w2, int hidden, int lowp, int overwrite, float* dh);
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E);
 void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp,
                           float* table);
-void launch_fill(hipStream_t s, float* p, size_t n, float v);
 void launch_round(hipStream_t s, float* dst, const float* src, size_t n, int rnd);   // no-op for rnd = 0
 
 }  // namespace mace
