@@ -303,40 +303,68 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
 // a fixed order.
 constexpr int kReadoutNodes = 4;
 
-// z_j of the last-layer readout, in every lane whose hidden index is j
-__device__ __forceinline__ float readout_hidden_z(const float* __restrict__ hrow, int K,
-                                                  const float* __restrict__ w1, int hidden, int lowp, int lane) {
+constexpr int kReadoutHiddenMax = 16;
+
+// z_j of the last-layer readout, in every lane whose hidden index is j (each
+// lane's loads are issued together, then summed in k order). sw1: W1 in LDS,
+// already rounded, row pitch hp.
+template <int K>
+__device__ __forceinline__ float readout_hidden_z(const float* __restrict__ hrow, const float* sw1, int hp,
+                                                  int hidden, int lowp, int lane) {
   const int j = lane & 15, q = lane >> 4;
-  const int kq = K / 4;
+  constexpr int kq = K / 4;
+  float hv[kq], wv[kq];
+#pragma unroll
+  for (int i = 0; i < kq; ++i) {
+    hv[i] = j < hidden ? hrow[q * kq + i] : 0.f;
+    wv[i] = j < hidden ? sw1[(q * kq + i) * hp + j] : 0.f;
+  }
   float z = 0.f;
-  if (j < hidden)
-    for (int k = q * kq; k < (q + 1) * kq; ++k) z += lowp_round(hrow[k], lowp) * lowp_round(w1[(size_t)k * hidden + j], lowp);
+#pragma unroll
+  for (int i = 0; i < kq; ++i) z += lowp_round(hv[i], lowp) * wv[i];
   z += __shfl_xor(z, 16);
   z += __shfl_xor(z, 32);
   return z;
 }
 
 // dE/dh[n][0][k] = sum_j W1[k][j] w2[j] silu'(z_j) of the last-layer readout,
-// stored to drow or added to it (the energy reaches the last layer's output, a
-// single scalar component, only through this readout)
-__device__ __forceinline__ void readout_mlp_grad(float z, int K, const float* __restrict__ w1,
-                                                 const float* __restrict__ w2, int hidden, int lowp, int lane,
-                                                 int overwrite, float* __restrict__ drow) {
+// stored to drow (the energy reaches the last layer's output, a single scalar
+// component, only through this readout)
+template <int K>
+__device__ __forceinline__ void readout_mlp_grad(float z, const float* sw1, int hp, const float* __restrict__ w2,
+                                                 int hidden, int lowp, int lane, float* __restrict__ drow) {
   const int j = lane & 15;
   const float gz = j < hidden ? lowp_round(lowp_round(w2[j], lowp) * silu_grad(z), lowp) : 0.f;
-  for (int k = lane; k < K; k += 64) {
-    float acc = 0.f;
-    for (int jj = 0; jj < hidden; ++jj) acc += __shfl(gz, jj) * lowp_round(w1[(size_t)k * hidden + jj], lowp);
-    drow[k] = overwrite ? acc : drow[k] + acc;
+  float gs[kReadoutHiddenMax];
+#pragma unroll
+  for (int jj = 0; jj < kReadoutHiddenMax; ++jj) gs[jj] = __shfl(gz, jj);
+#pragma unroll
+  for (int r = 0; r < (K + 63) / 64; ++r) {
+    const int k = lane + 64 * r;
+    if (k < K) {
+      float wv[kReadoutHiddenMax];
+#pragma unroll
+      for (int jj = 0; jj < kReadoutHiddenMax; ++jj) wv[jj] = jj < hidden ? sw1[k * hp + jj] : 0.f;
+      float acc = 0.f;
+#pragma unroll
+      for (int jj = 0; jj < kReadoutHiddenMax; ++jj)
+        if (jj < hidden) acc += gs[jj] * wv[jj];
+      drow[k] = acc;
+    }
   }
 }
 
 // sum_k h[k] w[k] of a linear readout, in every lane (fixed order: strided
 // partial sums, then an xor-butterfly)
-__device__ __forceinline__ float readout_linear(const float* __restrict__ hrow, int K, const float* __restrict__ w,
-                                                int lowp, int lane) {
+template <int K>
+__device__ __forceinline__ float readout_linear(const float* __restrict__ hrow, const float* __restrict__ w, int lowp,
+                                                int lane) {
   float v = 0.f;
-  for (int k = lane; k < K; k += 64) v += lowp_round(hrow[k], lowp) * lowp_round(w[k], lowp);
+#pragma unroll
+  for (int r = 0; r < (K + 63) / 64; ++r) {
+    const int k = lane + 64 * r;
+    if (k < K) v += lowp_round(hrow[k], lowp) * lowp_round(w[k], lowp);
+  }
 #pragma unroll
   for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m);
   return v;
@@ -347,7 +375,8 @@ __device__ __forceinline__ float readout_linear(const float* __restrict__ hrow, 
 // readout (h non-null, the last layer) reads h. dh (MLP readout only, null
 // otherwise): its gradient is stored there as well, so that the backward pass
 // starts from it.
-__global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, int K, ReadoutLin lin,
+template <int K>
+__global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, ReadoutLin lin,
                                                                          const float* __restrict__ h, int h_stride,
                                                                          const float* __restrict__ w1,
                                                                          const float* __restrict__ w2, int hidden,
@@ -355,22 +384,30 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, 
                                                                          float* __restrict__ eps,
                                                                          float* __restrict__ dh) {
   const int n = blockIdx.x * kReadoutNodes + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  // W1 rounded into LDS, row pitch hidden + 1 (the gradient's lanes run over k)
+  __shared__ float sw1[K * (kReadoutHiddenMax + 1)];
+  const int hp = hidden + 1;
+  if (h) {
+    for (int idx = threadIdx.x; idx < K * hidden; idx += blockDim.x)
+      sw1[(idx / hidden) * hp + idx % hidden] = lowp_round(w1[idx], lowp);
+    __syncthreads();
+  }
   if (n >= N) return;
   bool have = accumulate != 0;
   float v = have ? eps[n] : 0.f;
   for (int i = 0; i < lin.n; ++i) {
-    const float r = readout_linear(lin.h[i] + (size_t)n * lin.stride[i], K, lin.w[i], lowp, lane);
+    const float r = readout_linear<K>(lin.h[i] + (size_t)n * lin.stride[i], lin.w[i], lowp, lane);
     v = have ? v + r : r;
     have = true;
   }
   if (h) {
-    const float z = readout_hidden_z(h + (size_t)n * h_stride, K, w1, hidden, lowp, lane);
+    const float z = readout_hidden_z<K>(h + (size_t)n * h_stride, sw1, hp, hidden, lowp, lane);
     const int j = lane & 15;
     float r = j < hidden ? lowp_round(silu(z), lowp) * lowp_round(w2[j], lowp) : 0.f;
 #pragma unroll
     for (int m = 8; m > 0; m >>= 1) r += __shfl_xor(r, m);
     v = have ? v + r : r;
-    if (dh) readout_mlp_grad(z, K, w1, w2, hidden, lowp, lane, 1, dh + (size_t)n * h_stride);
+    if (dh) readout_mlp_grad<K>(z, sw1, hp, w2, hidden, lowp, lane, dh + (size_t)n * h_stride);
   }
   if (lane == 0) eps[n] = v;
 }
@@ -415,8 +452,14 @@ void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, cons
                         const float* w1, const float* w2, int hidden, int lowp, int accumulate, float* eps,
                         float* dh) {
   if (N <= 0 || (lin.n == 0 && !h)) return;
-  readout_fwd_kernel<<<(N + kReadoutNodes - 1) / kReadoutNodes, 64 * kReadoutNodes, 0, s>>>(
-      N, K, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, h ? dh : nullptr);
+  const dim3 grid((N + kReadoutNodes - 1) / kReadoutNodes), block(64 * kReadoutNodes);
+  float* dhx = h ? dh : nullptr;
+  switch (K) {
+    case 32: readout_fwd_kernel<32><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
+    case 64: readout_fwd_kernel<64><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
+    case 96: readout_fwd_kernel<96><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
+    case 128: readout_fwd_kernel<128><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
+  }
 }
 void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
   if (G <= 0) return;
