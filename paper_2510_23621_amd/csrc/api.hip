@@ -164,8 +164,7 @@ struct Buffers {
   float* w_round = nullptr;   // precision study: rounded copies of the last radial layers' weights
   unsigned short *wbf = nullptr, *wbfT = nullptr;   // 16-bit K-packed copies (BF16- / FP16-linear modes)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
-      *snd_perm = nullptr, *graph_off = nullptr, *node_order = nullptr, *tile_start = nullptr,
-      *tile_count = nullptr, *tile_species = nullptr, *quad_tile = nullptr, *quad_count = nullptr;
+      *snd_perm = nullptr, *graph_off = nullptr, *quad_node = nullptr, *quad_species = nullptr;
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
@@ -203,13 +202,9 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.snd_off = c.take<int>(N + 1);
   b.snd_perm = c.take<int>(std::max<int64_t>(E, 1));
   b.graph_off = c.take<int>(G + 1);
-  b.node_order = c.take<int>(N);
-  int64_t nt = n_tiles_bound(N, (int)S);
-  b.tile_start = c.take<int>(nt);
-  b.tile_count = c.take<int>(nt);
-  b.tile_species = c.take<int>(nt);
-  b.quad_tile = c.take<int>(nt);
-  b.quad_count = c.take<int>(nt);
+  const int64_t nt = n_tiles_bound(N, (int)S);   // also bounds the number of quads
+  b.quad_node = c.take<int>(nt * kLinQuad * kLinTileNodes);
+  b.quad_species = c.take<int>(nt);
   b.shift = c.take<double4>(std::max<int64_t>(E, 1));
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
@@ -510,13 +505,8 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.w = transposed ? h->b.wT : h->b.w;
   a.wt = transposed ? h->b.w : h->b.wT;
   a.wbf = transposed ? h->b.wbfT : h->b.wbf;
-  a.tile_start = h->b.tile_start;
-  a.tile_count = h->b.tile_count;
-  a.tile_species = h->b.tile_species;
-  a.node_order = h->b.node_order;
-  a.n_tiles = h->n_tiles;
-  a.quad_tile = h->b.quad_tile;
-  a.quad_count = h->b.quad_count;
+  a.quad_node = h->b.quad_node;
+  a.quad_species = h->b.quad_species;
   a.n_quads = h->n_quads;
   a.K = h->m.d.K;
   a.KI = 0;
@@ -1056,6 +1046,14 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
     t += n;
   }
   h->n_quads = (int)qtile.size();
+  std::vector<int32_t> qnode((size_t)h->n_quads * kLinQuad * kLinTileNodes, -1), qspec(h->n_quads);
+  for (int q = 0; q < h->n_quads; ++q) {
+    qspec[q] = tspec[qtile[q]];
+    for (int w = 0; w < qcount[q]; ++w) {
+      const int t = qtile[q] + w;
+      for (int r = 0; r < tcount[t]; ++r) qnode[((size_t)q * kLinQuad + w) * kLinTileNodes + r] = order[tstart[t] + r];
+    }
+  }
   Carver c{reinterpret_cast<char*>(workspace)};
   carve(h->m, N, E, G, c, h->b);
   Buffers& b = h->b;
@@ -1087,12 +1085,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       inv_vol[gi] = det != 0.0 ? 1.0 / std::fabs(det) : 0.0;
     }
   chk(up(b.inv_vol, inv_vol.data(), G * 8));
-  chk(up(b.node_order, order.data(), N * 4));
-  chk(up(b.tile_start, tstart.data(), tstart.size() * 4));
-  chk(up(b.tile_count, tcount.data(), tcount.size() * 4));
-  chk(up(b.tile_species, tspec.data(), tspec.size() * 4));
-  chk(up(b.quad_tile, qtile.data(), qtile.size() * 4));
-  chk(up(b.quad_count, qcount.data(), qcount.size() * 4));
+  chk(up(b.quad_node, qnode.data(), qnode.size() * 4));
+  chk(up(b.quad_species, qspec.data(), qspec.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
   chk(hipMemsetAsync(b.status, 0, sizeof(int), s));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),

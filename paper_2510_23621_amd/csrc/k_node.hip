@@ -47,6 +47,7 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   constexpr bool BF16 = LP != 0;   // any 16-bit path
   const LinLaunch& L = *Lp;
   static_assert(KI % 32 == 0 && K % 16 == 0, "KI is a multiple of 32, K of 16");
+  static_assert(kLinTileNodes == 16, "a node tile is the 16 rows of one MFMA");
   static_assert(!BF16 || KI == K, "16-bit linears are square");
   constexpr int PF = KI + 4;   // FP32 panel row pitch in floats (4 mod 32: conflict-free 16-byte reads)
   constexpr int PB = KI + 8;   // 16-bit panel row pitch in elements (68 dwords at K = 128)
@@ -61,16 +62,13 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
   const int ncol = min(16 * CT, K - 16 * ct0);   // valid panel columns (K = 32 or 96: the last 64 are partial)
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int quad = blockIdx.x;
-  const int tile0 = a.quad_tile[quad], ntile = a.quad_count[quad];
-  const int tile = tile0 + min(w, ntile - 1);   // spare waves shadow a valid tile and store nothing
-  const bool active = w < ntile;
-  const int t0 = a.tile_start[tile], cnt = a.tile_count[tile];
-  const int z = a.tile_species[tile0];
+  const int z = a.quad_species[quad];
   const int64_t zstride = (int64_t)z * L.plan.w_sstride;
-  // A rows: node of MFMA row l%16 (rows past the tile's count re-read its
-  // last node and are zeroed)
-  const int node = a.node_order[t0 + min(l & 15, cnt - 1)];
-  const float keep = (l & 15) < cnt ? 1.f : 0.f;
+  // A rows: node of MFMA row l%16 (a row without a node reads node 0 and is
+  // zeroed; a spare wave has none and stores nothing)
+  const int row_node = a.quad_node[((size_t)quad * kLinQuad + w) * kLinTileNodes + (l & 15)];
+  const int node = max(row_node, 0);
+  const float keep = row_node >= 0 ? 1.f : 0.f;
   f4 acc[CT];
 #pragma unroll
   for (int j = 0; j < CT; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
@@ -171,7 +169,9 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
         }
     }
   }
-  if (!active) return;
+  int out_node[4];   // node of result row 4 (l / 16) + r, -1 for none
+#pragma unroll
+  for (int r = 0; r < 4; ++r) out_node[r] = __shfl(row_node, 4 * (l >> 4) + r);
   float* y = grp.dst ? a.y2 : a.y;
   const int cout = grp.dst ? L.plan.cout2 : L.plan.cout;
   const float* residual = grp.dst ? nullptr : a.residual;
@@ -181,9 +181,8 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
     if (ct >= nct) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int q = 4 * (l >> 4) + r;
-      if (q >= cnt) continue;
-      const size_t o = ((size_t)a.node_order[t0 + q] * cout + grp.out_c0 + c) * K + 16 * ct + (l & 15);
+      if (out_node[r] < 0) continue;
+      const size_t o = ((size_t)out_node[r] * cout + grp.out_c0 + c) * K + 16 * ct + (l & 15);
       float v = acc[j][r];
       if (residual) v += residual[o];
       if (a.accumulate) v += y[o];

@@ -384,13 +384,10 @@ struct LinArgs {
   const float* w;           // weight base (FP32, row-major [in][out])
   const float* wt;          // the same blob with every K x K block transposed ([out][in])
   const unsigned short* wbf;  // same tensors in the low precision (bf16 or binary16 bits), each K x K block packed [K/8][K][8]
-  const int* tile_start;    // [n_tiles] start in node_order
-  const int* tile_count;    // [n_tiles]
-  const int* tile_species;  // [n_tiles]
-  const int* node_order;    // nodes grouped by species
-  const int* quad_tile;     // [n_quads] first tile of a run of <= kLinQuad tiles of one species
-  const int* quad_count;    // [n_quads] tiles in the run
-  int n_tiles, n_quads;
+  const int* quad_node;     // [n_quads][kLinQuad][16]: node of MFMA row r of wave w of a block, -1 for none
+                            // (a block's nodes are up to kLinQuad tiles of 16 nodes of one species)
+  const int* quad_species;  // [n_quads]
+  int n_quads;
   int K;                    // channels per component of y (and of x unless KI is set)
   int KI;                   // channels per component of x (0: K)
   int accumulate;           // y += instead of y =
