@@ -652,7 +652,9 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
   }
 }
 
-void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
+// Ends with the forces F and, in the same launch, the per-graph energies
+// graph_e of the node energies eps.
+void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F, const float* eps, double* graph_e) {
   const Model& m = h->m;
   Buffers& b = h->b;
   const int N = (int)h->N, E = (int)h->E, K = m.d.K, T = m.d.n_layers;
@@ -734,7 +736,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F) {
   }
   {
     PROF(KID_FORCES);
-    launch_forces(s, N, b.rcv_off, b.snd_off, b.snd_perm, b.g, F);
+    launch_forces(s, N, b.rcv_off, b.snd_off, b.snd_perm, b.g, F, h->G, b.graph_off, eps, graph_e);
   }
 }
 
@@ -1125,12 +1127,7 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
   if (!g || !positions || !node_energy || !graph_energy || !forces) return MACE_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   run_forward(g, s, positions, node_energy, true);
-  {
-    mace_graph* h = g;
-    PROF(KID_GRAPH_ENERGY);
-    launch_graph_energy(s, g->G, g->b.graph_off, node_energy, graph_energy);
-  }
-  run_backward(g, s, positions, forces);
+  run_backward(g, s, positions, forces, node_energy, graph_energy);
   return hip_ok(hipGetLastError());
 }
 

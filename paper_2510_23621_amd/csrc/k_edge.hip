@@ -27,13 +27,43 @@ __global__ void __launch_bounds__(256) edge_vjp_kernel(int E, const float* __res
   g[e] = edge_geometry_vjp(e, pos, snd, rcv, shift, rc, p, nb, dyv, de + (size_t)e * nb);
 }
 
-// One wave per atom: lanes take the atom's receiver edges and sender edges
-// in strides of 64, FP64 partial sums (the two sums cancel to a small net
-// force), then a fixed xor-tree across lanes: deterministic.
+// Per-graph energy of graph gi in FP64, fixed order: strided partial sums,
+// then a tree (a block of 256 threads).
+__device__ __forceinline__ void graph_energy_block(int gi, const int* __restrict__ off, const float* __restrict__ eps,
+                                                   double* __restrict__ E) {
+  __shared__ double red[256];
+  double acc = 0.0;
+  for (int i = off[gi] + threadIdx.x; i < off[gi + 1]; i += blockDim.x) acc += (double)eps[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) E[gi] = red[0];
+}
+
+__global__ void __launch_bounds__(256) graph_energy_kernel(int G, const int* __restrict__ off,
+                                                           const float* __restrict__ eps, double* __restrict__ E) {
+  graph_energy_block(blockIdx.x, off, eps, E);
+}
+
+// Forces: one wave per atom, lanes take the atom's receiver edges and sender
+// edges in strides of 64, FP64 partial sums (the two sums cancel to a small net
+// force), then a fixed xor-tree across lanes: deterministic. The blocks after
+// the atoms' ((N + 3) / 4 of them) compute the per-graph energies, which are
+// independent of the forces: one launch for both.
 __global__ void __launch_bounds__(256) forces_kernel(int N, const int* __restrict__ rcv_off,
                                                      const int* __restrict__ snd_off,
                                                      const int* __restrict__ snd_perm,
-                                                     const float4* __restrict__ g, float* __restrict__ F) {
+                                                     const float4* __restrict__ g, float* __restrict__ F,
+                                                     const int* __restrict__ graph_off,
+                                                     const float* __restrict__ eps, double* __restrict__ E) {
+  const int nfb = (N + 3) / 4;
+  if ((int)blockIdx.x >= nfb) {
+    graph_energy_block(blockIdx.x - nfb, graph_off, eps, E);
+    return;
+  }
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= N) return;
@@ -115,9 +145,14 @@ void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, con
 }
 
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
-                   const float4* g, float* F) {
+                   const float4* g, float* F, int G, const int* graph_off, const float* eps, double* E) {
   if (N <= 0) return;
-  forces_kernel<<<(N + 3) / 4, 256, 0, s>>>(N, rcv_off, snd_off, snd_perm, g, F);
+  forces_kernel<<<(N + 3) / 4 + G, 256, 0, s>>>(N, rcv_off, snd_off, snd_perm, g, F, graph_off, eps, E);
+}
+
+void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
+  if (G <= 0) return;
+  graph_energy_kernel<<<G, 256, 0, s>>>(G, graph_off, eps, E);
 }
 
 // dst[i] = src[i] rounded to nearest even (rnd 1: bfloat16, 2: binary16); in

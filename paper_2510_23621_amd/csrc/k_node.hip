@@ -411,22 +411,6 @@ __global__ void __launch_bounds__(64 * kReadoutNodes) readout_fwd_kernel(int N, 
   if (lane == 0) eps[n] = v;
 }
 
-// Per-graph energy in FP64, fixed order: strided partial sums, then a tree.
-__global__ void __launch_bounds__(256) graph_energy_kernel(int G, const int* __restrict__ off,
-                                                           const float* __restrict__ eps, double* __restrict__ E) {
-  __shared__ double red[256];
-  const int g = blockIdx.x;
-  double acc = 0.0;
-  for (int i = off[g] + threadIdx.x; i < off[g + 1]; i += blockDim.x) acc += (double)eps[i];
-  red[threadIdx.x] = acc;
-  __syncthreads();
-  for (int st = 128; st > 0; st >>= 1) {
-    if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) E[g] = red[0];
-}
-
 // table[z][k] = sum_k' emb[z][k'] Wup[k'][k]: layer-0 features depend only on
 // species. Accumulated in FP64 (one rounding, once per graph setup): a
 // rounding error here is shared by every atom of the species.
@@ -459,10 +443,6 @@ void launch_readout_fwd(hipStream_t s, int N, int K, const ReadoutLin& lin, cons
     case 96: readout_fwd_kernel<96><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
     case 128: readout_fwd_kernel<128><<<grid, block, 0, s>>>(N, lin, h, h_stride, w1, w2, hidden, lowp, accumulate, eps, dhx); break;
   }
-}
-void launch_graph_energy(hipStream_t s, int G, const int* graph_off, const float* eps, double* E) {
-  if (G <= 0) return;
-  graph_energy_kernel<<<G, 256, 0, s>>>(G, graph_off, eps, E);
 }
 void launch_species_table(hipStream_t s, int S, int K, const float* emb, const float* wup, int lowp, float* table) {
   species_table_kernel<<<(S * K + 127) / 128, 128, 0, s>>>(S, K, emb, wup, lowp, table);

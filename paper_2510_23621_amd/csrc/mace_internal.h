@@ -417,8 +417,10 @@ constexpr int kL0MaxSpecies = 4;
 void launch_edge_prologue(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv,
                           const double4* shift, double rc, int p, int nb, float* Y, float* rbf,
                           const RadialSet& rs, int* status);
+// F from the per-edge g; the same launch writes the per-graph energies E from
+// the node energies eps (as launch_graph_energy).
 void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm,
-                   const float4* g, float* F);
+                   const float4* g, float* F, int G, const int* graph_off, const float* eps, double* E);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate, int rnd);
 void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
