@@ -297,6 +297,81 @@ def build_graph(system, d: ModelDesc) -> Graph:
                  int(system.n_graphs))
 
 
+def _edge_features(d: ModelDesc, graph: Graph, pos: torch.Tensor, sl=slice(None)):
+    """Y [e,16] and the radial basis [e, n_basis] of the edges in slice sl
+    (graph problem statement; reading R3 for the edge vector)."""
+    snd, rcv = graph.sender[sl], graph.receiver[sl]
+    vec = pos[snd] + graph.shift_vec[sl] - pos[rcv]                      # R3
+    r = torch.sqrt((vec * vec).sum(-1))
+    u = vec / r[:, None]
+    Y = so3.sh_all(u, d.sh_lmax)                                         # [e,16]
+    rb = bessel_basis(r, d.r_cut, d.n_bessel, d.envelope_p)              # [e,8]
+    return Y, rb
+
+
+def _edge_messages(d: ModelDesc, W: dict, t: int, ht: dict, snd: torch.Tensor, Y: torch.Tensor,
+                   rb: torch.Tensor, bf16_radial: bool = False, rtp=None, rrad=None):
+    """Eq. 26 before the neighbour sum, per path p = (l_h, l_Y, l_out):
+    m[e, m3, k] = R[e, p, k] sum_{m1, m2} C[m1, m2, m3] ht[s_e, m1, k] Y[e, m2]
+    for the edges whose senders, harmonics and radial basis are given.
+    Returns a list over paths of [e, 2 l_out + 1, K]."""
+    rtp = rtp or (lambda x: x)
+    paths = tp_paths(d, t)
+    R = rtp(radial_mlp(rb, W, t, len(d.radial_hidden), bf16_radial, rnd=rrad).reshape(-1, len(paths), d.K))
+    out = []
+    for p, (lh, ly, lo) in enumerate(paths):
+        C = torch.from_numpy(so3.real_cg(lh, ly, lo))
+        hs = rtp(ht[lh][snd])                                             # [e, 2lh+1, K]
+        Yl = rtp(Y[:, ly * ly: ly * ly + 2 * ly + 1])                     # [e, 2ly+1]
+        out.append(torch.einsum("abc,eak,eb->eck", C, hs, Yl) * R[:, p, None, :])
+    return out
+
+
+def _linear_up(d: ModelDesc, W: dict, t: int, h: dict, lin) -> dict:
+    """Eq. 26's sender features W h^t, per l of the layer's input."""
+    return {l: lin(h[l], W[f"{t}.up.{l}"]) for l in layer_in_ls(d, t)}
+
+
+def _node_update(d: ModelDesc, W: dict, t: int, At: list, h: dict, z: torch.Tensor, lin, rsc=None):
+    """Everything of layer t after the neighbour sum, node by node: the
+    path-merging linear, the species linear (layer 0) or residual (t >= 1,
+    R7), the product basis (Eq. 27) with its weights, the product linear and
+    the layer's readout. At: per path [n, 2 l_out + 1, K], already divided
+    by c_norm; h: the layer's input features. Returns (h^{t+1}, eps_t [n])."""
+    in_ls, out_ls = layer_in_ls(d, t), layer_out_ls(d, t)
+    paths = tp_paths(d, t)
+    K = d.K
+    n = z.shape[0]
+    sc = {}
+    if t > 0:
+        for L in out_ls:
+            if L in in_ls:
+                sc[L] = lin.species(h[L], W[f"{t}.skip.{L}"], z)
+    A = []
+    for l in range(d.sh_lmax + 1):
+        acc = torch.zeros(n, 2 * l + 1, K, dtype=DT)
+        for p, (_, _, lo) in enumerate(paths):
+            if lo == l:
+                acc = acc + lin(At[p], W[f"{t}.linear.{p}"])
+        A.append(acc)
+    if t == 0:                                                             # R7
+        A = [lin.species(A[l], W[f"{t}.skip.{l}"], z) for l in range(d.sh_lmax + 1)]
+    Afull = torch.cat(A, dim=1)                                            # [n,16,K]
+    hn = {}
+    for L in out_ls:
+        B = symmetric_contraction(Afull, W, t, L, z, d.correlation, rnd=rsc)
+        hn[L] = lin(B, W[f"{t}.prod.{L}"])
+        if L in sc:
+            hn[L] = hn[L] + sc[L]
+    s0 = hn[0][:, 0, :]                                                    # [n,K]
+    if t < d.n_layers - 1:
+        e_t = lin(s0, W[f"{t}.readout"][:, None])[:, 0]
+    else:
+        hid = silu(lin(s0, W[f"{t}.readout.0"]))
+        e_t = lin(hid, W[f"{t}.readout.1"][:, None])[:, 0]
+    return hn, e_t, Afull
+
+
 def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
                   bf16_linear: bool = False, edge_chunk: int = 1 << 16,
                   return_intermediates: bool = False, fp16_linear: bool = False, bf16_radial: bool = False,
@@ -315,59 +390,24 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
     K = d.K
     snd, rcv = graph.sender, graph.receiver
     E = len(snd)
-    vec = pos[snd] + graph.shift_vec - pos[rcv]                          # R3
-    r = torch.sqrt((vec * vec).sum(-1))
-    u = vec / r[:, None]
-    Y = so3.sh_all(u, d.sh_lmax)                                         # [E,16]
-    rb = bessel_basis(r, d.r_cut, d.n_bessel, d.envelope_p)              # [E,8]
+    Y, rb = _edge_features(d, graph, pos)
     inter = {"Y": Y, "rbf": rb}
 
     # node embedding: linear on one-hot species
     h = {0: W["embed"][z][:, None, :]}                                   # {l: [N, 2l+1, K]}
     eps = torch.zeros(N, dtype=DT)
-    nh = len(d.radial_hidden)
     for t in range(d.n_layers):
-        in_ls, out_ls = layer_in_ls(d, t), layer_out_ls(d, t)
         paths = tp_paths(d, t)
-        sc = {}
-        if t > 0:
-            for L in out_ls:
-                if L in in_ls:
-                    sc[L] = lin.species(h[L], W[f"{t}.skip.{L}"], z)
-        ht = {l: lin(h[l], W[f"{t}.up.{l}"]) for l in in_ls}            # linear_up
+        ht = _linear_up(d, W, t, h, lin)                                  # linear_up
         At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
         for e0 in range(0, E, edge_chunk):
             sl = slice(e0, e0 + edge_chunk)
-            R = rtp(radial_mlp(rb[sl], W, t, nh, bf16_radial, rnd=rrad).reshape(-1, len(paths), K))  # [e,P,K]
-            for p, (lh, ly, lo) in enumerate(paths):
-                C = torch.from_numpy(so3.real_cg(lh, ly, lo))
-                hs = rtp(ht[lh][snd[sl]])                                 # [e, 2lh+1, K]
-                Yl = rtp(Y[sl, ly * ly: ly * ly + 2 * ly + 1])            # [e, 2ly+1]
-                msg = torch.einsum("abc,eak,eb->eck", C, hs, Yl) * R[:, p, None, :]
-                At[p] = At[p].index_add(0, rcv[sl], msg)
+            msg = _edge_messages(d, W, t, ht, snd[sl], Y[sl], rb[sl], bf16_radial, rtp, rrad)
+            for p in range(len(paths)):
+                At[p] = At[p].index_add(0, rcv[sl], msg[p])
         At = [a / d.c_norm for a in At]                                   # R6
-        A = []
-        for l in range(d.sh_lmax + 1):
-            acc = torch.zeros(N, 2 * l + 1, K, dtype=DT)
-            for p, (_, _, lo) in enumerate(paths):
-                if lo == l:
-                    acc = acc + lin(At[p], W[f"{t}.linear.{p}"])
-            A.append(acc)
-        if t == 0:                                                         # R7
-            A = [lin.species(A[l], W[f"{t}.skip.{l}"], z) for l in range(d.sh_lmax + 1)]
-        Afull = torch.cat(A, dim=1)                                        # [N,16,K]
-        hn = {}
-        for L in out_ls:
-            B = symmetric_contraction(Afull, W, t, L, z, d.correlation, rnd=rsc)
-            hn[L] = lin(B, W[f"{t}.prod.{L}"])
-            if L in sc:
-                hn[L] = hn[L] + sc[L]
-        s0 = hn[0][:, 0, :]                                                # [N,K]
-        if t < d.n_layers - 1:
-            eps = eps + lin(s0, W[f"{t}.readout"][:, None])[:, 0]
-        else:
-            hid = silu(lin(s0, W[f"{t}.readout.0"]))
-            eps = eps + lin(hid, W[f"{t}.readout.1"][:, None])[:, 0]
+        hn, e_t, Afull = _node_update(d, W, t, At, h, z, lin, rsc)
+        eps = eps + e_t
         if return_intermediates:
             inter[f"{t}.A"] = Afull
             inter[f"{t}.h"] = hn
@@ -375,6 +415,150 @@ def node_energies(d: ModelDesc, W: dict, graph: Graph, pos: torch.Tensor,
     if return_intermediates:
         return eps, inter
     return eps
+
+
+def energy_forces_chunked(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
+                          bf16_linear: bool = False, fp16_linear: bool = False, edge_chunk: int = 1 << 15,
+                          node_chunk: int = 256):
+    """Energies and forces of large graphs in bounded memory, by a two-pass
+    vector-Jacobian product over edge and node chunks.
+
+    The neighbour sum of Eq. 26 is linear in the edge messages, so with
+    g_t = dE/dAt_t known at the nodes, the gradient reaching edge e is
+    g_t[r_e] / c_norm and the edges can be back-propagated chunk by chunk;
+    every step after the neighbour sum acts node by node, so its backward
+    runs in node chunks. Pass 1 (no gradients) evaluates the model as
+    node_energies does and keeps each layer's input h^t and summed messages
+    At_t. Pass 2 walks the layers from the last: the node-level backward
+    of layer t gives dE/dAt_t and the direct part of dE/dh^t (residual);
+    the edge chunks, recomputed with gradients, give dE/dpos (through the
+    harmonics and the radial basis) and dE/d(W h^t) at the senders, which
+    linear_up carries back to h^t and on to layer t-1. F = -dE/dpos
+    (force equation). Same arithmetic as energy_forces up to summation
+    order. Returns dict(eps, energy, forces, graph)."""
+    W = unpack_weights(d, blob)
+    if graph is None:
+        graph = build_graph(system, d)
+    lin = _Lin(bf16_linear, fp16_linear)
+    z = graph.species
+    snd, rcv = graph.sender, graph.receiver
+    N, E, K = len(z), len(snd), d.K
+    pos0 = torch.tensor(system.positions, dtype=DT)
+    echunks = [slice(e0, min(e0 + edge_chunk, E)) for e0 in range(0, E, edge_chunk)]
+    nchunks = [slice(n0, min(n0 + node_chunk, N)) for n0 in range(0, N, node_chunk)]
+
+    def node_slice(At, h, sl):
+        return [a[sl] for a in At], {l: v[sl] for l, v in h.items()}
+
+    # pass 1: forward, no gradients
+    hs, Ats = [], []
+    eps = torch.zeros(N, dtype=DT)
+    with torch.no_grad():
+        h = {0: W["embed"][z][:, None, :]}
+        for t in range(d.n_layers):
+            paths = tp_paths(d, t)
+            ht = _linear_up(d, W, t, h, lin)
+            At = [torch.zeros(N, 2 * lo + 1, K, dtype=DT) for (_, _, lo) in paths]
+            for sl in echunks:
+                Y, rb = _edge_features(d, graph, pos0, sl)
+                msg = _edge_messages(d, W, t, ht, snd[sl], Y, rb)
+                for p in range(len(paths)):
+                    At[p].index_add_(0, rcv[sl], msg[p])
+            At = [a / d.c_norm for a in At]
+            hn = {l: [] for l in layer_out_ls(d, t)}
+            for sl in nchunks:
+                a_s, h_s = node_slice(At, h, sl)
+                hn_s, e_s, _ = _node_update(d, W, t, a_s, h_s, z[sl], lin)
+                for l in hn:
+                    hn[l].append(hn_s[l])
+                eps[sl] += e_s
+            hs.append(h)
+            Ats.append(At)
+            h = {l: torch.cat(v, dim=0) for l, v in hn.items()}
+
+    # pass 2: backward, last layer first
+    pos = pos0.clone().requires_grad_(True)
+    g_next = None                                                         # dE/dh^{t+1}
+    for t in reversed(range(d.n_layers)):
+        paths = tp_paths(d, t)
+        in_ls = layer_in_ls(d, t)
+        h = hs[t]
+        gAt = [torch.zeros_like(a) for a in Ats[t]]
+        gh = {l: torch.zeros_like(h[l]) for l in in_ls}
+        for sl in nchunks:
+            a_s, h_s = node_slice(Ats[t], h, sl)
+            a_s = [a.clone().requires_grad_(True) for a in a_s]
+            h_s = {l: v.clone().requires_grad_(True) for l, v in h_s.items()}
+            hn_s, e_s, _ = _node_update(d, W, t, a_s, h_s, z[sl], lin)
+            L = e_s.sum()
+            if g_next is not None:
+                for l, v in hn_s.items():
+                    L = L + (v * g_next[l][sl]).sum()
+            leaves = a_s + [h_s[l] for l in in_ls]
+            grads = torch.autograd.grad(L, leaves, allow_unused=True)
+            for p in range(len(paths)):
+                if grads[p] is not None:
+                    gAt[p][sl] = grads[p]
+            for j, l in enumerate(in_ls):
+                if grads[len(paths) + j] is not None:
+                    gh[l][sl] = grads[len(paths) + j]
+        # the edge chunks: messages recomputed with gradients, contracted with
+        # dE/dAt at their receivers (the adjoint of the neighbour sum)
+        h_leaf = {l: h[l].clone().requires_grad_(True) for l in in_ls}
+        ht = _linear_up(d, W, t, h_leaf, lin)
+        ht_leaf = {l: v.detach().clone().requires_grad_(True) for l, v in ht.items()}
+        for sl in echunks:
+            Y, rb = _edge_features(d, graph, pos, sl)
+            msg = _edge_messages(d, W, t, ht_leaf, snd[sl], Y, rb)
+            r_s = rcv[sl]
+            L = sum((msg[p] * gAt[p][r_s]).sum() for p in range(len(paths))) / d.c_norm
+            L.backward()
+        if t > 0:
+            gup = torch.autograd.grad([ht[l] for l in in_ls], [h_leaf[l] for l in in_ls],
+                                      grad_outputs=[ht_leaf[l].grad for l in in_ls], allow_unused=True)
+            g_next = {l: gh[l] + (gup[j] if gup[j] is not None else 0.0) for j, l in enumerate(in_ls)}
+    F = -pos.grad if pos.grad is not None else torch.zeros_like(pos0)
+    Eg = torch.zeros(graph.n_graphs, dtype=DT).index_add(0, graph.graph_of_atom, eps)
+    return {"eps": eps.numpy(), "energy": Eg.numpy(), "forces": F.detach().numpy(), "graph": graph}
+
+
+def contraction_order_shares(d: ModelDesc, blob: np.ndarray, system, graph: Graph | None = None,
+                             node_chunk: int = 256):
+    """Share of each correlation order nu in the product basis of Eq. 27,
+    share[t][L][nu] = sum |B_nu| / sum_nu' sum |B_nu'| over nodes, channels
+    and components, B_nu being the nu-th term of the sum over correlation
+    orders (weights of the other orders set to zero). A parity case that
+    claims to exercise Eq. 27 beyond nu = 1 needs every share to be
+    non-negligible."""
+    W = unpack_weights(d, blob)
+    if graph is None:
+        graph = build_graph(system, d)
+    z = graph.species
+    N = len(z)
+    pos = torch.tensor(system.positions, dtype=DT)
+    with torch.no_grad():
+        _, inter = node_energies(d, W, graph, pos, return_intermediates=True)
+    out = {}
+    for t in range(d.n_layers):
+        A = inter[f"{t}.A"]
+        out[t] = {}
+        for L in layer_out_ls(d, t):
+            tot = {}
+            for nu in range(1, d.correlation + 1):
+                if not so3.n_eta(nu, L):
+                    continue
+                Wn = dict(W)
+                for mu in range(1, d.correlation + 1):
+                    if mu != nu and so3.n_eta(mu, L):
+                        Wn[f"{t}.symc.{L}.{mu}"] = torch.zeros_like(W[f"{t}.symc.{L}.{mu}"])
+                s = 0.0
+                for n0 in range(0, N, node_chunk):
+                    sl = slice(n0, n0 + node_chunk)
+                    s += float(symmetric_contraction(A[sl], Wn, t, L, z[sl], d.correlation).abs().sum())
+                tot[nu] = s
+            S = sum(tot.values())
+            out[t][L] = {nu: v / S for nu, v in tot.items()}
+    return out
 
 
 def graph_energies(eps: torch.Tensor, graph: Graph) -> torch.Tensor:
