@@ -124,6 +124,10 @@ mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, 
                                       int64_t* n_edges, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Validate and pack a graph and the weights into the workspace.
+ * Paper: "Graph representation of atomic configurations" (atoms are nodes
+ * with coordinates r_i and species z_i, edges join atoms within the cutoff;
+ * here every periodic image within the cutoff is an edge of its own) and the
+ * architecture-breakdown table of the appendix (the weights).
  * weights (dev) FP32 blob in mace_weight_layout order; species (dev) [N] in
  * 0..S-1; edge_index (dev) [2][E]: row 0 senders j, row 1 receivers i,
  * receivers nondecreasing; unit_shifts (dev) [E][3] or NULL (no
@@ -138,17 +142,29 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
                              int32_t n_graphs, mace_precision prec, void* workspace, size_t workspace_bytes,
                              void* stream, mace_graph** out);
 
-/* Energies: positions (dev) [N][3] FP32; node_energy (dev) [N] FP32;
- * graph_energy (dev) [G] FP64.  No host synchronisation, no allocation. */
+/* Energies.  Paper: "Higher-order Message Passing in MACE" -- the two-body
+ * edge embedding (Eq. 26), the node-local product basis (Eq. 27), the message
+ * over correlation orders, the linear update with residual and the readouts;
+ * and the energy equation of "MACE inference: energy and forces", eps_i from
+ * the invariant features, E = sum_i eps_i (here per graph, summed in FP64 in
+ * a fixed order).  positions (dev) [N][3] FP32; node_energy (dev) [N] FP32;
+ * graph_energy (dev) [G] FP64.  No host synchronisation, no allocation.
+ * MACE_EUNSUPPORTED (nothing enqueued) if the handle's settings select an
+ * edge-product instance that is not built. */
 mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                                 void* stream);
 
-/* Energies and forces: as mace_forward_energy plus forces (dev) [N][3] FP32. */
+/* Energies and forces.  Paper: the force equation of "MACE inference:
+ * energy and forces", F_i = -dE/dr_i = -sum_j d eps_j / d r_i, evaluated by
+ * the reverse pass of every step of mace_forward_energy (a hand-written
+ * vector-Jacobian product, deterministic: no floating-point atomics).  As
+ * mace_forward_energy plus forces (dev) [N][3] FP32. */
 mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                         float* forces, void* stream);
 
-/* Energies, forces and the stress of every graph (the pressure of the paper's
- * NPT metrics is p = -tr(sigma)/3). stress (dev) [G][3][3] FP64 row-major:
+/* Energies, forces and the stress of every graph.  Paper: the NPT
+ * observables of "Precision-loss metrics" monitor the pressure p(t) of a
+ * periodic box, p = -tr(sigma)/3; sigma itself is not defined there. stress (dev) [G][3][3] FP64 row-major:
  * sigma_g[a][b] = (1/V_g) dE_g/d(epsilon_ab) for a homogeneous strain acting
  * on row vectors, x -> x (I + epsilon), applied to the graph's positions and
  * cell rows; equivalently (1/V_g) sum over the graph's edges of d_e[a] g_e[b]

@@ -179,11 +179,16 @@ struct Buffers {
   int* snd_z = nullptr;                    // [E] species of each edge's sender
   float4* g = nullptr;
   double* inv_vol = nullptr;      // [G] 1/|det cell|, or 1 without cells
+  int2* stress_chunks = nullptr;  // [n_stress_chunks] edge ranges of the stress reduction
+  int* stress_chunk_off = nullptr;   // [G + 1] first chunk of each graph
+  double* stress_part = nullptr;  // [n_stress_chunks][9] partial sums
   int* status = nullptr;          // device status word (kStatus* bits)
   LinLaunch* lin_dev = nullptr;   // 6 plans per layer + 6
 };
 
 int64_t n_tiles_bound(int64_t N, int S) { return (N + kLinTileNodes - 1) / kLinTileNodes + S; }
+// every graph has at least one chunk; a graph of n edges has ceil(n / kStressChunk)
+int64_t stress_chunk_bound(int64_t E, int G) { return G + E / kStressChunk + 1; }
 
 void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   const int64_t K = m.d.K, S = m.d.n_species, T = m.d.n_layers;
@@ -243,6 +248,10 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.dht = c.take<float>(N * m.max_din * K);
   b.g = c.take<float4>(std::max<int64_t>(E, 1));
   b.inv_vol = c.take<double>(G);
+  const int64_t n_sc = stress_chunk_bound(E, G);
+  b.stress_chunks = c.take<int2>(n_sc);
+  b.stress_chunk_off = c.take<int>(G + 1);
+  b.stress_part = c.take<double>(n_sc * 9);
   b.lin_dev = c.take<LinLaunch>(6 * T + 6);
   b.snd_z = c.take<int>(std::max<int64_t>(E, 1));
   if (m.l0_ki) {
@@ -278,6 +287,7 @@ struct mace_graph {
   int64_t N = 0, E = 0;
   int G = 1;
   int n_tiles = 0, n_quads = 0;
+  int n_stress_chunks = 0;
   mace_precision prec = MACE_FP32;
   // linear plans per layer (host copy for the grid, device copy for the kernel)
   std::vector<LinPlanRef> upskip, upskipT, lin, linT, prod, prodT;
@@ -333,6 +343,14 @@ bool a3_presplit(const mace_graph* h, int t) {
 }
 int radial_mode(const mace_graph* h, int t) {
   return h->prec == MACE_BF16_RADIAL ? 1 : (!h->radial_split ? 0 : (a3_presplit(h, t) ? 3 : 2));
+}
+
+// Every edge product the handle's settings will launch has a kernel instance
+// (checked before anything is enqueued; the launchers check again).
+bool launchable(const mace_graph* h) {
+  for (int t = 0; t < h->m.d.n_layers; ++t)
+    if (!layer_factorised(h, t) && !tpr_supported(h->m.layers[t].lh_max, radial_mode(h, t))) return false;
+  return true;
 }
 
 // A linear launch, bracketed for profiling; while the linear class is
@@ -611,7 +629,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
       {
         PROF(KID_TP_FWD);
         const float* a3t = a3_presplit(h, t) ? reinterpret_cast<const float*>(b.a3x[t]) : b.a3[t];
-        launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, a3t, wr3 + m.off.at(pre + "radial.3"),
+        (void)launch_tpr_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, src_map, a3t, wr3 + m.off.at(pre + "radial.3"),
                        b.Y, src, inv_c, b.At, radial_mode(h, t), h->tp_round);
       }
       if (t == 0 && !lowp) {
@@ -704,7 +722,7 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F, cons
       const float* src = t == 0 ? (h->tp_round ? b.sp_round : b.sp_table) : b.ht[t];
       const int* src_map = t == 0 ? b.species : nullptr;
       PROF(KID_TP_BWD);
-      launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map,
+      (void)launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map,
                      a3_presplit(h, t) ? reinterpret_cast<const float*>(b.a3x[t]) : b.a3[t],
                      (h->rad_round ? b.w_round : b.w) + m.off.at(pre + "radial.3"),
                      b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, radial_mode(h, t), h->tp_round);
@@ -1056,7 +1074,9 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       for (int r = 0; r < tcount[t]; ++r) qnode[((size_t)q * kLinQuad + w) * kLinTileNodes + r] = order[tstart[t] + r];
     }
   }
-  Carver c{reinterpret_cast<char*>(workspace)};
+  // the buffers are carved from the workspace base rounded up to 256 bytes
+  // (mace_workspace_bytes includes that slack)
+  Carver c{reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(workspace) + 255) & ~uintptr_t(255))};
   carve(h->m, N, E, G, c, h->b);
   Buffers& b = h->b;
   auto up = [&](void* dst, const void* src, size_t bytes) {
@@ -1087,6 +1107,24 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       inv_vol[gi] = det != 0.0 ? 1.0 / std::fabs(det) : 0.0;
     }
   chk(up(b.inv_vol, inv_vol.data(), G * 8));
+  {
+    std::vector<int2> sch;
+    std::vector<int32_t> sco(G + 1, 0);
+    for (int gi = 0; gi < G; ++gi) {
+      const int e0 = rcv_off[goff[gi]], e1 = rcv_off[goff[gi + 1]];
+      sco[gi] = (int32_t)sch.size();
+      int e = e0;
+      do {
+        const int ee = std::min(e1, e + kStressChunk);
+        sch.push_back(make_int2(e, ee));
+        e = ee;
+      } while (e < e1);
+    }
+    sco[G] = (int32_t)sch.size();
+    h->n_stress_chunks = (int)sch.size();
+    chk(up(b.stress_chunks, sch.data(), sch.size() * sizeof(int2)));
+    chk(up(b.stress_chunk_off, sco.data(), (G + 1) * 4));
+  }
   chk(up(b.quad_node, qnode.data(), qnode.size() * 4));
   chk(up(b.quad_species, qspec.data(), qspec.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
@@ -1112,6 +1150,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
 mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                                 void* stream) {
   if (!g || !positions || !node_energy || !graph_energy) return MACE_EINVAL;
+  if (!launchable(g)) return MACE_EUNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
   run_forward(g, s, positions, node_energy, false);
   {
@@ -1125,6 +1164,7 @@ mace_status mace_forward_energy(mace_graph* g, const float* positions, float* no
 mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
                         float* forces, void* stream) {
   if (!g || !positions || !node_energy || !graph_energy || !forces) return MACE_EINVAL;
+  if (!launchable(g)) return MACE_EUNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
   run_forward(g, s, positions, node_energy, true);
   run_backward(g, s, positions, forces, node_energy, graph_energy);
@@ -1140,8 +1180,8 @@ mace_status mace_forces_stress(mace_graph* g, const float* positions, float* nod
   {
     mace_graph* h = g;
     PROF(KID_FORCES);
-    launch_stress(s, g->G, g->b.graph_off, g->b.rcv_off, positions, g->b.snd, g->b.rcv, g->b.shift, g->b.g,
-                  g->b.inv_vol, stress);
+    launch_stress(s, g->G, g->n_stress_chunks, g->b.stress_chunks, g->b.stress_chunk_off, positions, g->b.snd,
+                  g->b.rcv, g->b.shift, g->b.g, g->b.inv_vol, g->b.stress_part, stress);
   }
   return hip_ok(hipGetLastError());
 }
@@ -1171,7 +1211,9 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
   if (request == MACE_L0_AUTO) g->l0_fact = l0_auto(g->m, g->N, g->E);
   else if (request == MACE_L0_EDGE) g->l0_fact = false;
   else if (request == MACE_L0_FACTORED) g->l0_fact = true;
-  if (in_use) *in_use = g->l0_fact ? MACE_L0_FACTORED : MACE_L0_EDGE;
+  // the form the next calls will run: the precision study's edge-product and
+  // radial-MLP rounding force the per-edge form whatever was requested
+  if (in_use) *in_use = layer_factorised(g, 0) ? MACE_L0_FACTORED : MACE_L0_EDGE;
   return MACE_OK;
 }
 

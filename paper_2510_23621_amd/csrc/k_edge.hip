@@ -90,23 +90,25 @@ __global__ void __launch_bounds__(256) forces_kernel(int N, const int* __restric
 }
 
 // stress[gi][a][b] = inv_vol[gi] * sum over the graph's edges of d_e[a] g_e[b]
-// (d_e = x_snd - x_rcv + shift in FP64). One block per graph; the graph's
-// edges are contiguous (atoms are grouped by graph, edges by receiver).
-// FP64 partial sums per thread in edge order, then a fixed tree: bitwise
-// reproducible.
-__global__ void __launch_bounds__(256) stress_kernel(int G, const int* __restrict__ graph_off,
-                                                     const int* __restrict__ rcv_off, const float* __restrict__ pos,
-                                                     const int* __restrict__ snd, const int* __restrict__ rcv,
-                                                     const double4* __restrict__ shift,
-                                                     const float4* __restrict__ g, const double* __restrict__ inv_vol,
-                                                     double* __restrict__ stress) {
+// (d_e = x_snd - x_rcv + shift in FP64). A graph's edges are contiguous (atoms
+// are grouped by graph, edges by receiver) and split at setup into chunks of
+// at most kStressChunk edges. Pass 1: one block per chunk, FP64 partial sums
+// per thread in edge order, then a fixed tree, into part[chunk][9]. Pass 2:
+// one thread per (graph, component) adds its graph's chunk partials in chunk
+// order. Bitwise reproducible, and a single large graph is spread over the
+// whole chip.
+__global__ void __launch_bounds__(256) stress_partial_kernel(const int2* __restrict__ chunks,
+                                                             const float* __restrict__ pos,
+                                                             const int* __restrict__ snd, const int* __restrict__ rcv,
+                                                             const double4* __restrict__ shift,
+                                                             const float4* __restrict__ g, double* __restrict__ part) {
   __shared__ double red[9][256];
-  const int gi = blockIdx.x, t = threadIdx.x;
-  const int e_beg = rcv_off[graph_off[gi]], e_end = rcv_off[graph_off[gi + 1]];
+  const int t = threadIdx.x;
+  const int2 ch = chunks[blockIdx.x];
   double acc[9];
 #pragma unroll
   for (int c = 0; c < 9; ++c) acc[c] = 0.0;
-  for (int e = e_beg + t; e < e_end; e += blockDim.x) {
+  for (int e = ch.x + t; e < ch.y; e += blockDim.x) {
     const int s = snd[e], r = rcv[e];
     const double4 sh = shift[e];
     const double d[3] = {((double)pos[3 * s + 0] - (double)pos[3 * r + 0]) + sh.x,
@@ -128,14 +130,25 @@ __global__ void __launch_bounds__(256) stress_kernel(int G, const int* __restric
       for (int c = 0; c < 9; ++c) red[c][t] += red[c][t + st];
     __syncthreads();
   }
-  if (t < 9) stress[(size_t)gi * 9 + t] = red[t][0] * inv_vol[gi];
+  if (t < 9) part[(size_t)blockIdx.x * 9 + t] = red[t][0];
 }
 
-void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
+__global__ void stress_final_kernel(int G, const int* __restrict__ chunk_off, const double* __restrict__ part,
+                                    const double* __restrict__ inv_vol, double* __restrict__ stress) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 9 * G) return;
+  const int gi = i / 9, c = i % 9;
+  double acc = 0.0;
+  for (int k = chunk_off[gi]; k < chunk_off[gi + 1]; ++k) acc += part[(size_t)k * 9 + c];
+  stress[i] = acc * inv_vol[gi];
+}
+
+void launch_stress(hipStream_t s, int G, int n_chunks, const int2* chunks, const int* chunk_off, const float* pos,
                    const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
-                   double* stress) {
-  if (G <= 0) return;
-  stress_kernel<<<G, 256, 0, s>>>(G, graph_off, rcv_off, pos, snd, rcv, shift, g, inv_vol, stress);
+                   double* part, double* stress) {
+  if (G <= 0 || n_chunks <= 0) return;
+  stress_partial_kernel<<<n_chunks, 256, 0, s>>>(chunks, pos, snd, rcv, shift, g, part);
+  stress_final_kernel<<<(9 * G + 255) / 256, 256, 0, s>>>(G, chunk_off, part, inv_vol, stress);
 }
 
 void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv, const double4* shift,

@@ -1061,6 +1061,259 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
   }
 }
 
+// ---- FP32 backward at l_h = 2 in the edge-lane layout.
+//
+// At P = 17 the split-BF16 parts of W3 in both layouts (209 KB) do not fit the
+// LDS, so both radial products run on FP32 MFMA (v_mfma_f32_16x16x4_f32, one
+// K value per lane), which needs one copy of W3's slice only: both products
+// read it from the same padded layout sW[(p 64 + j) kEPitch + kk].
+//   R (edge on the lane): D[channel][edge] = sum_j W3[j][p, channel] a3[edge][j];
+//     in K step s, lane group g supplies j = 16 g + s, so that the lane's a3
+//     values are one contiguous run of 16 (four float4 loads).
+//   dE/da3: D[j][edge] = sum_(p, c) W3[j][p, c] dR[edge][p, c]; in K step
+//     (p, c') lane group g supplies channel 4 g + c', which is the lane's own
+//     register r[p][c']: dR is the B operand as it stands.
+// The CG part is the edge-lane contraction of the l_h = 1 backward (G table of
+// the receiver in LDS, two multiply-adds per coupling pair and channel). One
+// wave per SIMD (the G tables of four receivers and the W3 slice take 122 KB),
+// so the next tile's operands (sender rows, harmonics, a3) are loaded while
+// the current tile is contracted.
+constexpr int kEPitch = 17;
+
+template <int P>
+__device__ __forceinline__ void load_w3_slice_el(const float* __restrict__ W3, int K, int ct, float* sW) {
+  const int PK = P * K;
+  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+    sW[(p * 64 + j) * kEPitch + kk] = W3[(size_t)j * PK + p * K + 16 * ct + kk];
+  }
+}
+
+// One wave per SIMD leaves no other wave to hide latency, so the body keeps
+// its own reads in flight: every LDS operand is requested a fixed number of
+// uses ahead (a ring of registers indexed by compile-time constants), the
+// sender rows and harmonics of a tile are requested before its radial MFMAs,
+// and the next tile's a3 and sender index before its CG contraction.
+constexpr int kRingW = 16;   // W3 operands in flight (one MFMA each)
+constexpr int kRingG = 8;    // G-table entries in flight (one coupling pair each)
+
+// sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
+template <int DIN>
+__device__ __forceinline__ void el_load_hy(f4* hv, f4* y4, int src, int e, int kb, const float* __restrict__ h,
+                                           const float* __restrict__ Y, int K) {
+#pragma unroll
+  for (int c = 0; c < DIN; ++c) hv[c] = *reinterpret_cast<const f4*>(h + ((size_t)src * DIN + c) * K + kb);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) y4[v] = reinterpret_cast<const f4*>(Y + (size_t)e * 16)[v];
+}
+
+// a3[e][16 g .. 16 g + 15]
+__device__ __forceinline__ void el_load_a3(f4* a, int e, int g, const float* __restrict__ a3) {
+#pragma unroll
+  for (int v = 0; v < 4; ++v) a[v] = reinterpret_cast<const f4*>(a3 + (size_t)e * 64 + 16 * g)[v];
+}
+
+template <int NW, bool RND>
+__device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
+    int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
+    const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
+    const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd, float* sW, float* sGall) {
+  constexpr int LHMAX = 2;
+  constexpr int P = path_count(LHMAX);
+  constexpr int MID = mid_count(LHMAX);
+  constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
+  constexpr int NPAIR = PairCount<LHMAX>::value;
+  constexpr int NW3 = P * 16;   // MFMAs per radial product
+  const int ct = blockIdx.y;
+  load_w3_slice_el<P>(W3, K, ct, sW);
+  __syncthreads();
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int g = l >> 4, kk = l & 15;
+  const int kb = 16 * ct + 4 * g;   // the lane's four channels
+  float* sg = sGall + w * NPAIR * 16;   // this wave's G table [pair][channel]
+  float* dYc = dYp + (size_t)ct * E * 16;
+  float* da3c = da3p + (size_t)ct * E * 64;
+  // R operand of MFMA f = 16 p + s: W3[j = 16 g + s][p, 16 ct + kk]
+  const float* wR = sW + (16 * g) * kEPitch + kk;
+  // dE/da3 operand of MFMA f = 16 p + 4 c + jt: W3[j = 16 jt + kk][p, 16 ct + 4 g + c]
+  const float* wD = sW + kk * kEPitch + 4 * g;
+  auto wr_at = [&](int f) { return wR[((f >> 4) * 64 + (f & 15)) * kEPitch]; };
+  auto wd_at = [&](int f) { return wD[((f >> 4) * 64 + 16 * (f & 3)) * kEPitch + ((f >> 2) & 3)]; };
+  for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
+    const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
+    if (e_beg == e_end) continue;
+    {
+      // G_p of this receiver for channel 16 ct + l%16; the four lane groups
+      // compute the same values and the first one stores
+      float gv[MID];
+#pragma unroll
+      for (int c = 0; c < MID; ++c) gv[c] = dAt[((size_t)i * MID + c) * K + 16 * ct + kk] * inv_c;
+      __builtin_amdgcn_wave_barrier();   // the previous receiver's reads come first
+      for_paths<LHMAX>([&](auto tag) {
+        using T = decltype(tag);
+        using C = mt::CG<T::lh, T::ly, T::lo>;
+        constexpr int goff = PathPairOffset<T::index>::value;
+        float Gp[C::npair];
+#pragma unroll
+        for (int u = 0; u < C::npair; ++u) Gp[u] = 0.f;
+        C::each_p([&](int m1, int m2, int m3, float cg, int pi) { Gp[pi] += cg * gv[T::offset + m3]; });
+        if (g == 0) {
+#pragma unroll
+          for (int u = 0; u < C::npair; ++u) sg[(goff + u) * 16 + kk] = Gp[u];
+        }
+      });
+      __builtin_amdgcn_wave_barrier();
+    }
+    int e = min(e_beg + kk, e_end - 1);
+    int src = snd[e];
+    if (src_map) src = src_map[src];
+    f4 a[4];
+    el_load_a3(a, e, g, a3);
+    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      __asm__ volatile("" ::: "memory");   // the G table is read per tile, not held in registers
+      const bool valid = e0 + kk < e_end;
+      const bool more = e0 + 16 < e_end;
+      f4 hv[DIN], y4[4];
+      el_load_hy<DIN>(hv, y4, src, e, kb, h, Y, K);
+      // R of the tile, edge on the lane (rows past e_end are computed from a
+      // valid edge's a3 and never stored: every output row depends on its own
+      // edge only)
+      f4 r[P];
+      {
+        float ring[kRingW];
+#pragma unroll
+        for (int f = 0; f < kRingW; ++f) ring[f] = wr_at(f);
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_s_setprio(1);
+        // (a scheduling fence per step keeps each read kRingW MFMAs ahead of its use)
+        static_for<0, NW3>([&](auto F) {
+          constexpr int f = decltype(F)::value;
+          __builtin_amdgcn_sched_barrier(0);
+          const float wv = ring[f % kRingW];
+          if constexpr (f + kRingW < NW3) ring[f % kRingW] = wr_at(f + kRingW);
+          acc = mfma4(wv, a[(f & 15) >> 2][f & 3], acc);
+          if constexpr ((f & 15) == 15) {
+            r[f >> 4] = acc;
+            acc = f4{0.f, 0.f, 0.f, 0.f};
+          }
+        });
+        __builtin_amdgcn_s_setprio(0);
+      }
+      if constexpr (RND) round_tile<P>(r, rnd);
+      // the next tile's sender index and a3, in flight during the contraction
+      int src_n = src, e_n = e;
+      if (more) {
+        e_n = min(e0 + 16 + kk, e_end - 1);
+        src_n = snd[e_n];
+        if (src_map) src_n = src_map[src_n];
+        el_load_a3(a, e_n, g, a3);
+      }
+      float y[16];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        y[4 * v] = y4[v][0];
+        y[4 * v + 1] = y4[v][1];
+        y[4 * v + 2] = y4[v][2];
+        y[4 * v + 3] = y4[v][3];
+      }
+      float dy[16];
+#pragma unroll
+      for (int m = 0; m < 16; ++m) dy[m] = 0.f;
+      f4 dh[DIN];
+#pragma unroll
+      for (int c = 0; c < DIN; ++c) dh[c] = f4{0.f, 0.f, 0.f, 0.f};
+      {
+        const float* gq = sg + 4 * g;
+        f4 gring[kRingG];
+#pragma unroll
+        for (int u = 0; u < kRingG; ++u) gring[u] = *reinterpret_cast<const f4*>(gq + u * 16);
+        for_paths<LHMAX>([&](auto tag) {
+          using T = decltype(tag);
+          constexpr int lh = T::lh, ly = T::ly;
+          constexpr int goff = PathPairOffset<T::index>::value;
+          const f4 rv = r[T::index];
+          f4 Dm[2 * lh + 1], Rh[2 * lh + 1];
+#pragma unroll
+          for (int m = 0; m < 2 * lh + 1; ++m) {
+            Dm[m] = f4{0.f, 0.f, 0.f, 0.f};
+            Rh[m] = rv * hv[lh * lh + m];
+          }
+          mt::CG<lh, ly, T::lo>::each_pair([&](int m1, int m2, int pi) {
+            const int gi = goff + pi;   // a constant after inlining
+            __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingG pairs ahead of its use
+            const f4 G = gring[gi % kRingG];
+            if (gi + kRingG < NPAIR) gring[gi % kRingG] = *reinterpret_cast<const f4*>(gq + (gi + kRingG) * 16);
+            const float yv = y[ly * ly + m2];
+            Dm[m1] += G * yv;
+            float t = dy[ly * ly + m2];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) t += G[c] * Rh[m1][c];
+            dy[ly * ly + m2] = t;
+          });
+          f4 d = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int m = 0; m < 2 * lh + 1; ++m) {
+            d += hv[lh * lh + m] * Dm[m];
+            dh[lh * lh + m] += rv * Dm[m];
+          }
+          r[T::index] = d;   // dR
+        });
+      }
+      // dE/dY over the tile's 16 channels: halve over lane bit 5, then bit 4;
+      // lane group q ends with m2 = 4q .. 4q + 3
+      {
+        const bool hi5 = g >= 2;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+          const float send = hi5 ? dy[m] : dy[m + 8];
+          const float keep = hi5 ? dy[m + 8] : dy[m];
+          dy[m] = keep + __shfl_xor(send, 32);
+        }
+        const bool hi4 = g & 1;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const float send = hi4 ? dy[m] : dy[m + 4];
+          const float keep = hi4 ? dy[m + 4] : dy[m];
+          dy[m] = keep + __shfl_xor(send, 16);
+        }
+      }
+      const int ev = e0 + kk;
+      if (valid) {
+        *reinterpret_cast<f4*>(dYc + (size_t)ev * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
+        if (Q) {
+#pragma unroll
+          for (int c = 0; c < DIN; ++c) *reinterpret_cast<f4*>(Q + ((size_t)ev * DIN + c) * K + kb) = dh[c];
+        }
+      }
+      // dE/da3 partial: d3[jt][rr] = D[j = 16 jt + 4 g + rr][edge e0 + l%16]
+      f4 d3[4];
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+      {
+        float ring[kRingW];
+#pragma unroll
+        for (int f = 0; f < kRingW; ++f) ring[f] = wd_at(f);
+        __builtin_amdgcn_s_setprio(1);
+        static_for<0, NW3>([&](auto F) {
+          constexpr int f = decltype(F)::value;
+          __builtin_amdgcn_sched_barrier(0);
+          const float wv = ring[f % kRingW];
+          if constexpr (f + kRingW < NW3) ring[f % kRingW] = wd_at(f + kRingW);
+          d3[f & 3] = mfma4(wv, r[f >> 4][(f >> 2) & 3], d3[f & 3]);
+        });
+        __builtin_amdgcn_s_setprio(0);
+      }
+      if (valid) {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) *reinterpret_cast<f4*>(da3c + (size_t)ev * 64 + 16 * jt + 4 * g) = d3[jt];
+      }
+      src = src_n;
+      e = e_n;
+    }
+  }
+}
+
 template <int LHMAX, int RM, int NW = TprShape<LHMAX, true, RM>::waves>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, true, RM>::per_simd, TprShape<LHMAX, true, RM>::per_simd)))
@@ -1072,6 +1325,19 @@ tpr_bwd_kernel(
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
+  else if constexpr (LHMAX == 2 && RM == 0) {
+    // W3's slice (one layout for both products) and a G table per wave; the
+    // precision study's operand rounding runs as its own instance (a uniform
+    // branch, taken once)
+    __shared__ float sW[path_count(2) * 64 * kEPitch];
+    __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
+    if (rnd)
+      tpr_bwd_l2_edge_lanes_body<NW, true>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
+                                           rnd, sW, sG);
+    else
+      tpr_bwd_l2_edge_lanes_body<NW, false>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
+                                            0, sW, sG);
+  }
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                          rnd);
@@ -1108,17 +1374,25 @@ void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, cons
 }
 }  // namespace
 
-void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+// Instances built: every l_h <= 2 with radial mode 0 (FP32), 1 (BF16) or 2
+// (split BF16; the l_h = 2 backward runs it on FP32 MFMA), and mode 3 (split
+// BF16 with pre-split a3) at l_h = 1.
+bool tpr_supported(int lh_max, int radial_mode) {
+  if (lh_max < 0 || lh_max > 2 || radial_mode < 0 || radial_mode > 3) return false;
+  return radial_mode != 3 || lh_max == 1;
+}
+
+bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, float* At, int radial_mode, int tp_round) {
-  if (N <= 0) return;
+  if (!tpr_supported(lh_max, radial_mode)) return false;
+  if (N <= 0) return true;
 #define MACE_TPRF(LH, RM) tpr_fwd_launch<LH, RM>(s, N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, tp_round)
-  // radial_mode 3 (pre-split a3) is requested for l_h = 1 only
   switch (lh_max) {
     case 0:
       if (radial_mode == 1) MACE_TPRF(0, 1);
       else if (radial_mode == 2) MACE_TPRF(0, 2);
-      else if (radial_mode == 0) MACE_TPRF(0, 0);
+      else MACE_TPRF(0, 0);
       break;
     case 1:
       if (radial_mode == 1) MACE_TPRF(1, 1);
@@ -1126,20 +1400,22 @@ void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
       else if (radial_mode == 3) MACE_TPRF(1, 3);
       else MACE_TPRF(1, 0);
       break;
-    case 2:
+    default:
       if (radial_mode == 1) MACE_TPRF(2, 1);
       else if (radial_mode == 2) MACE_TPRF(2, 2);
-      else if (radial_mode == 0) MACE_TPRF(2, 0);
+      else MACE_TPRF(2, 0);
       break;
   }
 #undef MACE_TPRF
+  return true;
 }
 
-void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
+bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
                     int tp_round) {
-  if (N <= 0 || E <= 0) return;
+  if (!tpr_supported(lh_max, radial_mode)) return false;
+  if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
   tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
   switch (lh_max) {
@@ -1154,12 +1430,13 @@ void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
       else if (radial_mode == 3) MACE_TPRB(1, 3);
       else MACE_TPRB(1, 0);
       break;
-    case 2:   // split BF16 falls back to FP32 MFMA here
+    default:   // split BF16 (mode 2) runs on FP32 MFMA here
       if (radial_mode == 1) MACE_TPRB(2, 1);
       else MACE_TPRB(2, 0);
       break;
   }
 #undef MACE_TPRB
+  return true;
 }
 
 }  // namespace mace

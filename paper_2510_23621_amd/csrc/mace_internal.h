@@ -423,15 +423,24 @@ void launch_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off,
                    const float4* g, float* F, int G, const int* graph_off, const float* eps, double* E);
 void launch_radial_bwd(hipStream_t s, int E, const float* rbf, int nb, const float* W, const float* da3p,
                        const float* dYp, int n_part, float* dY, float* de, int accumulate, int rnd);
-void launch_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const float* pos,
+// Stress of every graph from the edge gradients g: per-chunk FP64 partials
+// (chunks [beg, end) of at most kStressChunk edges of one graph, graph gi's
+// chunks at chunk_off[gi] .. chunk_off[gi + 1]), then their ordered sum.
+constexpr int kStressChunk = 8192;
+void launch_stress(hipStream_t s, int G, int n_chunks, const int2* chunks, const int* chunk_off, const float* pos,
                    const int* snd, const int* rcv, const double4* shift, const float4* g, const double* inv_vol,
-                   double* stress);
+                   double* part, double* stress);
 void launch_edge_vjp(hipStream_t s, int E, const float* pos, const int* snd, const int* rcv, const double4* shift,
                      double rc, int p, int nb, const float* dY, const float* de, float4* g);
-void launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
+// Edge-product launchers: radial 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate),
+// 3 split BF16 with a3 pre-split (l_h = 1); tp_round 0/1/2 none/bf16/fp16.
+// They return false, enqueuing nothing, for an (l_h, radial mode) without an
+// instance (tpr_supported is false).
+bool tpr_supported(int lh_max, int radial_mode);
+bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
-                    float inv_c, float* At, int radial_mode, int tp_round);   // radial 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate), 3 split BF16 with a3 pre-split (l_h = 1); tp_round 0/1/2 none/bf16/fp16
-void launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
+                    float inv_c, float* At, int radial_mode, int tp_round);
+bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
                     int tp_round);   // as launch_tpr_fwd; split BF16 runs on FP32 MFMA for l_h = 2

@@ -1,17 +1,22 @@
 """Parity at the workloads' full sizes, in the configuration bench.py times.
 
 * 1536-atom water (K=128, 0e+1o): every per-atom energy and force against
-  the FP64 oracle, FP32 and BF16-linear.
-* 4608- and 36,864-atom water: per-atom energies of sampled atoms against
-  the oracle evaluated on a cluster cut of radius 2 r_c + margin around the
-  atom (eps_i depends only on atoms within 2 r_c: layer 1 sums h^(1) of
-  neighbours, which sum their own neighbours), plus properties that hold at
-  any size: sum F = 0, rotation covariance of the whole periodic box (forces
-  and stress), determinism, BF16-linear vs FP32.
-* 1536-atom water also checks the stress against the oracle.
+  the FP64 oracle, FP32 and BF16-linear; the stress against the oracle.
+* 1536-atom water with the stress inputs (c_norm 1, last radial layer x4),
+  where every correlation order of Eq. 27 contributes (the oracle-side share
+  of each order is asserted by a CPU test): every atom, FP32.
+* 4608- and 36,864-atom water: every per-atom energy and force against FP64
+  oracle references written by tests/golden/make_fullsize_refs.py (the
+  oracle's two-pass chunked VJP), FP32 and BF16-linear; the inputs'
+  fingerprint is checked first. Plus properties that hold at any size:
+  sum F = 0, rotation covariance of the whole periodic box (forces and
+  stress), determinism.
 * 512-molecule batch: sampled molecules are whole graphs, so their energy
   and forces are compared exactly.
 """
+import os
+import sys
+
 import numpy as np
 import pytest
 import torch
@@ -22,11 +27,13 @@ from synth.configs import CONFIGS, make_system, model_params
 pytestmark = pytest.mark.gpu
 
 B = pytest.importorskip("paper_2510_23621_amd.binding")
-from gpu_common import (TOL, assert_parity, cluster_cut, errors, lib_blob, oracle_blob, oracle_stress,  # noqa: E402
+from gpu_common import (TOL, assert_parity, errors, lib_blob, oracle_blob, oracle_stress,  # noqa: E402
                         run_gpu, run_oracle, stress_error)
-from oracle import so3  # noqa: E402
+from oracle import mace, so3  # noqa: E402
 
-PER_ATOM_TOL = {B.MACE_FP32: 2e-5, B.MACE_BF16_LINEAR: 5e-2}
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+sys.path.insert(0, GOLDEN)
+import make_fullsize_refs as refs  # noqa: E402
 
 
 @pytest.fixture(autouse=True, scope="module")
@@ -35,15 +42,23 @@ def _need_gpu():
         pytest.skip("no GPU")
 
 
-def _per_atom_check(gpu_eps, ref_eps, atoms, scale, prec, label):
-    err = np.abs(gpu_eps[atoms] - ref_eps) / scale
-    print(f"[fullsize] {label} per-atom max rel err {err.max():.3e} (n={len(atoms)})", flush=True)
-    assert err.max() <= PER_ATOM_TOL[prec], (label, err)
-
-
 def _rotate(system, R):
     cells = None if system.cells is None else system.cells @ R.T
     return synth.System(system.positions @ R.T, system.species, cells, system.graph_of_atom, system.n_graphs)
+
+
+def _stored_ref(name):
+    """(params, system, blob, ref) of a stored FP64 reference, after checking
+    that the library's neighbour list and the seeded inputs reproduce the
+    fingerprint the reference was written for."""
+    params, sysm, blob = refs.workload(name)
+    z = np.load(refs.ref_path(name))
+    snd, rcv, sh = B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells, sysm.graph_of_atom,
+                                        sysm.n_graphs)
+    assert len(snd) == int(z["n_edges"])
+    assert refs.fingerprint(sysm, blob, snd, rcv, sh) == str(z["fingerprint"]), name
+    ref = dict(eps=z["eps"], energy=z["energy"], forces=z["forces"])
+    return params, sysm, blob, ref
 
 
 # ------------------------------------------------------------------ 1536 atoms, complete
@@ -54,7 +69,7 @@ def cfg1():
     sysm = make_system(1, seed=0)
     blob = oracle_blob(params, 0)
     assert np.array_equal(blob, lib_blob(params, 0))
-    ref = run_oracle(params, sysm, blob)
+    ref = mace.energy_forces_chunked(mace.ModelDesc(**params), blob, sysm)
     return params, sysm, blob, ref
 
 
@@ -62,6 +77,7 @@ def test_cfg1_full_fp32(cfg1):
     params, sysm, blob, ref = cfg1
     gpu = run_gpu(params, sysm, blob, stress=True)
     assert gpu["n_edges"] == len(ref["graph"].sender)
+    # the chunked oracle against the whole-graph one is pinned on the CPU
     assert_parity(gpu, ref, B.MACE_FP32, "water1536 full")
     sref = oracle_stress(params, sysm, blob)
     err = stress_error(gpu["stress"], sref)
@@ -75,30 +91,35 @@ def test_cfg1_full_bf16(cfg1):
     assert_parity(gpu, ref, B.MACE_BF16_LINEAR, "water1536 full bf16")
 
 
-# ------------------------------------------------------------------ larger periodic boxes
+# ------------------------------------------------------------------ stress inputs, every order of Eq. 27
+
+def test_cfg1_full_stress_inputs_fp32():
+    params, sysm, blob, ref = _stored_ref("water1536_k128_l1_stress")
+    gpu = run_gpu(params, sysm, blob)
+    assert_parity(gpu, ref, B.MACE_FP32, "water1536 stress inputs full")
+
+
+# ------------------------------------------------------------------ larger periodic boxes, every atom
+
+@pytest.mark.parametrize("prec", [B.MACE_FP32, B.MACE_BF16_LINEAR])
+@pytest.mark.parametrize("name", ["water4608_k128_l1", "water36864_k128_l2"])
+def test_large_water_every_atom_vs_fp64(name, prec):
+    params, sysm, blob, ref = _stored_ref(name)
+    gpu = run_gpu(params, sysm, blob, prec=prec)
+    print(f"[fullsize] {name}: {gpu['n_edges']} edges", flush=True)
+    assert_parity(gpu, ref, prec, f"{name} every atom")
+
 
 @pytest.mark.parametrize("cfg", [2, 3])
-def test_large_water_sampled_and_properties(cfg):
+def test_large_water_properties(cfg):
     params = model_params(cfg)
     sysm = make_system(cfg, seed=0)
     blob = lib_blob(params, 0)
     g32 = run_gpu(params, sysm, blob)
     N = sysm.n_atoms
     F = g32["forces"]
-    print(f"[fullsize] water{N}: {g32['n_edges']} edges", flush=True)
     # sum of forces vanishes (translation invariance)
     assert np.abs(F.sum(0)).max() <= 1e-5 * np.abs(F).max() * np.sqrt(N)
-    # sampled per-atom energies against the oracle on cluster cuts
-    rng = np.random.default_rng(cfg)
-    atoms = rng.choice(N, size=3, replace=False)
-    rc = params["r_cut"]
-    ref = []
-    for i in atoms:
-        cl, _ = cluster_cut(sysm, int(i), 2 * rc + 0.5)
-        out = run_oracle(params, cl, oracle_blob(params, 0), forces=False)
-        ref.append(out["eps"][0])
-    scale = np.abs(g32["eps"]).mean()
-    _per_atom_check(g32["eps"], np.array(ref), atoms, scale, B.MACE_FP32, f"water{N}")
     # rotation covariance of the whole box (GPU against GPU)
     R = so3.random_rotation(np.random.default_rng(100 + cfg))
     rot = _rotate(sysm, R)
@@ -111,11 +132,6 @@ def test_large_water_sampled_and_properties(cfg):
     print(f"[fullsize] water{N} rotation: energy {e_err:.2e} forces {f_err:.2e} stress {s_err:.2e}", flush=True)
     assert e_err <= 2 * TOL[B.MACE_FP32]["energy"] and f_err <= 2 * TOL[B.MACE_FP32]["forces"]
     assert s_err <= 2 * TOL[B.MACE_FP32]["forces"]
-    # BF16-linear against FP32 at full size
-    g16 = run_gpu(params, sysm, blob, prec=B.MACE_BF16_LINEAR)
-    err = errors(g16, g32)
-    print(f"[fullsize] water{N} bf16 vs fp32 {err}", flush=True)
-    assert err["energy"] <= TOL[B.MACE_BF16_LINEAR]["energy"] and err["forces"] <= TOL[B.MACE_BF16_LINEAR]["forces"]
     # determinism at full size
     again = run_gpu(params, sysm, blob)
     assert np.array_equal(again["forces"], F) and np.array_equal(again["eps"], g32["eps"])
