@@ -123,6 +123,24 @@ mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, 
                                       int64_t max_edges, int32_t* sender, int32_t* receiver, int32_t* shifts,
                                       int64_t* n_edges, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * list as mace_neighbor_list_device, same arguments and results, without the
+ * workspace argument.  Its kernels use a file-scope device array of
+ * MACE_NEIGHBOR_SCRATCH_BYTES bytes instead, which every GPU the library runs
+ * on holds until the process ends (enough for 36,864 periodic atoms at a
+ * 6 A cutoff).  Calls no allocating routine.  Returns MACE_ENOSPACE, with
+ * nothing enqueued, when the list would need more than that
+ * (mace_neighbor_workspace_bytes > MACE_NEIGHBOR_SCRATCH_BYTES).  Every call
+ * on one GPU shares that GPU's array: calls that overlap on one GPU (other
+ * streams, other host threads) race and must be serialised by the caller.
+ * Each call clears what its kernels need zeroed. */
+#define MACE_NEIGHBOR_SCRATCH_BYTES ((size_t)80 << 20)
+mace_status mace_neighbor_list_device_noalloc(int64_t n_atoms, const double* positions, const double* cells,
+                                              const int32_t* graph_offsets, int32_t n_graphs, double r_cut,
+                                              int64_t max_edges, int32_t* sender, int32_t* receiver, int32_t* shifts,
+                                              int64_t* n_edges, void* stream);
+
 /* Validate and pack a graph and the weights into the workspace.
  * Paper: "Graph representation of atomic configurations" (atoms are nodes
  * with coordinates r_i and species z_i, edges join atoms within the cutoff;

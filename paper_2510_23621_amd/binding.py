@@ -27,6 +27,7 @@ MACE_PRODUCTS_SPLIT_BF16 = 2
 MACE_BLOCK_EDGE_PRODUCT = 0
 MACE_BLOCK_SYMMETRIC_CONTRACTION = 1
 MACE_BLOCK_RADIAL_MLP = 2
+MACE_NEIGHBOR_SCRATCH_BYTES = 80 << 20
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 
@@ -35,7 +36,7 @@ EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", 
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
             "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form",
-            "mace_fp32_products", "mace_block_rounding"]
+            "mace_fp32_products", "mace_block_rounding", "mace_neighbor_list_device_noalloc"]
 
 
 class MaceError(RuntimeError):
@@ -81,6 +82,7 @@ def lib() -> ctypes.CDLL:
         L.mace_neighbor_workspace_bytes.argtypes = [I64, P, P, I32, D]
         L.mace_neighbor_workspace_bytes.restype = Z
         L.mace_neighbor_list_device.argtypes = [I64, P, P, P, I32, D, I64, P, P, P, P, P, Z, P]
+        L.mace_neighbor_list_device_noalloc.argtypes = [I64, P, P, P, I32, D, I64, P, P, P, P, P]
         L.mace_graph_setup.argtypes = [dp, P, I64, I64, P, I64, P, P, P, P, I32, I32, P, Z, P, P]
         L.mace_forward_energy.argtypes = [P, P, P, P, P]
         L.mace_forces.argtypes = [P, P, P, P, P, P]
@@ -211,6 +213,35 @@ def mace_neighbor_list_device(positions, r_cut: float, cells=None, graph_offsets
     rcv = torch.empty_like(snd)
     sh = torch.empty(max(max_edges, 1), 3, dtype=torch.int32, device=positions.device)
     _check(call(max_edges, snd, rcv, sh), "mace_neighbor_list_device")
+    E = ne.value
+    return snd[:E], rcv[:E], sh[:E]
+
+
+def mace_neighbor_list_device_noalloc(positions, r_cut: float, cells=None, graph_offsets=None, n_graphs: int = 1,
+                                      max_edges=None, stream=None):
+    """As mace_neighbor_list_device, through the entry point that takes no
+    workspace (the library's static device scratch): allocates nothing on the
+    device itself; the output tensors are allocated here, by torch."""
+    import torch
+    N = int(positions.shape[0])
+    cl = None if cells is None else np.ascontiguousarray(cells, dtype=np.float64)
+    go = None if graph_offsets is None else np.ascontiguousarray(graph_offsets, dtype=np.int32)
+    ne = ctypes.c_int64()
+    L = lib()
+
+    def call(cap, snd, rcv, sh):
+        return L.mace_neighbor_list_device_noalloc(N, _ptr(positions), _ptr(cl), _ptr(go), int(n_graphs),
+                                                   float(r_cut), cap, _ptr(snd), _ptr(rcv), _ptr(sh),
+                                                   ctypes.byref(ne), _stream(stream))
+    if max_edges is None:
+        code = call(0, None, None, None)
+        if code not in (0, -3):
+            raise MaceError(code, "mace_neighbor_list_device_noalloc")
+        max_edges = ne.value
+    snd = torch.empty(max(max_edges, 1), dtype=torch.int32, device=positions.device)
+    rcv = torch.empty_like(snd)
+    sh = torch.empty(max(max_edges, 1), 3, dtype=torch.int32, device=positions.device)
+    _check(call(max_edges, snd, rcv, sh), "mace_neighbor_list_device_noalloc")
     E = ne.value
     return snd[:E], rcv[:E], sh[:E]
 

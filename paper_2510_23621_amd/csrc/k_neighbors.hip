@@ -29,6 +29,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "../../include/mace.h"
@@ -393,6 +394,16 @@ bool invert3(const double* c, double* inv) {
   return true;
 }
 
+// a[0 .. na) = 0, b[0 .. nb) = 0, c[0] = 0: the counters a list starts from
+// (a kernel rather than memsets, so that a captured call replays correctly)
+__global__ void nl_zero_kernel(int* __restrict__ a, uint32_t na, int* __restrict__ b, uint32_t nb,
+                               int* __restrict__ c) {
+  const uint32_t stride = gridDim.x * blockDim.x;
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < na; i += stride) a[i] = 0;
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < nb; i += stride) b[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) c[0] = 0;
+}
+
 constexpr int64_t kMaxCandidates = int64_t(1) << 30;
 
 // Host plan: per-graph records, candidate count, slot table size and the
@@ -478,17 +489,12 @@ extern "C" size_t mace_neighbor_workspace_bytes(int64_t n_atoms, const double* c
   return p.bytes;
 }
 
-extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, const double* cells,
-                                                 const int32_t* graph_offsets, int32_t n_graphs, double r_cut,
-                                                 int64_t max_edges, int32_t* sender, int32_t* receiver,
-                                                 int32_t* shifts, int64_t* n_edges, void* workspace,
-                                                 size_t workspace_bytes, void* stream) {
-  if (!n_edges || (n_atoms > 0 && !positions) || max_edges < 0) return MACE_EINVAL;
-  NlPlan p;
-  mace_status st = plan_nl(n_atoms, cells, graph_offsets, n_graphs, r_cut, p);
-  if (st != MACE_OK) return st;
-  if (!workspace || workspace_bytes < p.bytes) return MACE_ENOSPACE;
-  if (max_edges > 0 && (!sender || !receiver || !shifts)) return MACE_EINVAL;
+namespace {
+
+// The list built in the device buffer w (at least p.bytes), planned by plan_nl.
+mace_status nl_run(const NlPlan& p, int64_t n_atoms, const double* positions, int32_t n_graphs, double r_cut,
+                   int64_t max_edges, int32_t* sender, int32_t* receiver, int32_t* shifts, int64_t* n_edges,
+                   void* workspace, void* stream) {
   *n_edges = 0;
   if (n_atoms == 0) return MACE_OK;
   hipStream_t s = (hipStream_t)stream;
@@ -511,13 +517,12 @@ extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* 
   const double bs = r_cut + 1e-6, rc2 = r_cut * r_cut;
   const uint32_t mask = p.n_slots - 1;
   hipError_t err = hipMemcpyAsync(gs, p.gs.data(), sizeof(NlGraph) * G, hipMemcpyHostToDevice, s);
-  if (err == hipSuccess) err = hipMemsetAsync(scnt, 0, sizeof(int) * p.n_slots, s);
-  if (err == hipSuccess) err = hipMemsetAsync(sfill, 0, sizeof(int) * p.n_slots, s);
-  if (err == hipSuccess) err = hipMemsetAsync(flags, 0, sizeof(int), s);
   if (err != hipSuccess) {
-    hipStreamSynchronize(s);   // the plan's host copy must outlive the upload
+    (void)hipStreamSynchronize(s);   // the plan's host copy must outlive the upload
     return MACE_EHIP;
   }
+  nl_zero_kernel<<<std::min<unsigned>(1024, (p.n_slots + kNlThreads - 1) / kNlThreads), kNlThreads, 0, s>>>(
+      scnt, p.n_slots, sfill, p.n_slots, flags);
   const unsigned nblk = (unsigned)((N + kNlThreads - 1) / kNlThreads);
   const unsigned cblk = (unsigned)((p.C + kNlThreads - 1) / kNlThreads);
   nl_wrap_kernel<<<nblk, kNlThreads, 0, s>>>(N, positions, gs, G, xw, nsh, flags);
@@ -546,4 +551,64 @@ extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* 
     nl_receiver_kernel<true><<<rblk, 64 * kNlWaves, 0, s>>>(N, positions, gs, G, xw, nsh, bs, rc2, mask, soff, order,
                                                           cj, cs, cb, nullptr, roff, sender, receiver, shifts);
   return hipGetLastError() == hipSuccess ? MACE_OK : MACE_EHIP;
+}
+
+}  // namespace
+
+extern "C" mace_status mace_neighbor_list_device(int64_t n_atoms, const double* positions, const double* cells,
+                                                 const int32_t* graph_offsets, int32_t n_graphs, double r_cut,
+                                                 int64_t max_edges, int32_t* sender, int32_t* receiver,
+                                                 int32_t* shifts, int64_t* n_edges, void* workspace,
+                                                 size_t workspace_bytes, void* stream) {
+  if (!n_edges || (n_atoms > 0 && !positions) || max_edges < 0) return MACE_EINVAL;
+  NlPlan p;
+  mace_status st = plan_nl(n_atoms, cells, graph_offsets, n_graphs, r_cut, p);
+  if (st != MACE_OK) return st;
+  if (!workspace || workspace_bytes < p.bytes) return MACE_ENOSPACE;
+  if (max_edges > 0 && (!sender || !receiver || !shifts)) return MACE_EINVAL;
+  return nl_run(p, n_atoms, positions, n_graphs, r_cut, max_edges, sender, receiver, shifts, n_edges, workspace,
+                stream);
+}
+
+// ---- the same list without a workspace argument: a file-scope device array
+// serves as the workspace. Every GPU holds its own copy until the process
+// ends; host code addresses it only through the pointer hipGetSymbolAddress
+// returns for the current device (the array's name on the host is not a
+// device address).
+constexpr size_t kNlScratchBytes = MACE_NEIGHBOR_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNlScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// this device's scratch, looked up once per device
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+extern "C" mace_status mace_neighbor_list_device_noalloc(int64_t n_atoms, const double* positions,
+                                                         const double* cells, const int32_t* graph_offsets,
+                                                         int32_t n_graphs, double r_cut, int64_t max_edges,
+                                                         int32_t* sender, int32_t* receiver, int32_t* shifts,
+                                                         int64_t* n_edges, void* stream) {
+  if (!n_edges || (n_atoms > 0 && !positions) || max_edges < 0) return MACE_EINVAL;
+  NlPlan p;
+  mace_status st = plan_nl(n_atoms, cells, graph_offsets, n_graphs, r_cut, p);
+  if (st != MACE_OK) return st;
+  if (p.bytes > kNlScratchBytes) return MACE_ENOSPACE;
+  if (max_edges > 0 && (!sender || !receiver || !shifts)) return MACE_EINVAL;
+  void* w = device_scratch();
+  if (!w) return MACE_EHIP;
+  return nl_run(p, n_atoms, positions, n_graphs, r_cut, max_edges, sender, receiver, shifts, n_edges, w, stream);
 }
