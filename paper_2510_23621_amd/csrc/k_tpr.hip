@@ -1061,41 +1061,33 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
   }
 }
 
-// ---- FP32 backward at l_h = 2 in the edge-lane layout.
+// ---- FP32-accurate backward at l_h = 2 in the edge-lane layout.
 //
 // At P = 17 the split-BF16 parts of W3 in both layouts (209 KB) do not fit the
-// LDS, so both radial products run on FP32 MFMA (v_mfma_f32_16x16x4_f32, one
-// K value per lane), which needs one copy of W3's slice only: both products
-// read it from the same padded layout sW[(p 64 + j) kEPitch + kk].
-//   R (edge on the lane): D[channel][edge] = sum_j W3[j][p, channel] a3[edge][j];
-//     in K step s, lane group g supplies j = 16 g + s, so that the lane's a3
-//     values are one contiguous run of 16 (four float4 loads).
+// LDS beside the G tables. The R recompute runs on split-BF16 MFMA with W3's
+// three parts in LDS (the swizzled forward layout of the l_h <= 1 backward,
+// 104 KB) and a3 split per tile in registers; dE/da3 runs on FP32 MFMA
+// (v_mfma_f32_16x16x4_f32, one K value per lane) with its W3 operand read as
+// float4 straight from the blob (the layer's W3 is 557 KB, resident in the
+// XCD's L2):
 //   dE/da3: D[j][edge] = sum_(p, c) W3[j][p, c] dR[edge][p, c]; in K step
 //     (p, c') lane group g supplies channel 4 g + c', which is the lane's own
-//     register r[p][c']: dR is the B operand as it stands.
+//     register r[p][c']: dR is the B operand as it stands, and one float4 of
+//     W3's row j = 16 jt + l%16 (channels 16 ct + 4 g .. +3) feeds four MFMAs.
 // The CG part is the edge-lane contraction of the l_h = 1 backward (G table of
 // the receiver in LDS, two multiply-adds per coupling pair and channel). One
-// wave per SIMD (the G tables of four receivers and the W3 slice take 122 KB),
-// so the next tile's operands (sender rows, harmonics, a3) are loaded while
-// the current tile is contracted.
-constexpr int kEPitch = 17;
-
-template <int P>
-__device__ __forceinline__ void load_w3_slice_el(const float* __restrict__ W3, int K, int ct, float* sW) {
-  const int PK = P * K;
-  for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
-    const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
-    sW[(p * 64 + j) * kEPitch + kk] = W3[(size_t)j * PK + p * K + 16 * ct + kk];
-  }
-}
-
-// One wave per SIMD leaves no other wave to hide latency, so the body keeps
-// its own reads in flight: every LDS operand is requested a fixed number of
-// uses ahead (a ring of registers indexed by compile-time constants), the
-// sender rows and harmonics of a tile are requested before its radial MFMAs,
-// and the next tile's a3 and sender index before its CG contraction.
-constexpr int kRingW = 16;   // W3 operands in flight (one MFMA each)
-constexpr int kRingG = 8;    // G-table entries in flight (one coupling pair each)
+// wave per SIMD (W3's parts and four G tables take 149 KB), so the body keeps
+// its own reads in flight: every LDS or global operand is requested a fixed
+// number of uses ahead (a ring of registers indexed by compile-time
+// constants, held in issue order by scheduling fences), the sender rows and
+// harmonics of a tile are requested before its radial MFMAs, and the next
+// tile's a3 and sender index before its CG contraction.
+// last dword of a raw buffer descriptor (32-bit data format, no swizzle): loads
+// past num_records return zero
+constexpr int kBufferRsrcWord3 = 0x00020000;
+constexpr int kRingR = 3;    // split-W3 operand triples in flight (six MFMAs each)
+constexpr int kRingD = 2;    // paths' W3 rows in flight (four float4, sixteen MFMAs each)
+constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
 
 // sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
 template <int DIN>
@@ -1107,10 +1099,12 @@ __device__ __forceinline__ void el_load_hy(f4* hv, f4* y4, int src, int e, int k
   for (int v = 0; v < 4; ++v) y4[v] = reinterpret_cast<const f4*>(Y + (size_t)e * 16)[v];
 }
 
-// a3[e][16 g .. 16 g + 15]
+// the lane's a3 operands of the split R product: a3[e][32 ks + 8 g .. +7],
+// a[2 ks] (first four) and a[2 ks + 1]
 __device__ __forceinline__ void el_load_a3(f4* a, int e, int g, const float* __restrict__ a3) {
 #pragma unroll
-  for (int v = 0; v < 4; ++v) a[v] = reinterpret_cast<const f4*>(a3 + (size_t)e * 64 + 16 * g)[v];
+  for (int v = 0; v < 4; ++v)
+    a[v] = *reinterpret_cast<const f4*>(a3 + (size_t)e * 64 + 32 * (v >> 1) + 8 * g + 4 * (v & 1));
 }
 
 template <int NW, bool RND>
@@ -1118,15 +1112,30 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
-    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd, float* sW, float* sGall) {
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd, unsigned short* sWf,
+    float* sGall) {
   constexpr int LHMAX = 2;
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
   constexpr int NPAIR = PairCount<LHMAX>::value;
-  constexpr int NW3 = P * 16;   // MFMAs per radial product
+  constexpr int part = P * 16 * 64;
+  constexpr int NR = P * 2;    // (path, K step) steps of the split R product
+  constexpr int ND = P * 4;    // (path, row tile) steps of the dE/da3 product
   const int ct = blockIdx.y;
-  load_w3_slice_el<P>(W3, K, ct, sW);
+  const int PK = P * K;
+  {
+    // W3's three parts in the swizzled forward layout: row p 16 + kk of 64 j
+    for (int idx = threadIdx.x; idx < P * 16 * 64; idx += blockDim.x) {
+      const int kk = idx & 15, j = (idx >> 4) & 63, p = idx >> 10;
+      unsigned short x0, x1, x2;
+      split3(W3[(size_t)j * PK + p * K + 16 * ct + kk], x0, x1, x2);
+      const int of = swz_fwd(p * 16 + kk, j >> 3) + (j & 7);
+      sWf[of] = x0;
+      sWf[part + of] = x1;
+      sWf[2 * part + of] = x2;
+    }
+  }
   __syncthreads();
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int g = l >> 4, kk = l & 15;
@@ -1134,30 +1143,44 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
   float* sg = sGall + w * NPAIR * 16;   // this wave's G table [pair][channel]
   float* dYc = dYp + (size_t)ct * E * 16;
   float* da3c = da3p + (size_t)ct * E * 64;
-  // R operand of MFMA f = 16 p + s: W3[j = 16 g + s][p, 16 ct + kk]
-  const float* wR = sW + (16 * g) * kEPitch + kk;
-  // dE/da3 operand of MFMA f = 16 p + 4 c + jt: W3[j = 16 jt + kk][p, 16 ct + 4 g + c]
-  const float* wD = sW + kk * kEPitch + 4 * g;
-  auto wr_at = [&](int f) { return wR[((f >> 4) * 64 + (f & 15)) * kEPitch]; };
-  auto wd_at = [&](int f) { return wD[((f >> 4) * 64 + 16 * (f & 3)) * kEPitch + ((f >> 2) & 3)]; };
+  // split R operand of step f = 2 p + ks: row p 16 + kk, chunk 4 ks + g
+  auto wr_at = [&](int f, us8v* o) {
+    const unsigned short* q = sWf + swz_fwd((f >> 1) * 16 + kk, 4 * (f & 1) + g);
+    o[0] = *reinterpret_cast<const us8v*>(q);
+    o[1] = *reinterpret_cast<const us8v*>(q + part);
+    o[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
+  };
+  // dE/da3 operand of step f = 4 p + jt: W3[j = 16 jt + kk][p K + 16 ct + 4 g .. +3],
+  // a buffer load with the lane's part of the offset in one register and the
+  // step's part as a scalar (flat addresses for all 68 steps, hoisted out of the
+  // edge loop, would not fit the registers); the descriptor covers W3 exactly
+  const __amdgpu_buffer_rsrc_t w3r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(W3), (short)0, 64 * PK * 4, kBufferRsrcWord3);
+  const int wd_lane = (kk * PK + 16 * ct + 4 * g) * 4;
+  auto wd_at = [&](int f) {
+    return __builtin_bit_cast(
+        f4, __builtin_amdgcn_raw_buffer_load_b128(w3r, wd_lane, (16 * (f & 3) * PK + (f >> 2) * K) * 4, 0));
+  };
   for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
     if (e_beg == e_end) continue;
     {
-      // G_p of this receiver for channel 16 ct + l%16; the four lane groups
-      // compute the same values and the first one stores
-      float gv[MID];
-#pragma unroll
-      for (int c = 0; c < MID; ++c) gv[c] = dAt[((size_t)i * MID + c) * K + 16 * ct + kk] * inv_c;
+      // G_p of this receiver for channel 16 ct + l%16, path by path (only the
+      // path's own dE/dAt values live); the four lane groups compute the same
+      // values and the first one stores
+      const float* gsrc = dAt + (size_t)i * MID * K + 16 * ct + kk;
       __builtin_amdgcn_wave_barrier();   // the previous receiver's reads come first
       for_paths<LHMAX>([&](auto tag) {
         using T = decltype(tag);
         using C = mt::CG<T::lh, T::ly, T::lo>;
         constexpr int goff = PathPairOffset<T::index>::value;
+        float gv[2 * T::lo + 1];
+#pragma unroll
+        for (int m = 0; m < 2 * T::lo + 1; ++m) gv[m] = gsrc[(size_t)(T::offset + m) * K] * inv_c;
         float Gp[C::npair];
 #pragma unroll
         for (int u = 0; u < C::npair; ++u) Gp[u] = 0.f;
-        C::each_p([&](int m1, int m2, int m3, float cg, int pi) { Gp[pi] += cg * gv[T::offset + m3]; });
+        C::each_p([&](int m1, int m2, int m3, float cg, int pi) { Gp[pi] += cg * gv[m3]; });
         if (g == 0) {
 #pragma unroll
           for (int u = 0; u < C::npair; ++u) sg[(goff + u) * 16 + kk] = Gp[u];
@@ -1172,43 +1195,43 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     el_load_a3(a, e, g, a3);
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
       __asm__ volatile("" ::: "memory");   // the G table is read per tile, not held in registers
-      const bool valid = e0 + kk < e_end;
+      // Lanes past the receiver's last edge work on that edge (ec is clamped):
+      // their inputs, hence every value they compute, equal the last valid
+      // lane's, so they store the same values to the same rows, and the stores
+      // need no branch.
+      const int ec = e;
       const bool more = e0 + 16 < e_end;
       f4 hv[DIN], y4[4];
       el_load_hy<DIN>(hv, y4, src, e, kb, h, Y, K);
-      // R of the tile, edge on the lane (rows past e_end are computed from a
-      // valid edge's a3 and never stored: every output row depends on its own
-      // edge only)
+      // R of the tile, edge on the lane, split-BF16 products
       f4 r[P];
-      {
-        float ring[kRingW];
 #pragma unroll
-        for (int f = 0; f < kRingW; ++f) ring[f] = wr_at(f);
-        f4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+      {
+        us8v x[2][3];
+        split3_x8(a[0], a[1], x[0][0], x[0][1], x[0][2]);
+        split3_x8(a[2], a[3], x[1][0], x[1][1], x[1][2]);
+        us8v ring[kRingR][3];
+#pragma unroll
+        for (int f = 0; f < kRingR; ++f) wr_at(f, ring[f]);
         __builtin_amdgcn_s_setprio(1);
-        // (a scheduling fence per step keeps each read kRingW MFMAs ahead of its use)
-        static_for<0, NW3>([&](auto F) {
+        static_for<0, NR>([&](auto F) {
           constexpr int f = decltype(F)::value;
-          __builtin_amdgcn_sched_barrier(0);
-          const float wv = ring[f % kRingW];
-          if constexpr (f + kRingW < NW3) ring[f % kRingW] = wr_at(f + kRingW);
-          acc = mfma4(wv, a[(f & 15) >> 2][f & 3], acc);
-          if constexpr ((f & 15) == 15) {
-            r[f >> 4] = acc;
-            acc = f4{0.f, 0.f, 0.f, 0.f};
-          }
+          constexpr int p = f >> 1, ks = f & 1;
+          __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingR steps ahead of its use
+          const us8v b0 = ring[f % kRingR][0], b1 = ring[f % kRingR][1], b2 = ring[f % kRingR][2];
+          if constexpr (f + kRingR < NR) wr_at(f + kRingR, ring[f % kRingR]);
+          f4 acc = r[p];
+          acc = mfma_bf16(b0, x[ks][2], acc);
+          acc = mfma_bf16(b1, x[ks][1], acc);
+          acc = mfma_bf16(b2, x[ks][0], acc);
+          acc = mfma_bf16(b0, x[ks][1], acc);
+          acc = mfma_bf16(b1, x[ks][0], acc);
+          r[p] = mfma_bf16(b0, x[ks][0], acc);
         });
         __builtin_amdgcn_s_setprio(0);
       }
       if constexpr (RND) round_tile<P>(r, rnd);
-      // the next tile's sender index and a3, in flight during the contraction
-      int src_n = src, e_n = e;
-      if (more) {
-        e_n = min(e0 + 16 + kk, e_end - 1);
-        src_n = snd[e_n];
-        if (src_map) src_n = src_map[src_n];
-        el_load_a3(a, e_n, g, a3);
-      }
       float y[16];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
@@ -1258,6 +1281,13 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
             dh[lh * lh + m] += rv * Dm[m];
           }
           r[T::index] = d;   // dR
+          // the paths come ordered by l_h: after the last one of an l_h block
+          // that block of the sender gradient is complete and leaves registers
+          if constexpr (T::index + 1 == P || PathAt<T::index + 1>::lh != lh) {
+#pragma unroll
+            for (int m = 0; m < 2 * lh + 1; ++m)
+              *reinterpret_cast<f4*>(Q + ((size_t)ec * DIN + lh * lh + m) * K + kb) = dh[lh * lh + m];
+          }
         });
       }
       // dE/dY over the tile's 16 channels: halve over lane bit 5, then bit 4;
@@ -1278,38 +1308,45 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
           dy[m] = keep + __shfl_xor(send, 16);
         }
       }
-      const int ev = e0 + kk;
-      if (valid) {
-        *reinterpret_cast<f4*>(dYc + (size_t)ev * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
-        if (Q) {
-#pragma unroll
-          for (int c = 0; c < DIN; ++c) *reinterpret_cast<f4*>(Q + ((size_t)ev * DIN + c) * K + kb) = dh[c];
-        }
+      *reinterpret_cast<f4*>(dYc + (size_t)ec * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
+      // the next tile's sender index and a3, in flight during the dE/da3 product
+      if (more) {
+        e = min(e0 + 16 + kk, e_end - 1);
+        src = snd[e];
+        if (src_map) src = src_map[src];
+        el_load_a3(a, e, g, a3);
       }
       // dE/da3 partial: d3[jt][rr] = D[j = 16 jt + 4 g + rr][edge e0 + l%16]
       f4 d3[4];
 #pragma unroll
       for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
       {
-        float ring[kRingW];
+        // a path's four W3 rows per step; the four accumulators interleave
+        f4 ring[kRingD][4];
 #pragma unroll
-        for (int f = 0; f < kRingW; ++f) ring[f] = wd_at(f);
+        for (int f = 0; f < kRingD; ++f)
+#pragma unroll
+          for (int jt = 0; jt < 4; ++jt) ring[f][jt] = wd_at(4 * f + jt);
         __builtin_amdgcn_s_setprio(1);
-        static_for<0, NW3>([&](auto F) {
-          constexpr int f = decltype(F)::value;
-          __builtin_amdgcn_sched_barrier(0);
-          const float wv = ring[f % kRingW];
-          if constexpr (f + kRingW < NW3) ring[f % kRingW] = wd_at(f + kRingW);
-          d3[f & 3] = mfma4(wv, r[f >> 4][(f >> 2) & 3], d3[f & 3]);
+        static_for<0, P>([&](auto PI) {
+          constexpr int p = decltype(PI)::value;
+          __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingD paths ahead of its use
+          f4 wv[4];
+#pragma unroll
+          for (int jt = 0; jt < 4; ++jt) wv[jt] = ring[p % kRingD][jt];
+          if constexpr (p + kRingD < P) {
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) ring[p % kRingD][jt] = wd_at(4 * (p + kRingD) + jt);
+          }
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(wv[jt][c], r[p][c], d3[jt]);
         });
         __builtin_amdgcn_s_setprio(0);
       }
-      if (valid) {
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt) *reinterpret_cast<f4*>(da3c + (size_t)ev * 64 + 16 * jt + 4 * g) = d3[jt];
-      }
-      src = src_n;
-      e = e_n;
+      for (int jt = 0; jt < 4; ++jt) *reinterpret_cast<f4*>(da3c + (size_t)ec * 64 + 16 * jt + 4 * g) = d3[jt];
     }
   }
 }
@@ -1329,7 +1366,7 @@ tpr_bwd_kernel(
     // W3's slice (one layout for both products) and a G table per wave; the
     // precision study's operand rounding runs as its own instance (a uniform
     // branch, taken once)
-    __shared__ float sW[path_count(2) * 64 * kEPitch];
+    __shared__ __align__(16) unsigned short sW[3 * path_count(2) * 16 * 64];
     __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
     if (rnd)
       tpr_bwd_l2_edge_lanes_body<NW, true>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
