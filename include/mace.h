@@ -44,10 +44,15 @@ typedef enum {
   MACE_FP16_LINEAR = 2,   /* the same with IEEE binary16 (round to nearest even;
                              an input or weight beyond 65504 becomes infinite and
                              the outputs then hold non-finite values) */
-  MACE_BF16_RADIAL = 3    /* MACE_BF16_LINEAR, and the last layer of the radial
+  MACE_BF16_RADIAL = 3,   /* MACE_BF16_LINEAR, and the last layer of the radial
                              MLP (the P*K-wide one) on BF16 operands with FP32
                              accumulation: R = bf16(a3) bf16(W) forward and
                              dE/da3 = bf16(dE/dR) bf16(W)^T backward */
+  MACE_FP64 = 4           /* debug precision: every step in FP64 on the vector
+                             units (plain kernels, not tuned for speed), every
+                             layer in per-edge form; positions, node energies
+                             and forces are FP64 (the FP64 baseline every
+                             precision arm of the paper is measured against) */
 } mace_precision;
 
 /* Model hyper-parameters (host).  Supported: sh_lmax = 3, correlation = 3,
@@ -160,25 +165,29 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
                              int32_t n_graphs, mace_precision prec, void* workspace, size_t workspace_bytes,
                              void* stream, mace_graph** out);
 
-/* Energies.  Paper: "Higher-order Message Passing in MACE" -- the two-body
+/* Positions, node energies and forces are FP32 (float) for every precision
+ * but MACE_FP64, where they are FP64 (double); per-graph energies and the
+ * stress are FP64 always.
+ *
+ * Energies.  Paper: "Higher-order Message Passing in MACE" -- the two-body
  * edge embedding (Eq. 26), the node-local product basis (Eq. 27), the message
  * over correlation orders, the linear update with residual and the readouts;
  * and the energy equation of "MACE inference: energy and forces", eps_i from
  * the invariant features, E = sum_i eps_i (here per graph, summed in FP64 in
- * a fixed order).  positions (dev) [N][3] FP32; node_energy (dev) [N] FP32;
+ * a fixed order).  positions (dev) [N][3]; node_energy (dev) [N];
  * graph_energy (dev) [G] FP64.  No host synchronisation, no allocation.
  * MACE_EUNSUPPORTED (nothing enqueued) if the handle's settings select an
  * edge-product instance that is not built. */
-mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+mace_status mace_forward_energy(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
                                 void* stream);
 
 /* Energies and forces.  Paper: the force equation of "MACE inference:
  * energy and forces", F_i = -dE/dr_i = -sum_j d eps_j / d r_i, evaluated by
  * the reverse pass of every step of mace_forward_energy (a hand-written
  * vector-Jacobian product, deterministic: no floating-point atomics).  As
- * mace_forward_energy plus forces (dev) [N][3] FP32. */
-mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
-                        float* forces, void* stream);
+ * mace_forward_energy plus forces (dev) [N][3]. */
+mace_status mace_forces(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
+                        void* forces, void* stream);
 
 /* Energies, forces and the stress of every graph.  Paper: the NPT
  * observables of "Precision-loss metrics" monitor the pressure p(t) of a
@@ -190,8 +199,8 @@ mace_status mace_forces(mace_graph* g, const float* positions, float* node_energ
  * handle set up without cells V = 1 (the bare strain derivative). Summed in
  * FP64 in a fixed order (bitwise reproducible). Other arguments and behaviour
  * as mace_forces. */
-mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
-                               float* forces, double* stress, void* stream);
+mace_status mace_forces_stress(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
+                               void* forces, double* stress, void* stream);
 
 /* How the first interaction layer forms its message.  Its sender features
  * depend on the species only (the embedding through linear_up) and its paths

@@ -19,6 +19,7 @@ MACE_FP32 = 0
 MACE_BF16_LINEAR = 1
 MACE_FP16_LINEAR = 2
 MACE_BF16_RADIAL = 3
+MACE_FP64 = 4
 MACE_L0_AUTO = 0
 MACE_L0_EDGE = 1
 MACE_L0_FACTORED = 2

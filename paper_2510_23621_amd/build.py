@@ -1,6 +1,7 @@
 """Build the gfx950 library in-tree.
 
 1. compile and run the table generator (host C++) -> csrc/generated/mace_tables.h
+   (FP32 immediates) and mace_tables64.h (FP64, for the debug precision)
 2. compile the host neighbour list with g++ (-ffp-contract=off: its FP64
    arithmetic must round exactly as written)
 3. hipcc every kernel file and the host runtime for gfx950 -> libmace_amd.so
@@ -18,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmace_amd.so")
 HIP_SOURCES = ["api.hip", "k_edge.hip", "k_radial.hip", "k_tpr.hip", "k_layer0.hip", "k_sender.hip", "k_symcon.hip", "k_node.hip",
-               "k_neighbors.hip"]
+               "k_neighbors.hip", "k_fp64.hip"]
 # files whose FP64 arithmetic must round exactly as written (no fused multiply-adds)
 NO_CONTRACT = {"k_neighbors.hip"}
 HIPCC_FLAGS = [
@@ -44,7 +45,8 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     os.makedirs(os.path.join(CSRC, "generated"), exist_ok=True)
     gen = os.path.join(BUILD, "gen_tables")
     _run(["g++", "-O2", "-std=c++17", "-ffp-contract=off", "-o", gen, os.path.join(CSRC, "gen_tables.cpp")], verbose)
-    _run([gen, os.path.join(CSRC, "generated", "mace_tables.h")], verbose)
+    _run([gen, os.path.join(CSRC, "generated", "mace_tables.h"), os.path.join(CSRC, "generated", "mace_tables64.h")],
+         verbose)
     nl_obj = os.path.join(BUILD, "neighbors.o")
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wno-unknown-pragmas", "-c",
           os.path.join(CSRC, "neighbors.cpp"), "-o", nl_obj], verbose)

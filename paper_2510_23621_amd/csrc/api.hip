@@ -261,6 +261,54 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.status = c.take<int>(64);
 }
 
+// Buffers of the FP64 debug precision (carved after the FP32 ones, for
+// MACE_FP64 handles only).
+struct Buffers64 {
+  double* w = nullptr;                          // the weight blob in FP64
+  double *Y = nullptr, *rb = nullptr;           // [E][16], [E][nb]
+  std::vector<double*> z;                       // per layer 3 x [E][64]: radial pre-activations
+  std::vector<double*> h;                       // h^t, t = 0..T: [N][d_t][K]
+  std::vector<double*> A;                       // per layer [N][16][K]
+  std::vector<double*> ht;                      // per layer: sender features W h^t [N][din][K]
+  double *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
+  double *dh0 = nullptr, *dh1 = nullptr, *dB = nullptr, *dA = nullptr, *dApre = nullptr, *dAt = nullptr,
+         *dht = nullptr, *dY = nullptr, *de = nullptr, *da3 = nullptr, *Q = nullptr;
+  double4* g = nullptr;                         // [E] dE/dd
+};
+
+void carve64(const Model& m, int64_t N, int64_t E, Carver& c, Buffers64& b) {
+  const int64_t K = m.d.K, T = m.d.n_layers, E1 = std::max<int64_t>(E, 1);
+  b.w = c.take<double>(m.total);
+  b.Y = c.take<double>(E1 * 16);
+  b.rb = c.take<double>(E1 * m.d.n_bessel);
+  b.z.assign(3 * T, nullptr);
+  for (auto& z : b.z) z = c.take<double>(E1 * 64);
+  b.h.assign(T + 1, nullptr);
+  b.h[0] = c.take<double>(N * K);
+  for (int t = 0; t < T; ++t) b.h[t + 1] = c.take<double>(N * m.layers[t].dout * K);
+  b.A.assign(T, nullptr);
+  for (auto& a : b.A) a = c.take<double>(N * 16 * K);
+  const int64_t dmax = std::max<int64_t>(m.max_din, m.max_dout);
+  b.ht.assign(T, nullptr);
+  for (int t = 0; t < T; ++t) b.ht[t] = c.take<double>(N * m.layers[t].din * K);
+  b.sc = c.take<double>(N * m.max_dout * K);
+  b.At = c.take<double>(N * m.max_mid * K);
+  b.Apre = c.take<double>(N * 16 * K);
+  b.B = c.take<double>(N * m.max_dout * K);
+  b.dh0 = c.take<double>(N * dmax * K);
+  b.dh1 = c.take<double>(N * dmax * K);
+  b.dB = c.take<double>(N * m.max_dout * K);
+  b.dA = c.take<double>(N * 16 * K);
+  b.dApre = c.take<double>(N * 16 * K);
+  b.dAt = c.take<double>(N * m.max_mid * K);
+  b.dht = c.take<double>(N * m.max_din * K);
+  b.dY = c.take<double>(E1 * 16);
+  b.de = c.take<double>(E1 * m.d.n_bessel);
+  b.da3 = c.take<double>(E1 * 64);
+  b.Q = c.take<double>(E1 * m.max_din * K);
+  b.g = c.take<double4>(E1);
+}
+
 }  // namespace
 
 enum KernelId {
@@ -284,6 +332,7 @@ struct mace_graph {
   double prof_flops = 0.0, prof_bytes = 0.0;   // algorithmic work of the profiled launches
   Model m;
   Buffers b;
+  Buffers64 b64;   // MACE_FP64 handles only
   int64_t N = 0, E = 0;
   int G = 1;
   int n_tiles = 0, n_quads = 0;
@@ -758,6 +807,158 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F, cons
   }
 }
 
+// ---------------------------------------------------------------- FP64 debug precision
+// The same model in FP64 on simple kernels (k_fp64.hip), every layer in
+// per-edge form; positions, node energies and forces are FP64.
+
+// a linear of blocks of components (see Lin64); spec for the species-dependent ones
+struct Lin64Builder {
+  Lin64 L;
+  Lin64Builder(int cin, int cout, bool transpose) {
+    std::memset(&L, 0, sizeof(L));
+    L.cin = cin;
+    L.cout = cout;
+    L.transpose = transpose;
+  }
+  Lin64Builder& add(int cx, int cy, int nc, int64_t woff, bool spec) {
+    const int t = L.n_terms++;
+    L.cx[t] = cx;
+    L.cy[t] = cy;
+    L.nc[t] = nc;
+    L.woff[t] = woff;
+    L.spec[t] = spec;
+    return *this;
+  }
+};
+
+SymW64 symw64(const mace_graph* h, int t) {
+  SymW64 w;
+  std::memset(&w, 0, sizeof(w));
+  for (int Lo : h->m.layers[t].out_ls)
+    for (int nu = 1; nu <= 3; ++nu) {
+      auto it = h->m.off.find(std::to_string(t) + ".symc." + std::to_string(Lo) + "." + std::to_string(nu));
+      if (it != h->m.off.end()) w.w[Lo][nu] = h->b64.w + it->second;
+    }
+  return w;
+}
+
+bool f64_supported(const mace_graph* h) {
+  if (h->m.d.n_layers > 8 || h->m.d.n_bessel > 16) return false;
+  for (const LayerPlan& L : h->m.layers)
+    if (L.lh_max > 2 || L.lout_max > 2 || (int)L.paths.size() > kMaxLin64Terms) return false;
+  return true;
+}
+
+void run_forward64(mace_graph* h, hipStream_t s, const double* pos, double* eps, bool seed_grad) {
+  const Model& m = h->m;
+  Buffers& b = h->b;
+  Buffers64& d = h->b64;
+  const int N = (int)h->N, E = (int)h->E, K = m.d.K, nb = m.d.n_bessel;
+  const double* W = d.w;
+  f64_geom(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, nb, d.Y, d.rb, b.status);
+  f64_embed(s, N, K, b.species, W + m.off.at("embed"), d.h[0]);
+  const double inv_c = 1.0 / m.d.c_norm;
+  for (int t = 0; t < m.d.n_layers; ++t) {
+    const LayerPlan& L = m.layers[t];
+    const std::string pre = std::to_string(t) + ".";
+    double** z = d.z.data() + 3 * t;
+    f64_radial_fwd(s, E, nb, d.rb, W + m.off.at(pre + "radial.0"), W + m.off.at(pre + "radial.1"),
+                   W + m.off.at(pre + "radial.2"), z[0], z[1], z[2]);
+    // linear_up, and the residual species linear of the layers above the first
+    Lin64Builder up(L.din, L.din, false);
+    for (int l : L.in_ls) up.add(l * l, l * l, 2 * l + 1, m.off.at(pre + "up." + std::to_string(l)), false);
+    f64_linear(s, N, K, up.L, b.species, W, d.h[t], d.ht[t], nullptr);
+    const double* sc = nullptr;
+    if (t > 0) {
+      Lin64Builder sk(L.din, L.dout, false);
+      for (int Lo : L.out_ls)
+        if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end())
+          sk.add(Lo * Lo, Lo * Lo, 2 * Lo + 1, m.off.at(pre + "skip." + std::to_string(Lo)), true);
+      f64_linear(s, N, K, sk.L, b.species, W, d.h[t], d.sc, nullptr);
+      sc = d.sc;
+    }
+    f64_tp_fwd(s, L.lh_max, N, K, b.rcv_off, b.snd, z[2], W + m.off.at(pre + "radial.3"), d.Y, d.ht[t], inv_c,
+               d.At);
+    // path-merging linear (at the first layer followed by the species linear)
+    Lin64Builder lin(L.mid, 16, false);
+    for (int q = 0; q < L.P; ++q) {
+      const int lo = L.paths[q].lo;
+      lin.add(L.path_off[q], lo * lo, 2 * lo + 1, m.off.at(pre + "linear." + std::to_string(q)), false);
+    }
+    if (t == 0) {
+      f64_linear(s, N, K, lin.L, b.species, W, d.At, d.Apre, nullptr);
+      Lin64Builder sk0(16, 16, false);
+      for (int l = 0; l <= 3; ++l) sk0.add(l * l, l * l, 2 * l + 1, m.off.at(pre + "skip." + std::to_string(l)), true);
+      f64_linear(s, N, K, sk0.L, b.species, W, d.Apre, d.A[t], nullptr);
+    } else {
+      f64_linear(s, N, K, lin.L, b.species, W, d.At, d.A[t], nullptr);
+    }
+    f64_symcon_fwd(s, L.lout_max, N, K, b.species, d.A[t], symw64(h, t), d.B);
+    Lin64Builder prod(L.dout, L.dout, false);
+    for (int Lo : L.out_ls) prod.add(Lo * Lo, Lo * Lo, 2 * Lo + 1, m.off.at(pre + "prod." + std::to_string(Lo)), false);
+    f64_linear(s, N, K, prod.L, b.species, W, d.B, d.h[t + 1], sc);
+    if (!L.last)
+      f64_readout(s, N, K, d.h[t + 1], L.dout * K, W + m.off.at(pre + "readout"), nullptr, 0, eps, t > 0, nullptr);
+    else
+      f64_readout(s, N, K, d.h[t + 1], L.dout * K, W + m.off.at(pre + "readout.0"), W + m.off.at(pre + "readout.1"),
+                  m.d.readout_hidden, eps, t > 0, seed_grad ? d.dh0 : nullptr);
+  }
+}
+
+void run_backward64(mace_graph* h, hipStream_t s, const double* pos, double* F) {
+  const Model& m = h->m;
+  Buffers& b = h->b;
+  Buffers64& d = h->b64;
+  const int N = (int)h->N, E = (int)h->E, K = m.d.K, nb = m.d.n_bessel, T = m.d.n_layers;
+  const double* W = d.w;
+  const double inv_c = 1.0 / m.d.c_norm;
+  double* dnext = d.dh0;   // dE/dh^{t+1}; the last readout seeded it
+  double* dprev = d.dh1;
+  for (int t = T - 1; t >= 0; --t) {
+    const LayerPlan& L = m.layers[t];
+    const std::string pre = std::to_string(t) + ".";
+    double** z = d.z.data() + 3 * t;
+    if (!L.last) f64_add_readout_grad(s, N, K, L.dout * K, W + m.off.at(pre + "readout"), dnext);
+    Lin64Builder prodT(L.dout, L.dout, true);
+    for (int Lo : L.out_ls) prodT.add(Lo * Lo, Lo * Lo, 2 * Lo + 1, m.off.at(pre + "prod." + std::to_string(Lo)), false);
+    f64_linear(s, N, K, prodT.L, b.species, W, dnext, d.dB, nullptr);
+    f64_symcon_bwd(s, L.lout_max, N, K, b.species, d.A[t], symw64(h, t), d.dB, d.dA);
+    const double* dA = d.dA;
+    if (t == 0) {
+      Lin64Builder sk0T(16, 16, true);
+      for (int l = 0; l <= 3; ++l) sk0T.add(l * l, l * l, 2 * l + 1, m.off.at(pre + "skip." + std::to_string(l)), true);
+      f64_linear(s, N, K, sk0T.L, b.species, W, d.dA, d.dApre, nullptr);
+      dA = d.dApre;
+    }
+    Lin64Builder linT(16, L.mid, true);
+    for (int q = 0; q < L.P; ++q) {
+      const int lo = L.paths[q].lo;
+      linT.add(lo * lo, L.path_off[q], 2 * lo + 1, m.off.at(pre + "linear." + std::to_string(q)), false);
+    }
+    f64_linear(s, N, K, linT.L, b.species, W, dA, d.dAt, nullptr);
+    f64_tp_bwd(s, L.lh_max, E, K, b.snd, b.rcv, z[2], W + m.off.at(pre + "radial.3"), d.Y, d.ht[t], d.dAt, inv_c,
+               d.dY, t < T - 1, d.da3, t > 0 ? d.Q : nullptr);
+    f64_radial_bwd(s, E, nb, W + m.off.at(pre + "radial.0"), W + m.off.at(pre + "radial.1"),
+                   W + m.off.at(pre + "radial.2"), z[0], z[1], z[2], d.da3, d.de, t < T - 1);
+    if (t > 0) {
+      // dE/dh^t: through linear_up (the sender sum of the per-edge gradients)
+      // and through the residual species linear
+      f64_sender_sum(s, N, L.din, K, b.snd_off, b.snd_perm, d.Q, d.dht);
+      Lin64Builder upT(L.din, L.din, true);
+      for (int l : L.in_ls) upT.add(l * l, l * l, 2 * l + 1, m.off.at(pre + "up." + std::to_string(l)), false);
+      f64_linear(s, N, K, upT.L, b.species, W, d.dht, dprev, nullptr);
+      Lin64Builder skT(L.dout, L.din, true);
+      for (int Lo : L.out_ls)
+        if (std::find(L.in_ls.begin(), L.in_ls.end(), Lo) != L.in_ls.end())
+          skT.add(Lo * Lo, Lo * Lo, 2 * Lo + 1, m.off.at(pre + "skip." + std::to_string(Lo)), true);
+      f64_linear(s, N, K, skT.L, b.species, W, dnext, dprev, dprev);
+      std::swap(dnext, dprev);
+    }
+  }
+  f64_edge_vjp(s, E, pos, b.snd, b.rcv, b.shift, m.d.r_cut, m.d.envelope_p, nb, d.dY, d.de, d.g);
+  f64_forces(s, N, b.rcv_off, b.snd_off, b.snd_perm, d.g, F);
+}
+
 }  // namespace
 
 // ================================================================== C ABI
@@ -800,12 +1001,15 @@ mace_status mace_weight_layout(const mace_model_desc* desc, int32_t max_tensors,
 
 size_t mace_workspace_bytes(const mace_model_desc* desc, int64_t n_atoms, int64_t n_edges, int32_t n_graphs,
                             mace_precision prec) {
-  (void)prec;
   Model m;
   if (build_model(desc, m) != MACE_OK || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return 0;
   Carver c{nullptr};
   Buffers b;
   carve(m, n_atoms, n_edges, n_graphs, c, b);
+  if (prec == MACE_FP64) {
+    Buffers64 b64;
+    carve64(m, n_atoms, n_edges, c, b64);
+  }
   return c.used + 256;
 }
 
@@ -821,7 +1025,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   if (st != MACE_OK) return st;
   if (!weights || !species || !workspace || n_atoms < 1 || n_edges < 0 || n_graphs < 1) return MACE_EINVAL;
   if (n_edges > 0 && !edge_index) return MACE_EINVAL;
-  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR && prec != MACE_FP16_LINEAR && prec != MACE_BF16_RADIAL)
+  if (prec != MACE_FP32 && prec != MACE_BF16_LINEAR && prec != MACE_FP16_LINEAR && prec != MACE_BF16_RADIAL &&
+      prec != MACE_FP64)
     return MACE_EINVAL;
   if (weight_floats != m.total) return MACE_EINVAL;
   if (n_atoms > (1LL << 30) || n_edges > (1LL << 31) - 1) return MACE_EUNSUPPORTED;
@@ -1078,6 +1283,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   // (mace_workspace_bytes includes that slack)
   Carver c{reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(workspace) + 255) & ~uintptr_t(255))};
   carve(h->m, N, E, G, c, h->b);
+  if (prec == MACE_FP64) carve64(h->m, N, E, c, h->b64);
   Buffers& b = h->b;
   auto up = [&](void* dst, const void* src, size_t bytes) {
     return bytes ? hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s) : hipSuccess;
@@ -1131,6 +1337,7 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   chk(hipMemsetAsync(b.status, 0, sizeof(int), s));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
                        lowp_mode(prec), b.sp_table);
+  if (prec == MACE_FP64) f64_widen(s, (size_t)m.total, b.w, h->b64.w);
   chk(hipGetLastError());
   chk(hipStreamSynchronize(s));  // host vectors go out of scope below
   if (err != hipSuccess) {
@@ -1147,40 +1354,61 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   return MACE_OK;
 }
 
-mace_status mace_forward_energy(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
+mace_status mace_forward_energy(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
                                 void* stream) {
   if (!g || !positions || !node_energy || !graph_energy) return MACE_EINVAL;
-  if (!launchable(g)) return MACE_EUNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
-  run_forward(g, s, positions, node_energy, false);
+  if (g->prec == MACE_FP64) {
+    if (!f64_supported(g)) return MACE_EUNSUPPORTED;
+    run_forward64(g, s, static_cast<const double*>(positions), static_cast<double*>(node_energy), false);
+    f64_graph_energy(s, g->G, g->b.graph_off, static_cast<const double*>(node_energy), graph_energy);
+    return hip_ok(hipGetLastError());
+  }
+  if (!launchable(g)) return MACE_EUNSUPPORTED;
+  run_forward(g, s, static_cast<const float*>(positions), static_cast<float*>(node_energy), false);
   {
     mace_graph* h = g;
     PROF(KID_GRAPH_ENERGY);
-    launch_graph_energy(s, g->G, g->b.graph_off, node_energy, graph_energy);
+    launch_graph_energy(s, g->G, g->b.graph_off, static_cast<const float*>(node_energy), graph_energy);
   }
   return hip_ok(hipGetLastError());
 }
 
-mace_status mace_forces(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
-                        float* forces, void* stream) {
+mace_status mace_forces(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
+                        void* forces, void* stream) {
   if (!g || !positions || !node_energy || !graph_energy || !forces) return MACE_EINVAL;
-  if (!launchable(g)) return MACE_EUNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
-  run_forward(g, s, positions, node_energy, true);
-  run_backward(g, s, positions, forces, node_energy, graph_energy);
+  if (g->prec == MACE_FP64) {
+    if (!f64_supported(g)) return MACE_EUNSUPPORTED;
+    const double* pos = static_cast<const double*>(positions);
+    run_forward64(g, s, pos, static_cast<double*>(node_energy), true);
+    run_backward64(g, s, pos, static_cast<double*>(forces));
+    f64_graph_energy(s, g->G, g->b.graph_off, static_cast<const double*>(node_energy), graph_energy);
+    return hip_ok(hipGetLastError());
+  }
+  if (!launchable(g)) return MACE_EUNSUPPORTED;
+  const float* pos = static_cast<const float*>(positions);
+  run_forward(g, s, pos, static_cast<float*>(node_energy), true);
+  run_backward(g, s, pos, static_cast<float*>(forces), static_cast<const float*>(node_energy), graph_energy);
   return hip_ok(hipGetLastError());
 }
 
-mace_status mace_forces_stress(mace_graph* g, const float* positions, float* node_energy, double* graph_energy,
-                               float* forces, double* stress, void* stream) {
+mace_status mace_forces_stress(mace_graph* g, const void* positions, void* node_energy, double* graph_energy,
+                               void* forces, double* stress, void* stream) {
   if (!g || !positions || !node_energy || !graph_energy || !forces || !stress) return MACE_EINVAL;
   mace_status st = mace_forces(g, positions, node_energy, graph_energy, forces, stream);
   if (st != MACE_OK) return st;
   hipStream_t s = (hipStream_t)stream;
+  if (g->prec == MACE_FP64) {
+    f64_stress(s, g->G, g->b.graph_off, g->b.rcv_off, static_cast<const double*>(positions), g->b.snd, g->b.rcv,
+               g->b.shift, g->b64.g, g->b.inv_vol, stress);
+    return hip_ok(hipGetLastError());
+  }
   {
     mace_graph* h = g;
     PROF(KID_FORCES);
-    launch_stress(s, g->G, g->n_stress_chunks, g->b.stress_chunks, g->b.stress_chunk_off, positions, g->b.snd,
+    launch_stress(s, g->G, g->n_stress_chunks, g->b.stress_chunks, g->b.stress_chunk_off,
+                  static_cast<const float*>(positions), g->b.snd,
                   g->b.rcv, g->b.shift, g->b.g, g->b.inv_vol, g->b.stress_part, stress);
   }
   return hip_ok(hipGetLastError());
@@ -1207,6 +1435,11 @@ void mace_graph_destroy(mace_graph* g) {
 
 mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
   if (!g || request > MACE_L0_FACTORED) return MACE_EINVAL;
+  if (g->prec == MACE_FP64) {   // every layer in per-edge form
+    if (request == MACE_L0_FACTORED) return MACE_EUNSUPPORTED;
+    if (in_use) *in_use = MACE_L0_EDGE;
+    return MACE_OK;
+  }
   if (request == MACE_L0_FACTORED && !g->m.l0_ki) return MACE_EUNSUPPORTED;
   if (request == MACE_L0_AUTO) g->l0_fact = l0_auto(g->m, g->N, g->E);
   else if (request == MACE_L0_EDGE) g->l0_fact = false;
@@ -1218,7 +1451,7 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
 }
 
 mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use) {
-  if (!g) return MACE_EINVAL;
+  if (!g || (g->prec == MACE_FP64 && request >= 0)) return MACE_EINVAL;
   if (request >= 0) {
     if (g->prec == MACE_BF16_RADIAL || (request != MACE_PRODUCTS_FP32 && request != MACE_PRODUCTS_SPLIT_BF16))
       return MACE_EINVAL;
@@ -1230,7 +1463,7 @@ mace_status mace_fp32_products(mace_graph* g, int32_t request, int32_t* in_use) 
 
 mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, int32_t* in_use) {
   if (!g || (block != MACE_BLOCK_EDGE_PRODUCT && block != MACE_BLOCK_SYMMETRIC_CONTRACTION &&
-             block != MACE_BLOCK_RADIAL_MLP) || format > 2)
+             block != MACE_BLOCK_RADIAL_MLP) || format > 2 || (g->prec == MACE_FP64 && format > 0))
     return MACE_EINVAL;
   int& r = block == MACE_BLOCK_EDGE_PRODUCT ? g->tp_round
                                             : (block == MACE_BLOCK_SYMMETRIC_CONTRACTION ? g->sc_round : g->rad_round);

@@ -446,6 +446,52 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
                     int tp_round);   // as launch_tpr_fwd; split BF16 runs on FP32 MFMA for l_h = 2
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
+// ---- FP64 debug precision (k_fp64.hip)
+// A channel-mixing linear as blocks of components: term t maps input
+// components cx[t] .. cx[t] + nc[t] - 1 to output components cy[t] .. with
+// the K x K weights at woff[t] (row-major [in][out]; per species, K K apart,
+// when spec[t]); transpose applies W^T (the backward).
+constexpr int kMaxLin64Terms = 32;
+struct Lin64 {
+  int n_terms = 0, cin = 0, cout = 0, transpose = 0;
+  int cx[kMaxLin64Terms], cy[kMaxLin64Terms], nc[kMaxLin64Terms], spec[kMaxLin64Terms];
+  long long woff[kMaxLin64Terms];
+};
+struct SymW64 {
+  const double* w[4][4];    // [L][nu] -> [S][n_eta][K] or null
+};
+void f64_widen(hipStream_t s, size_t n, const float* src, double* dst);
+void f64_geom(hipStream_t s, int E, const double* pos, const int* snd, const int* rcv, const double4* shift,
+              double rc, int p, int nb, double* Y, double* rb, int* status);
+void f64_radial_fwd(hipStream_t s, int E, int nb, const double* rb, const double* W0, const double* W1,
+                    const double* W2, double* z1, double* z2, double* z3);
+void f64_radial_bwd(hipStream_t s, int E, int nb, const double* W0, const double* W1, const double* W2,
+                    const double* z1, const double* z2, const double* z3, const double* da3, double* de, int acc);
+bool f64_tp_fwd(hipStream_t s, int lh, int N, int K, const int* rcv_off, const int* snd, const double* z3,
+                const double* W3, const double* Y, const double* h, double inv_c, double* At);
+bool f64_tp_bwd(hipStream_t s, int lh, int E, int K, const int* snd, const int* rcv, const double* z3,
+                const double* W3, const double* Y, const double* h, const double* dAt, double inv_c, double* dY,
+                int accY, double* da3, double* Q);
+void f64_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm, const double* Q,
+                    double* out);
+void f64_linear(hipStream_t s, int N, int K, const Lin64& L, const int* species, const double* W, const double* x,
+                double* y, const double* res);
+bool f64_symcon_fwd(hipStream_t s, int lout, int N, int K, const int* species, const double* A, const SymW64& w,
+                    double* B);
+bool f64_symcon_bwd(hipStream_t s, int lout, int N, int K, const int* species, const double* A, const SymW64& w,
+                    const double* dB, double* dA);
+void f64_readout(hipStream_t s, int N, int K, const double* h, int stride, const double* w, const double* w2,
+                 int hid, double* eps, int acc, double* dh0);
+void f64_add_readout_grad(hipStream_t s, int N, int K, int stride, const double* w, double* dst);
+void f64_embed(hipStream_t s, int N, int K, const int* species, const double* W, double* h0);
+void f64_edge_vjp(hipStream_t s, int E, const double* pos, const int* snd, const int* rcv, const double4* shift,
+                  double rc, int p, int nb, const double* dY, const double* de, double4* g);
+void f64_forces(hipStream_t s, int N, const int* rcv_off, const int* snd_off, const int* snd_perm, const double4* g,
+                double* F);
+void f64_graph_energy(hipStream_t s, int G, const int* graph_off, const double* eps, double* E);
+void f64_stress(hipStream_t s, int G, const int* graph_off, const int* rcv_off, const double* pos, const int* snd,
+                const int* rcv, const double4* shift, const double4* g, const double* inv_vol, double* stress);
+
 struct SymW {
   const float* w[4][4];     // [L][nu] -> [S][n_eta][K] or null
 };

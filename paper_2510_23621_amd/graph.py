@@ -42,26 +42,31 @@ class MaceGraph:
                                          self.n_graphs, prec, self.workspace, stream)
         self.device = dev
 
+    @property
+    def dtype(self):
+        """dtype of positions, node energies and forces (FP64 in the debug precision)."""
+        return torch.float64 if self.prec == B.MACE_FP64 else torch.float32
+
     def outputs(self, forces: bool):
-        eps = torch.empty(self.n_atoms, dtype=torch.float32, device=self.device)
+        eps = torch.empty(self.n_atoms, dtype=self.dtype, device=self.device)
         E = torch.empty(self.n_graphs, dtype=torch.float64, device=self.device)
-        F = torch.empty(self.n_atoms, 3, dtype=torch.float32, device=self.device) if forces else None
+        F = torch.empty(self.n_atoms, 3, dtype=self.dtype, device=self.device) if forces else None
         return eps, E, F
 
     def energy(self, positions, stream=None):
-        pos = positions.to(device=self.device, dtype=torch.float32).contiguous()
+        pos = positions.to(device=self.device, dtype=self.dtype).contiguous()
         eps, E, _ = self.outputs(False)
         B.mace_forward_energy(self.handle, pos, eps, E, stream)
         return eps, E
 
     def energy_forces(self, positions, stream=None):
-        pos = positions.to(device=self.device, dtype=torch.float32).contiguous()
+        pos = positions.to(device=self.device, dtype=self.dtype).contiguous()
         eps, E, F = self.outputs(True)
         B.mace_forces(self.handle, pos, eps, E, F, stream)
         return eps, E, F
 
     def energy_forces_stress(self, positions, stream=None):
-        pos = positions.to(device=self.device, dtype=torch.float32).contiguous()
+        pos = positions.to(device=self.device, dtype=self.dtype).contiguous()
         eps, E, F = self.outputs(True)
         S = torch.empty(self.n_graphs, 3, 3, dtype=torch.float64, device=self.device)
         B.mace_forces_stress(self.handle, pos, eps, E, F, S, stream)

@@ -16,7 +16,8 @@ STRESS = dict(c_norm=1.0)
 STRESS_GAINS = {".radial.3": 4.0}
 
 TOL = {B.MACE_FP32: dict(energy=1e-6, forces=1e-5), B.MACE_BF16_LINEAR: dict(energy=5e-3, forces=2e-2),
-       B.MACE_FP16_LINEAR: dict(energy=5e-3, forces=2e-2), B.MACE_BF16_RADIAL: dict(energy=5e-3, forces=2e-2)}
+       B.MACE_FP16_LINEAR: dict(energy=5e-3, forces=2e-2), B.MACE_BF16_RADIAL: dict(energy=5e-3, forces=2e-2),
+       B.MACE_FP64: dict(energy=1e-10, forces=1e-10)}
 
 # Per-atom bounds, asserted beside the aggregate ones: the worst atom energy
 # relative to the mean |eps_i|, and the worst per-atom force error relative to
@@ -25,7 +26,8 @@ TOL = {B.MACE_FP32: dict(energy=1e-6, forces=1e-5), B.MACE_BF16_LINEAR: dict(ene
 # rounds (FP32 2^-24, bfloat16 2^-8) times the depth of the computation an
 # atom's energy goes through: FP32 300 u = 1.8e-5; 16-bit linears
 # (and the bfloat16 radial layer) 25 u_bf16 = 0.1.
-PER_ATOM_TOL = {B.MACE_FP32: dict(energy=2e-5, forces=2e-5),
+PER_ATOM_TOL = {B.MACE_FP64: dict(energy=1e-10, forces=1e-10),
+                B.MACE_FP32: dict(energy=2e-5, forces=2e-5),
                 B.MACE_BF16_LINEAR: dict(energy=0.1, forces=0.1),
                 B.MACE_FP16_LINEAR: dict(energy=0.1, forces=0.1),
                 B.MACE_BF16_RADIAL: dict(energy=0.1, forces=0.1)}
@@ -57,7 +59,7 @@ def run_gpu(params: dict, system, blob: np.ndarray, prec=B.MACE_FP32, forces=Tru
     for blk, fmt in (rounding or {}).items():
         B.mace_block_rounding(g.handle, blk, fmt)
     form = B.mace_layer0_form(g.handle, -1)   # the form the calls below run
-    pos = torch.from_numpy(system.positions.astype(np.float32)).cuda()
+    pos = torch.from_numpy(system.positions.astype(np.float64 if prec == B.MACE_FP64 else np.float32)).cuda()
     outs = []
     for _ in range(repeats):
         S = None
