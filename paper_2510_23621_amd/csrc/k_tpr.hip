@@ -1061,6 +1061,37 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
   }
 }
 
+// ---- W3's three bfloat16 parts for the dE/da3 product of the l_h = 2
+// backward, in the edge-lane order per channel tile: element
+// ((ks 64 + j) 4 + g) 8 + pl 4 + c of part q of channel tile ct (blocks of
+// KS 2048 elements, (ct 3 + q) blocks in) holds part q of
+// W3[j][(2 ks + pl) K + 16 ct + 4 g + c], zero for a path 2 ks + pl >= P.
+// Built once per weight set (a 16-byte run per lane and K step).
+__global__ void w3x_el_kernel(const float* __restrict__ W3, int K, int P, unsigned short* __restrict__ out) {
+  const int KS = (P + 1) / 2;
+  const size_t per_ct = (size_t)KS * 2048;
+  const size_t n = (size_t)(K / 16) * per_ct;
+  for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n; idx += (size_t)gridDim.x * blockDim.x) {
+    const int ct = (int)(idx / per_ct);
+    const int r = (int)(idx % per_ct);
+    const int ks = r / 2048, j = (r / 32) % 64, g = (r / 8) % 4, pl = (r / 4) % 2, c = r % 4;
+    const int p = 2 * ks + pl;
+    unsigned short x0 = 0, x1 = 0, x2 = 0;
+    if (p < P) split3(W3[(size_t)j * P * K + p * K + 16 * ct + 4 * g + c], x0, x1, x2);
+    const size_t base = (size_t)ct * 3 * per_ct + r;
+    out[base] = x0;
+    out[base + per_ct] = x1;
+    out[base + 2 * per_ct] = x2;
+  }
+}
+
+size_t w3x_el_elems(int K, int P) { return (size_t)(K / 16) * 3 * ((P + 1) / 2) * 2048; }
+
+void launch_w3x_el(hipStream_t s, const float* W3, int K, int P, unsigned short* out) {
+  const size_t n = (size_t)(K / 16) * ((P + 1) / 2) * 2048;
+  w3x_el_kernel<<<(unsigned)std::min<size_t>((n + 255) / 256, 2048), 256, 0, s>>>(W3, K, P, out);
+}
+
 // ---- FP32-accurate backward at l_h = 2 in the edge-lane layout.
 //
 // At P = 17 the split-BF16 parts of W3 in both layouts (209 KB) do not fit the
@@ -1086,7 +1117,7 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
 // past num_records return zero
 constexpr int kBufferRsrcWord3 = 0x00020000;
 constexpr int kRingR = 3;    // split-W3 operand triples in flight (six MFMAs each)
-constexpr int kRingD = 2;    // paths' W3 rows in flight (four float4, sixteen MFMAs each)
+constexpr int kRingD = 3;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
 constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
 
 // sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
@@ -1112,8 +1143,8 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
-    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd, unsigned short* sWf,
-    float* sGall) {
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd,
+    const unsigned short* __restrict__ w3x, unsigned short* sWf, float* sGall) {
   constexpr int LHMAX = 2;
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
@@ -1150,16 +1181,20 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     o[1] = *reinterpret_cast<const us8v*>(q + part);
     o[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
   };
-  // dE/da3 operand of step f = 4 p + jt: W3[j = 16 jt + kk][p K + 16 ct + 4 g .. +3],
-  // a buffer load with the lane's part of the offset in one register and the
-  // step's part as a scalar (flat addresses for all 68 steps, hoisted out of the
-  // edge loop, would not fit the registers); the descriptor covers W3 exactly
-  const __amdgpu_buffer_rsrc_t w3r =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(W3), (short)0, 64 * PK * 4, kBufferRsrcWord3);
-  const int wd_lane = (kk * PK + 16 * ct + 4 * g) * 4;
-  auto wd_at = [&](int f) {
-    return __builtin_bit_cast(
-        f4, __builtin_amdgcn_raw_buffer_load_b128(w3r, wd_lane, (16 * (f & 3) * PK + (f >> 2) * K) * 4, 0));
+  // dE/da3 operands, W3's parts in the edge-lane order (w3x_el_kernel), by buffer
+  // loads: the lane's part of the offset in one register, the step's (part,
+  // K step, row tile) as a scalar; the descriptor covers this channel tile
+  constexpr int KS = (P + 1) / 2;
+  constexpr int NDX = KS * 4;   // (K step, row tile) steps
+  const __amdgpu_buffer_rsrc_t w3r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<unsigned short*>(w3x) + (size_t)ct * 3 * KS * 2048, (short)0, 3 * KS * 2048 * 2, kBufferRsrcWord3);
+  const int wd_lane = ((kk * 4 + g) * 8) * 2;
+  auto wd_at = [&](int f, us8v* o) {
+    const int ks = f >> 2, jt = f & 3;
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+      o[q] = __builtin_bit_cast(us8v, __builtin_amdgcn_raw_buffer_load_b128(
+                                          w3r, wd_lane, ((q * KS + ks) * 2048 + 16 * jt * 32) * 2, 0));
   };
   for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
@@ -1316,37 +1351,46 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         if (src_map) src = src_map[src];
         el_load_a3(a, e, g, a3);
       }
-      // dE/da3 partial: d3[jt][rr] = D[j = 16 jt + 4 g + rr][edge e0 + l%16]
+      // dE/da3 partial on split-BF16 products (dR split per K step):
+      // d3[jt][rr] = D[edge e0 + 4 g + rr][j = 16 jt + kk]; in K step ks the
+      // lane's eight reduction values are (path 2 ks + pl, channel 4 g + c)
       f4 d3[4];
 #pragma unroll
       for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
       {
-        // a path's four W3 rows per step; the four accumulators interleave
-        f4 ring[kRingD][4];
+        us8v ring[kRingD][3];
 #pragma unroll
-        for (int f = 0; f < kRingD; ++f)
-#pragma unroll
-          for (int jt = 0; jt < 4; ++jt) ring[f][jt] = wd_at(4 * f + jt);
+        for (int f = 0; f < kRingD; ++f) wd_at(f, ring[f]);
+        us8v x[3];
         __builtin_amdgcn_s_setprio(1);
-        static_for<0, P>([&](auto PI) {
-          constexpr int p = decltype(PI)::value;
-          __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingD paths ahead of its use
-          f4 wv[4];
-#pragma unroll
-          for (int jt = 0; jt < 4; ++jt) wv[jt] = ring[p % kRingD][jt];
-          if constexpr (p + kRingD < P) {
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) ring[p % kRingD][jt] = wd_at(4 * (p + kRingD) + jt);
+        static_for<0, NDX>([&](auto F) {
+          constexpr int f = decltype(F)::value;
+          constexpr int ks = f >> 2, jt = f & 3;
+          __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingD steps ahead of its use
+          if constexpr (jt == 0) {
+            const f4 hi = 2 * ks + 1 < P ? r[2 * ks + 1 < P ? 2 * ks + 1 : 0] : f4{0.f, 0.f, 0.f, 0.f};
+            split3_x8(r[2 * ks], hi, x[0], x[1], x[2]);
           }
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) d3[jt] = mfma4(wv[jt][c], r[p][c], d3[jt]);
+          const us8v b0 = ring[f % kRingD][0], b1 = ring[f % kRingD][1], b2 = ring[f % kRingD][2];
+          if constexpr (f + kRingD < NDX) wd_at(f + kRingD, ring[f % kRingD]);
+          f4 acc = d3[jt];
+          acc = mfma_bf16(x[2], b0, acc);
+          acc = mfma_bf16(x[1], b1, acc);
+          acc = mfma_bf16(x[0], b2, acc);
+          acc = mfma_bf16(x[1], b0, acc);
+          acc = mfma_bf16(x[0], b1, acc);
+          d3[jt] = mfma_bf16(x[0], b0, acc);
         });
         __builtin_amdgcn_s_setprio(0);
       }
+      // rows past the receiver's last edge hold that edge's values (their A rows
+      // came from lanes working on it): stored to its row, no branch
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) *reinterpret_cast<f4*>(da3c + (size_t)ec * 64 + 16 * jt + 4 * g) = d3[jt];
+      for (int rr = 0; rr < 4; ++rr) {
+        const size_t row = (size_t)min(e0 + 4 * g + rr, e_end - 1) * 64;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) da3c[row + 16 * jt + kk] = d3[jt][rr];
+      }
     }
   }
 }
@@ -1358,7 +1402,8 @@ tpr_bwd_kernel(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
-    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd,
+    const unsigned short* __restrict__ w3x) {
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
@@ -1370,10 +1415,10 @@ tpr_bwd_kernel(
     __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
     if (rnd)
       tpr_bwd_l2_edge_lanes_body<NW, true>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                           rnd, sW, sG);
+                                           rnd, w3x, sW, sG);
     else
       tpr_bwd_l2_edge_lanes_body<NW, false>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                            0, sW, sG);
+                                            0, w3x, sW, sG);
   }
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
@@ -1402,12 +1447,12 @@ void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* 
 template <int LH, int RM>
 void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
-                    const float* dAt, float* dYp, float* Q, float* da3p, int rnd) {
+                    const float* dAt, float* dYp, float* Q, float* da3p, int rnd, const unsigned short* w3x) {
   using S = TprShape<LH, true, RM>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
   tpr_bwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
-                                                    Q, da3p, rnd);
+                                                    Q, da3p, rnd, w3x);
 }
 }  // namespace
 
@@ -1450,11 +1495,12 @@ bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
 bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
-                    int tp_round) {
+                    int tp_round, const unsigned short* w3x) {
   if (!tpr_supported(lh_max, radial_mode)) return false;
+  if (lh_max == 2 && radial_mode != 1 && (!w3x || !Q)) return false;
   if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
-  tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
+  tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round, w3x)
   switch (lh_max) {
     case 0:
       if (radial_mode == 1) MACE_TPRB(0, 1);
