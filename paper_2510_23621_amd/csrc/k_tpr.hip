@@ -1117,7 +1117,7 @@ void launch_w3x_el(hipStream_t s, const float* W3, int K, int P, unsigned short*
 // past num_records return zero
 constexpr int kBufferRsrcWord3 = 0x00020000;
 constexpr int kRingR = 3;    // split-W3 operand triples in flight (six MFMAs each)
-constexpr int kRingD = 3;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
+constexpr int kRingD = 6;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
 constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
 
 // sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
