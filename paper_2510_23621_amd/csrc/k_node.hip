@@ -35,7 +35,7 @@ __device__ __forceinline__ unsigned short lowp_bits(float x) {
   else return fp16_bits(x);
 }
 
-constexpr int kLinCt = 2;        // column tiles per block (measured: 2 < 4 < 1 < 8 in time per step)
+constexpr int kLinCt = 4;        // column tiles per block (measured at 1,536 and 36,864 atoms: 4 beats 2, most in the 16-bit modes)
 constexpr int kLinSmallGrid = 512;   // blocks below which a square linear takes one column tile per block
 
 // LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
