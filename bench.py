@@ -43,7 +43,7 @@ KERNEL_SOURCES = {"edge_prologue_kernel": "k_radial.hip", "radial_bwd_kernel": "
 EDGE_PRODUCT = ("tpr_fwd_kernel", "tpr_bwd_kernel")
 METRIC = "atoms/s and edges/s for MACE energy+forces (FP32, BF16-linear); % roofline"
 PREC_NAMES = {"fp32": "MACE_FP32", "bf16": "MACE_BF16_LINEAR", "fp16": "MACE_FP16_LINEAR",
-              "bf16radial": "MACE_BF16_RADIAL"}
+              "bf16radial": "MACE_BF16_RADIAL", "fp64": "MACE_FP64"}
 
 
 def source_hash(kname):
@@ -171,7 +171,7 @@ class Arm:
         self.g = MaceGraph(desc, blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
                            sh if periodic else None, sysm.cells if periodic else None,
                            sysm.graph_of_atom.astype(np.int32) if sysm.n_graphs > 1 else None, sysm.n_graphs, prec)
-        self.pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
+        self.pos = torch.from_numpy(sysm.positions).to(self.g.dtype).cuda()
         self.out = self.g.outputs(True)
         self.stream = torch.cuda.current_stream()
 
@@ -259,8 +259,10 @@ class Arm:
                     "work": "per edge 2*64*P*K (radial layer, MFMA) + 2K(nnz+mid) (CG, VALU), x2 backward",
                     "mfma_flops_per_launch": int(mf), "valu_flops_per_launch": int(vf),
                     # MFMA and VALU issue do not overlap on a gfx950 SIMD: the
-                    # ideal time is the sum of the two pipes' times at peak
-                    "pipe_time_frac": round((mf / (FP32_MFMA_PEAK_TFLOPS * 1e12)
+                    # ideal time is the sum of the two pipes' times at peak, the
+                    # FP32-accurate radial products running as six BF16 MFMA
+                    # products each (split operands) and the CG on FP32 VALU
+                    "pipe_time_frac": round((6 * mf / (BF16_MFMA_PEAK_TFLOPS * 1e12)
                                              + vf / (FP32_VALU_PEAK_TFLOPS * 1e12)) / (avg_ms * 1e-3), 4),
                     "compulsory_bytes_per_launch": int(cb)}
         else:
@@ -370,15 +372,20 @@ def main():
     secondary = None
     if args.secondary_config >= 0 and args.secondary_config != args.config:
         secondary = {}
-        for pname in ("fp32", "bf16"):
+        for pname in ("fp32", "bf16", "fp64"):
             s = Arm(B, args.secondary_config, getattr(B, PREC_NAMES[pname]))
-            sk = s.dominant_kernel()
-            sms, (sk_ms, sk_n) = s.timed(100, 100, B.kernel_ids()[sk])
-            sroof, _ = s.roofline(sk, sk_ms, sk_n, 100, sms, f"{s.name}_{pname}")
-            secondary[pname] = {"workload": s.name, "n_atoms": s.N, "n_edges": s.E,
-                                "atoms_per_s": round(s.N / (sms * 1e-3), 1),
-                                "edges_per_s": round(s.E / (sms * 1e-3), 1), "ms_per_step": round(sms, 4),
-                                "roofline": sroof}
+            if pname == "fp64":   # the debug precision: plain FP64 kernels, a few steps
+                sms, _ = s.timed(1, 3)
+                secondary[pname] = {"workload": s.name, "atoms_per_s": round(s.N / (sms * 1e-3), 1),
+                                    "ms_per_step": round(sms, 3)}
+            else:
+                sk = s.dominant_kernel()
+                sms, (sk_ms, sk_n) = s.timed(100, 100, B.kernel_ids()[sk])
+                sroof, _ = s.roofline(sk, sk_ms, sk_n, 100, sms, f"{s.name}_{pname}")
+                secondary[pname] = {"workload": s.name, "n_atoms": s.N, "n_edges": s.E,
+                                    "atoms_per_s": round(s.N / (sms * 1e-3), 1),
+                                    "edges_per_s": round(s.E / (sms * 1e-3), 1), "ms_per_step": round(sms, 4),
+                                    "roofline": sroof}
             s.close()
             del s
             torch.cuda.empty_cache()
