@@ -1407,7 +1407,7 @@ tpr_bwd_kernel(
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
-  else if constexpr (LHMAX == 2 && RM == 0) {
+  else if constexpr (LHMAX == 2 && RM == 2) {
     // W3's slice (one layout for both products) and a G table per wave; the
     // precision study's operand rounding runs as its own instance (a uniform
     // branch, taken once)
@@ -1457,8 +1457,9 @@ void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, cons
 }  // namespace
 
 // Instances built: every l_h <= 2 with radial mode 0 (FP32), 1 (BF16) or 2
-// (split BF16; the l_h = 2 backward runs it on FP32 MFMA), and mode 3 (split
-// BF16 with pre-split a3) at l_h = 1.
+// (split BF16), and mode 3 (split BF16 with pre-split a3) at l_h = 1. The
+// l_h = 2 backward in mode 2 reads W3's parts in edge-lane order (w3x) and
+// needs Q.
 bool tpr_supported(int lh_max, int radial_mode) {
   if (lh_max < 0 || lh_max > 2 || radial_mode < 0 || radial_mode > 3) return false;
   return radial_mode != 3 || lh_max == 1;
@@ -1497,7 +1498,7 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
                     int tp_round, const unsigned short* w3x) {
   if (!tpr_supported(lh_max, radial_mode)) return false;
-  if (lh_max == 2 && radial_mode != 1 && (!w3x || !Q)) return false;
+  if (lh_max == 2 && radial_mode == 2 && (!w3x || !Q)) return false;
   if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
   tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round, w3x)
@@ -1513,8 +1514,9 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
       else if (radial_mode == 3) MACE_TPRB(1, 3);
       else MACE_TPRB(1, 0);
       break;
-    default:   // split BF16 (mode 2) runs on FP32 MFMA here
+    default:
       if (radial_mode == 1) MACE_TPRB(2, 1);
+      else if (radial_mode == 2) MACE_TPRB(2, 2);
       else MACE_TPRB(2, 0);
       break;
   }
