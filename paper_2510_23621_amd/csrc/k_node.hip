@@ -35,7 +35,14 @@ __device__ __forceinline__ unsigned short lowp_bits(float x) {
   else return fp16_bits(x);
 }
 
-constexpr int kLinCt = 4;        // column tiles per block (measured at 1,536 and 36,864 atoms: 4 beats 2, most in the 16-bit modes)
+// Column tiles of 16 per block. Four by default (measured at 1,536 and 36,864
+// atoms: 4 beats 2, most in the 16-bit modes); at K = 128 all eight when the
+// launch still has kLinWideGrid blocks, so that each input row is read by one
+// block only (36,864 atoms: FP32 linears 4.24 -> 3.64 ms per step; at 1,536
+// atoms, 384 blocks, eight was slower).
+constexpr int kLinCt = 4;
+constexpr int kLinCtWide = 8;
+constexpr int kLinWideGrid = 2048;
 constexpr int kLinSmallGrid = 512;   // blocks below which a square linear takes one column tile per block
 
 // LP: 0 FP32, 1 BF16, 2 FP16 (the 16-bit paths share everything but the
@@ -236,6 +243,23 @@ void launch_linear(hipStream_t s, const LinPlanRef& P, const LinArgs& a) {
   const int halves = (a.K / 16 + kLinCt - 1) / kLinCt;
   dim3 grid(a.n_quads, P.host.n_gc, halves), block(64 * kLinQuad);
   const int KI0 = a.KI > 0 ? a.KI : a.K;
+  if (a.K == 128 && KI0 <= 128 && (int64_t)a.n_quads * P.host.n_gc >= kLinWideGrid) {
+    // wide blocks: all 128 output columns, each input row read once
+    dim3 gw(a.n_quads, P.host.n_gc, 1);
+    if (KI0 != a.K) {
+      if (a.lowp) return;
+      switch (KI0) {
+        case 32: linear_kernel<128, 32, 0, kLinCtWide><<<gw, block, 0, s>>>(L, a); break;
+        case 64: linear_kernel<128, 64, 0, kLinCtWide><<<gw, block, 0, s>>>(L, a); break;
+        case 96: linear_kernel<128, 96, 0, kLinCtWide><<<gw, block, 0, s>>>(L, a); break;
+      }
+      return;
+    }
+    if (a.lowp == 1) linear_kernel<128, 128, 1, kLinCtWide><<<gw, block, 0, s>>>(L, a);
+    else if (a.lowp == 2) linear_kernel<128, 128, 2, kLinCtWide><<<gw, block, 0, s>>>(L, a);
+    else linear_kernel<128, 128, 0, kLinCtWide><<<gw, block, 0, s>>>(L, a);
+    return;
+  }
   if (KI0 == a.K && (int64_t)a.n_quads * P.host.n_gc * halves < kLinSmallGrid) {
     // small launch: one column tile per block, kLinCt times the blocks
     dim3 g1(a.n_quads, P.host.n_gc, a.K / 16);
