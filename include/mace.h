@@ -296,6 +296,16 @@ const char* mace_kernel_name(int32_t kernel);
  * residual is added; 16-bit weights count 2 bytes). */
 mace_status mace_profile_work(mace_graph* g, double* flops, double* bytes);
 
+/* Test switch (host) for callers that check the fused first-layer linears:
+ * in the 16-bit modes, with K = 128 and a 128-wide factorised contraction,
+ * the first layer's contraction, path-merging and species linears (and their
+ * transposes) run as one launch each way, bit for bit equal to three
+ * separate launches. request 1 fuses them (the default), 0 runs them
+ * separately, < 0 only queries; *in_use (host, may be NULL) = 1 when the fused
+ * launches will run for this handle's mode, shapes and first-layer form.
+ * MACE_EINVAL for a NULL handle or another request value. */
+mace_status mace_debug_fused_linears(mace_graph* g, int32_t request, int32_t* in_use);
+
 /* Table export for checking the library's couplings (host). */
 /* real CG C^{l3}_{l1 l2}[m1][m2][m3] into out (host) [(2l1+1)(2l2+1)(2l3+1)] */
 mace_status mace_debug_real_cg(int32_t l1, int32_t l2, int32_t l3, double* out);

@@ -37,7 +37,8 @@ EXPORTED = ["mace_weight_layout", "mace_workspace_bytes", "mace_neighbor_list", 
             "mace_debug_real_cg", "mace_debug_trees", "mace_debug_edge_features", "mace_profile_select",
             "mace_profile_read", "mace_kernel_name", "mace_graph_check", "mace_profile_work",
             "mace_neighbor_workspace_bytes", "mace_neighbor_list_device", "mace_layer0_form",
-            "mace_fp32_products", "mace_block_rounding", "mace_neighbor_list_device_noalloc"]
+            "mace_fp32_products", "mace_block_rounding", "mace_neighbor_list_device_noalloc",
+            "mace_debug_fused_linears"]
 
 
 class MaceError(RuntimeError):
@@ -93,6 +94,7 @@ def lib() -> ctypes.CDLL:
         L.mace_profile_work.argtypes = [P, P, P]
         L.mace_layer0_form.argtypes = [P, I32, P]
         L.mace_fp32_products.argtypes = [P, I32, P]
+        L.mace_debug_fused_linears.argtypes = [P, I32, P]
         L.mace_block_rounding.argtypes = [P, I32, I32, P]
         L.mace_graph_destroy.restype = None
         L.mace_status_string.argtypes = [I32]
@@ -324,6 +326,15 @@ def mace_layer0_form(handle, request: int = -1) -> int:
     query the form of the first layer's message; returns the form in use."""
     used = ctypes.c_int32(0)
     _check(lib().mace_layer0_form(handle, request, ctypes.byref(used)), "mace_layer0_form")
+    return used.value
+
+
+def mace_debug_fused_linears(handle, request: int = -1) -> int:
+    """Fuse (1, the default) or separate (0) the 16-bit modes' first-layer
+    linears, or with request < 0 only query; returns 1 when the fused launches
+    will run for this handle."""
+    used = ctypes.c_int32(0)
+    _check(lib().mace_debug_fused_linears(handle, request, ctypes.byref(used)), "mace_debug_fused_linears")
     return used.value
 
 

@@ -352,6 +352,7 @@ struct mace_graph {
   // precision study: operand rounding of the edge product / contraction / radial MLP
   int tp_round = 0, sc_round = 0, rad_round = 0;
   bool w3x_valid = false;   // W3's parts for the l_h = 2 backward match the W3 in effect
+  bool l0_chain = true;     // 16-bit modes: the first layer's linears fused (mace_debug_fused_linears)
 };
 
 namespace {
@@ -424,6 +425,74 @@ mace_status hip_ok(hipError_t e) { return e == hipSuccess ? MACE_OK : MACE_EHIP;
 // rounding mode of the channel-mixing linears: 0 FP32, 1 bfloat16, 2 binary16
 int lowp_mode(mace_precision p) {
   return (p == MACE_BF16_LINEAR || p == MACE_BF16_RADIAL) ? 1 : (p == MACE_FP16_LINEAR ? 2 : 0);
+}
+
+// The 16-bit modes' factorised first layer runs its three linears (the FP32
+// contraction, then the 16-bit path-merging and species linears; backward,
+// their transposes) as one launch each way where the shapes allow it:
+// K = 128, a 128-wide contraction (two species) and plans of one term per l
+// whose input component is the output component.
+bool chain_stage_of(const LinPlanRef& P, int lowp, ChainStage* cs) {
+  const LinPlan& p = P.host.plan;
+  if (p.n_groups != 4 || p.cin != 16 || p.cout != 16) return false;
+  int species = -1;
+  for (int gi = 0; gi < 4; ++gi) {
+    const LinGroup& G = p.g[gi];
+    if (G.out_c0 != gi * gi || G.ncomp != 2 * gi + 1 || G.t1 - G.t0 != 1 || G.dst) return false;
+    const LinTerm& t = p.t[G.t0];
+    if (t.in_c0 != G.out_c0 || t.src) return false;
+    if (species >= 0 && species != t.species) return false;
+    species = t.species;
+    cs->w_off[gi] = t.w_off;
+  }
+  cs->w_sstride = species ? p.w_sstride : 0;
+  cs->lowp = lowp;
+  return true;
+}
+
+bool run_l0_chain(mace_graph* h, hipStream_t s, bool backward) {
+  const Model& m = h->m;
+  const int lowp = lowp_mode(h->prec);
+  if (!h->l0_chain || !lowp || m.d.K != 128 || m.l0_ki != 128 || m.layers[0].mid != 16) return false;
+  Buffers& b = h->b;
+  ChainArgs a;
+  const LinPlanRef* P[3];
+  if (!backward) {
+    a.x = b.U0;
+    a.y = b.A[0];
+    a.wt = b.wT;
+    a.wbf = b.wbf;
+    P[0] = &h->l0f;
+    P[1] = &h->lin[0];
+    P[2] = &h->skip0;
+  } else {
+    a.x = b.dA;
+    a.y = b.gU0;
+    a.wt = b.w;
+    a.wbf = b.wbfT;
+    P[0] = &h->skip0T;
+    P[1] = &h->linT[0];
+    P[2] = &h->l0fT;
+  }
+  const int fp32_stage = backward ? 2 : 0;
+  for (int q = 0; q < 3; ++q)
+    if (!chain_stage_of(*P[q], q == fp32_stage ? 0 : lowp, &a.st[q])) return false;
+  a.quad_node = b.quad_node;
+  a.quad_species = b.quad_species;
+  a.n_quads = h->n_quads;
+  a.lowp = lowp;
+  ProfScope ps(h, KID_LINEAR, s);
+  if (ps.on && a.n_quads > 0) {
+    // algorithmic work: three K x K products per node and component; the
+    // input and output rows once, and each stage's weight blocks
+    const double K = m.d.K, N = (double)h->N, S = m.d.n_species;
+    h->prof_flops += 3.0 * 2.0 * K * K * N * 16.0;
+    double wb = 0.0;
+    for (int q = 0; q < 3; ++q) wb += 4.0 * K * K * (a.st[q].lowp ? 2.0 : 4.0) * (a.st[q].w_sstride ? S : 1.0);
+    h->prof_bytes += 2.0 * N * 16.0 * K * 4.0 + wb;
+  }
+  launch_linear_chain3(s, a);
+  return true;
 }
 
 LinPlan plan_single_per_l(const std::vector<int>& ls, const std::string& pre, const Model& m, int cin, int cout,
@@ -663,7 +732,7 @@ void run_forward(mace_graph* h, hipStream_t s, const float* pos, float* eps, boo
       }
       if (!lowp) {
         run_linear(h, s, h->l0f, largs_l0(h, b.U0, b.A[0], false));
-      } else {
+      } else if (!run_l0_chain(h, s, false)) {
         run_linear(h, s, h->l0f, largs_l0(h, b.U0, b.At, false));
         run_linear(h, s, h->lin[0], largs(h, b.At, b.Apre, nullptr, false, 0));
         run_linear(h, s, h->skip0, largs(h, b.Apre, b.A[0], nullptr, false, 0));
@@ -752,17 +821,20 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F, cons
     // dE/dAt (the transposes of the linears after the edge product); the
     // factorised first layer ends in dE/dU instead
     const float* dApre = b.dA;
-    if (t == 0 && lowp) {   // 16-bit modes: each linear's own transpose
+    const bool chained = fact && lowp && run_l0_chain(h, s, true);   // dE/dA -> dE/dU in one launch
+    if (t == 0 && lowp && !chained) {   // 16-bit modes: each linear's own transpose
       run_linear(h, s, h->skip0T, largs(h, b.dA, b.dApre, nullptr, true, 0));
       dApre = b.dApre;
     }
-    if (fact && !lowp) {
-      run_linear(h, s, h->l0fT, largs_l0(h, b.dA, b.gU0, true));
-    } else if (t == 0 && !lowp) {
-      run_linear(h, s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
-    } else {
-      run_linear(h, s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
-      if (fact) run_linear(h, s, h->l0fT, largs_l0(h, b.dAt, b.gU0, true));
+    if (!chained) {
+      if (fact && !lowp) {
+        run_linear(h, s, h->l0fT, largs_l0(h, b.dA, b.gU0, true));
+      } else if (t == 0 && !lowp) {
+        run_linear(h, s, h->comb0T, largs(h, b.dA, b.dAt, nullptr, true, 0));
+      } else {
+        run_linear(h, s, h->linT[t], largs(h, dApre, b.dAt, nullptr, true, 0));
+        if (fact) run_linear(h, s, h->l0fT, largs_l0(h, b.dAt, b.gU0, true));
+      }
     }
     int n_part = K / 16;
     if (fact) {
@@ -1458,6 +1530,19 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
   // the form the next calls will run: the precision study's edge-product and
   // radial-MLP rounding force the per-edge form whatever was requested
   if (in_use) *in_use = layer_factorised(g, 0) ? MACE_L0_FACTORED : MACE_L0_EDGE;
+  return MACE_OK;
+}
+
+mace_status mace_debug_fused_linears(mace_graph* g, int32_t request, int32_t* in_use) {
+  if (!g || request > 1) return MACE_EINVAL;
+  if (request >= 0) g->l0_chain = request == 1;
+  if (in_use) {
+    const Model& m = g->m;
+    ChainStage cs;
+    *in_use = g->l0_chain && lowp_mode(g->prec) && m.d.K == 128 && m.l0_ki == 128 && m.layers[0].mid == 16 &&
+              layer_factorised(g, 0) && chain_stage_of(g->l0f, 0, &cs) && chain_stage_of(g->lin[0], 1, &cs) &&
+              chain_stage_of(g->skip0, 1, &cs);
+  }
   return MACE_OK;
 }
 

@@ -5,6 +5,7 @@
 #include <utility>
 
 #include "mace_internal.h"
+#include "static_loops.h"
 
 namespace mace {
 
@@ -197,6 +198,125 @@ __global__ void __launch_bounds__(64 * kLinQuad) linear_kernel(const LinLaunch* 
       y[o] = v;
     }
   }
+}
+
+// Three linears in a row on one component, in one launch (the 16-bit modes'
+// first layer: the FP32 contraction U -> At, then the 16-bit path-merging and
+// species linears; backward, their transposes in reverse order). A block owns
+// up to four 16-node tiles of one species, one of the 16 components and all
+// 128 output columns. Each stage multiplies exactly as linear_kernel does
+// (same operand layouts, the same k order, inputs of a 16-bit stage rounded
+// from their FP32 values) and leaves its FP32 result in the wave's LDS rows,
+// which the next stage reads as linear_kernel reads its input rows: the
+// output equals that of three linear_kernel launches bit for bit, without the
+// two intermediate arrays going through HBM.
+template <int LP>
+__global__ void __launch_bounds__(64 * kLinQuad) linear_chain3_kernel(ChainArgs a) {
+  constexpr int K = 128, CT = 8;
+  constexpr int PF = 64 + 4;    // FP32 panel pitch: a 64-wide half of the k range (4 mod 32)
+  constexpr int PB = K + 8;     // 16-bit panel pitch (elements)
+  constexpr int PT = K + 4;     // stage output row pitch (floats)
+  constexpr int kPanelF = 16 * CT * PF;
+  constexpr int kPanelB = (16 * CT * PB + 1) / 2;
+  constexpr int kPanel = kPanelF > kPanelB ? kPanelF : kPanelB;
+  __shared__ __align__(16) float sB[kPanel];
+  __shared__ __align__(16) float sT[kLinQuad * 16 * PT];
+  unsigned short* sBb = reinterpret_cast<unsigned short*>(sB);
+  const int c = blockIdx.y;                        // component l^2 + m
+  const int lc = (c >= 1) + (c >= 4) + (c >= 9);   // its l
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int quad = blockIdx.x;
+  const int z = a.quad_species[quad];
+  const int row_node = a.quad_node[((size_t)quad * kLinQuad + w) * kLinTileNodes + (l & 15)];
+  const int node = max(row_node, 0);
+  const float keep = row_node >= 0 ? 1.f : 0.f;
+  float* T = sT + w * 16 * PT;
+  f4 acc[CT];
+  static_for<0, 3>([&](auto S) {
+    constexpr int st = decltype(S)::value;
+    const ChainStage& cs = a.st[st];
+    const int64_t woff = cs.w_off[lc] + (int64_t)z * cs.w_sstride;
+    // input row of MFMA row l%16: the launch input for the first stage, the
+    // previous stage's result (this wave's LDS rows) after it
+    const float* xrow = st == 0 ? a.x + ((size_t)node * 16 + c) * K : T + (l & 15) * PT;
+    const float xk = st == 0 ? keep : 1.f;
+#pragma unroll
+    for (int j = 0; j < CT; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+    if (cs.lowp == 0) {
+      // FP32: k = 16 q + 4 s + cc as in linear_kernel, the panel in two halves of k
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh) {
+        __syncthreads();   // every wave is done with the previous panel
+        for (int idx = tid; idx < 16 * CT * 16; idx += 64 * kLinQuad) {
+          const int col = idx >> 4, k4 = idx & 15;
+          *reinterpret_cast<f4*>(sB + col * PF + 4 * k4) =
+              *reinterpret_cast<const f4*>(a.wt + woff + (size_t)col * K + 64 * kh + 4 * k4);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f4 av = *reinterpret_cast<const f4*>(xrow + 64 * kh + 16 * q + 4 * (l >> 4)) * xk;
+#pragma unroll
+          for (int j = 0; j < CT; ++j) {
+            const f4 b = *reinterpret_cast<const f4*>(sB + (16 * j + (l & 15)) * PF + 16 * q + 4 * (l >> 4));
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[cc], b[cc], acc[j], 0, 0, 0);
+          }
+        }
+      }
+    } else {
+      __syncthreads();
+      for (int idx = tid; idx < 16 * CT * (K / 8); idx += 64 * kLinQuad) {
+        const int col = idx / (K / 8), kc = idx % (K / 8);
+        *reinterpret_cast<us8*>(sBb + col * PB + 8 * kc) = *reinterpret_cast<const us8*>(a.wbf + woff + ((size_t)kc * K + col) * 8);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < K / 32; ++ks) {
+        const f4 lo = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4)) * xk;
+        const f4 hi = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4) + 4) * xk;
+        us8 v;
+        v[0] = lowp_bits<LP>(lo[0]); v[1] = lowp_bits<LP>(lo[1]); v[2] = lowp_bits<LP>(lo[2]); v[3] = lowp_bits<LP>(lo[3]);
+        v[4] = lowp_bits<LP>(hi[0]); v[5] = lowp_bits<LP>(hi[1]); v[6] = lowp_bits<LP>(hi[2]); v[7] = lowp_bits<LP>(hi[3]);
+#pragma unroll
+        for (int j = 0; j < CT; ++j) {
+          const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));
+          if constexpr (LP == 1)
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, v), __builtin_bit_cast(bf8, b), acc[j], 0, 0, 0);
+          else
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, v), __builtin_bit_cast(h8, b), acc[j], 0, 0, 0);
+        }
+      }
+    }
+    if constexpr (st < 2) {
+      // the result into this wave's rows (its input reads are done: the
+      // products that used them come first); LDS operations of a wave
+      // complete in order, and the barriers keep the compiler's order
+      __asm__ volatile("" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int j = 0; j < CT; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) T[(4 * (l >> 4) + r) * PT + 16 * j + (l & 15)] = acc[j][r];
+      __asm__ volatile("" ::: "memory");
+      __builtin_amdgcn_wave_barrier();
+    }
+  });
+  int out_node[4];   // node of result row 4 (l / 16) + r, -1 for none
+#pragma unroll
+  for (int r = 0; r < 4; ++r) out_node[r] = __shfl(row_node, 4 * (l >> 4) + r);
+#pragma unroll
+  for (int j = 0; j < CT; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (out_node[r] >= 0) a.y[((size_t)out_node[r] * 16 + c) * K + 16 * j + (l & 15)] = acc[j][r];
+}
+
+void launch_linear_chain3(hipStream_t s, const ChainArgs& a) {
+  if (a.n_quads <= 0) return;
+  dim3 grid(a.n_quads, 16), block(64 * kLinQuad);
+  if (a.lowp == 2) linear_chain3_kernel<2><<<grid, block, 0, s>>>(a);
+  else linear_chain3_kernel<1><<<grid, block, 0, s>>>(a);
 }
 
 LinLaunch make_lin_launch(const LinPlan& plan) {

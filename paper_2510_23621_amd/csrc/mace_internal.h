@@ -395,6 +395,29 @@ struct LinArgs {
   const float* bias0;       // [K] or null: rounded like the weights and added last to component 0 of y
 };
 
+// Three channel-mixing linears in a row on the 16 components of the first
+// layer (the 16-bit modes at K = 128 with a 128-wide factorised contraction):
+// stage s multiplies by the weight block of the output's l at st[s].w_off[l]
+// (+ species * w_sstride), FP32 (panel from wt, stored [out][in]) or 16-bit
+// (panel from wbf, packed [K/8][K][8]).
+struct ChainStage {
+  int64_t w_off[4];
+  int64_t w_sstride;   // 0: the same weights for every species
+  int lowp;            // 0: FP32 operands; 1, 2: bfloat16, binary16 (inputs rounded)
+};
+struct ChainArgs {
+  const float* x;              // [N][16][128]
+  float* y;                    // [N][16][128]
+  const float* wt;
+  const unsigned short* wbf;
+  const int* quad_node;        // as LinArgs
+  const int* quad_species;
+  int n_quads;
+  int lowp;                    // the 16-bit format of the 16-bit stages
+  ChainStage st[3];
+};
+void launch_linear_chain3(hipStream_t s, const ChainArgs& a);
+
 constexpr int kMaxRadialLayers = 4;
 // hidden-layer weights (W0 of the layer, W1 and W2 follow it) and a3 outputs
 // of up to kMaxRadialLayers interaction layers

@@ -124,3 +124,50 @@ def test_factorised_form_deterministic():
     outs = run_gpu(params, sysm, bl, B.MACE_FP32, repeats=3, l0_form=B.MACE_L0_FACTORED)
     for o in outs[1:]:
         assert np.array_equal(o["eps"], outs[0]["eps"]) and np.array_equal(o["forces"], outs[0]["forces"])
+
+
+@pytest.mark.parametrize("prec", [B.MACE_BF16_LINEAR, B.MACE_FP16_LINEAR, B.MACE_BF16_RADIAL])
+def test_fused_first_layer_linears_bitwise(prec):
+    """In the 16-bit modes at K = 128 with two species the factorised first
+    layer's three linears (and their transposes) run as one launch each way;
+    energies, forces and stress equal those of the separate launches bit for
+    bit, on a 1,536-atom box (24 node quads of mixed species) and on a
+    96-atom one."""
+    for cfg, seed in ((1, 0), (0, 3)):
+        params = model_params(cfg, K=128, hidden_lmax=1, **STRESS)
+        sysm = make_system(cfg, seed=seed)
+        bl = lib_blob(params, seed, STRESS_GAINS)
+        snd, rcv, sh = B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells)
+        g = MaceGraph(B.make_desc(**params), bl, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                      sh, sysm.cells, None, 1, prec)
+        assert B.mace_layer0_form(g.handle, -1) == B.MACE_L0_FACTORED
+        pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
+        outs = []
+        for fuse in (1, 0, 1):
+            assert B.mace_debug_fused_linears(g.handle, fuse) == fuse
+            eps, E, F, S = g.energy_forces_stress(pos)
+            torch.cuda.synchronize()
+            outs.append([t.cpu().numpy() for t in (eps, E, F, S)])
+        for a, b in zip(outs[0], outs[1]):
+            assert np.array_equal(a, b), f"cfg {cfg}: fused and separate first-layer linears differ"
+        for a, b in zip(outs[0], outs[2]):
+            assert np.array_equal(a, b)
+        g.close()
+
+
+def test_fused_first_layer_linears_only_where_shapes_allow():
+    """FP32 composes the first layer's linears on the host (nothing to fuse);
+    K = 64 and the per-edge first layer keep separate launches."""
+    sysm = make_system(0, seed=0)
+    snd, rcv, sh = B.mace_neighbor_list(sysm.positions, 5.0, sysm.cells)
+    for K, prec, form, want in ((128, B.MACE_FP32, None, 0), (64, B.MACE_BF16_LINEAR, None, 0),
+                                (128, B.MACE_BF16_LINEAR, B.MACE_L0_EDGE, 0), (128, B.MACE_FP16_LINEAR, None, 1)):
+        params = model_params(0, K=K, hidden_lmax=1)
+        g = MaceGraph(B.make_desc(**params), lib_blob(params, 0), sysm.species.astype(np.int32),
+                      np.stack([snd, rcv]).astype(np.int32), sh, sysm.cells, None, 1, prec)
+        if form is not None:
+            B.mace_layer0_form(g.handle, form)
+        assert B.mace_debug_fused_linears(g.handle) == want, (K, prec, form)
+        g.close()
+    with pytest.raises(B.MaceError):
+        B.mace_debug_fused_linears(None, 0)
