@@ -1,6 +1,7 @@
 // Node-level kernels: the channel-mixing linears (linear_up, path-merging
 // linear, species-dependent linears, product-basis linear and their
 // transposes), readouts, per-graph energy sums, the layer-0 species table.
+#include <algorithm>
 #include <set>
 #include <utility>
 
@@ -330,6 +331,20 @@ LinLaunch make_lin_launch(const LinPlan& plan) {
       ++n;
     }
   L.n_gc = n;
+  // Blocks run in blockIdx.y-major order. Where every group has one term
+  // (a transposed path-merging linear: several outputs read each input
+  // component), order the (group, component) units by the input component
+  // they read, so that the blocks reading one input row run one after
+  // another and find it in L2 instead of HBM.
+  bool single = plan.n_groups > 0;
+  for (int g = 0; g < plan.n_groups; ++g) single = single && plan.g[g].t1 - plan.g[g].t0 == 1;
+  if (single) {
+    auto key = [&](const LinGC& u) {
+      const LinTerm& t = plan.t[plan.g[u.g].t0];
+      return t.src * 4096 + t.in_c0 + u.c;
+    };
+    std::stable_sort(L.gc, L.gc + n, [&](const LinGC& a, const LinGC& b) { return key(a) < key(b); });
+  }
   return L;
 }
 
