@@ -296,14 +296,16 @@ const char* mace_kernel_name(int32_t kernel);
  * residual is added; 16-bit weights count 2 bytes). */
 mace_status mace_profile_work(mace_graph* g, double* flops, double* bytes);
 
-/* Test switch (host) for callers that check the fused first-layer linears:
- * in the 16-bit modes, with K = 128 and a 128-wide factorised contraction,
- * the first layer's contraction, path-merging and species linears (and their
- * transposes) run as one launch each way, bit for bit equal to three
- * separate launches. request 1 fuses them (the default), 0 runs them
- * separately, < 0 only queries; *in_use (host, may be NULL) = 1 when the fused
- * launches will run for this handle's mode, shapes and first-layer form.
- * MACE_EINVAL for a NULL handle or another request value. */
+/* Test switch (host) for callers that check the 16-bit modes' linear
+ * layouts against the plain ones, which they equal bit for bit. Bit 0: with
+ * K = 128 and a 128-wide factorised contraction, the first layer's
+ * contraction, path-merging and species linears (and their transposes) run
+ * as one launch each way instead of three. Bit 1: on graphs of at least 256
+ * blocks of four 16-node tiles, the wide 16-bit linears take eight tiles per
+ * block. request 3 (both, the default) to 0 (neither) sets them, < 0 only
+ * queries; *in_use (host, may be NULL) = the bits in effect for this
+ * handle's mode, shapes and first-layer form. MACE_EINVAL for a NULL handle
+ * or a request above 3. */
 mace_status mace_debug_fused_linears(mace_graph* g, int32_t request, int32_t* in_use);
 
 /* Table export for checking the library's couplings (host). */

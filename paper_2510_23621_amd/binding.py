@@ -330,9 +330,10 @@ def mace_layer0_form(handle, request: int = -1) -> int:
 
 
 def mace_debug_fused_linears(handle, request: int = -1) -> int:
-    """Fuse (1, the default) or separate (0) the 16-bit modes' first-layer
-    linears, or with request < 0 only query; returns 1 when the fused launches
-    will run for this handle."""
+    """Test switch of the 16-bit modes' linear layouts: bit 0 fuses the
+    first-layer linears, bit 1 takes eight node tiles per wide block on large
+    graphs (3, the default: both; 0: neither); request < 0 only queries.
+    Returns the bits in effect for this handle."""
     used = ctypes.c_int32(0)
     _check(lib().mace_debug_fused_linears(handle, request, ctypes.byref(used)), "mace_debug_fused_linears")
     return used.value

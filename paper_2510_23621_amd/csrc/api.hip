@@ -164,7 +164,8 @@ struct Buffers {
   float* w_round = nullptr;   // precision study: rounded copies of the last radial layers' weights
   unsigned short *wbf = nullptr, *wbfT = nullptr;   // 16-bit K-packed copies (BF16- / FP16-linear modes)
   int *species = nullptr, *snd = nullptr, *rcv = nullptr, *rcv_off = nullptr, *snd_off = nullptr,
-      *snd_perm = nullptr, *graph_off = nullptr, *quad_node = nullptr, *quad_species = nullptr;
+      *snd_perm = nullptr, *graph_off = nullptr, *quad_node = nullptr, *quad_species = nullptr,
+      *quad_node8 = nullptr, *quad_species8 = nullptr;
   double4* shift = nullptr;
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
@@ -211,6 +212,8 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   const int64_t nt = n_tiles_bound(N, (int)S);   // also bounds the number of quads
   b.quad_node = c.take<int>(nt * kLinQuad * kLinTileNodes);
   b.quad_species = c.take<int>(nt);
+  b.quad_node8 = c.take<int>(nt * kLinQuadWide * kLinTileNodes);
+  b.quad_species8 = c.take<int>(nt);
   b.shift = c.take<double4>(std::max<int64_t>(E, 1));
   b.Y = c.take<float>(std::max<int64_t>(E, 1) * 16);
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
@@ -339,6 +342,7 @@ struct mace_graph {
   int64_t N = 0, E = 0;
   int G = 1;
   int n_tiles = 0, n_quads = 0;
+  int n_quads8 = 0;   // blocks of the kLinQuadWide grouping (16-bit modes, large graphs), 0: not used
   int n_stress_chunks = 0;
   mace_precision prec = MACE_FP32;
   // linear plans per layer (host copy for the grid, device copy for the kernel)
@@ -352,7 +356,8 @@ struct mace_graph {
   // precision study: operand rounding of the edge product / contraction / radial MLP
   int tp_round = 0, sc_round = 0, rad_round = 0;
   bool w3x_valid = false;   // W3's parts for the l_h = 2 backward match the W3 in effect
-  bool l0_chain = true;     // 16-bit modes: the first layer's linears fused (mace_debug_fused_linears)
+  bool l0_chain = true;     // 16-bit modes: the first layer's linears fused (mace_debug_fused_linears bit 0)
+  bool wide_tiles = true;   // 16-bit modes, large graphs: eight node tiles per wide linear block (bit 1)
 };
 
 namespace {
@@ -477,9 +482,11 @@ bool run_l0_chain(mace_graph* h, hipStream_t s, bool backward) {
   const int fp32_stage = backward ? 2 : 0;
   for (int q = 0; q < 3; ++q)
     if (!chain_stage_of(*P[q], q == fp32_stage ? 0 : lowp, &a.st[q])) return false;
-  a.quad_node = b.quad_node;
-  a.quad_species = b.quad_species;
+  const bool eight = h->wide_tiles && h->n_quads8 > 0;
   a.n_quads = h->n_quads;
+  a.n_quads8 = eight ? h->n_quads8 : 0;
+  a.quad_node = eight ? b.quad_node8 : b.quad_node;
+  a.quad_species = eight ? b.quad_species8 : b.quad_species;
   a.lowp = lowp;
   ProfScope ps(h, KID_LINEAR, s);
   if (ps.on && a.n_quads > 0) {
@@ -648,6 +655,9 @@ LinArgs largs(mace_graph* h, const float* x, float* y, const float* residual, bo
   a.quad_node = h->b.quad_node;
   a.quad_species = h->b.quad_species;
   a.n_quads = h->n_quads;
+  a.quad_node8 = h->b.quad_node8;
+  a.quad_species8 = h->b.quad_species8;
+  a.n_quads8 = h->wide_tiles ? h->n_quads8 : 0;
   a.K = h->m.d.K;
   a.KI = 0;
   a.accumulate = accumulate;
@@ -1362,6 +1372,23 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
       for (int r = 0; r < tcount[t]; ++r) qnode[((size_t)q * kLinQuad + w) * kLinTileNodes + r] = order[tstart[t] + r];
     }
   }
+  // 16-bit modes on large graphs: the same tiles in runs of up to kLinQuadWide
+  // (the wide 16-bit linears and the fused first-layer linears take them)
+  std::vector<int32_t> qnode8, qspec8;
+  if (lowp_mode(prec) && h->n_quads >= kLinQuadWideMinQuads) {
+    for (int t = 0; t < h->n_tiles;) {
+      int n = 1;
+      while (n < kLinQuadWide && t + n < h->n_tiles && tspec[t + n] == tspec[t]) ++n;
+      const size_t q = qspec8.size();
+      qspec8.push_back(tspec[t]);
+      qnode8.resize((q + 1) * kLinQuadWide * kLinTileNodes, -1);
+      for (int w = 0; w < n; ++w)
+        for (int r = 0; r < tcount[t + w]; ++r)
+          qnode8[(q * kLinQuadWide + w) * kLinTileNodes + r] = order[tstart[t + w] + r];
+      t += n;
+    }
+    h->n_quads8 = (int)qspec8.size();
+  }
   // the buffers are carved from the workspace base rounded up to 256 bytes
   // (mace_workspace_bytes includes that slack)
   Carver c{reinterpret_cast<char*>((reinterpret_cast<uintptr_t>(workspace) + 255) & ~uintptr_t(255))};
@@ -1416,6 +1443,8 @@ mace_status mace_graph_setup(const mace_model_desc* desc, const float* weights, 
   }
   chk(up(b.quad_node, qnode.data(), qnode.size() * 4));
   chk(up(b.quad_species, qspec.data(), qspec.size() * 4));
+  chk(up(b.quad_node8, qnode8.data(), qnode8.size() * 4));
+  chk(up(b.quad_species8, qspec8.data(), qspec8.size() * 4));
   chk(up(b.shift, shv.data(), E * sizeof(double4)));
   chk(hipMemsetAsync(b.status, 0, sizeof(int), s));
   launch_species_table(s, (int)S, (int)K, b.w + m.off.at("embed"), b.w + m.off.at("0.up.0"),
@@ -1534,14 +1563,19 @@ mace_status mace_layer0_form(mace_graph* g, int32_t request, int32_t* in_use) {
 }
 
 mace_status mace_debug_fused_linears(mace_graph* g, int32_t request, int32_t* in_use) {
-  if (!g || request > 1) return MACE_EINVAL;
-  if (request >= 0) g->l0_chain = request == 1;
+  if (!g || request > 3) return MACE_EINVAL;
+  if (request >= 0) {
+    g->l0_chain = (request & 1) != 0;
+    g->wide_tiles = (request & 2) != 0;
+  }
   if (in_use) {
     const Model& m = g->m;
     ChainStage cs;
-    *in_use = g->l0_chain && lowp_mode(g->prec) && m.d.K == 128 && m.l0_ki == 128 && m.layers[0].mid == 16 &&
-              layer_factorised(g, 0) && chain_stage_of(g->l0f, 0, &cs) && chain_stage_of(g->lin[0], 1, &cs) &&
-              chain_stage_of(g->skip0, 1, &cs);
+    const bool chain = g->l0_chain && lowp_mode(g->prec) && m.d.K == 128 && m.l0_ki == 128 &&
+                       m.layers[0].mid == 16 && layer_factorised(g, 0) && chain_stage_of(g->l0f, 0, &cs) &&
+                       chain_stage_of(g->lin[0], 1, &cs) && chain_stage_of(g->skip0, 1, &cs);
+    const bool eight = g->wide_tiles && g->n_quads8 > 0 && m.d.K == 128;
+    *in_use = (chain ? 1 : 0) | (eight ? 2 : 0);
   }
   return MACE_OK;
 }

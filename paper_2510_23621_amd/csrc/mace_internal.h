@@ -16,6 +16,8 @@ constexpr int kMaxTerms = 48;
 constexpr int kMaxGroups = 24;
 constexpr int kLinTileNodes = 16;   // nodes per MFMA tile of the channel-mixing linear
 constexpr int kLinQuad = 4;         // node tiles (one per wave) per block of the linear
+constexpr int kLinQuadWide = 8;     // the same for the wide 16-bit launches on large graphs
+constexpr int kLinQuadWideMinQuads = 256;   // kLinQuad blocks from which a 16-bit handle also groups by kLinQuadWide
 
 // ----------------------------------------------------------------- numerics
 // e^(-x) on the hardware base-2 exponential (v_exp_f32, about 1 ulp): the
@@ -388,6 +390,11 @@ struct LinArgs {
                             // (a block's nodes are up to kLinQuad tiles of 16 nodes of one species)
   const int* quad_species;  // [n_quads]
   int n_quads;
+  // the same grouping with kLinQuadWide tiles per block ([n_quads8][kLinQuadWide][16]),
+  // taken by the wide 16-bit launches when n_quads8 > 0
+  const int* quad_node8;
+  const int* quad_species8;
+  int n_quads8;
   int K;                    // channels per component of y (and of x unless KI is set)
   int KI;                   // channels per component of x (0: K)
   int accumulate;           // y += instead of y =
@@ -410,9 +417,10 @@ struct ChainArgs {
   float* y;                    // [N][16][128]
   const float* wt;
   const unsigned short* wbf;
-  const int* quad_node;        // as LinArgs
+  const int* quad_node;        // as LinArgs (kLinQuad tiles per block, or kLinQuadWide when n_quads8 > 0)
   const int* quad_species;
   int n_quads;
+  int n_quads8;                // > 0: quad_node / quad_species hold the kLinQuadWide grouping
   int lowp;                    // the 16-bit format of the 16-bit stages
   ChainStage st[3];
 };

@@ -30,6 +30,7 @@ B = pytest.importorskip("paper_2510_23621_amd.binding")
 from gpu_common import (TOL, assert_parity, errors, lib_blob, oracle_blob, oracle_stress,  # noqa: E402
                         run_gpu, run_oracle, stress_error)
 from oracle import mace, so3  # noqa: E402
+from paper_2510_23621_amd.graph import MaceGraph  # noqa: E402
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 sys.path.insert(0, GOLDEN)
@@ -108,6 +109,29 @@ def test_large_water_every_atom_vs_fp64(name, prec):
     gpu = run_gpu(params, sysm, blob, prec=prec)
     print(f"[fullsize] {name}: {gpu['n_edges']} edges", flush=True)
     assert_parity(gpu, ref, prec, f"{name} every atom")
+
+
+@pytest.mark.parametrize("prec", [B.MACE_BF16_LINEAR, B.MACE_FP16_LINEAR])
+def test_large_water_16bit_linear_layouts_bitwise(prec):
+    """On the 36,864-atom box the 16-bit modes fuse the first layer's linears
+    and give the wide linear blocks eight node tiles; energies and forces
+    equal those of the plain layout (three launches, four tiles) bit for bit."""
+    params = model_params(3)
+    sysm = make_system(3, seed=0)
+    blob = lib_blob(params, 0)
+    snd, rcv, sh = B.mace_neighbor_list(sysm.positions, params["r_cut"], sysm.cells)
+    g = MaceGraph(B.make_desc(**params), blob, sysm.species.astype(np.int32), np.stack([snd, rcv]).astype(np.int32),
+                  sh, sysm.cells, None, 1, prec)
+    pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
+    outs = []
+    for layout in (3, 0):
+        assert B.mace_debug_fused_linears(g.handle, layout) == layout
+        eps, E, F = g.energy_forces(pos)
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy() for t in (eps, E, F)])
+    g.close()
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
 
 
 @pytest.mark.parametrize("cfg", [2, 3])

@@ -143,8 +143,8 @@ def test_fused_first_layer_linears_bitwise(prec):
         assert B.mace_layer0_form(g.handle, -1) == B.MACE_L0_FACTORED
         pos = torch.from_numpy(sysm.positions.astype(np.float32)).cuda()
         outs = []
-        for fuse in (1, 0, 1):
-            assert B.mace_debug_fused_linears(g.handle, fuse) == fuse
+        for fuse in (3, 0, 3):
+            assert B.mace_debug_fused_linears(g.handle, fuse) == (fuse & 1)   # no eight-tile blocks at these sizes
             eps, E, F, S = g.energy_forces_stress(pos)
             torch.cuda.synchronize()
             outs.append([t.cpu().numpy() for t in (eps, E, F, S)])
@@ -162,6 +162,7 @@ def test_fused_first_layer_linears_only_where_shapes_allow():
     snd, rcv, sh = B.mace_neighbor_list(sysm.positions, 5.0, sysm.cells)
     for K, prec, form, want in ((128, B.MACE_FP32, None, 0), (64, B.MACE_BF16_LINEAR, None, 0),
                                 (128, B.MACE_BF16_LINEAR, B.MACE_L0_EDGE, 0), (128, B.MACE_FP16_LINEAR, None, 1)):
+        # (bit 1, eight node tiles per block, needs at least 256 four-tile blocks: not at 96 atoms)
         params = model_params(0, K=K, hidden_lmax=1)
         g = MaceGraph(B.make_desc(**params), lib_blob(params, 0), sysm.species.astype(np.int32),
                       np.stack([snd, rcv]).astype(np.int32), sh, sysm.cells, None, 1, prec)
