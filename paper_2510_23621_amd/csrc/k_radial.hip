@@ -6,10 +6,16 @@
 //
 // The three hidden layers run here (a3 [E][64] is written out, 256 bytes per
 // edge); the wide last layer is computed inside the tensor-product kernels,
-// which also hand back dE/da3 as per-channel-tile partials. Hidden layers on
-// FP32 MFMA (v_mfma_f32_16x16x4_f32): a block
-// owns a 64-edge tile (4 row tiles of 16) and has 4 waves; lane l supplies
-// A[l%16][l/16], B[l/16][l%16], and result register r holds D[4*(l/16)+r][l%16].
+// which also hand back dE/da3 as per-channel-tile partials. A block owns a
+// 64-edge tile (4 row tiles of 16) and has 4 waves, wave w the 16 columns
+// 16w .. 16w + 15 of a layer; result register r of lane l holds
+// D[4*(l/16)+r][l%16]. The 64-wide layers (and their transposed products in
+// the backward pass) run as FP32-accurate products on the bfloat16 MFMA pipe
+// (v_mfma_f32_16x16x32_bf16; each FP32 operand carried as three bfloat16
+// parts, six partial products, as in the edge product): lane l supplies
+// A[l%16][8(l/16) + i] and B[8(l/16) + i][l%16], i = 0..7. The narrow input
+// layer (nb <= 16 inputs) and the precision study's rounded instances run on
+// FP32 MFMA (v_mfma_f32_16x16x4_f32, A[l%16][l/16], B[l/16][l%16]).
 #include <type_traits>
 
 #include "mace_internal.h"
@@ -100,6 +106,89 @@ __device__ __forceinline__ void hidden_mma(const float* __restrict__ in, int ldi
   }
 }
 
+// ---- 64-wide layers on split-BF16 MFMA
+typedef unsigned short us8v __attribute__((ext_vector_type(8)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+typedef unsigned u4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma_b16(us8v a, us8v b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a), __builtin_bit_cast(bf8v, b), c, 0, 0, 0);
+}
+
+// the three bfloat16 parts of eight FP32 values, element i of each operand
+// word holding value i (two values per conversion)
+__device__ __forceinline__ void split8(f4 lo, f4 hi, us8v& p0, us8v& p1, us8v& p2) {
+  u4v w0, w1, w2;
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    const f2v x = h < 2 ? f2v{lo[2 * h], lo[2 * h + 1]} : f2v{hi[2 * h - 4], hi[2 * h - 3]};
+    unsigned a, b, c;
+    split3_pair(x, a, b, c);
+    w0[h] = a;
+    w1[h] = b;
+    w2[h] = c;
+  }
+  p0 = __builtin_bit_cast(us8v, w0);
+  p1 = __builtin_bit_cast(us8v, w1);
+  p2 = __builtin_bit_cast(us8v, w2);
+}
+
+// B operand parts of a 64 x 64 layer for this wave's 16 columns: W[k][col]
+// (TR: W[col][k], the transposed product) for k = 32 ks + 8 (l/16) + i
+template <bool TR>
+__device__ __forceinline__ void load_b_parts64(const float* __restrict__ W, us8v (&b)[2][3]) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = 16 * w + (l & 15);
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = 32 * ks + 8 * (l >> 4) + i;
+      v[i] = TR ? W[col * kH + k] : W[k * kH + col];
+    }
+    split8(f4{v[0], v[1], v[2], v[3]}, f4{v[4], v[5], v[6], v[7]}, b[ks][0], b[ks][1], b[ks][2]);
+  }
+}
+
+// acc[rt] = in[rows of tile rt][0..64) x B for the tile's 64 edges, FP32-accurate;
+// in: LDS rows of stride ldin (a multiple of 4)
+__device__ __forceinline__ void mma64_x3(const float* __restrict__ in, int ldin, const us8v (&b)[2][3], f4* acc) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const float* ar = in + (16 * rt + (l & 15)) * ldin + 32 * ks + 8 * (l >> 4);
+      us8v a0, a1, a2;
+      split8(*reinterpret_cast<const f4*>(ar), *reinterpret_cast<const f4*>(ar + 4), a0, a1, a2);
+      f4 c = acc[rt];
+      c = mfma_b16(a2, b[ks][0], c);
+      c = mfma_b16(a1, b[ks][1], c);
+      c = mfma_b16(a0, b[ks][2], c);
+      c = mfma_b16(a1, b[ks][0], c);
+      c = mfma_b16(a0, b[ks][1], c);
+      acc[rt] = mfma_b16(a0, b[ks][0], c);
+    }
+}
+
+// hidden_mma for a 64-input layer on split-BF16 products
+template <bool STORE>
+__device__ __forceinline__ void hidden_mma_x3(const float* __restrict__ in, int ldin, const us8v (&b)[2][3],
+                                              float* __restrict__ out, f4* z) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = 16 * w + (l & 15);
+  mma64_x3(in, ldin, b, z);
+  if constexpr (STORE) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(z[rt][r]);
+  }
+}
+
 template <bool RND = false>
 __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __restrict__ rbf, int nb, int nb_pad,
                                                 float* xs, int rnd = 0) {
@@ -153,14 +242,27 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
     const float* W1 = W0 + nb * kH;
     const float* W2 = W1 + kH * kH;
     f4 z[4];
-    load_b_frag<kH, RND>(W1, kH, bn, rs.rnd);
-    hidden_mma<NBP, true, RND>(xs, kXPad, bc, ha, z, rs.rnd);
-    __syncthreads();
-    load_b_frag<kH, RND>(W2, kH, bc, rs.rnd);
-    hidden_mma<kH, true, RND>(ha, kPad, bn, hb, z, rs.rnd);
-    __syncthreads();
-    if (t + 1 < rs.n) load_b_frag<NBP, RND>(rs.W[t + 1], nb, bn, rs.rnd);
-    hidden_mma<kH, true, RND>(hb, kPad, bc, ha, z, rs.rnd);
+    if constexpr (RND) {
+      load_b_frag<kH, RND>(W1, kH, bn, rs.rnd);
+      hidden_mma<NBP, true, RND>(xs, kXPad, bc, ha, z, rs.rnd);
+      __syncthreads();
+      load_b_frag<kH, RND>(W2, kH, bc, rs.rnd);
+      hidden_mma<kH, true, RND>(ha, kPad, bn, hb, z, rs.rnd);
+      __syncthreads();
+      if (t + 1 < rs.n) load_b_frag<NBP, RND>(rs.W[t + 1], nb, bn, rs.rnd);
+      hidden_mma<kH, true, RND>(hb, kPad, bc, ha, z, rs.rnd);
+    } else {
+      // the 64-wide layers on split-BF16 products, the next layer's parts in flight meanwhile
+      us8v b1[2][3], b2[2][3];
+      load_b_parts64<false>(W1, b1);
+      hidden_mma<NBP, true, false>(xs, kXPad, bc, ha, z);
+      __syncthreads();
+      load_b_parts64<false>(W2, b2);
+      hidden_mma_x3<true>(ha, kPad, b1, hb, z);
+      __syncthreads();
+      if (t + 1 < rs.n) load_b_frag<NBP, false>(rs.W[t + 1], nb, bn);
+      hidden_mma_x3<true>(hb, kPad, b2, ha, z);
+    }
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
@@ -195,7 +297,7 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 // dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
 // to instead of overwritten.
 template <int NBP, int NPART, bool RND>
-__global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                          const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
@@ -248,11 +350,18 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   load_basis_tile<RND>(E, e0, rbf, nb, (nb + 3) & ~3, xs, rnd);
   __syncthreads();
   f4 z0[4], z1[4], z2[4];
-  load_b_frag<kH, RND>(W1, kH, bn, rnd);
+  us8v bp[2][3];   // split parts of the next 64-wide layer's B operand (not the rounded instance)
+  if constexpr (RND) load_b_frag<kH, RND>(W1, kH, bn, rnd);
+  else load_b_parts64<false>(W1, bp);
   hidden_mma<NBP, true, RND>(xs, kXPad, bc, ta, z0, rnd);
   __syncthreads();
-  load_b_frag<kH, RND>(W2, kH, bc, rnd);
-  hidden_mma<kH, true, RND>(ta, kPad, bn, tb, z1, rnd);
+  if constexpr (RND) {
+    load_b_frag<kH, RND>(W2, kH, bc, rnd);
+    hidden_mma<kH, true, RND>(ta, kPad, bn, tb, z1, rnd);
+  } else {
+    hidden_mma_x3<true>(ta, kPad, bp, tb, z1);
+    load_b_parts64<false>(W2, bp);
+  }
   __syncthreads();   // every wave is done with ta
   auto store_partials = [&]() {
 #pragma unroll
@@ -262,17 +371,20 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
     }
   };
   if (parts_first) store_partials();
-  hidden_mma<kH, false, RND>(tb, kPad, bc, nullptr, z2, rnd);   // z2 only (a3 itself is not needed)
+  // z2 only (a3 itself is not needed)
+  if constexpr (RND) hidden_mma<kH, false, RND>(tb, kPad, bc, nullptr, z2, rnd);
+  else hidden_mma_x3<false>(tb, kPad, bp, nullptr, z2);
   if (!parts_first) {
     sum_partials();
     store_partials();
   }
   // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
-  float b2[kH / 4];
+  float b2[RND ? kH / 4 : 1];
+  if constexpr (RND) {
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) {
-    b2[ks] = W2[col * kH + 4 * ks + (l >> 4)];
-    if constexpr (RND) b2[ks] = lowp_round(b2[ks], rnd);
+    for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = lowp_round(W2[col * kH + 4 * ks + (l >> 4)], rnd);
+  } else {
+    load_b_parts64<true>(W2, bp);
   }
   __syncthreads();
   // dz2 = da3 silu'(z2), in place (result layout)
@@ -283,32 +395,38 @@ __global__ void __launch_bounds__(256) radial_bwd_kernel(int E, const float* __r
   __syncthreads();
   f4 acc[4];
   // dz1 = (dz2 W2^T) silu'(z1) into tb; the next stage's B = W1^T requested meanwhile
-  float b1[kH / 4];
+  float b1[RND ? kH / 4 : 1];
+  if constexpr (RND) {
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks) {
-    b1[ks] = W1[col * kH + 4 * ks + (l >> 4)];
-    if constexpr (RND) b1[ks] = lowp_round(b1[ks], rnd);
+    for (int ks = 0; ks < kH / 4; ++ks) b1[ks] = lowp_round(W1[col * kH + 4 * ks + (l >> 4)], rnd);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kH / 4; ++ks)
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        acc[rt] = mfma4(ta[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b2[ks], acc[rt]);
+  } else {
+    mma64_x3(ta, kPad, bp, acc);
+    load_b_parts64<true>(W1, bp);   // B of the next product, W1^T, in flight during the stores and barrier below
   }
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks)
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-      acc[rt] = mfma4(ta[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b2[ks], acc[rt]);
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) tb[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z1[rt][r]);
   __syncthreads();
   // dz0 = (dz1 W1^T) silu'(z0) into ta (every wave has read ta before the barrier above)
+  if constexpr (RND) {
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ks = 0; ks < kH / 4; ++ks)
+    for (int ks = 0; ks < kH / 4; ++ks)
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-      acc[rt] = mfma4(tb[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b1[ks], acc[rt]);
+      for (int rt = 0; rt < 4; ++rt)
+        acc[rt] = mfma4(tb[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b1[ks], acc[rt]);
+  } else {
+    mma64_x3(tb, kPad, bp, acc);
+  }
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
