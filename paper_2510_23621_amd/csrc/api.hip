@@ -170,7 +170,6 @@ struct Buffers {
   float *Y = nullptr, *rbf = nullptr;
   std::vector<float*> a3;   // per layer: [E][64] last radial hidden layer
   std::vector<unsigned short*> a3x;   // per layer: its three bfloat16 parts [E][3][64] (split-BF16 products)
-  std::vector<unsigned short*> w3x;   // per l_h = 2 layer: W3's parts for the backward's dE/da3 product
   std::vector<float*> A, hin, ht;
   float *hlast = nullptr, *sc = nullptr, *At = nullptr, *Apre = nullptr, *B = nullptr;
   // backward
@@ -219,7 +218,6 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
   b.rbf = c.take<float>(std::max<int64_t>(E, 1) * nb);
   b.a3.resize(T);
   b.a3x.resize(T);
-  b.w3x.assign(T, nullptr);
   b.A.resize(T);
   b.hin.assign(T, nullptr);
   b.ht.assign(T, nullptr);
@@ -227,7 +225,6 @@ void carve(const Model& m, int64_t N, int64_t E, int G, Carver& c, Buffers& b) {
     const LayerPlan& L = m.layers[t];
     b.a3[t] = c.take<float>(std::max<int64_t>(E, 1) * 64);
     b.a3x[t] = c.take<unsigned short>(std::max<int64_t>(E, 1) * 3 * 64);
-    if (L.lh_max == 2) b.w3x[t] = c.take<unsigned short>(w3x_el_elems((int)K, L.P));
     b.A[t] = c.take<float>(N * 16 * K);
     if (t > 0) {
       b.hin[t] = c.take<float>(N * L.din * K);
@@ -355,7 +352,6 @@ struct mace_graph {
   bool radial_split = true;   // FP32 last radial layer on split-BF16 MFMA (mace_fp32_products)
   // precision study: operand rounding of the edge product / contraction / radial MLP
   int tp_round = 0, sc_round = 0, rad_round = 0;
-  bool w3x_valid = false;   // W3's parts for the l_h = 2 backward match the W3 in effect
   bool l0_chain = true;     // 16-bit modes: the first layer's linears fused (mace_debug_fused_linears bit 0)
   bool wide_tiles = true;   // 16-bit modes, large graphs: eight node tiles per wide linear block (bit 1)
 };
@@ -856,18 +852,11 @@ void run_backward(mace_graph* h, hipStream_t s, const float* pos, float* F, cons
     } else {
       const float* src = t == 0 ? (h->tp_round ? b.sp_round : b.sp_table) : b.ht[t];
       const int* src_map = t == 0 ? b.species : nullptr;
-      const float* w3 = (h->rad_round ? b.w_round : b.w) + m.off.at(pre + "radial.3");
-      if (b.w3x[t] && (!h->w3x_valid || h->rad_round)) {
-        // built from the W3 in effect (the precision study rounds a copy each call)
-        launch_w3x_el(s, w3, K, L.P, b.w3x[t]);
-        if (t == 0 || !b.w3x[t - 1]) h->w3x_valid = !h->rad_round;
-      }
       PROF(KID_TP_BWD);
       (void)launch_tpr_bwd(s, L.lh_max, N, K, E, b.rcv_off, b.snd, src_map,
                      a3_presplit(h, t) ? reinterpret_cast<const float*>(b.a3x[t]) : b.a3[t],
                      (h->rad_round ? b.w_round : b.w) + m.off.at(pre + "radial.3"),
-                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, radial_mode(h, t), h->tp_round,
-                     b.w3x[t]);
+                     b.Y, src, inv_c, b.dAt, b.dYp, t > 0 ? b.Q : nullptr, b.da3p, radial_mode(h, t), h->tp_round);
     }
     // The edge backward wrote Q and the partials (about 390 MB at K = 128,
     // more than the last-level cache holds); the sender sum reads Q first
@@ -1598,7 +1587,6 @@ mace_status mace_block_rounding(mace_graph* g, int32_t block, int32_t format, in
   int& r = block == MACE_BLOCK_EDGE_PRODUCT ? g->tp_round
                                             : (block == MACE_BLOCK_SYMMETRIC_CONTRACTION ? g->sc_round : g->rad_round);
   if (format >= 0) r = format;
-  if (format >= 0) g->w3x_valid = false;   // rebuilt from the W3 in effect at the next call
   if (in_use) *in_use = r;
   return MACE_OK;
 }

@@ -1061,50 +1061,19 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
   }
 }
 
-// ---- W3's three bfloat16 parts for the dE/da3 product of the l_h = 2
-// backward, in the edge-lane order per channel tile: element
-// ((ks 64 + j) 4 + g) 8 + pl 4 + c of part q of channel tile ct (blocks of
-// KS 2048 elements, (ct 3 + q) blocks in) holds part q of
-// W3[j][(2 ks + pl) K + 16 ct + 4 g + c], zero for a path 2 ks + pl >= P.
-// Built once per weight set (a 16-byte run per lane and K step).
-__global__ void w3x_el_kernel(const float* __restrict__ W3, int K, int P, unsigned short* __restrict__ out) {
-  const int KS = (P + 1) / 2;
-  const size_t per_ct = (size_t)KS * 2048;
-  const size_t n = (size_t)(K / 16) * per_ct;
-  for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n; idx += (size_t)gridDim.x * blockDim.x) {
-    const int ct = (int)(idx / per_ct);
-    const int r = (int)(idx % per_ct);
-    const int ks = r / 2048, j = (r / 32) % 64, g = (r / 8) % 4, pl = (r / 4) % 2, c = r % 4;
-    const int p = 2 * ks + pl;
-    unsigned short x0 = 0, x1 = 0, x2 = 0;
-    if (p < P) split3(W3[(size_t)j * P * K + p * K + 16 * ct + 4 * g + c], x0, x1, x2);
-    const size_t base = (size_t)ct * 3 * per_ct + r;
-    out[base] = x0;
-    out[base + per_ct] = x1;
-    out[base + 2 * per_ct] = x2;
-  }
-}
-
-size_t w3x_el_elems(int K, int P) { return (size_t)(K / 16) * 3 * ((P + 1) / 2) * 2048; }
-
-void launch_w3x_el(hipStream_t s, const float* W3, int K, int P, unsigned short* out) {
-  const size_t n = (size_t)(K / 16) * ((P + 1) / 2) * 2048;
-  w3x_el_kernel<<<(unsigned)std::min<size_t>((n + 255) / 256, 2048), 256, 0, s>>>(W3, K, P, out);
-}
-
 // ---- FP32-accurate backward at l_h = 2 in the edge-lane layout.
 //
-// At P = 17 the split-BF16 parts of W3 in both layouts (209 KB) do not fit the
-// LDS beside the G tables. The R recompute runs on split-BF16 MFMA with W3's
-// three parts in LDS (the swizzled forward layout of the l_h <= 1 backward,
-// 104 KB) and a3 split per tile in registers; dE/da3 runs on FP32 MFMA
-// (v_mfma_f32_16x16x4_f32, one K value per lane) with its W3 operand read as
-// float4 straight from the blob (the layer's W3 is 557 KB, resident in the
-// XCD's L2):
-//   dE/da3: D[j][edge] = sum_(p, c) W3[j][p, c] dR[edge][p, c]; in K step
-//     (p, c') lane group g supplies channel 4 g + c', which is the lane's own
-//     register r[p][c']: dR is the B operand as it stands, and one float4 of
-//     W3's row j = 16 jt + l%16 (channels 16 ct + 4 g .. +3) feeds four MFMAs.
+// Both products with W3 run on split-BF16 MFMA (FP32-accurate) from one copy of
+// W3's three bfloat16 parts in LDS, the swizzled forward layout of the l_h <= 1
+// backward (104 KB at P = 17; the transposed layout would not fit beside the G
+// tables):
+//   R recompute: A = W3's parts (rows p 16 + channel, 16-byte reads), B = a3's
+//     parts split per tile in registers;
+//   dE/da3: D[edge][j] = sum_(p, c) dR[edge][p, c] W3[j][p, c]; dR is already
+//     on the lane that owns the edge (split per K step in registers), and W3's
+//     parts reach the B operand through LDS transposing reads
+//     (ds_read_b64_tr_b16), which hand each lane one column j of four
+//     consecutive rows (channels) of the forward layout.
 // The CG part is the edge-lane contraction of the l_h = 1 backward (G table of
 // the receiver in LDS, two multiply-adds per coupling pair and channel). One
 // wave per SIMD (W3's parts and four G tables take 149 KB), so the body keeps
@@ -1112,12 +1081,10 @@ void launch_w3x_el(hipStream_t s, const float* W3, int K, int P, unsigned short*
 // number of uses ahead (a ring of registers indexed by compile-time
 // constants, held in issue order by scheduling fences), the sender rows and
 // harmonics of a tile are requested before its radial MFMAs, and the next
-// tile's a3 and sender index before its CG contraction.
-// last dword of a raw buffer descriptor (32-bit data format, no swizzle): loads
-// past num_records return zero
-constexpr int kBufferRsrcWord3 = 0x00020000;
+// tile's a3 and sender index before its dE/da3 products.
 constexpr int kRingR = 3;    // split-W3 operand triples in flight (six MFMAs each)
-constexpr int kRingD = 6;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
+constexpr int kRingD = 4;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
+typedef short s4v __attribute__((ext_vector_type(4)));
 constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
 
 // sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
@@ -1144,7 +1111,7 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
     float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd,
-    const unsigned short* __restrict__ w3x, unsigned short* sWf, float* sGall) {
+    unsigned short* sWf, float* sGall) {
   constexpr int LHMAX = 2;
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
@@ -1181,20 +1148,30 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     o[1] = *reinterpret_cast<const us8v*>(q + part);
     o[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
   };
-  // dE/da3 operands, W3's parts in the edge-lane order (w3x_el_kernel), by buffer
-  // loads: the lane's part of the offset in one register, the step's (part,
-  // K step, row tile) as a scalar; the descriptor covers this channel tile
+  // dE/da3 operands from the forward-layout parts in LDS, by transposing reads
+  // (ds_read_b64_tr_b16: in each 16-lane group, lane j receives element r of
+  // the 8-byte row that lane 4 r + j / 4 addressed, at position j % 4). Lane kk
+  // of lane group g addresses the columns 16 jt + 4 (kk % 4) .. + 3 of row
+  // 4 g + kk / 4 of a path, so that it receives column 16 jt + kk of the
+  // path's rows (channels) 4 g .. 4 g + 3: the B operand's K slots 4 pl .. 4 pl + 3
+  // for path 2 ks + pl (zero past the last path).
   constexpr int KS = (P + 1) / 2;
   constexpr int NDX = KS * 4;   // (K step, row tile) steps
-  const __amdgpu_buffer_rsrc_t w3r = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<unsigned short*>(w3x) + (size_t)ct * 3 * KS * 2048, (short)0, 3 * KS * 2048 * 2, kBufferRsrcWord3);
-  const int wd_lane = ((kk * 4 + g) * 8) * 2;
+  const int t_row = 4 * g + (kk >> 2), t_col = 4 * (kk & 3);
+  auto tr_at = [&](int q, int p, int jt) {
+    const int col = 16 * jt + t_col;
+    unsigned short* a = sWf + q * part + swz_fwd(p * 16 + t_row, col >> 3) + (col & 7);
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4v*)a);
+  };
   auto wd_at = [&](int f, us8v* o) {
     const int ks = f >> 2, jt = f & 3;
 #pragma unroll
-    for (int q = 0; q < 3; ++q)
-      o[q] = __builtin_bit_cast(us8v, __builtin_amdgcn_raw_buffer_load_b128(
-                                          w3r, wd_lane, ((q * KS + ks) * 2048 + 16 * jt * 32) * 2, 0));
+    for (int q = 0; q < 3; ++q) {
+      const s4v lo = tr_at(q, 2 * ks, jt);
+      const s4v hi = 2 * ks + 1 < P ? tr_at(q, 2 * ks + 1, jt) : s4v{0, 0, 0, 0};
+      o[q] = us8v{(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
+                  (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
+    }
   };
   for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
@@ -1402,8 +1379,7 @@ tpr_bwd_kernel(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
     const float* __restrict__ Y, const float* __restrict__ h, float inv_c, const float* __restrict__ dAt,
-    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd,
-    const unsigned short* __restrict__ w3x) {
+    float* __restrict__ dYp, float* __restrict__ Q, float* __restrict__ da3p, int rnd) {
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
@@ -1415,10 +1391,10 @@ tpr_bwd_kernel(
     __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
     if (rnd)
       tpr_bwd_l2_edge_lanes_body<NW, true>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                           rnd, w3x, sW, sG);
+                                           rnd, sW, sG);
     else
       tpr_bwd_l2_edge_lanes_body<NW, false>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                            0, w3x, sW, sG);
+                                            0, sW, sG);
   }
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
@@ -1447,19 +1423,18 @@ void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* 
 template <int LH, int RM>
 void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, const int* snd, const int* src_map,
                     const float* a3, const float* W3, const float* Y, const float* h, float inv_c,
-                    const float* dAt, float* dYp, float* Q, float* da3p, int rnd, const unsigned short* w3x) {
+                    const float* dAt, float* dYp, float* Q, float* da3p, int rnd) {
   using S = TprShape<LH, true, RM>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
   tpr_bwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp,
-                                                    Q, da3p, rnd, w3x);
+                                                    Q, da3p, rnd);
 }
 }  // namespace
 
 // Instances built: every l_h <= 2 with radial mode 0 (FP32), 1 (BF16) or 2
 // (split BF16), and mode 3 (split BF16 with pre-split a3) at l_h = 1. The
-// l_h = 2 backward in mode 2 reads W3's parts in edge-lane order (w3x) and
-// needs Q.
+// l_h = 2 backward in mode 2 needs Q.
 bool tpr_supported(int lh_max, int radial_mode) {
   if (lh_max < 0 || lh_max > 2 || radial_mode < 0 || radial_mode > 3) return false;
   return radial_mode != 3 || lh_max == 1;
@@ -1496,12 +1471,12 @@ bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
 bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
-                    int tp_round, const unsigned short* w3x) {
+                    int tp_round) {
   if (!tpr_supported(lh_max, radial_mode)) return false;
-  if (lh_max == 2 && radial_mode == 2 && (!w3x || !Q)) return false;
+  if (lh_max == 2 && radial_mode == 2 && !Q) return false;
   if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
-  tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round, w3x)
+  tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
   switch (lh_max) {
     case 0:
       if (radial_mode == 1) MACE_TPRB(0, 1);

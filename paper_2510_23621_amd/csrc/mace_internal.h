@@ -471,15 +471,11 @@ bool tpr_supported(int lh_max, int radial_mode);
 bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, float* At, int radial_mode, int tp_round);
-// As launch_tpr_fwd. The FP32-accurate l_h = 2 backward needs w3x, W3's
-// parts from launch_w3x_el, and Q (false otherwise).
+// As launch_tpr_fwd. The FP32-accurate l_h = 2 backward needs Q (false otherwise).
 bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* rcv_off, const int* snd,
                     const int* src_map, const float* a3, const float* W3, const float* Y, const float* h,
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
-                    int tp_round, const unsigned short* w3x);
-// W3's bfloat16 parts in the order of the l_h = 2 backward's dE/da3 product
-size_t w3x_el_elems(int K, int P);
-void launch_w3x_el(hipStream_t s, const float* W3, int K, int P, unsigned short* out);
+                    int tp_round);
 void launch_sender_sum(hipStream_t s, int N, int C, int K, const int* snd_off, const int* snd_perm,
                        const float* Q, float* out);
 // ---- FP64 debug precision (k_fp64.hip)
