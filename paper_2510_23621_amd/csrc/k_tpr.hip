@@ -1105,7 +1105,10 @@ __device__ __forceinline__ void el_load_a3(f4* a, int e, int g, const float* __r
     a[v] = *reinterpret_cast<const f4*>(a3 + (size_t)e * 64 + 32 * (v >> 1) + 8 * g + 4 * (v & 1));
 }
 
-template <int NW, bool RND>
+// NPROD: partial products per operand pair, 6 (split-BF16 operands,
+// FP32-accurate) or 1 (the BF16 radial mode: the operands' bfloat16 roundings,
+// which are the first split parts, with FP32 accumulation).
+template <int NW, bool RND, int NPROD>
 __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
@@ -1145,8 +1148,10 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
   auto wr_at = [&](int f, us8v* o) {
     const unsigned short* q = sWf + swz_fwd((f >> 1) * 16 + kk, 4 * (f & 1) + g);
     o[0] = *reinterpret_cast<const us8v*>(q);
-    o[1] = *reinterpret_cast<const us8v*>(q + part);
-    o[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
+    if constexpr (NPROD == 6) {
+      o[1] = *reinterpret_cast<const us8v*>(q + part);
+      o[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
+    }
   };
   // dE/da3 operands from the forward-layout parts in LDS, by transposing reads
   // (ds_read_b64_tr_b16: in each 16-lane group, lane j receives element r of
@@ -1166,7 +1171,7 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
   auto wd_at = [&](int f, us8v* o) {
     const int ks = f >> 2, jt = f & 3;
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
+    for (int q = 0; q < (NPROD == 6 ? 3 : 1); ++q) {
       const s4v lo = tr_at(q, 2 * ks, jt);
       const s4v hi = 2 * ks + 1 < P ? tr_at(q, 2 * ks + 1, jt) : s4v{0, 0, 0, 0};
       o[q] = us8v{(unsigned short)lo[0], (unsigned short)lo[1], (unsigned short)lo[2], (unsigned short)lo[3],
@@ -1234,11 +1239,13 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
           const us8v b0 = ring[f % kRingR][0], b1 = ring[f % kRingR][1], b2 = ring[f % kRingR][2];
           if constexpr (f + kRingR < NR) wr_at(f + kRingR, ring[f % kRingR]);
           f4 acc = r[p];
-          acc = mfma_bf16(b0, x[ks][2], acc);
-          acc = mfma_bf16(b1, x[ks][1], acc);
-          acc = mfma_bf16(b2, x[ks][0], acc);
-          acc = mfma_bf16(b0, x[ks][1], acc);
-          acc = mfma_bf16(b1, x[ks][0], acc);
+          if constexpr (NPROD == 6) {
+            acc = mfma_bf16(b0, x[ks][2], acc);
+            acc = mfma_bf16(b1, x[ks][1], acc);
+            acc = mfma_bf16(b2, x[ks][0], acc);
+            acc = mfma_bf16(b0, x[ks][1], acc);
+            acc = mfma_bf16(b1, x[ks][0], acc);
+          }
           r[p] = mfma_bf16(b0, x[ks][0], acc);
         });
         __builtin_amdgcn_s_setprio(0);
@@ -1351,11 +1358,13 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
           const us8v b0 = ring[f % kRingD][0], b1 = ring[f % kRingD][1], b2 = ring[f % kRingD][2];
           if constexpr (f + kRingD < NDX) wd_at(f + kRingD, ring[f % kRingD]);
           f4 acc = d3[jt];
-          acc = mfma_bf16(x[2], b0, acc);
-          acc = mfma_bf16(x[1], b1, acc);
-          acc = mfma_bf16(x[0], b2, acc);
-          acc = mfma_bf16(x[1], b0, acc);
-          acc = mfma_bf16(x[0], b1, acc);
+          if constexpr (NPROD == 6) {
+            acc = mfma_bf16(x[2], b0, acc);
+            acc = mfma_bf16(x[1], b1, acc);
+            acc = mfma_bf16(x[0], b2, acc);
+            acc = mfma_bf16(x[1], b0, acc);
+            acc = mfma_bf16(x[0], b1, acc);
+          }
           d3[jt] = mfma_bf16(x[0], b0, acc);
         });
         __builtin_amdgcn_s_setprio(0);
@@ -1383,18 +1392,19 @@ tpr_bwd_kernel(
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
-  else if constexpr (LHMAX == 2 && RM == 2) {
+  else if constexpr (LHMAX == 2 && (RM == 2 || RM == 1)) {
     // W3's slice (one layout for both products) and a G table per wave; the
     // precision study's operand rounding runs as its own instance (a uniform
     // branch, taken once)
     __shared__ __align__(16) unsigned short sW[3 * path_count(2) * 16 * 64];
     __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
+    constexpr int NPROD = RM == 1 ? 1 : 6;
     if (rnd)
-      tpr_bwd_l2_edge_lanes_body<NW, true>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                           rnd, sW, sG);
+      tpr_bwd_l2_edge_lanes_body<NW, true, NPROD>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q,
+                                                  da3p, rnd, sW, sG);
     else
-      tpr_bwd_l2_edge_lanes_body<NW, false>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
-                                            0, sW, sG);
+      tpr_bwd_l2_edge_lanes_body<NW, false, NPROD>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q,
+                                                   da3p, 0, sW, sG);
   }
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
@@ -1434,7 +1444,7 @@ void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, cons
 
 // Instances built: every l_h <= 2 with radial mode 0 (FP32), 1 (BF16) or 2
 // (split BF16), and mode 3 (split BF16 with pre-split a3) at l_h = 1. The
-// l_h = 2 backward in mode 2 needs Q.
+// l_h = 2 backward in modes 1 and 2 (the edge-lane form) needs Q.
 bool tpr_supported(int lh_max, int radial_mode) {
   if (lh_max < 0 || lh_max > 2 || radial_mode < 0 || radial_mode > 3) return false;
   return radial_mode != 3 || lh_max == 1;
@@ -1473,7 +1483,7 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
                     int tp_round) {
   if (!tpr_supported(lh_max, radial_mode)) return false;
-  if (lh_max == 2 && radial_mode == 2 && !Q) return false;
+  if (lh_max == 2 && (radial_mode == 2 || radial_mode == 1) && !Q) return false;
   if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
   tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
