@@ -538,14 +538,19 @@ tpr_fwd_kernel(
         for_paths<LHMAX>([&](auto tag) {
           using T = decltype(tag);
           constexpr int lh = T::lh, ly = T::ly, lo = T::lo;
-          // R folded into the sender features first: acc += C (R h[m1]) Y[m2],
-          // one product per coupled pair and one multiply-add per coefficient
+          // R folded into the sender features (R h[m1]) and the coefficients'
+          // magnitudes into the harmonics (|C| Y[m2], one product per distinct
+          // pair of the path): acc[m3] += (+-R h[m1]) (|C| Y[m2]), one
+          // multiply-add per coefficient with its sign on an operand
+          using C = mt::CG<lh, ly, lo>;
           const float rv = r[T::index][q];
           float hr[2 * lh + 1];
 #pragma unroll
           for (int m = 0; m < 2 * lh + 1; ++m) hr[m] = rv * hv[lh * lh + m];
-          mt::CG<lh, ly, lo>::each([&](int m1, int m2, int m3, float cg) {
-            acc[T::offset + m3] += cg * (hr[m1] * y[ly * ly + m2]);
+          float yc[C::nyc];
+          C::each_yc([&](int m2, float av, int u) { yc[u] = av * y[ly * ly + m2]; });
+          C::each_ys([&](int m1, int m2, int m3, int sg, int u) {
+            acc[T::offset + m3] = __builtin_fmaf(sg > 0 ? hr[m1] : -hr[m1], yc[u], acc[T::offset + m3]);
           });
         });
         if constexpr (q < 3) {
