@@ -1088,9 +1088,43 @@ __device__ __forceinline__ void tpr_bwd_edge_lanes_body(
 // harmonics of a tile are requested before its radial MFMAs, and the next
 // tile's a3 and sender index before its dE/da3 products.
 constexpr int kRingR = 3;    // split-W3 operand triples in flight (six MFMAs each)
-constexpr int kRingD = 4;    // split-W3 operand triples of the dE/da3 product in flight (six MFMAs each)
+constexpr int kRingW = 2;    // W3 operand sets of the dE/da3 product held (one in use, one in flight)
 typedef short s4v __attribute__((ext_vector_type(4)));
 constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
+
+// Where the dE/da3 MFMAs go in the l_h = 2 backward: K step ks of the
+// product (paths 2 ks and 2 ks + 1, 4 NPROD MFMAs) can start once the
+// contraction has produced dR of both paths, i.e. at the first coupling pair
+// of path 2 ks + 2. The MFMAs are issued in order, at most two per coupling
+// pair, between the pairs' multiply-adds (one MFMA runs in the shadow of a
+// pair's vector work); whatever the contraction cannot take (the last K step)
+// follows it. first[gi] is the first MFMA issued at pair gi; first[NPAIR],
+// the number issued inside the contraction.
+template <int NPAIR, int P, int NPROD>
+struct Da3Plan {
+  static constexpr int KS = (P + 1) / 2;
+  static constexpr int MPK = 4 * NPROD;
+  static constexpr int NM = KS * MPK;
+  int first[NPAIR + 1];
+  template <class Off>
+  constexpr Da3Plan(Off off) : first{} {
+    int n = 0;
+    for (int gi = 0; gi < NPAIR; ++gi) {
+      first[gi] = n;
+      for (int k = 0; k < 2 && n < NM; ++k) {
+        const int ks = n / MPK;
+        if (2 * ks + 2 >= P || gi < off(2 * ks + 2)) break;
+        ++n;
+      }
+    }
+    first[NPAIR] = n;
+  }
+};
+template <int I, int N>
+constexpr int path_pair_offset_of(int p) {
+  if constexpr (I >= N) return -1;
+  else return p == I ? PathPairOffset<I>::value : path_pair_offset_of<I + 1, N>(p);
+}
 
 // sender rows (channels kb .. kb + 3) and harmonics of the lane's edge
 template <int DIN>
@@ -1270,6 +1304,38 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
       f4 dh[DIN];
 #pragma unroll
       for (int c = 0; c < DIN; ++c) dh[c] = f4{0.f, 0.f, 0.f, 0.f};
+      // dE/da3 partial on split-BF16 products (dR split per K step):
+      // d3[jt][rr] = D[edge e0 + 4 g + rr][j = 16 jt + kk]; in K step ks the
+      // lane's eight reduction values are (path 2 ks + pl, channel 4 g + c).
+      // Its MFMAs are spread over the contraction of the later paths (Da3Plan);
+      // the split dR of two K steps (x) and kRingW W3 operand sets (wring) are
+      // live at a time.
+      using Plan = Da3Plan<NPAIR, P, NPROD>;
+      constexpr Plan plan([](int q) { return path_pair_offset_of<0, P>(q); });
+      f4 d3[4];
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
+      us8v x[2][NPROD == 6 ? 3 : 1];
+      us8v wring[kRingW][NPROD == 6 ? 3 : 1];
+#pragma unroll
+      for (int t = 0; t + 1 < kRingW; ++t) wd_at(t, wring[t]);
+      // MFMA n of the product: operand set t = n / NPROD (K step t / 4, row
+      // tile t % 4), partial product n % NPROD; the first one of a set requests
+      // the set kRingW - 1 ahead
+      auto da3_mfma = [&](int n) {
+        const int t = n / NPROD, pr = n % NPROD;
+        const int ks = t >> 2, jt = t & 3;
+        if (pr == 0 && t + kRingW - 1 < NDX) wd_at(t + kRingW - 1, wring[(t + kRingW - 1) % kRingW]);
+        const us8v* b = wring[t % kRingW];
+        const us8v* xa = x[ks & 1];
+        if constexpr (NPROD == 6) {
+          // smallest terms first, as in the other split products
+          constexpr int ia[6] = {2, 1, 0, 1, 0, 0}, ib[6] = {0, 1, 2, 0, 1, 0};
+          d3[jt] = mfma_bf16(xa[ia[pr]], b[ib[pr]], d3[jt]);
+        } else {
+          d3[jt] = mfma_bf16(xa[0], b[0], d3[jt]);
+        }
+      };
       {
         const float* gq = sg + 4 * g;
         f4 gring[kRingG];
@@ -1297,6 +1363,9 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
 #pragma unroll
             for (int c = 0; c < 4; ++c) t += G[c] * Rh[m1][c];
             dy[ly * ly + m2] = t;
+            // the dE/da3 MFMAs planned for this pair
+#pragma unroll
+            for (int n = plan.first[gi]; n < plan.first[gi + 1]; ++n) da3_mfma(n);
           });
           f4 d = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1305,6 +1374,16 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
             dh[lh * lh + m] += rv * Dm[m];
           }
           r[T::index] = d;   // dR
+          // a completed K step of the dE/da3 product: its dR in split form
+          if constexpr (T::index % 2 == 1 || T::index + 1 == P) {
+            constexpr int ks = T::index / 2;
+            const f4 hi = 2 * ks + 1 < P ? r[2 * ks + 1 < P ? 2 * ks + 1 : 0] : f4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (NPROD == 6) split3_x8(r[2 * ks], hi, x[ks & 1][0], x[ks & 1][1], x[ks & 1][2]);
+            else {
+              us8v x1, x2;
+              split3_x8(r[2 * ks], hi, x[ks & 1][0], x1, x2);
+            }
+          }
           // the paths come ordered by l_h: after the last one of an l_h block
           // that block of the sender gradient is complete and leaves registers
           if constexpr (T::index + 1 == P || PathAt<T::index + 1>::lh != lh) {
@@ -1333,47 +1412,21 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         }
       }
       *reinterpret_cast<f4*>(dYc + (size_t)ec * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
-      // the next tile's sender index and a3, in flight during the dE/da3 product
+      // the next tile's sender index and a3, in flight during the rest of the
+      // dE/da3 product
       if (more) {
         e = min(e0 + 16 + kk, e_end - 1);
         src = snd[e];
         if (src_map) src = src_map[src];
         el_load_a3(a, e, g, a3);
       }
-      // dE/da3 partial on split-BF16 products (dR split per K step):
-      // d3[jt][rr] = D[edge e0 + 4 g + rr][j = 16 jt + kk]; in K step ks the
-      // lane's eight reduction values are (path 2 ks + pl, channel 4 g + c)
-      f4 d3[4];
-#pragma unroll
-      for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
-      {
-        us8v ring[kRingD][3];
-#pragma unroll
-        for (int f = 0; f < kRingD; ++f) wd_at(f, ring[f]);
-        us8v x[3];
-        __builtin_amdgcn_s_setprio(1);
-        static_for<0, NDX>([&](auto F) {
-          constexpr int f = decltype(F)::value;
-          constexpr int ks = f >> 2, jt = f & 3;
-          __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingD steps ahead of its use
-          if constexpr (jt == 0) {
-            const f4 hi = 2 * ks + 1 < P ? r[2 * ks + 1 < P ? 2 * ks + 1 : 0] : f4{0.f, 0.f, 0.f, 0.f};
-            split3_x8(r[2 * ks], hi, x[0], x[1], x[2]);
-          }
-          const us8v b0 = ring[f % kRingD][0], b1 = ring[f % kRingD][1], b2 = ring[f % kRingD][2];
-          if constexpr (f + kRingD < NDX) wd_at(f + kRingD, ring[f % kRingD]);
-          f4 acc = d3[jt];
-          if constexpr (NPROD == 6) {
-            acc = mfma_bf16(x[2], b0, acc);
-            acc = mfma_bf16(x[1], b1, acc);
-            acc = mfma_bf16(x[0], b2, acc);
-            acc = mfma_bf16(x[1], b0, acc);
-            acc = mfma_bf16(x[0], b1, acc);
-          }
-          d3[jt] = mfma_bf16(x[0], b0, acc);
-        });
-        __builtin_amdgcn_s_setprio(0);
-      }
+      // the MFMAs the contraction could not take
+      __builtin_amdgcn_s_setprio(1);
+      static_for<plan.first[NPAIR], Plan::NM>([&](auto N) {
+        __builtin_amdgcn_sched_barrier(0);   // keeps each operand read kRingW - 1 sets ahead of its use
+        da3_mfma(decltype(N)::value);
+      });
+      __builtin_amdgcn_s_setprio(0);
       // rows past the receiver's last edge hold that edge's values (their A rows
       // came from lanes working on it): stored to its row, no branch
 #pragma unroll
