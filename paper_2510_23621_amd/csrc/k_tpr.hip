@@ -1092,32 +1092,64 @@ constexpr int kRingW = 2;    // W3 operand sets of the dE/da3 product held (one 
 typedef short s4v __attribute__((ext_vector_type(4)));
 constexpr int kRingG = 6;    // G-table entries in flight (one coupling pair each)
 
-// Where the dE/da3 MFMAs go in the l_h = 2 backward: K step ks of the
-// product (paths 2 ks and 2 ks + 1, 4 NPROD MFMAs) can start once the
-// contraction has produced dR of both paths, i.e. at the first coupling pair
-// of path 2 ks + 2. The MFMAs are issued in order, at most two per coupling
-// pair, between the pairs' multiply-adds (one MFMA runs in the shadow of a
-// pair's vector work); whatever the contraction cannot take (the last K step)
-// follows it. first[gi] is the first MFMA issued at pair gi; first[NPAIR],
-// the number issued inside the contraction.
-template <int NPAIR, int P, int NPROD>
-struct Da3Plan {
+// The MFMAs of the l_h = 2 backward that run between the contraction's
+// coupling pairs, in program order, at most MAXPER per pair (each runs in the
+// shadow of a pair's multiply-adds):
+//   - K step ks of the dE/da3 product (paths 2 ks and 2 ks + 1, 4 NPROD
+//     MFMAs), once the contraction has produced dR of both paths, i.e. from
+//     the first coupling pair of path 2 ks + 2;
+//   - with PIPE, the next tile's R product of paths 2 ks and 2 ks + 1
+//     (2 NPROD MFMAs each), into the registers of R values already
+//     contracted, from the same pair and not before pair XA (the next tile's
+//     a3 has to arrive).
+// Both kinds keep their own order; between them the earlier K step goes
+// first. Whatever the contraction cannot take (the last K step) follows it.
+// order[first[gi] .. first[gi + 1]) are the MFMAs at pair gi; an MFMA id below
+// ND is a dE/da3 one, the others the R product's. `valid` says that every
+// dE/da3 K step is issued before its split operands' registers are reused
+// (by the split of K step ks + 2, at the end of path 2 ks + 5).
+template <int NPAIR, int P, int NPROD, int XA, bool PIPE, int MAXPER>
+struct BwdPlan {
   static constexpr int KS = (P + 1) / 2;
-  static constexpr int MPK = 4 * NPROD;
-  static constexpr int NM = KS * MPK;
+  static constexpr int ND = KS * 4 * NPROD;
+  static constexpr int NRM = PIPE ? P * 2 * NPROD : 0;
+  static constexpr int NT = ND + NRM;
+  static constexpr int kNever = 1 << 20;
   int first[NPAIR + 1];
+  int order[NT];
+  bool valid;
   template <class Off>
-  constexpr Da3Plan(Off off) : first{} {
-    int n = 0;
+  constexpr BwdPlan(Off off) : first{}, order{}, valid(true) {
+    auto avail_ks = [&](int ks) { return 2 * ks + 2 < P ? off(2 * ks + 2) : kNever; };
+    auto pos_d = [&](int n) { return (n / (4 * NPROD)) * 8 * NPROD + n % (4 * NPROD); };
+    auto pos_r = [&](int m) { return (m / (4 * NPROD)) * 8 * NPROD + 4 * NPROD + m % (4 * NPROD); };
+    int k = 0, dn = 0, rn = 0;
+    int last_d[KS] = {};
     for (int gi = 0; gi < NPAIR; ++gi) {
-      first[gi] = n;
-      for (int k = 0; k < 2 && n < NM; ++k) {
-        const int ks = n / MPK;
-        if (2 * ks + 2 >= P || gi < off(2 * ks + 2)) break;
-        ++n;
+      first[gi] = k;
+      for (int c = 0; c < MAXPER; ++c) {
+        const bool dav = dn < ND && gi >= avail_ks(dn / (4 * NPROD));
+        const int ra = rn < NRM ? avail_ks(rn / (4 * NPROD)) : kNever;
+        const bool rav = rn < NRM && gi >= (ra > XA ? ra : XA);
+        if (!dav && !rav) break;
+        if (dav && (!rav || pos_d(dn) < pos_r(rn))) {
+          last_d[dn / (4 * NPROD)] = gi;
+          order[k++] = dn++;
+        } else {
+          order[k++] = ND + rn++;
+        }
       }
     }
-    first[NPAIR] = n;
+    first[NPAIR] = k;
+    for (int ks = 0; ks + 2 < KS; ++ks) {
+      if ((ks + 1) * 4 * NPROD > dn) valid = false;   // left for after the contraction
+      else if (2 * ks + 6 < P && last_d[ks] >= off(2 * ks + 6)) valid = false;
+    }
+    // the rest in list order
+    while (dn < ND || rn < NRM) {
+      if (dn < ND && (rn >= NRM || pos_d(dn) < pos_r(rn))) order[k++] = dn++;
+      else order[k++] = ND + rn++;
+    }
   }
 };
 template <int I, int N>
@@ -1217,9 +1249,65 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
                   (unsigned short)hi[0], (unsigned short)hi[1], (unsigned short)hi[2], (unsigned short)hi[3]};
     }
   };
-  for (int i = blockIdx.x * NW + w; i < N; i += gridDim.x * NW) {
+  // PIPE (the one-product radial mode): a software pipeline over the wave's
+  // tiles. The R product of the next tile (this receiver's next, else the
+  // first of the wave's next receiver) runs inside the current tile's
+  // contraction, into the registers of R values already contracted; its a3,
+  // sender rows and harmonics are requested during the current tile, and
+  // `prep` says r, hv and y4 hold the upcoming tile's. With six products per
+  // operand pair the MFMAs of both products would outrun the contraction's
+  // vector work (measured slower), so there each tile forms its R product
+  // before its contraction, and the next tile's a3 is requested during the
+  // dE/da3 product.
+  constexpr bool PIPE = NPROD == 1;
+  using Plan = BwdPlan<NPAIR, P, NPROD, 40, PIPE, PIPE ? 3 : 2>;
+  constexpr Plan plan([](int q) { return path_pair_offset_of<0, P>(q); });
+  static_assert(plan.valid, "a dE/da3 K step would outlive its split operands");
+  const int stride = gridDim.x * NW;
+  bool prep = false;
+  int e = 0, src = 0;   // src: without PIPE, the sender of the tile's edge
+  f4 r[P], hv[DIN], y4[4];
+  f4 a[4];   // without PIPE, the a3 of the tile's edge
+  // R of the tile whose a3 is a0 .. a3 (edge on the lane), split-BF16 products
+  auto r_standalone = [&](f4 av0, f4 av1, f4 av2, f4 av3) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+    us8v x[2][3];
+    split3_x8(av0, av1, x[0][0], x[0][1], x[0][2]);
+    split3_x8(av2, av3, x[1][0], x[1][1], x[1][2]);
+    us8v ring[kRingR][3];
+#pragma unroll
+    for (int f = 0; f < kRingR; ++f) wr_at(f, ring[f]);
+    __builtin_amdgcn_s_setprio(1);
+    static_for<0, NR>([&](auto F) {
+      constexpr int f = decltype(F)::value;
+      constexpr int p = f >> 1, ks = f & 1;
+      __builtin_amdgcn_sched_barrier(0);   // keeps each read kRingR steps ahead of its use
+      const us8v b0 = ring[f % kRingR][0], b1 = ring[f % kRingR][1], b2 = ring[f % kRingR][2];
+      if constexpr (f + kRingR < NR) wr_at(f + kRingR, ring[f % kRingR]);
+      f4 acc = r[p];
+      if constexpr (NPROD == 6) {
+        acc = mfma_bf16(b0, x[ks][2], acc);
+        acc = mfma_bf16(b1, x[ks][1], acc);
+        acc = mfma_bf16(b2, x[ks][0], acc);
+        acc = mfma_bf16(b0, x[ks][1], acc);
+        acc = mfma_bf16(b1, x[ks][0], acc);
+      }
+      r[p] = mfma_bf16(b0, x[ks][0], acc);
+    });
+    __builtin_amdgcn_s_setprio(0);
+  };
+  for (int i = blockIdx.x * NW + w; i < N; i += stride) {
     const int e_beg = rcv_off[i], e_end = rcv_off[i + 1];
-    if (e_beg == e_end) continue;
+    if (e_beg == e_end) {
+      prep = false;
+      continue;
+    }
+    int nb = 0, ne = 0;   // the wave's next receiver's edges
+    if (i + stride < N) {
+      nb = rcv_off[i + stride];
+      ne = rcv_off[i + stride + 1];
+    }
     {
       // G_p of this receiver for channel 16 ct + l%16, path by path (only the
       // path's own dE/dAt values live); the four lane groups compute the same
@@ -1244,29 +1332,21 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
       });
       __builtin_amdgcn_wave_barrier();
     }
-    int e = min(e_beg + kk, e_end - 1);
-    int src = snd[e];
-    if (src_map) src = src_map[src];
-    f4 a[4];
-    el_load_a3(a, e, g, a3);
-    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
-      __asm__ volatile("" ::: "memory");   // the G table is read per tile, not held in registers
-      // Lanes past the receiver's last edge work on that edge (ec is clamped):
-      // their inputs, hence every value they compute, equal the last valid
-      // lane's, so they store the same values to the same rows, and the stores
-      // need no branch.
-      const int ec = e;
-      const bool more = e0 + 16 < e_end;
-      f4 hv[DIN], y4[4];
-      el_load_hy<DIN>(hv, y4, src, e, kb, h, Y, K);
-      // R of the tile, edge on the lane, split-BF16 products
-      f4 r[P];
+    if (!prep) {
+      // the receiver's first tile (with PIPE: when no earlier tile prepared it)
+      e = min(e_beg + kk, e_end - 1);
+      int s0 = snd[e];
+      if (src_map) s0 = src_map[s0];
+      if constexpr (PIPE) {
+        f4 a0[4];
+        el_load_a3(a0, e, g, a3);
+        el_load_hy<DIN>(hv, y4, s0, e, kb, h, Y, K);
+        // (written out here: as a call of r_standalone it costs registers)
 #pragma unroll
-      for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
-      {
+        for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
         us8v x[2][3];
-        split3_x8(a[0], a[1], x[0][0], x[0][1], x[0][2]);
-        split3_x8(a[2], a[3], x[1][0], x[1][1], x[1][2]);
+        split3_x8(a0[0], a0[1], x[0][0], x[0][1], x[0][2]);
+        split3_x8(a0[2], a0[3], x[1][0], x[1][1], x[1][2]);
         us8v ring[kRingR][3];
 #pragma unroll
         for (int f = 0; f < kRingR; ++f) wr_at(f, ring[f]);
@@ -1288,6 +1368,31 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
           r[p] = mfma_bf16(b0, x[ks][0], acc);
         });
         __builtin_amdgcn_s_setprio(0);
+      } else {
+        src = s0;
+        el_load_a3(a, e, g, a3);
+      }
+    }
+    for (int e0 = e_beg; e0 < e_end; e0 += 16) {
+      __asm__ volatile("" ::: "memory");   // the G table is read per tile, not held in registers
+      // Lanes past the receiver's last edge work on that edge (ec is clamped):
+      // their inputs, hence every value they compute, equal the last valid
+      // lane's, so they store the same values to the same rows, and the stores
+      // need no branch.
+      const int ec = e;
+      const bool more = e0 + 16 < e_end;
+      if constexpr (!PIPE) {
+        el_load_hy<DIN>(hv, y4, src, e, kb, h, Y, K);
+        r_standalone(a[0], a[1], a[2], a[3]);
+      }
+      // with PIPE, the next tile's edge; after the wave's last tile, this
+      // tile's again (its products are then discarded)
+      const int e_n = more ? min(e0 + 16 + kk, e_end - 1) : (nb < ne ? min(nb + kk, ne - 1) : ec);
+      int src_n = 0;
+      f4 an[4];
+      if constexpr (PIPE) {
+        src_n = snd[e_n];
+        el_load_a3(an, e_n, g, a3);
       }
       if constexpr (RND) round_tile<P>(r, rnd);
       float y[16];
@@ -1298,6 +1403,10 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         y[4 * v + 2] = y4[v][2];
         y[4 * v + 3] = y4[v][3];
       }
+      if constexpr (PIPE) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) y4[v] = reinterpret_cast<const f4*>(Y + (size_t)e_n * 16)[v];
+      }
       float dy[16];
 #pragma unroll
       for (int m = 0; m < 16; ++m) dy[m] = 0.f;
@@ -1307,11 +1416,8 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
       // dE/da3 partial on split-BF16 products (dR split per K step):
       // d3[jt][rr] = D[edge e0 + 4 g + rr][j = 16 jt + kk]; in K step ks the
       // lane's eight reduction values are (path 2 ks + pl, channel 4 g + c).
-      // Its MFMAs are spread over the contraction of the later paths (Da3Plan);
-      // the split dR of two K steps (x) and kRingW W3 operand sets (wring) are
+      // The split dR of two K steps (x) and kRingW W3 operand sets (wring) are
       // live at a time.
-      using Plan = Da3Plan<NPAIR, P, NPROD>;
-      constexpr Plan plan([](int q) { return path_pair_offset_of<0, P>(q); });
       f4 d3[4];
 #pragma unroll
       for (int jt = 0; jt < 4; ++jt) d3[jt] = f4{0.f, 0.f, 0.f, 0.f};
@@ -1319,9 +1425,9 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
       us8v wring[kRingW][NPROD == 6 ? 3 : 1];
 #pragma unroll
       for (int t = 0; t + 1 < kRingW; ++t) wd_at(t, wring[t]);
-      // MFMA n of the product: operand set t = n / NPROD (K step t / 4, row
-      // tile t % 4), partial product n % NPROD; the first one of a set requests
-      // the set kRingW - 1 ahead
+      // MFMA n of the dE/da3 product: operand set t = n / NPROD (K step t / 4,
+      // row tile t % 4), partial product n % NPROD; the first one of a set
+      // requests the set kRingW - 1 ahead
       auto da3_mfma = [&](int n) {
         const int t = n / NPROD, pr = n % NPROD;
         const int ks = t >> 2, jt = t & 3;
@@ -1335,6 +1441,40 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         } else {
           d3[jt] = mfma_bf16(xa[0], b[0], d3[jt]);
         }
+      };
+      // MFMA m of the next tile's R product: operand set f = m / NPROD (path
+      // f / 2, K step f % 2 of a3), partial product m % NPROD, in the order of
+      // the standalone product (a path's first one starts from zero); the next
+      // tile's a3 is split at the first one
+      us8v xn[2][NPROD == 6 ? 3 : 1];
+      us8v rring[2][NPROD == 6 ? 3 : 1];
+      if constexpr (PIPE) wr_at(0, rring[0]);
+      auto r_mfma = [&](int m) {
+        const int f = m / NPROD, pr = m % NPROD;
+        const int p = f >> 1, kq = f & 1;
+        if (m == 0) {
+          if constexpr (NPROD == 6) {
+            split3_x8(an[0], an[1], xn[0][0], xn[0][1], xn[0][2]);
+            split3_x8(an[2], an[3], xn[1][0], xn[1][1], xn[1][2]);
+          } else {
+            us8v t1, t2;
+            split3_x8(an[0], an[1], xn[0][0], t1, t2);
+            split3_x8(an[2], an[3], xn[1][0], t1, t2);
+          }
+        }
+        if (pr == 0 && f + 1 < NR) wr_at(f + 1, rring[(f + 1) & 1]);
+        const us8v* b = rring[f & 1];
+        const f4 acc = (kq == 0 && pr == 0) ? f4{0.f, 0.f, 0.f, 0.f} : r[p];
+        if constexpr (NPROD == 6) {
+          constexpr int ib[6] = {0, 1, 2, 0, 1, 0}, ia[6] = {2, 1, 0, 1, 0, 0};
+          r[p] = mfma_bf16(b[ib[pr]], xn[kq][ia[pr]], acc);
+        } else {
+          r[p] = mfma_bf16(b[0], xn[kq][0], acc);
+        }
+      };
+      auto mfma_item = [&](int id) {
+        if (id < Plan::ND) da3_mfma(id);
+        else r_mfma(id - Plan::ND);
       };
       {
         const float* gq = sg + 4 * g;
@@ -1363,9 +1503,9 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
 #pragma unroll
             for (int c = 0; c < 4; ++c) t += G[c] * Rh[m1][c];
             dy[ly * ly + m2] = t;
-            // the dE/da3 MFMAs planned for this pair
+            // the MFMAs planned for this pair
 #pragma unroll
-            for (int n = plan.first[gi]; n < plan.first[gi + 1]; ++n) da3_mfma(n);
+            for (int j = plan.first[gi]; j < plan.first[gi + 1]; ++j) mfma_item(plan.order[j]);
           });
           f4 d = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1385,11 +1525,19 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
             }
           }
           // the paths come ordered by l_h: after the last one of an l_h block
-          // that block of the sender gradient is complete and leaves registers
+          // that block of the sender gradient is complete and leaves registers,
+          // and the block's sender rows are free for the next tile's
           if constexpr (T::index + 1 == P || PathAt<T::index + 1>::lh != lh) {
 #pragma unroll
             for (int m = 0; m < 2 * lh + 1; ++m)
               *reinterpret_cast<f4*>(Q + ((size_t)ec * DIN + lh * lh + m) * K + kb) = dh[lh * lh + m];
+            if constexpr (!PIPE) {
+            } else if constexpr (lh == 0) {
+              if (src_map) src_n = src_map[src_n];
+            } else if constexpr (lh == 1) {
+#pragma unroll
+              for (int c = 0; c < 4; ++c) hv[c] = *reinterpret_cast<const f4*>(h + ((size_t)src_n * DIN + c) * K + kb);
+            }
           }
         });
       }
@@ -1412,19 +1560,24 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         }
       }
       *reinterpret_cast<f4*>(dYc + (size_t)ec * 16 + 4 * g) = f4{dy[0], dy[1], dy[2], dy[3]};
-      // the next tile's sender index and a3, in flight during the rest of the
-      // dE/da3 product
-      if (more) {
-        e = min(e0 + 16 + kk, e_end - 1);
-        src = snd[e];
-        if (src_map) src = src_map[src];
-        el_load_a3(a, e, g, a3);
+      if constexpr (PIPE) {
+#pragma unroll
+        for (int c = 4; c < DIN; ++c) hv[c] = *reinterpret_cast<const f4*>(h + ((size_t)src_n * DIN + c) * K + kb);
+      } else {
+        if (more) {
+          // the next tile's sender index and a3, in flight during the rest of
+          // the dE/da3 product
+          e = min(e0 + 16 + kk, e_end - 1);
+          src = snd[e];
+          if (src_map) src = src_map[src];
+          el_load_a3(a, e, g, a3);
+        }
       }
       // the MFMAs the contraction could not take
       __builtin_amdgcn_s_setprio(1);
-      static_for<plan.first[NPAIR], Plan::NM>([&](auto N) {
-        __builtin_amdgcn_sched_barrier(0);   // keeps each operand read kRingW - 1 sets ahead of its use
-        da3_mfma(decltype(N)::value);
+      static_for<plan.first[NPAIR], Plan::NT>([&](auto J) {
+        __builtin_amdgcn_sched_barrier(0);   // keeps each operand read one set ahead of its use
+        mfma_item(plan.order[decltype(J)::value]);
       });
       __builtin_amdgcn_s_setprio(0);
       // rows past the receiver's last edge hold that edge's values (their A rows
@@ -1435,7 +1588,9 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) da3c[row + 16 * jt + kk] = d3[jt][rr];
       }
+      if constexpr (PIPE) e = e_n;
     }
+    prep = PIPE && nb < ne;
   }
 }
 
