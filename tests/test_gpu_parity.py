@@ -230,6 +230,33 @@ def test_bf16_radial_vs_fp64_and_emulation(case):
         assert se <= 2e-2, se
 
 
+def test_bf16_radial_waves_over_several_receivers():
+    """The l_h = 2 backward of the BF16-radial mode forms the next tile's R
+    product inside the current contraction, also across the receivers that
+    one wave walks: 336 atoms at K = 128 give each wave two or three
+    receivers, and six isolated atoms (empty receivers) sit where a wave's
+    first receiver, and the receiver after a non-empty one, are empty."""
+    params = model_params(0, K=128, hidden_lmax=2, **STRESS)
+    w = synth.water_box(110, seed=3, box=15.0)
+    pos, spec = w.positions.copy(), w.species.copy()
+    isolated = [40, 41, 170, 171, 300, 301]
+    for k, at in enumerate(isolated):
+        pos = np.insert(pos, at, [500.0 + 60.0 * k, 7.0, -3.0], axis=0)
+        spec = np.insert(spec, at, k % 2)
+    sysm = synth.System(pos, spec.astype(np.int32), None, np.zeros(len(pos), np.int32), 1)
+    bo = oracle_blob(params, 8, STRESS_GAINS)
+    bl = lib_blob(params, 8, STRESS_GAINS)
+    ref = run_oracle(params, sysm, bo)
+    gr = run_gpu(params, sysm, bl, prec=B.MACE_BF16_RADIAL)
+    assert gr["n_edges"] == len(ref["graph"].sender)
+    assert_parity(gr, ref, B.MACE_BF16_RADIAL, "bf16-radial, several receivers per wave")
+    assert np.all(gr["forces"][isolated] == 0.0)
+    emu = run_oracle(params, sysm, bo, bf16_radial=True)
+    err = errors(gr, emu)
+    print(f"[parity] bf16-radial, several receivers per wave, vs emulating oracle {err}", flush=True)
+    assert err["energy"] <= 1e-3 and err["forces"] <= 1e-2, err
+
+
 def test_device_status_word_flags_bad_positions():
     """Device-detected errors: a NaN coordinate sets flag 1 (MACE_ENONFINITE),
     two atoms joined by an edge moved onto each other set flag 2
