@@ -55,9 +55,16 @@ typedef enum {
                              precision arm of the paper is measured against) */
 } mace_precision;
 
+#define MACE_MAX_LAYERS 8
+
 /* Model hyper-parameters (host).  Supported: sh_lmax = 3, correlation = 3,
  * 1 <= n_bessel <= 16, radial_hidden = {64, 64, 64}, 1 <= readout_hidden <= 16,
- * 0 <= hidden_lmax <= 2, K in {32, 64, 96, 128}, n_layers >= 1. */
+ * 0 <= hidden_lmax[t] <= 2 and non-increasing in t, K in {32, 64, 96, 128},
+ * 1 <= n_layers <= MACE_MAX_LAYERS (other values: MACE_EUNSUPPORTED, or
+ * MACE_EINVAL for n_layers).  Layer t's input irreps are 0e for t = 0 and
+ * 0e+...+l for l = hidden_lmax[t - 1] after it (the architecture table's
+ * hidden irreps, alternating parity); its output irreps are those of
+ * hidden_lmax[t], and 0e for the last layer. */
 typedef struct mace_model_desc {
   int32_t n_species;       /* S */
   int32_t K;               /* channels */
@@ -68,7 +75,8 @@ typedef struct mace_model_desc {
   int32_t envelope_p;      /* polynomial envelope exponent */
   int32_t radial_hidden[3];
   int32_t readout_hidden;  /* hidden width of the last readout MLP */
-  int32_t hidden_lmax;     /* lmax of hidden features leaving non-last layers */
+  int32_t hidden_lmax[MACE_MAX_LAYERS];  /* [t]: lmax of the features leaving layer t, for
+                                            t < n_layers - 1; later entries are ignored */
   double r_cut;            /* cutoff radius (A) */
   double c_norm;           /* neighbour-sum normalisation constant */
 } mace_model_desc;

@@ -72,7 +72,7 @@ DT = torch.float64
 class ModelDesc:
     n_species: int
     K: int
-    hidden_lmax: int            # lmax of the hidden irreps leaving non-last layers
+    hidden_lmax: int | tuple    # lmax of the hidden irreps leaving non-last layers (one, or one per layer)
     r_cut: float
     c_norm: float
     n_layers: int = 2
@@ -84,12 +84,17 @@ class ModelDesc:
     readout_hidden: int = 16
 
 
+def hidden_lmax_of(d: ModelDesc, t: int) -> int:
+    """lmax of the hidden irreps leaving layer t (t < n_layers - 1)."""
+    return d.hidden_lmax if isinstance(d.hidden_lmax, int) else int(d.hidden_lmax[t])
+
+
 def layer_in_ls(d: ModelDesc, t: int):
-    return [0] if t == 0 else list(range(d.hidden_lmax + 1))
+    return [0] if t == 0 else list(range(hidden_lmax_of(d, t - 1) + 1))
 
 
 def layer_out_ls(d: ModelDesc, t: int):
-    return [0] if t == d.n_layers - 1 else list(range(d.hidden_lmax + 1))
+    return [0] if t == d.n_layers - 1 else list(range(hidden_lmax_of(d, t) + 1))
 
 
 def tp_paths(d: ModelDesc, t: int):

@@ -29,6 +29,7 @@ MACE_BLOCK_EDGE_PRODUCT = 0
 MACE_BLOCK_SYMMETRIC_CONTRACTION = 1
 MACE_BLOCK_RADIAL_MLP = 2
 MACE_NEIGHBOR_SCRATCH_BYTES = 80 << 20
+MAX_LAYERS = 8   # MACE_MAX_LAYERS
 STATUS = {0: "MACE_OK", -1: "MACE_EINVAL", -2: "MACE_ERANGE", -3: "MACE_ENOSPACE", -4: "MACE_EHIP",
           -5: "MACE_ENONFINITE", -6: "MACE_ESTATE", -7: "MACE_EUNSUPPORTED"}
 
@@ -51,7 +52,7 @@ class mace_model_desc(ctypes.Structure):
     _fields_ = [("n_species", ctypes.c_int32), ("K", ctypes.c_int32), ("n_layers", ctypes.c_int32),
                 ("sh_lmax", ctypes.c_int32), ("correlation", ctypes.c_int32), ("n_bessel", ctypes.c_int32),
                 ("envelope_p", ctypes.c_int32), ("radial_hidden", ctypes.c_int32 * 3),
-                ("readout_hidden", ctypes.c_int32), ("hidden_lmax", ctypes.c_int32),
+                ("readout_hidden", ctypes.c_int32), ("hidden_lmax", ctypes.c_int32 * MAX_LAYERS),
                 ("r_cut", ctypes.c_double), ("c_norm", ctypes.c_double)]
 
 
@@ -61,7 +62,12 @@ def make_desc(n_species, K, hidden_lmax, r_cut, c_norm, n_layers=2, sh_lmax=3, c
     d.n_species, d.K, d.n_layers = n_species, K, n_layers
     d.sh_lmax, d.correlation, d.n_bessel, d.envelope_p = sh_lmax, correlation, n_bessel, envelope_p
     d.radial_hidden[:] = list(radial_hidden)
-    d.readout_hidden, d.hidden_lmax = readout_hidden, hidden_lmax
+    d.readout_hidden = readout_hidden
+    # one l_max for every non-last layer, or one per layer
+    hl = [hidden_lmax] * (n_layers - 1) if isinstance(hidden_lmax, (int, np.integer)) else list(hidden_lmax)
+    if len(hl) < n_layers - 1 or n_layers > MAX_LAYERS:
+        raise ValueError("hidden_lmax needs an entry per non-last layer, at most MACE_MAX_LAYERS layers")
+    d.hidden_lmax[:] = (hl + [0] * MAX_LAYERS)[:MAX_LAYERS]
     d.r_cut, d.c_norm = float(r_cut), float(c_norm)
     return d
 

@@ -68,14 +68,22 @@ int n_eta(int nu, int L) {
 mace_status build_model(const mace_model_desc* desc, Model& m) {
   if (!desc) return MACE_EINVAL;
   const mace_model_desc& d = *desc;
-  if (d.n_species < 1 || d.n_layers < 1 || !(d.r_cut > 0) || !(d.c_norm > 0) || d.envelope_p < 1)
+  if (d.n_species < 1 || d.n_layers < 1 || d.n_layers > MACE_MAX_LAYERS || !(d.r_cut > 0) || !(d.c_norm > 0) ||
+      d.envelope_p < 1)
     return MACE_EINVAL;
   if (d.sh_lmax != 3 || d.correlation != 3 || d.n_bessel < 1 || d.n_bessel > 16 || d.radial_hidden[0] != 64 ||
       d.radial_hidden[1] != 64 || d.radial_hidden[2] != 64 || d.readout_hidden < 1 || d.readout_hidden > 16 ||
-      d.hidden_lmax < 0 || d.hidden_lmax > 2 || !(d.K == 32 || d.K == 64 || d.K == 96 || d.K == 128))
+      !(d.K == 32 || d.K == 64 || d.K == 96 || d.K == 128))
     return MACE_EUNSUPPORTED;
+  // per layer 0..2, non-increasing: every output irrep of a layer after the
+  // first is also an input irrep, so the residual species linear covers it
+  for (int t = 0; t + 1 < d.n_layers; ++t)
+    if (d.hidden_lmax[t] < 0 || d.hidden_lmax[t] > 2 || (t > 0 && d.hidden_lmax[t] > d.hidden_lmax[t - 1]))
+      return MACE_EUNSUPPORTED;
   m.d = d;
-  m.dh = (d.hidden_lmax + 1) * (d.hidden_lmax + 1);
+  // the largest hidden feature width (components per channel) between layers
+  m.dh = 1;
+  for (int t = 0; t + 1 < d.n_layers; ++t) m.dh = std::max(m.dh, (d.hidden_lmax[t] + 1) * (d.hidden_lmax[t] + 1));
   const int64_t S = d.n_species, K = d.K;
   int64_t o = 0;
   auto add = [&](const std::string& name, std::vector<int64_t> shape, int64_t fan) {
@@ -90,9 +98,9 @@ mace_status build_model(const mace_model_desc* desc, Model& m) {
     L.t = t;
     L.last = (t == d.n_layers - 1);
     if (t == 0) L.in_ls = {0};
-    else for (int l = 0; l <= d.hidden_lmax; ++l) L.in_ls.push_back(l);
+    else for (int l = 0; l <= d.hidden_lmax[t - 1]; ++l) L.in_ls.push_back(l);
     if (L.last) L.out_ls = {0};
-    else for (int l = 0; l <= d.hidden_lmax; ++l) L.out_ls.push_back(l);
+    else for (int l = 0; l <= d.hidden_lmax[t]; ++l) L.out_ls.push_back(l);
     L.lh_max = L.in_ls.back();
     L.lout_max = L.out_ls.back();
     L.paths = so3h::tp_paths(L.lh_max, d.sh_lmax);

@@ -19,10 +19,11 @@ def _paths(lh_max, sh_lmax=3):
 def layer_shapes(params: dict) -> dict:
     T = params.get("n_layers", 2)
     hl = params["hidden_lmax"]
+    hl = [hl] * max(T - 1, 0) if isinstance(hl, int) else list(hl)
     layers = []
     for t in range(T):
-        lh = 0 if t == 0 else hl
-        lo = 0 if t == T - 1 else hl
+        lh = 0 if t == 0 else hl[t - 1]
+        lo = 0 if t == T - 1 else hl[t]
         paths = _paths(lh)
         nnz = sum(int((B.mace_debug_real_cg(*p) != 0).sum()) for p in paths)
         layers.append(dict(P=len(paths), mid=sum(2 * p[2] + 1 for p in paths), din=(lh + 1) ** 2,

@@ -59,6 +59,13 @@ def test_small_water_hidden_l_fp64(K, hl):
            label=f"water102 K={K} l={hl}", stress=True)
 
 
+def test_per_layer_hidden_l_fp64():
+    """Three layers with hidden l_max 2 then 1 (one per layer)."""
+    params = model_params(0, K=32, n_layers=3, hidden_lmax=(2, 1), **STRESS)
+    _check(params, synth.water_box(34, seed=7, box=10.0), seed=3, gains=STRESS_GAINS,
+           label="water102 K=32 l=(2, 1)", stress=True)
+
+
 def test_molecule_batch_fp64():
     params = model_params(4, K=32, **STRESS)
     sysm = synth.molecule_batch(6, seed=5)

@@ -105,6 +105,21 @@ def test_bf16_linear_vs_fp64_and_fp32():
     assert err["energy"] < 5e-3
 
 
+@pytest.mark.parametrize("hl", [(2, 1), (2, 0), (1, 1, 0)])
+def test_per_layer_hidden_lmax_fp32(hl):
+    """One hidden l_max per layer: the edge product of each layer runs at its
+    own l_h (2 then 1, 2 then 0, ...), with the residual species linear on the
+    irreps a layer shares with its input."""
+    params = model_params(0, K=32, n_layers=len(hl) + 1, hidden_lmax=hl, **STRESS)
+    bo = oracle_blob(params, 4, STRESS_GAINS)
+    bl = lib_blob(params, 4, STRESS_GAINS)
+    assert np.array_equal(bo, bl)
+    sysm = synth.water_box(34, seed=7, box=10.0)
+    ref = run_oracle(params, sysm, bo)
+    gpu = run_gpu(params, sysm, bl)
+    assert_parity(gpu, ref, B.MACE_FP32, f"hidden l_max per layer {hl}")
+
+
 def test_isolated_atoms_and_empty_neighbourhoods():
     """Atoms with no neighbour (and a graph with no edge at all) get the
     species-only energy and zero force."""

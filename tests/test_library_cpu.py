@@ -53,6 +53,27 @@ def test_weight_layout_matches_oracle(cfg):
     assert tot == sum(n for _, n, _ in lay_o)
 
 
+@pytest.mark.parametrize("layers,hl", [(3, (2, 1)), (4, (2, 2, 0)), (3, (1, 1))])
+def test_weight_layout_per_layer_lmax_matches_oracle(layers, hl):
+    """One hidden l_max per layer (non-increasing) in the descriptor."""
+    od, ld = _desc_pair(0, K=32, n_layers=layers, hidden_lmax=hl)
+    lay_o = [(name, int(np.prod(s)), f) for name, s, f in mace.weight_layout(od)]
+    lay_l, tot = B.mace_weight_layout(ld)
+    assert lay_l == lay_o
+    assert tot == sum(n for _, n, _ in lay_o)
+
+
+def test_per_layer_lmax_refused_when_rising_or_too_many_layers():
+    with pytest.raises(B.MaceError) as e:
+        B.mace_weight_layout(B.make_desc(**model_params(0, K=32, n_layers=3, hidden_lmax=(1, 2))))
+    assert e.value.code == -7   # MACE_EUNSUPPORTED: a layer's output l not among its inputs
+    with pytest.raises(B.MaceError) as e:
+        B.mace_weight_layout(B.make_desc(**model_params(0, K=32, n_layers=3, hidden_lmax=(3, 1))))
+    assert e.value.code == -7
+    with pytest.raises(ValueError):
+        B.make_desc(**model_params(0, K=32, n_layers=9, hidden_lmax=1))
+
+
 def test_weight_blob_identical_from_both_layouts():
     od, ld = _desc_pair(1)
     blob_o = synth.weight_blob(mace.weight_layout(od), 5, {".radial.3": 4.0})
