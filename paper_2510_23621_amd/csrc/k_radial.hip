@@ -329,7 +329,6 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) r
 #pragma unroll
       for (int q = 0; q < NPART; ++q) v += *reinterpret_cast<const f4*>(da3p + ((size_t)q * E + e) * kH + 4 * c4);
       pacc[sr] = e0 + row < E ? v : f4{0.f, 0.f, 0.f, 0.f};
-      __builtin_amdgcn_sched_barrier(0);   // one row's loads in flight at a time
     }
     {
       const int e = e0 + (tid >> 2), c4 = tid & 3;
