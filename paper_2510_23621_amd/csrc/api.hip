@@ -397,12 +397,12 @@ bool l0_auto(const Model& m, int64_t N, int64_t E) {
 
 // The edge products of layer t run their last radial layer on split-BF16
 // operands, and both read a3 as the three parts the prologue writes (radial
-// mode 3; l_h = 1 only, the edge-lane backward), or split it per tile (2).
+// mode 3; the edge-lane backwards, l_h = 1 and 2), or split it per tile (2).
 bool layer_factorised(const mace_graph* h, int t) {
   return t == 0 && h->l0_fact && !h->tp_round && !h->rad_round;
 }
 bool a3_presplit(const mace_graph* h, int t) {
-  return h->radial_split && h->prec != MACE_BF16_RADIAL && h->m.layers[t].lh_max == 1 && !layer_factorised(h, t);
+  return h->radial_split && h->prec != MACE_BF16_RADIAL && h->m.layers[t].lh_max >= 1 && !layer_factorised(h, t);
 }
 int radial_mode(const mace_graph* h, int t) {
   return h->prec == MACE_BF16_RADIAL ? 1 : (!h->radial_split ? 0 : (a3_presplit(h, t) ? 3 : 2));

@@ -1176,10 +1176,21 @@ __device__ __forceinline__ void el_load_a3(f4* a, int e, int g, const float* __r
     a[v] = *reinterpret_cast<const f4*>(a3 + (size_t)e * 64 + 32 * (v >> 1) + 8 * g + 4 * (v & 1));
 }
 
+// the lane's a3 operands of the split R product from the pre-split rows
+// ([E][3][64] bfloat16): x[ks][q] = part q of a3[e][32 ks + 8 g .. +7]
+__device__ __forceinline__ void el_load_a3_parts(us8v (&x)[2][3], int e, int g, const unsigned short* __restrict__ a3x) {
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int q = 0; q < 3; ++q) x[ks][q] = *reinterpret_cast<const us8v*>(a3x + (size_t)e * 192 + 64 * q + 32 * ks + 8 * g);
+}
+
 // NPROD: partial products per operand pair, 6 (split-BF16 operands,
 // FP32-accurate) or 1 (the BF16 radial mode: the operands' bfloat16 roundings,
-// which are the first split parts, with FP32 accumulation).
-template <int NW, bool RND, int NPROD>
+// which are the first split parts, with FP32 accumulation). PRE: a3 arrives as
+// its three parts (the a3 argument then points at [E][3][64] bfloat16 written
+// by the edge prologue), six products only.
+template <int NW, bool RND, int NPROD, bool PRE>
 __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
     int N, int K, int E, const int* __restrict__ rcv_off, const int* __restrict__ snd,
     const int* __restrict__ src_map, const float* __restrict__ a3, const float* __restrict__ W3,
@@ -1267,14 +1278,25 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
   bool prep = false;
   int e = 0, src = 0;   // src: without PIPE, the sender of the tile's edge
   f4 r[P], hv[DIN], y4[4];
-  f4 a[4];   // without PIPE, the a3 of the tile's edge
-  // R of the tile whose a3 is a0 .. a3 (edge on the lane), split-BF16 products
+  static_assert(!(PRE && PIPE), "pre-split a3 goes with six products");
+  f4 a[4];           // without PIPE, the a3 of the tile's edge
+  us8v apre[2][3];   // with PRE instead, its parts
+  const unsigned short* a3x = reinterpret_cast<const unsigned short*>(a3);
+  // R of the tile whose a3 is a0 .. a3 (with PRE: apre), edge on the lane,
+  // split-BF16 products
   auto r_standalone = [&](f4 av0, f4 av1, f4 av2, f4 av3) {
 #pragma unroll
     for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
     us8v x[2][3];
-    split3_x8(av0, av1, x[0][0], x[0][1], x[0][2]);
-    split3_x8(av2, av3, x[1][0], x[1][1], x[1][2]);
+    if constexpr (PRE) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int q = 0; q < 3; ++q) x[ks][q] = apre[ks][q];
+    } else {
+      split3_x8(av0, av1, x[0][0], x[0][1], x[0][2]);
+      split3_x8(av2, av3, x[1][0], x[1][1], x[1][2]);
+    }
     us8v ring[kRingR][3];
 #pragma unroll
     for (int f = 0; f < kRingR; ++f) wr_at(f, ring[f]);
@@ -1370,7 +1392,8 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
         __builtin_amdgcn_s_setprio(0);
       } else {
         src = s0;
-        el_load_a3(a, e, g, a3);
+        if constexpr (PRE) el_load_a3_parts(apre, e, g, a3x);
+        else el_load_a3(a, e, g, a3);
       }
     }
     for (int e0 = e_beg; e0 < e_end; e0 += 16) {
@@ -1570,7 +1593,8 @@ __device__ __forceinline__ void tpr_bwd_l2_edge_lanes_body(
           e = min(e0 + 16 + kk, e_end - 1);
           src = snd[e];
           if (src_map) src = src_map[src];
-          el_load_a3(a, e, g, a3);
+          if constexpr (PRE) el_load_a3_parts(apre, e, g, a3x);
+          else el_load_a3(a, e, g, a3);
         }
       }
       // the MFMAs the contraction could not take
@@ -1605,7 +1629,7 @@ tpr_bwd_kernel(
   if constexpr (tpr_bwd_edge_lanes<LHMAX, RM>())
     tpr_bwd_edge_lanes_body<LHMAX, NW, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
                                         rnd);
-  else if constexpr (LHMAX == 2 && (RM == 2 || RM == 1)) {
+  else if constexpr (LHMAX == 2 && RM >= 1) {
     // W3's slice (one layout for both products) and a G table per wave; the
     // precision study's operand rounding runs as its own instance (a uniform
     // branch, taken once)
@@ -1613,11 +1637,11 @@ tpr_bwd_kernel(
     __shared__ __align__(16) float sG[NW * PairCount<2>::value * 16];
     constexpr int NPROD = RM == 1 ? 1 : 6;
     if (rnd)
-      tpr_bwd_l2_edge_lanes_body<NW, true, NPROD>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q,
-                                                  da3p, rnd, sW, sG);
+      tpr_bwd_l2_edge_lanes_body<NW, true, NPROD, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt,
+                                                           dYp, Q, da3p, rnd, sW, sG);
     else
-      tpr_bwd_l2_edge_lanes_body<NW, false, NPROD>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q,
-                                                   da3p, 0, sW, sG);
+      tpr_bwd_l2_edge_lanes_body<NW, false, NPROD, RM == 3>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt,
+                                                            dYp, Q, da3p, 0, sW, sG);
   }
   else
     tpr_bwd_channel_lanes<LHMAX, RM, NW>(N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p,
@@ -1656,11 +1680,11 @@ void tpr_bwd_launch(hipStream_t s, int N, int K, int E, const int* rcv_off, cons
 }  // namespace
 
 // Instances built: every l_h <= 2 with radial mode 0 (FP32), 1 (BF16) or 2
-// (split BF16), and mode 3 (split BF16 with pre-split a3) at l_h = 1. The
-// l_h = 2 backward in modes 1 and 2 (the edge-lane form) needs Q.
+// (split BF16), and mode 3 (split BF16 with pre-split a3) at l_h = 1 and 2.
+// The l_h = 2 backward in modes 1 to 3 (the edge-lane form) needs Q.
 bool tpr_supported(int lh_max, int radial_mode) {
   if (lh_max < 0 || lh_max > 2 || radial_mode < 0 || radial_mode > 3) return false;
-  return radial_mode != 3 || lh_max == 1;
+  return radial_mode != 3 || lh_max >= 1;
 }
 
 bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off, const int* snd,
@@ -1684,6 +1708,7 @@ bool launch_tpr_fwd(hipStream_t s, int lh_max, int N, int K, const int* rcv_off,
     default:
       if (radial_mode == 1) MACE_TPRF(2, 1);
       else if (radial_mode == 2) MACE_TPRF(2, 2);
+      else if (radial_mode == 3) MACE_TPRF(2, 3);
       else MACE_TPRF(2, 0);
       break;
   }
@@ -1696,7 +1721,7 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
                     float inv_c, const float* dAt, float* dYp, float* Q, float* da3p, int radial_mode,
                     int tp_round) {
   if (!tpr_supported(lh_max, radial_mode)) return false;
-  if (lh_max == 2 && (radial_mode == 2 || radial_mode == 1) && !Q) return false;
+  if (lh_max == 2 && radial_mode >= 1 && !Q) return false;
   if (N <= 0 || E <= 0) return true;
 #define MACE_TPRB(LH, RM) \
   tpr_bwd_launch<LH, RM>(s, N, K, E, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, dAt, dYp, Q, da3p, tp_round)
@@ -1715,6 +1740,7 @@ bool launch_tpr_bwd(hipStream_t s, int lh_max, int N, int K, int E, const int* r
     default:
       if (radial_mode == 1) MACE_TPRB(2, 1);
       else if (radial_mode == 2) MACE_TPRB(2, 2);
+      else if (radial_mode == 3) MACE_TPRB(2, 3);
       else MACE_TPRB(2, 0);
       break;
   }
