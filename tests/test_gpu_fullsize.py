@@ -102,9 +102,13 @@ def test_cfg1_full_stress_inputs_fp32():
 
 # ------------------------------------------------------------------ larger periodic boxes, every atom
 
-@pytest.mark.parametrize("prec", [B.MACE_FP32, B.MACE_BF16_LINEAR])
+@pytest.mark.parametrize("prec", [B.MACE_FP32, B.MACE_BF16_LINEAR, B.MACE_FP16_LINEAR, B.MACE_BF16_RADIAL])
 @pytest.mark.parametrize("name", ["water4608_k128_l1", "water36864_k128_l2"])
 def test_large_water_every_atom_vs_fp64(name, prec):
+    """Every atom against the stored FP64 reference, in every precision mode
+    (at 36,864 atoms the waves of the l_h = 2 backward walk about 36
+    receivers each: in the BF16-radial mode with the next tile's R product
+    pipelined across them)."""
     params, sysm, blob, ref = _stored_ref(name)
     gpu = run_gpu(params, sysm, blob, prec=prec)
     print(f"[fullsize] {name}: {gpu['n_edges']} edges", flush=True)
