@@ -228,13 +228,10 @@ __device__ __forceinline__ void load_w3_slice_x3(const float* __restrict__ W3, i
   }
 }
 
-// As tile_radial, FP32-accurate on split BF16 operands. The K steps are the
-// outer loop, so that only one step's A parts are live; within each step the
-// terms are added from the smallest to the largest.
-// PRE: a3 points at the pre-split parts ([E][3][64] bfloat16) instead.
+// tile_radial_x3 below l = 2 (described there)
 template <int P, bool PRE = false, bool TRP = false>
-__device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int e0, int e_end,
-                                               const unsigned short* __restrict__ sWx, f4* r) {
+__device__ __forceinline__ void tile_radial_x3_chain(const float* __restrict__ a3, int e0, int e_end,
+                                                     const unsigned short* __restrict__ sWx, f4* r) {
   constexpr int part = P * 16 * kWbPitch;
   const int l = threadIdx.x & 63;
   const int row = e0 + tile_edge<TRP>(l & 15);
@@ -271,6 +268,85 @@ __device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int
       r[p] = mfma_bf16(a0, b0, acc);
     }
   }
+  __builtin_amdgcn_s_setprio(0);
+}
+
+// As tile_radial, FP32-accurate on split BF16 operands: within each K step the
+// terms are added from the smallest to the largest.
+// PRE: a3 points at the pre-split parts ([E][3][64] bfloat16) instead.
+// Below l = 2 (P <= 10, four waves per SIMD at 128 registers) one path's chain
+// of six products at a time, only one K step's A parts live; at l = 2 (P = 17,
+// two waves per SIMD) both K steps' A parts are loaded first and the paths go
+// in pairs (below).
+template <int P, bool PRE = false, bool TRP = false>
+__device__ __forceinline__ void tile_radial_x3(const float* __restrict__ a3, int e0, int e_end,
+                                               const unsigned short* __restrict__ sWx, f4* r) {
+  if constexpr (P <= 10) {
+    tile_radial_x3_chain<P, PRE, TRP>(a3, e0, e_end, sWx, r);
+    return;
+  }
+  constexpr int part = P * 16 * kWbPitch;
+  const int l = threadIdx.x & 63;
+  const int row = e0 + tile_edge<TRP>(l & 15);
+  const float keep = row < e_end ? 1.f : 0.f;
+  const int crow = min(row, e_end - 1);
+  const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)crow * 64 + 8 * (l >> 4));
+  const unsigned short* wb = sWx + (l & 15) * kWbPitch + 8 * (l >> 4);
+#pragma unroll
+  for (int p = 0; p < P; ++p) r[p] = f4{0.f, 0.f, 0.f, 0.f};
+  __builtin_amdgcn_s_setprio(1);
+  us8v a[2][3];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    if constexpr (PRE) {
+      load_a3_parts(reinterpret_cast<const unsigned short*>(a3), crow, row < e_end, ks, a[ks][0], a[ks][1], a[ks][2]);
+    } else {
+      const f4 lo = arow[8 * ks] * keep, hi = arow[8 * ks + 1] * keep;
+      split3_x8(lo, hi, a[ks][0], a[ks][1], a[ks][2]);
+    }
+  }
+  // Steps s = ks P + p taken in pairs: the next pair's W3 parts are requested
+  // before this pair's MFMAs, and the two paths' six-product chains alternate
+  // so that neither waits on its own previous product. Each path's products
+  // are added in the same order as in a single chain.
+  constexpr int NS = 2 * P;   // even: the pairs are (2t, 2t + 1), t < P
+  us8v bb[2][2][3];
+  auto load_b = [&](int s, us8v (&b)[3]) {
+    const int ks = s / P, p = s % P;
+    const unsigned short* q = wb + p * 16 * kWbPitch + 32 * ks;
+    b[0] = *reinterpret_cast<const us8v*>(q);
+    b[1] = *reinterpret_cast<const us8v*>(q + part);
+    b[2] = *reinterpret_cast<const us8v*>(q + 2 * part);
+  };
+  load_b(0, bb[0][0]);
+  load_b(1, bb[0][1]);
+  static_for<0, P>([&](auto TI) {
+    constexpr int t = decltype(TI)::value;
+    constexpr int s0 = 2 * t, s1 = 2 * t + 1;
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (s1 + 2 < NS) {
+      load_b(s0 + 2, bb[(t + 1) & 1][0]);
+      load_b(s1 + 2, bb[(t + 1) & 1][1]);
+    }
+    constexpr int ks0 = s0 / P, p0 = s0 % P, ks1 = s1 / P, p1 = s1 % P;
+    const us8v(&b0)[3] = bb[t & 1][0];
+    const us8v(&b1)[3] = bb[t & 1][1];
+    f4 x = r[p0], y = r[p1];
+    x = mfma_bf16(a[ks0][2], b0[0], x);
+    y = mfma_bf16(a[ks1][2], b1[0], y);
+    x = mfma_bf16(a[ks0][1], b0[1], x);
+    y = mfma_bf16(a[ks1][1], b1[1], y);
+    x = mfma_bf16(a[ks0][0], b0[2], x);
+    y = mfma_bf16(a[ks1][0], b1[2], y);
+    x = mfma_bf16(a[ks0][1], b0[0], x);
+    y = mfma_bf16(a[ks1][1], b1[0], y);
+    x = mfma_bf16(a[ks0][0], b0[1], x);
+    y = mfma_bf16(a[ks1][0], b1[1], y);
+    x = mfma_bf16(a[ks0][0], b0[0], x);
+    y = mfma_bf16(a[ks1][0], b1[0], y);
+    r[p0] = x;
+    r[p1] = y;
+  });
   __builtin_amdgcn_s_setprio(0);
 }
 
