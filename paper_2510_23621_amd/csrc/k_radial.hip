@@ -189,6 +189,68 @@ __device__ __forceinline__ void hidden_mma_x3(const float* __restrict__ in, int 
   }
 }
 
+// ---- prologue layers with the operands' roles swapped: A = the weights'
+// column fragment of the wave's 16 columns, B = the activations of 16 edges,
+// so that result register r of lane l holds column 16w + 4(l/16) + r of edge
+// 16 rt + l%16 (four consecutive columns of one edge per lane). Each layer's
+// output is split into its three bfloat16 parts once, by the wave that
+// produced it, into part planes in LDS (row = edge, pitch kPP), which every
+// wave of the next layer reads as its B operand.
+constexpr int kPP = kH + 8;          // 72 bfloat16 per plane row (36 dwords, 4 mod 32)
+constexpr int kPlane = kTE * kPP;    // elements per part plane
+
+// silu(z) of the wave's columns, as three part planes
+__device__ __forceinline__ void store_parts_t(const f4* z, unsigned short* __restrict__ P) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) {
+    unsigned p0[2], p1[2], p2[2];
+    split3_pair(f2v{silu(z[rt][0]), silu(z[rt][1])}, p0[0], p1[0], p2[0]);
+    split3_pair(f2v{silu(z[rt][2]), silu(z[rt][3])}, p0[1], p1[1], p2[1]);
+    unsigned short* d = P + (16 * rt + (l & 15)) * kPP + 16 * w + 4 * (l >> 4);
+    *reinterpret_cast<uint2*>(d) = make_uint2(p0[0], p0[1]);
+    *reinterpret_cast<uint2*>(d + kPlane) = make_uint2(p1[0], p1[1]);
+    *reinterpret_cast<uint2*>(d + 2 * kPlane) = make_uint2(p2[0], p2[1]);
+  }
+}
+
+// the narrow input layer on FP32 MFMA, operands swapped: z = (x W0) of the
+// wave's columns for the tile's 64 edges (x: LDS rows of stride kXPad)
+template <int NIN_PAD>
+__device__ __forceinline__ void input_mma_t(const float* __restrict__ xs, const float* b, f4* z) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) z[rt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < NIN_PAD / 4; ++ks)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) z[rt] = mfma4(b[ks], xs[(16 * rt + (l & 15)) * kXPad + 4 * ks + (l >> 4)], z[rt]);
+}
+
+// a 64-input layer on split-BF16 products from part planes, operands swapped;
+// the six partial products of each K step in the order of mma64_x3
+__device__ __forceinline__ void mma64_x3t(const unsigned short* __restrict__ P, const us8v (&b)[2][3], f4* z) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) z[rt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const unsigned short* ar = P + (16 * rt + (l & 15)) * kPP + 32 * ks + 8 * (l >> 4);
+      const us8v a0 = *reinterpret_cast<const us8v*>(ar);
+      const us8v a1 = *reinterpret_cast<const us8v*>(ar + kPlane);
+      const us8v a2 = *reinterpret_cast<const us8v*>(ar + 2 * kPlane);
+      f4 c = z[rt];
+      c = mfma_b16(b[ks][0], a2, c);
+      c = mfma_b16(b[ks][1], a1, c);
+      c = mfma_b16(b[ks][2], a0, c);
+      c = mfma_b16(b[ks][0], a1, c);
+      c = mfma_b16(b[ks][1], a0, c);
+      z[rt] = mfma_b16(b[ks][0], a0, c);
+    }
+}
+
 template <bool RND = false>
 __device__ __forceinline__ void load_basis_tile(int E, int e0, const float* __restrict__ rbf, int nb, int nb_pad,
                                                 float* xs, int rnd = 0) {
@@ -212,8 +274,12 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
                                                             int nb, float* __restrict__ Y, float* __restrict__ rbf,
                                                             RadialSet rs, int* __restrict__ status) {
   __shared__ float xs[kTE * kXPad];
-  __shared__ float ha[kTE * kPad];
-  __shared__ float hb[kTE * kPad];
+  // RND: the FP32 activations ha, hb; otherwise the three part planes
+  __shared__ __align__(16) float hbuf[2 * kTE * kPad];
+  static_assert(3 * kPlane * sizeof(unsigned short) <= sizeof(hbuf), "part planes fit the activation buffers");
+  float* ha = hbuf;
+  float* hb = hbuf + kTE * kPad;
+  unsigned short* P = reinterpret_cast<unsigned short*>(hbuf);
   const int e0 = blockIdx.x * kTE;
   // B fragments: bc for the layer being computed, bn for the next one (in
   // flight meanwhile); the first is requested before the geometry
@@ -251,40 +317,70 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
       __syncthreads();
       if (t + 1 < rs.n) load_b_frag<NBP, RND>(rs.W[t + 1], nb, bn, rs.rnd);
       hidden_mma<kH, true, RND>(hb, kPad, bc, ha, z, rs.rnd);
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
+      float* a3 = rs.a3[t];
+      unsigned short* a3x = rs.a3x[t];
+      for (int idx = threadIdx.x; idx < kTE * kH / 4; idx += blockDim.x) {
+        const int e = idx >> 4, c4 = idx & 15;
+        if (e0 + e >= E) continue;
+        const f4 v = *reinterpret_cast<const f4*>(ha + e * kPad + 4 * c4);
+        if (a3x) {   // the three bfloat16 parts, [E][3][64]
+          unsigned p0[2], p1[2], p2[2];
+          split3_pair(f2v{v[0], v[1]}, p0[0], p1[0], p2[0]);
+          split3_pair(f2v{v[2], v[3]}, p0[1], p1[1], p2[1]);
+          unsigned short* row = a3x + (size_t)(e0 + e) * 3 * kH + 4 * c4;
+          *reinterpret_cast<uint2*>(row) = make_uint2(p0[0], p0[1]);
+          *reinterpret_cast<uint2*>(row + kH) = make_uint2(p1[0], p1[1]);
+          *reinterpret_cast<uint2*>(row + 2 * kH) = make_uint2(p2[0], p2[1]);
+        } else {
+          *reinterpret_cast<f4*>(a3 + (size_t)(e0 + e) * kH + 4 * c4) = v;
+        }
+      }
+      __syncthreads();   // ha is rewritten by the next layer's MLP
     } else {
-      // the 64-wide layers on split-BF16 products, the next layer's parts in flight meanwhile
+      // the 64-wide layers on split-BF16 products from part planes split once
+      // by their producer, the next layer's weight parts in flight meanwhile
       us8v b1[2][3], b2[2][3];
       load_b_parts64<false>(W1, b1);
-      hidden_mma<NBP, true, false>(xs, kXPad, bc, ha, z);
+      input_mma_t<NBP>(xs, bc, z);
+      __syncthreads();   // the previous interaction layer's reads of the planes are done
+      store_parts_t(z, P);
       __syncthreads();
       load_b_parts64<false>(W2, b2);
-      hidden_mma_x3<true>(ha, kPad, b1, hb, z);
+      mma64_x3t(P, b1, z);
+      __syncthreads();   // every wave has read the planes
+      store_parts_t(z, P);
       __syncthreads();
       if (t + 1 < rs.n) load_b_frag<NBP, false>(rs.W[t + 1], nb, bn);
-      hidden_mma_x3<true>(hb, kPad, b2, ha, z);
-    }
-    __syncthreads();
+      mma64_x3t(P, b2, z);
 #pragma unroll
-    for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
-    float* a3 = rs.a3[t];
-    unsigned short* a3x = rs.a3x[t];
-    for (int idx = threadIdx.x; idx < kTE * kH / 4; idx += blockDim.x) {
-      const int e = idx >> 4, c4 = idx & 15;
-      if (e0 + e >= E) continue;
-      const f4 v = *reinterpret_cast<const f4*>(ha + e * kPad + 4 * c4);
-      if (a3x) {   // the three bfloat16 parts, [E][3][64]
-        unsigned p0[2], p1[2], p2[2];
-        split3_pair(f2v{v[0], v[1]}, p0[0], p1[0], p2[0]);
-        split3_pair(f2v{v[2], v[3]}, p0[1], p1[1], p2[1]);
-        unsigned short* row = a3x + (size_t)(e0 + e) * 3 * kH + 4 * c4;
-        *reinterpret_cast<uint2*>(row) = make_uint2(p0[0], p0[1]);
-        *reinterpret_cast<uint2*>(row + kH) = make_uint2(p1[0], p1[1]);
-        *reinterpret_cast<uint2*>(row + 2 * kH) = make_uint2(p2[0], p2[1]);
-      } else {
-        *reinterpret_cast<f4*>(a3 + (size_t)(e0 + e) * kH + 4 * c4) = v;
+      for (int ks = 0; ks < NBP / 4; ++ks) bc[ks] = bn[ks];
+      // a3 = silu(z): four consecutive columns of one edge per lane, straight
+      // to memory (FP32, or the three bfloat16 parts [E][3][64])
+      const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+      const int c0 = 16 * w + 4 * (l >> 4);
+      float* a3 = rs.a3[t];
+      unsigned short* a3x = rs.a3x[t];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        const int e = e0 + 16 * rt + (l & 15);
+        if (e >= E) continue;
+        const f4 v = {silu(z[rt][0]), silu(z[rt][1]), silu(z[rt][2]), silu(z[rt][3])};
+        if (a3x) {
+          unsigned p0[2], p1[2], p2[2];
+          split3_pair(f2v{v[0], v[1]}, p0[0], p1[0], p2[0]);
+          split3_pair(f2v{v[2], v[3]}, p0[1], p1[1], p2[1]);
+          unsigned short* row = a3x + (size_t)e * 3 * kH + c0;
+          *reinterpret_cast<uint2*>(row) = make_uint2(p0[0], p0[1]);
+          *reinterpret_cast<uint2*>(row + kH) = make_uint2(p1[0], p1[1]);
+          *reinterpret_cast<uint2*>(row + 2 * kH) = make_uint2(p2[0], p2[1]);
+        } else {
+          *reinterpret_cast<f4*>(a3 + (size_t)e * kH + c0) = v;
+        }
       }
     }
-    __syncthreads();   // ha is rewritten by the next layer's MLP
   }
 }
 
