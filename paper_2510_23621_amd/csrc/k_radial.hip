@@ -8,14 +8,19 @@
 // edge); the wide last layer is computed inside the tensor-product kernels,
 // which also hand back dE/da3 as per-channel-tile partials. A block owns a
 // 64-edge tile (4 row tiles of 16) and has 4 waves, wave w the 16 columns
-// 16w .. 16w + 15 of a layer; result register r of lane l holds
-// D[4*(l/16)+r][l%16]. The 64-wide layers (and their transposed products in
-// the backward pass) run as FP32-accurate products on the bfloat16 MFMA pipe
-// (v_mfma_f32_16x16x32_bf16; each FP32 operand carried as three bfloat16
-// parts, six partial products, as in the edge product): lane l supplies
-// A[l%16][8(l/16) + i] and B[8(l/16) + i][l%16], i = 0..7. The narrow input
-// layer (nb <= 16 inputs) and the precision study's rounded instances run on
-// FP32 MFMA (v_mfma_f32_16x16x4_f32, A[l%16][l/16], B[l/16][l%16]).
+// 16w .. 16w + 15 of a layer. The 64-wide layers (and their transposed
+// products in the backward pass) run as FP32-accurate products on the
+// bfloat16 MFMA pipe (v_mfma_f32_16x16x32_bf16; each FP32 operand carried as
+// three bfloat16 parts, six partial products, as in the edge product): lane l
+// supplies A[l%16][8(l/16) + i] and B[8(l/16) + i][l%16], i = 0..7, and result
+// register r holds D[4(l/16) + r][l%16]. The weights are the A operand and
+// the activations of 16 edges the B operand, so that a lane's results are four
+// consecutive columns of one edge, which it splits into parts once for the
+// next layer. The narrow input layer (nb <= 16 inputs) runs on FP32 MFMA
+// (v_mfma_f32_16x16x4_f32, A[l%16][l/16], B[l/16][l%16]), with the same
+// operand roles; the precision study's rounded instances run every layer on
+// FP32 MFMA with the activations as A (results: rows 4(l/16) + r of column
+// l%16).
 #include <type_traits>
 
 #include "mace_internal.h"
@@ -151,44 +156,6 @@ __device__ __forceinline__ void load_b_parts64(const float* __restrict__ W, us8v
   }
 }
 
-// acc[rt] = in[rows of tile rt][0..64) x B for the tile's 64 edges, FP32-accurate;
-// in: LDS rows of stride ldin (a multiple of 4)
-__device__ __forceinline__ void mma64_x3(const float* __restrict__ in, int ldin, const us8v (&b)[2][3], f4* acc) {
-  const int l = threadIdx.x & 63;
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-      const float* ar = in + (16 * rt + (l & 15)) * ldin + 32 * ks + 8 * (l >> 4);
-      us8v a0, a1, a2;
-      split8(*reinterpret_cast<const f4*>(ar), *reinterpret_cast<const f4*>(ar + 4), a0, a1, a2);
-      f4 c = acc[rt];
-      c = mfma_b16(a2, b[ks][0], c);
-      c = mfma_b16(a1, b[ks][1], c);
-      c = mfma_b16(a0, b[ks][2], c);
-      c = mfma_b16(a1, b[ks][0], c);
-      c = mfma_b16(a0, b[ks][1], c);
-      acc[rt] = mfma_b16(a0, b[ks][0], c);
-    }
-}
-
-// hidden_mma for a 64-input layer on split-BF16 products
-template <bool STORE>
-__device__ __forceinline__ void hidden_mma_x3(const float* __restrict__ in, int ldin, const us8v (&b)[2][3],
-                                              float* __restrict__ out, f4* z) {
-  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int col = 16 * w + (l & 15);
-  mma64_x3(in, ldin, b, z);
-  if constexpr (STORE) {
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) out[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = silu(z[rt][r]);
-  }
-}
-
 // ---- prologue layers with the operands' roles swapped: A = the weights'
 // column fragment of the wave's 16 columns, B = the activations of 16 edges,
 // so that result register r of lane l holds column 16w + 4(l/16) + r of edge
@@ -199,14 +166,16 @@ __device__ __forceinline__ void hidden_mma_x3(const float* __restrict__ in, int 
 constexpr int kPP = kH + 8;          // 72 bfloat16 per plane row (36 dwords, 4 mod 32)
 constexpr int kPlane = kTE * kPP;    // elements per part plane
 
-// silu(z) of the wave's columns, as three part planes
+// silu(z) (SILU) or z of the wave's columns, as three part planes
+template <bool SILU = true>
 __device__ __forceinline__ void store_parts_t(const f4* z, unsigned short* __restrict__ P) {
   const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  auto act = [](float x) { return SILU ? silu(x) : x; };
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) {
     unsigned p0[2], p1[2], p2[2];
-    split3_pair(f2v{silu(z[rt][0]), silu(z[rt][1])}, p0[0], p1[0], p2[0]);
-    split3_pair(f2v{silu(z[rt][2]), silu(z[rt][3])}, p0[1], p1[1], p2[1]);
+    split3_pair(f2v{act(z[rt][0]), act(z[rt][1])}, p0[0], p1[0], p2[0]);
+    split3_pair(f2v{act(z[rt][2]), act(z[rt][3])}, p0[1], p1[1], p2[1]);
     unsigned short* d = P + (16 * rt + (l & 15)) * kPP + 16 * w + 4 * (l >> 4);
     *reinterpret_cast<uint2*>(d) = make_uint2(p0[0], p0[1]);
     *reinterpret_cast<uint2*>(d + kPlane) = make_uint2(p1[0], p1[1]);
@@ -228,7 +197,8 @@ __device__ __forceinline__ void input_mma_t(const float* __restrict__ xs, const 
 }
 
 // a 64-input layer on split-BF16 products from part planes, operands swapped;
-// the six partial products of each K step in the order of mma64_x3
+// within each K step the six partial products go from the smallest to the
+// largest
 __device__ __forceinline__ void mma64_x3t(const unsigned short* __restrict__ P, const us8v (&b)[2][3], f4* z) {
   const int l = threadIdx.x & 63;
 #pragma unroll
@@ -386,22 +356,26 @@ __global__ void __launch_bounds__(256) edge_prologue_kernel(int E, const float* 
 
 // de = VJP of the hidden layers given dE/da3, which arrives as n_part partials
 // da3p[part][E][64] summed here in part order. The pre-activations z0, z1, z2
-// are recomputed from the radial basis (three FP32 MFMA layers per 64-edge
-// tile; cheaper than storing silu'(z) for every edge and reading it back), so
+// are recomputed from the radial basis (three MFMA layers per 64-edge tile;
+// cheaper than storing silu'(z) for every edge and reading it back), so
 // the pass is dz2 = da3 silu'(z2), dz1 = (dz2 W2^T) silu'(z1),
 // dz0 = (dz1 W1^T) silu'(z0), de = dz0 W0^T. The same pass folds the partials
 // dYp[part][E][16] of dE/dY into dY. With accumulate set, de and dY are added
 // to instead of overwritten.
 template <int NBP, int NPART, bool RND>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RND ? 2 : 3))) radial_bwd_kernel(int E, const float* __restrict__ rbf, int nb,
                                                          const float* __restrict__ W,
                                                          const float* __restrict__ da3p,
                                                          const float* __restrict__ dYp,
                                                          float* __restrict__ dY, float* __restrict__ de,
                                                          int accumulate, int rnd) {
   __shared__ float xs[kTE * kXPad];
-  __shared__ float ta[kTE * kPad];
-  __shared__ float tb[kTE * kPad];
+  // RND: the FP32 tiles ta, tb; otherwise three part planes and one FP32 tile
+  constexpr int kPlanesF = 3 * kPlane / 2;   // floats taken by the part planes
+  __shared__ __align__(16) float tbuf[kPlanesF + kTE * kPad];
+  static_assert(2 * kTE * kPad <= kPlanesF + kTE * kPad, "the FP32 tiles fit");
+  float* ta = tbuf;
+  float* tb = tbuf + kTE * kPad;
   const int e0 = blockIdx.x * kTE;
   const float* W0 = W;
   const float* W1 = W0 + nb * kH;
@@ -438,60 +412,112 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) r
     }
   };
   const bool parts_first = (blockIdx.x & 1) == 0;
-  if (parts_first) sum_partials();
-  // forward fragments, then the hidden layers again
-  float bc[kH / 4], bn[kH / 4];
-  load_b_frag<NBP, RND>(W0, nb, bc, rnd);
-  load_basis_tile<RND>(E, e0, rbf, nb, (nb + 3) & ~3, xs, rnd);
-  __syncthreads();
-  f4 z0[4], z1[4], z2[4];
-  us8v bp[2][3];   // split parts of the next 64-wide layer's B operand (not the rounded instance)
-  if constexpr (RND) load_b_frag<kH, RND>(W1, kH, bn, rnd);
-  else load_b_parts64<false>(W1, bp);
-  hidden_mma<NBP, true, RND>(xs, kXPad, bc, ta, z0, rnd);
-  __syncthreads();
-  if constexpr (RND) {
-    load_b_frag<kH, RND>(W2, kH, bc, rnd);
-    hidden_mma<kH, true, RND>(ta, kPad, bn, tb, z1, rnd);
-  } else {
-    hidden_mma_x3<true>(ta, kPad, bp, tb, z1);
+  if constexpr (!RND) {
+    // The layers with the operands' roles swapped (as in the edge prologue):
+    // every 64-wide product reads its activations as part planes split once
+    // by the wave that produced them; lane l holds columns c0 .. c0 + 3 of
+    // edge 16 rt + l%16 of every result.
+    unsigned short* P = reinterpret_cast<unsigned short*>(tbuf);
+    float* F = tbuf + kPlanesF;   // [edge][kPad] FP32: dE/da3, then dz0
+    const int c0 = 16 * w + 4 * (l >> 4);
+    if (parts_first) sum_partials();
+    float bc[NBP / 4];
+    us8v bp[2][3];
+    load_b_frag<NBP, false>(W0, nb, bc);
+    load_b_parts64<false>(W1, bp);
+    load_basis_tile<false>(E, e0, rbf, nb, (nb + 3) & ~3, xs);
+    __syncthreads();
+    f4 z0[4], z1[4], z2[4], acc[4];
+    input_mma_t<NBP>(xs, bc, z0);
+    store_parts_t(z0, P);
+    __syncthreads();
+    mma64_x3t(P, bp, z1);
     load_b_parts64<false>(W2, bp);
-  }
-  __syncthreads();   // every wave is done with ta
-  auto store_partials = [&]() {
+    __syncthreads();   // every wave has read the planes
+    store_parts_t(z1, P);
+    __syncthreads();
+    mma64_x3t(P, bp, z2);   // z2 only (a3 itself is not needed)
+    if (!parts_first) sum_partials();
 #pragma unroll
     for (int sr = 0; sr < 4; ++sr) {
       const int idx = tid + 256 * sr;
-      *reinterpret_cast<f4*>(ta + (idx >> 4) * kPad + 4 * (idx & 15)) = pacc[sr];
+      *reinterpret_cast<f4*>(F + (idx >> 4) * kPad + 4 * (idx & 15)) = pacc[sr];
     }
-  };
-  if (parts_first) store_partials();
-  // z2 only (a3 itself is not needed)
-  if constexpr (RND) hidden_mma<kH, false, RND>(tb, kPad, bc, nullptr, z2, rnd);
-  else hidden_mma_x3<false>(tb, kPad, bp, nullptr, z2);
-  if (!parts_first) {
-    sum_partials();
-    store_partials();
-  }
-  // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
-  float b2[RND ? kH / 4 : 1];
-  if constexpr (RND) {
+    load_b_parts64<true>(W2, bp);   // A of dz2 W2^T: W2[i][j], i the wave's output column
+    __syncthreads();   // dE/da3 in F; every wave has read the planes
+    // dz2 = da3 silu'(z2)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const f4 g = *reinterpret_cast<const f4*>(F + (16 * rt + (l & 15)) * kPad + c0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[rt][r] = g[r] * silu_grad(z2[rt][r]);
+    }
+    store_parts_t<false>(acc, P);
+    __syncthreads();
+    // dz1 = (dz2 W2^T) silu'(z1)
+    mma64_x3t(P, bp, acc);
+    load_b_parts64<true>(W1, bp);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[rt][r] *= silu_grad(z1[rt][r]);
+    __syncthreads();   // every wave has read the planes
+    store_parts_t<false>(acc, P);
+    __syncthreads();
+    // dz0 = (dz1 W1^T) silu'(z0), FP32 into F for the input layer's product
+    mma64_x3t(P, bp, acc);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      f4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = acc[rt][r] * silu_grad(z0[rt][r]);
+      *reinterpret_cast<f4*>(F + (16 * rt + (l & 15)) * kPad + c0) = v;
+    }
+    __syncthreads();
+    ta = F;   // dz0 for the de product below
+  } else {
+    // the precision study's rounded instance: FP32 MFMA on rounded operands,
+    // FP32 tiles in the result layout (lane l: rows 4(l/16) + r, column col)
+    if (parts_first) sum_partials();
+    float bc[kH / 4], bn[kH / 4];
+    load_b_frag<NBP, RND>(W0, nb, bc, rnd);
+    load_basis_tile<RND>(E, e0, rbf, nb, (nb + 3) & ~3, xs, rnd);
+    __syncthreads();
+    f4 z0[4], z1[4], z2[4];
+    load_b_frag<kH, RND>(W1, kH, bn, rnd);
+    hidden_mma<NBP, true, RND>(xs, kXPad, bc, ta, z0, rnd);
+    __syncthreads();
+    load_b_frag<kH, RND>(W2, kH, bc, rnd);
+    hidden_mma<kH, true, RND>(ta, kPad, bn, tb, z1, rnd);
+    __syncthreads();   // every wave is done with ta
+    auto store_partials = [&]() {
+#pragma unroll
+      for (int sr = 0; sr < 4; ++sr) {
+        const int idx = tid + 256 * sr;
+        *reinterpret_cast<f4*>(ta + (idx >> 4) * kPad + 4 * (idx & 15)) = pacc[sr];
+      }
+    };
+    if (parts_first) store_partials();
+    // z2 only (a3 itself is not needed)
+    hidden_mma<kH, false, RND>(tb, kPad, bc, nullptr, z2, rnd);
+    if (!parts_first) {
+      sum_partials();
+      store_partials();
+    }
+    // operand of the first backward MFMA stage: B[k = j][col = i] = W2[i][j]
+    float b2[kH / 4];
 #pragma unroll
     for (int ks = 0; ks < kH / 4; ++ks) b2[ks] = lowp_round(W2[col * kH + 4 * ks + (l >> 4)], rnd);
-  } else {
-    load_b_parts64<true>(W2, bp);
-  }
-  __syncthreads();
-  // dz2 = da3 silu'(z2), in place (result layout)
+    __syncthreads();
+    // dz2 = da3 silu'(z2), in place
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] *= silu_grad(z2[rt][r]);
-  __syncthreads();
-  f4 acc[4];
-  // dz1 = (dz2 W2^T) silu'(z1) into tb; the next stage's B = W1^T requested meanwhile
-  float b1[RND ? kH / 4 : 1];
-  if constexpr (RND) {
+      for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] *= silu_grad(z2[rt][r]);
+    __syncthreads();
+    f4 acc[4];
+    // dz1 = (dz2 W2^T) silu'(z1) into tb
+    float b1[kH / 4];
 #pragma unroll
     for (int ks = 0; ks < kH / 4; ++ks) b1[ks] = lowp_round(W1[col * kH + 4 * ks + (l >> 4)], rnd);
 #pragma unroll
@@ -501,17 +527,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) r
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt)
         acc[rt] = mfma4(ta[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b2[ks], acc[rt]);
-  } else {
-    mma64_x3(ta, kPad, bp, acc);
-    load_b_parts64<true>(W1, bp);   // B of the next product, W1^T, in flight during the stores and barrier below
-  }
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) tb[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z1[rt][r]);
-  __syncthreads();
-  // dz0 = (dz1 W1^T) silu'(z0) into ta (every wave has read ta before the barrier above)
-  if constexpr (RND) {
+      for (int r = 0; r < 4; ++r) tb[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z1[rt][r]);
+    __syncthreads();
+    // dz0 = (dz1 W1^T) silu'(z0) into ta (every wave has read ta before the barrier above)
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) acc[rt] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -519,14 +540,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) r
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt)
         acc[rt] = mfma4(tb[(16 * rt + (l & 15)) * kPad + 4 * ks + (l >> 4)], b1[ks], acc[rt]);
-  } else {
-    mma64_x3(tb, kPad, bp, acc);
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z0[rt][r]);
+    __syncthreads();
   }
-#pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) ta[(16 * rt + 4 * (l >> 4) + r) * kPad + col] = acc[rt][r] * silu_grad(z0[rt][r]);
-  __syncthreads();
   // de[e][i] = sum_j dz0[e][j] W0[i][j] on MFMA: wave w takes the edge rows
   // 16w .. 16w + 15, the 16 result columns are i (zero past nb <= 16)
   {
