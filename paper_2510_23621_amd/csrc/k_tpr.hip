@@ -140,7 +140,10 @@ __device__ __forceinline__ void load_w3_slice_bf16(const float* __restrict__ W3,
   }
 }
 
-// As tile_radial, on BF16 operands: two MFMAs (k = 32 each) per path.
+// As tile_radial, on BF16 operands: two MFMAs (k = 32 each) per path. The W3
+// operands are read kBf16Ahead paths ahead of their MFMAs, so that the LDS
+// reads do not stall each path's pair of products.
+constexpr int kBf16Ahead = 4;
 template <int P, bool TRP = false>
 __device__ __forceinline__ void tile_radial_bf16(const float* __restrict__ a3, int e0, int e_end,
                                                  const unsigned short* __restrict__ sWb, f4* r) {
@@ -148,19 +151,26 @@ __device__ __forceinline__ void tile_radial_bf16(const float* __restrict__ a3, i
   const int row = e0 + tile_edge<TRP>(l & 15);
   const float keep = row < e_end ? 1.f : 0.f;
   const f4* arow = reinterpret_cast<const f4*>(a3 + (size_t)min(row, e_end - 1) * 64 + 8 * (l >> 4));
+  const unsigned short* wb = sWb + (l & 15) * kWbPitch + 8 * (l >> 4);
+  constexpr int D = kBf16Ahead < P ? kBf16Ahead : P;
+  us8v bw[D][2];
+  auto load_b = [&](int p, us8v (&b)[2]) {
+    b[0] = *reinterpret_cast<const us8v*>(wb + p * 16 * kWbPitch);
+    b[1] = *reinterpret_cast<const us8v*>(wb + p * 16 * kWbPitch + 32);
+  };
+#pragma unroll
+  for (int p = 0; p < D; ++p) load_b(p, bw[p]);
   us8v a[2];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) a[ks] = to_bf16x8(arow[8 * ks] * keep, arow[8 * ks + 1] * keep);
-  const unsigned short* wb = sWb + (l & 15) * kWbPitch + 8 * (l >> 4);
   __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-  for (int p = 0; p < P; ++p) {
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-      acc = mfma_bf16(a[ks], *reinterpret_cast<const us8v*>(wb + p * 16 * kWbPitch + 32 * ks), acc);
-    r[p] = acc;
-  }
+  static_for<0, P>([&](auto PI) {
+    constexpr int p = decltype(PI)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    const us8v b0 = bw[p % D][0], b1 = bw[p % D][1];
+    if constexpr (p + D < P) load_b(p + D, bw[p % D]);
+    r[p] = mfma_bf16(a[1], b1, mfma_bf16(a[0], b0, f4{0.f, 0.f, 0.f, 0.f}));
+  });
   __builtin_amdgcn_s_setprio(0);
 }
 
