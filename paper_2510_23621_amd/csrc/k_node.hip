@@ -31,10 +31,22 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef unsigned short us8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ unsigned short fp16_bits(float x) { return __builtin_bit_cast(unsigned short, (_Float16)x); }
+// eight values as MFMA operand bits: bfloat16 by the packed hardware
+// conversion (round to nearest even, for finite values the bits of
+// bf16_bits), binary16 one value at a time
 template <int LP>
-__device__ __forceinline__ unsigned short lowp_bits(float x) {
-  if constexpr (LP == 1) return bf16_bits(x);
-  else return fp16_bits(x);
+__device__ __forceinline__ us8 lowp_bits8(f4 lo, f4 hi) {
+  if constexpr (LP == 1) {
+    typedef unsigned u4_ __attribute__((ext_vector_type(4)));
+    const u4_ w = {bf16_pack2(f2v{lo[0], lo[1]}), bf16_pack2(f2v{lo[2], lo[3]}), bf16_pack2(f2v{hi[0], hi[1]}),
+                   bf16_pack2(f2v{hi[2], hi[3]})};
+    return __builtin_bit_cast(us8, w);
+  } else {
+    us8 v;
+    v[0] = fp16_bits(lo[0]); v[1] = fp16_bits(lo[1]); v[2] = fp16_bits(lo[2]); v[3] = fp16_bits(lo[3]);
+    v[4] = fp16_bits(hi[0]); v[5] = fp16_bits(hi[1]); v[6] = fp16_bits(hi[2]); v[7] = fp16_bits(hi[3]);
+    return v;
+  }
 }
 
 // Column tiles of 16 per block. Four by default (measured at 1,536 and 36,864
@@ -121,10 +133,7 @@ linear_kernel(const LinLaunch* __restrict__ Lp, LinArgs a) {
       for (int ks = 0; ks < K / 32; ++ks) {
         const f4 lo = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4)) * keep;
         const f4 hi = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4) + 4) * keep;
-        us8 v;
-        v[0] = lowp_bits<LP>(lo[0]); v[1] = lowp_bits<LP>(lo[1]); v[2] = lowp_bits<LP>(lo[2]); v[3] = lowp_bits<LP>(lo[3]);
-        v[4] = lowp_bits<LP>(hi[0]); v[5] = lowp_bits<LP>(hi[1]); v[6] = lowp_bits<LP>(hi[2]); v[7] = lowp_bits<LP>(hi[3]);
-        ab[ks] = v;
+        ab[ks] = lowp_bits8<LP>(lo, hi);
       }
       // packed [K/8][K][8]: 8 consecutive k of output column n are 16 contiguous bytes
       const unsigned short* Wp = a.wbf + term.w_off + zoff;
@@ -287,9 +296,7 @@ __global__ void __launch_bounds__(64 * QD) linear_chain3_kernel(ChainArgs a) {
       for (int ks = 0; ks < K / 32; ++ks) {
         const f4 lo = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4)) * xk;
         const f4 hi = *reinterpret_cast<const f4*>(xrow + 32 * ks + 8 * (l >> 4) + 4) * xk;
-        us8 v;
-        v[0] = lowp_bits<LP>(lo[0]); v[1] = lowp_bits<LP>(lo[1]); v[2] = lowp_bits<LP>(lo[2]); v[3] = lowp_bits<LP>(lo[3]);
-        v[4] = lowp_bits<LP>(hi[0]); v[5] = lowp_bits<LP>(hi[1]); v[6] = lowp_bits<LP>(hi[2]); v[7] = lowp_bits<LP>(hi[3]);
+        const us8 v = lowp_bits8<LP>(lo, hi);
 #pragma unroll
         for (int j = 0; j < CT; ++j) {
           const us8 b = *reinterpret_cast<const us8*>(sBb + (16 * j + (l & 15)) * PB + 32 * ks + 8 * (l >> 4));

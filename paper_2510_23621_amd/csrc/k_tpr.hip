@@ -119,11 +119,13 @@ __device__ __forceinline__ f4 mfma_bf16(us8v a, us8v b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8v, a), __builtin_bit_cast(bf8v, b), c, 0, 0,
                                                  0);
 }
+// bfloat16 bits of eight values, rounded to nearest even by the packed
+// hardware conversion (for finite values the bits of bf16_bits)
 __device__ __forceinline__ us8v to_bf16x8(f4 lo, f4 hi) {
-  us8v v;
-  v[0] = bf16_bits(lo[0]); v[1] = bf16_bits(lo[1]); v[2] = bf16_bits(lo[2]); v[3] = bf16_bits(lo[3]);
-  v[4] = bf16_bits(hi[0]); v[5] = bf16_bits(hi[1]); v[6] = bf16_bits(hi[2]); v[7] = bf16_bits(hi[3]);
-  return v;
+  typedef unsigned u4v_ __attribute__((ext_vector_type(4)));
+  const u4v_ w = {bf16_pack2(f2v{lo[0], lo[1]}), bf16_pack2(f2v{lo[2], lo[3]}), bf16_pack2(f2v{hi[0], hi[1]}),
+                  bf16_pack2(f2v{hi[2], hi[3]})};
+  return __builtin_bit_cast(us8v, w);
 }
 
 // Forward slice sWb[(p*16 + kk)*kWbPitch + j] = bf16(W3[j][p K + 16 ct + kk]);
