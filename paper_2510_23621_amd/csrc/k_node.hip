@@ -30,23 +30,19 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef unsigned short us8 __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ unsigned short fp16_bits(float x) { return __builtin_bit_cast(unsigned short, (_Float16)x); }
-// eight values as MFMA operand bits: bfloat16 by the packed hardware
-// conversion (round to nearest even, for finite values the bits of
-// bf16_bits), binary16 one value at a time
+// eight values as MFMA operand bits, two per packed hardware conversion,
+// rounded to nearest even (for finite values the bits of bf16_bits, or of a
+// conversion to _Float16 one value at a time)
 template <int LP>
 __device__ __forceinline__ us8 lowp_bits8(f4 lo, f4 hi) {
-  if constexpr (LP == 1) {
-    typedef unsigned u4_ __attribute__((ext_vector_type(4)));
-    const u4_ w = {bf16_pack2(f2v{lo[0], lo[1]}), bf16_pack2(f2v{lo[2], lo[3]}), bf16_pack2(f2v{hi[0], hi[1]}),
-                   bf16_pack2(f2v{hi[2], hi[3]})};
-    return __builtin_bit_cast(us8, w);
-  } else {
-    us8 v;
-    v[0] = fp16_bits(lo[0]); v[1] = fp16_bits(lo[1]); v[2] = fp16_bits(lo[2]); v[3] = fp16_bits(lo[3]);
-    v[4] = fp16_bits(hi[0]); v[5] = fp16_bits(hi[1]); v[6] = fp16_bits(hi[2]); v[7] = fp16_bits(hi[3]);
-    return v;
-  }
+  typedef unsigned u4_ __attribute__((ext_vector_type(4)));
+  typedef _Float16 h2_ __attribute__((ext_vector_type(2)));
+  auto pack = [](f2v x) -> unsigned {
+    if constexpr (LP == 1) return bf16_pack2(x);
+    else return __builtin_bit_cast(unsigned, __builtin_convertvector(x, h2_));
+  };
+  const u4_ w = {pack(f2v{lo[0], lo[1]}), pack(f2v{lo[2], lo[3]}), pack(f2v{hi[0], hi[1]}), pack(f2v{hi[2], hi[3]})};
+  return __builtin_bit_cast(us8, w);
 }
 
 // Column tiles of 16 per block. Four by default (measured at 1,536 and 36,864
