@@ -562,13 +562,16 @@ __device__ __forceinline__ void load_h_row(const float* __restrict__ h, int src,
 // RM, the operands of the last radial layer: 0 FP32, 1 BF16, 2 split BF16 (FP32-accurate),
 // 3 split BF16 with a3 arriving as its three parts (the a3 argument then points at
 // [E][3][64] bfloat16 written by the edge prologue)
-template <int LHMAX, int RM, int NW = TprShape<LHMAX, false>::waves>
+// KC: K as a compile-time constant (0: the argument K), so that the sender
+// rows' component strides become immediate load offsets.
+template <int LHMAX, int RM, int NW = TprShape<LHMAX, false>::waves, int KC = 0>
 __global__ void __launch_bounds__(64 * NW)
 __attribute__((amdgpu_waves_per_eu(TprShape<LHMAX, false>::per_simd, TprShape<LHMAX, false>::per_simd)))
 tpr_fwd_kernel(
-    int N, int K, const int* __restrict__ rcv_off, const int* __restrict__ snd, const int* __restrict__ src_map,
+    int N, int K_arg, const int* __restrict__ rcv_off, const int* __restrict__ snd, const int* __restrict__ src_map,
     const float* __restrict__ a3, const float* __restrict__ W3, const float* __restrict__ Y,
     const float* __restrict__ h, float inv_c, float* __restrict__ At, int rnd) {
+  const int K = KC ? KC : K_arg;
   constexpr int P = path_count(LHMAX);
   constexpr int MID = mid_count(LHMAX);
   constexpr int DIN = (LHMAX + 1) * (LHMAX + 1);
@@ -612,15 +615,19 @@ tpr_fwd_kernel(
       // carry R = 0); the scheduling barrier keeps one edge's operands live at
       // a time, and the next edge's h row is requested while this one is contracted
       const int nq = min(4, (e_end - e0 + 3) >> 2);
-      float hv[DIN];
-      load_h_row<DIN>(h, srcq[0], K, k, hv);
+      // the sender rows of edges q and q + 1 (in flight); at l = 2 the two
+      // buffers alternate, below it the next row is copied over (fewer registers)
+      constexpr bool ALT = LHMAX == 2;
+      float hb[2][DIN];
+      load_h_row<DIN>(h, srcq[0], K, k, hb[0]);
       static_for<0, 4>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
+        constexpr int cur = ALT ? (q & 1) : 0, nxt = ALT ? ((q + 1) & 1) : 1;
         __builtin_amdgcn_sched_barrier(0);
         if (q >= nq) return;
         const int row = 4 * q + g;   // the lane's edge e0 + row
-        float hn[DIN];
-        if constexpr (q < 3) load_h_row<DIN>(h, srcq[q + 1], K, k, hn);
+        if constexpr (q < 3) load_h_row<DIN>(h, srcq[q + 1], K, k, hb[nxt]);
+        const float(&hv)[DIN] = hb[cur];
         float y[16];
         read_y(sy, row, y);
         for_paths<LHMAX>([&](auto tag) {
@@ -641,9 +648,9 @@ tpr_fwd_kernel(
             acc[T::offset + m3] = __builtin_fmaf(sg > 0 ? hr[m1] : -hr[m1], yc[u], acc[T::offset + m3]);
           });
         });
-        if constexpr (q < 3) {
+        if constexpr (!ALT && q < 3) {
 #pragma unroll
-          for (int c = 0; c < DIN; ++c) hv[c] = hn[c];
+          for (int c = 0; c < DIN; ++c) hb[0][c] = hb[1][c];
         }
       });
     }
@@ -1752,6 +1759,13 @@ void tpr_fwd_launch(hipStream_t s, int N, int K, const int* rcv_off, const int* 
   using S = TprShape<LH, false>;
   const int n_ct = K / 16;
   dim3 grid(tpr_grid_x(N, n_ct, S::waves, S::blocks_per_cu), n_ct);
+  if constexpr (LH == 2 && (RM == 3 || RM == 1)) {
+    if (K == 128) {
+      tpr_fwd_kernel<LH, RM, S::waves, 128><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h,
+                                                                            inv_c, At, rnd);
+      return;
+    }
+  }
   tpr_fwd_kernel<LH, RM><<<grid, 64 * S::waves, 0, s>>>(N, K, rcv_off, snd, src_map, a3, W3, Y, h, inv_c, At, rnd);
 }
 
